@@ -1,0 +1,6 @@
+"""CPU oracle of the ResBM boundary module (test infrastructure only).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package; the product path never does.
+"""
+from .resbm_oracle import *  # noqa: F401,F403
