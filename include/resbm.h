@@ -1,0 +1,161 @@
+/*
+ * resbm.h -- C ABI of the ResBM residual bottleneck boundary module on MI355X.
+ *
+ * The module sits at a pipeline-stage boundary (paper Sec. 3.2): at the end
+ * of stage l an encoder maps the feed-forward output z (T x n) to a rank-r
+ * payload b and adds the attention output x_attn through the identity
+ * projection P^id (Eq. 2, Eq. 5); only b crosses the link, as bf16 (App. A.3);
+ * at the start of stage l+1 a decoder expands b back to width n.  The
+ * backward ops are the exact adjoints of these maps.
+ *
+ * Conventions shared by every op
+ * ------------------------------
+ *  - T = batch x sequence tokens, n = hidden width (paper H), r = bottleneck
+ *    rank (paper h).  Matrices are row-major and right-multiplied (x W):
+ *    W_e is n x r, W_d is r x n, both float32 masters.
+ *  - Activations, payloads and activation gradients are bfloat16 in
+ *    libresbm.so and float32 in the validation build libresbm_f32.so;
+ *    resbm_io_dtype() tells which.  "act" below means that element type.
+ *  - All pointers are device pointers.  `stream` is a hipStream_t passed as
+ *    void* (NULL = the default stream).  Every op is asynchronous on `stream`,
+ *    never synchronises and keeps no state between calls; calls on different
+ *    streams with disjoint outputs and workspaces may run concurrently.
+ *  - The caller owns every buffer, including the workspace `ws` of at least
+ *    resbm_workspace_bytes(T, n, r) bytes (256-byte aligned).  Its contents on
+ *    entry are ignored; it must not be reused by another call until this one
+ *    has completed on the stream.  The library allocates nothing.
+ *  - Shape rules: T >= 0 (T == 0 is a successful no-op that reads no
+ *    pointer); n % 64 == 0 and 64 <= n <= 65536; r % 4 == 0 and
+ *    4 <= r <= min(n, 256) (r = n is the full-rank case of Sec. 3.3);
+ *    every leading dimension ld >= n with ld % 8 == 0 (in elements).
+ *  - Alignment: activation, payload and a_save pointers 16-byte aligned,
+ *    weight pointers 16-byte aligned, ws 256-byte aligned.
+ *  - Rounding: accumulation in float32 (products of bf16 operands are exact;
+ *    float32 weights and float32 intermediates enter the matrix cores as a
+ *    high+low bf16 pair); outputs are rounded once, float32 -> bf16 round to
+ *    nearest even; NaN and Inf propagate; no flush to zero.  Results are
+ *    bitwise reproducible run to run for fixed (T, n, r).
+ *  - Errors: arguments are validated on the host before any HIP call; an
+ *    invalid call returns a negative status and launches nothing.  A HIP
+ *    launch failure returns RESBM_E_HIP.
+ *  - Outputs must not overlap inputs or each other except where stated.
+ */
+#ifndef RESBM_H
+#define RESBM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RESBM_OK            0
+#define RESBM_E_NULL       -1  /* a required pointer is NULL                    */
+#define RESBM_E_SHAPE      -2  /* T, n, r or a leading dimension breaks a rule  */
+#define RESBM_E_ALIGN      -3  /* a pointer is not aligned as required          */
+#define RESBM_E_WORKSPACE  -4  /* ws_bytes < resbm_workspace_bytes(T, n, r)     */
+#define RESBM_E_ACT        -5  /* unknown act, or SiLU backward without a_save  */
+#define RESBM_E_HIP        -6  /* a kernel launch failed                        */
+#define RESBM_E_ALIAS      -7  /* an output aliases an input it may not alias   */
+
+#define RESBM_ACT_IDENTITY  0
+#define RESBM_ACT_SILU      1  /* phi(a) = a * sigmoid(a)                        */
+
+#define RESBM_IO_BF16       0
+#define RESBM_IO_F32        1
+
+/*
+ * Encoder forward at the end of stage l (Sec. 3.2; Eq. 2 with P^id_l of
+ * Eq. 5 truncating n -> r, which keeps columns [0, r)):
+ *     a = z W_e                           (T x r, float32)
+ *     b = x_attn I_{n x r} + phi(a)       (T x r, the payload)
+ *  x_attn  T x n act, row stride ld_x; only columns [0, r) are read.
+ *  z       T x n act, row stride ld_z; may alias x_attn.
+ *  W_e     n x r float32, contiguous.
+ *  b       out, T x r act, packed row-major [T][r] (the wire layout of App. A.3).
+ *  a_save  out, T x r float32 contiguous, or NULL.  encode_bwd with SiLU needs it.
+ */
+int32_t resbm_encode_fwd(int64_t T, int32_t n, int32_t r, int32_t act,
+                         const void* x_attn, int64_t ld_x,
+                         const void* z, int64_t ld_z,
+                         const float* W_e,
+                         void* b, float* a_save,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Decoder forward at the start of stage l+1 (Sec. 3.2, D_{l+1}):
+ *     z_tilde = b W_d                 (add_identity == 0, the caller adds the
+ *                                      skip b I_{r x n} after its attention)
+ *     z_tilde = b W_d + b I_{r x n}   (add_identity != 0: Eq. 5 zero-pads r -> n)
+ *  b        T x r act, packed [T][r].
+ *  W_d      r x n float32, contiguous.
+ *  z_tilde  out, T x n act, row stride ld_zt.
+ */
+int32_t resbm_decode_fwd(int64_t T, int32_t n, int32_t r, int32_t add_identity,
+                         const void* b, const float* W_d,
+                         void* z_tilde, int64_t ld_zt,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Decoder backward (adjoint of decode_fwd; the r-wide result is what crosses
+ * the link backwards, App. A.3):
+ *     g_b  = g_zt W_d^T + g_id I_{n x r}     (T x r, act, packed)
+ *     dW_d = b^T g_zt   (+ the previous dW_d when accumulate != 0)
+ *  b      T x r act, packed (the payload the forward received).
+ *  g_zt   T x n act, row stride ld_gzt: dL/dz_tilde.
+ *  g_id   T x n act, row stride ld_gid, or NULL (no identity-path gradient);
+ *         only columns [0, r) are read.  Reading A of the decoder identity
+ *         (add_identity != 0 in the forward) passes g_id = g_zt.
+ *  g_b    out, T x r act, packed [T][r].
+ *  dW_d   r x n float32, contiguous; overwritten or accumulated into.
+ *         The token sum is formed in a fixed order (per-tile partial sums
+ *         added in tile order), so it is reproducible.
+ */
+int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r,
+                         const void* b, const float* W_d,
+                         const void* g_zt, int64_t ld_gzt,
+                         const void* g_id, int64_t ld_gid,
+                         void* g_b,
+                         float* dW_d, int32_t accumulate,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Encoder backward (adjoint of encode_fwd):
+ *     g_h  = g_b * phi'(a)                   (on chip, float32)
+ *     g_z  = g_h W_e^T                       (T x n act)
+ *     dW_e = z^T g_h    (+ the previous dW_e when accumulate != 0)
+ *     g_x[:, 0:r] += g_b                     (adjoint of P^id_l; when g_x != NULL)
+ *  z       T x n act, row stride ld_z (the forward's encoder input).
+ *  W_e     n x r float32.
+ *  a_save  T x r float32 from encode_fwd; may be NULL only when act is identity.
+ *  g_b     T x r act, packed: the wire gradient.
+ *  g_z     out, T x n act, row stride ld_gz.
+ *  g_x     T x n act, row stride ld_gx, updated in place (columns >= r are not
+ *          touched), or NULL.  g_x may equal g_z (same pointer and ld_gx ==
+ *          ld_gz): then g_z = g_h W_e^T + g_b I_{r x n}, rounded once.
+ *  dW_e    n x r float32; overwritten or accumulated into, fixed token order.
+ */
+int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act,
+                         const void* z, int64_t ld_z, const float* W_e,
+                         const float* a_save, const void* g_b,
+                         void* g_z, int64_t ld_gz,
+                         void* g_x, int64_t ld_gx,
+                         float* dW_e, int32_t accumulate,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes every op above needs for (T, n, r): the maximum over the
+ * four ops, a multiple of 256.  Returns 0 when (n, r) break the shape rules. */
+size_t resbm_workspace_bytes(int64_t T, int32_t n, int32_t r);
+
+/* RESBM_IO_BF16 for libresbm.so, RESBM_IO_F32 for the validation build. */
+int32_t resbm_io_dtype(void);
+
+/* A static, NUL-terminated description of a status code. */
+const char* resbm_strerror(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RESBM_H */

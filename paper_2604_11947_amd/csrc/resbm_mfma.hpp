@@ -1,0 +1,209 @@
+// Matrix-core building blocks for gfx950 (CDNA4), shared by the boundary kernels.
+//
+// Every contraction is expressed with 16x16 output tiles.  A lane l of a
+// 64-wide wave is addressed as (row16 = l % 16, grp = l / 16).  For one
+// 32-deep step of K the A operand fragment of lane l holds A[row16][8*grp + e]
+// and the B fragment holds B[8*grp + e][row16], e = 0..7; the accumulator
+// holds D[4*grp + v][row16], v = 0..3.  Because A and B use the same
+// lane/slot -> k assignment, the exact order in which the hardware visits k
+// inside the step does not matter.
+//
+// Two element types are supported:
+//   bf16 I/O  (default)   : one v_mfma_f32_16x16x32_bf16 per bf16 x bf16 product.
+//                           float32 operands (weights, on-chip gradients) are
+//                           split into hi + lo bf16 parts, hi = rne(w),
+//                           lo = rne(w - hi), which keeps ~16 significant bits.
+//   f32 I/O (validation)  : eight v_mfma_f32_16x16x4_f32 per step, slot e of
+//                           every lane feeding the e-th instruction.
+#pragma once
+
+#ifndef RESBM_IO_F32_BUILD
+#define RESBM_IO_F32_BUILD 0
+#endif
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace resbm {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// ---------------------------------------------------------------- bf16 helpers
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
+  return __builtin_bit_cast(float, bits16 << 16);
+}
+
+// float32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }
+
+// hi + lo split of a float32 value.  Infinite hi parts get a zero lo part so
+// that an infinite weight multiplies as infinity rather than inf + (-inf).
+__device__ __forceinline__ void split_hi_lo(float w, __bf16& hi, __bf16& lo) {
+  hi = to_bf16(w);
+  float h = (float)hi;
+  lo = __builtin_isinf(h) ? to_bf16(0.0f) : to_bf16(w - h);
+}
+
+// ---------------------------------------------------------------- fragments
+// An "exact" fragment carries 8 values that are representable in the I/O type
+// (activations, payloads).  A "split" fragment carries 8 float32 values
+// (weights, float32 intermediates) in the form the matrix cores consume.
+#if RESBM_IO_F32_BUILD
+struct XFrag { float v[8]; };
+struct SFrag { float v[8]; };
+#else
+struct XFrag { bf16x8 v; };
+struct SFrag { bf16x8 hi, lo; };
+#endif
+
+__device__ __forceinline__ XFrag xfrag_zero() {
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f.v[e] = 0.0f;
+#else
+  f.v = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
+#endif
+  return f;
+}
+
+__device__ __forceinline__ SFrag sfrag_from(const float (&w)[8]) {
+  SFrag f;
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f.v[e] = w[e];
+#else
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    __bf16 h, l;
+    split_hi_lo(w[e], h, l);
+    f.hi[e] = h;
+    f.lo[e] = l;
+  }
+#endif
+  return f;
+}
+
+__device__ __forceinline__ SFrag sfrag_zero() {
+  float w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  return sfrag_from(w);
+}
+
+// An exact fragment reinterpreted as a split one (lo = 0); used where a bf16
+// operand meets a split operand in the 3-product form.
+__device__ __forceinline__ float xfrag_get(const XFrag& f, int e) {
+#if RESBM_IO_F32_BUILD
+  return f.v[e];
+#else
+  return (float)f.v[e];
+#endif
+}
+
+// ---------------------------------------------------------------- products
+#if RESBM_IO_F32_BUILD
+__device__ __forceinline__ f32x4 mma8(const float (&a)[8], const float (&b)[8], f32x4 c) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
+  return c;
+}
+// split (A) x exact (B)
+__device__ __forceinline__ f32x4 mma_sx(const SFrag& a, const XFrag& b, f32x4 c) { return mma8(a.v, b.v, c); }
+// exact (A) x split (B)
+__device__ __forceinline__ f32x4 mma_xs(const XFrag& a, const SFrag& b, f32x4 c) { return mma8(a.v, b.v, c); }
+// exact x exact
+__device__ __forceinline__ f32x4 mma_xx(const XFrag& a, const XFrag& b, f32x4 c) { return mma8(a.v, b.v, c); }
+// split x split
+__device__ __forceinline__ f32x4 mma_ss(const SFrag& a, const SFrag& b, f32x4 c) { return mma8(a.v, b.v, c); }
+#else
+__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma_sx(const SFrag& a, const XFrag& b, f32x4 c) {
+  c = mfma(a.lo, b.v, c);
+  return mfma(a.hi, b.v, c);
+}
+__device__ __forceinline__ f32x4 mma_xs(const XFrag& a, const SFrag& b, f32x4 c) {
+  c = mfma(a.v, b.lo, c);
+  return mfma(a.v, b.hi, c);
+}
+__device__ __forceinline__ f32x4 mma_xx(const XFrag& a, const XFrag& b, f32x4 c) {
+  return mfma(a.v, b.v, c);
+}
+// (ah + al)(bh + bl) without the al*bl term (below 2^-16 relative).
+__device__ __forceinline__ f32x4 mma_ss(const SFrag& a, const SFrag& b, f32x4 c) {
+  c = mfma(a.lo, b.hi, c);
+  c = mfma(a.hi, b.lo, c);
+  return mfma(a.hi, b.hi, c);
+}
+#endif
+
+// ---------------------------------------------------------------- I/O element
+#if RESBM_IO_F32_BUILD
+typedef float io_t;
+#else
+typedef __bf16 io_t;
+#endif
+
+__device__ __forceinline__ float io_to_f32(io_t x) { return (float)x; }
+__device__ __forceinline__ io_t f32_to_io(float x) {
+#if RESBM_IO_F32_BUILD
+  return x;
+#else
+  return to_bf16(x);
+#endif
+}
+
+// 8 consecutive I/O elements starting at p (16-byte aligned for bf16,
+// 32-byte aligned for f32).
+__device__ __forceinline__ XFrag load_x8(const io_t* p) {
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+  float4 a = *reinterpret_cast<const float4*>(p);
+  float4 b = *reinterpret_cast<const float4*>(p + 4);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+#else
+  f.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+#endif
+  return f;
+}
+
+// 4 consecutive I/O elements (8-byte aligned for bf16, 16 for f32).
+__device__ __forceinline__ void load_x4(const io_t* p, float (&out)[4]) {
+#if RESBM_IO_F32_BUILD
+  float4 a = *reinterpret_cast<const float4*>(p);
+  out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+#else
+  uint2 u = *reinterpret_cast<const uint2*>(p);
+  out[0] = bf16_bits_to_f32(u.x & 0xffffu);
+  out[1] = bf16_bits_to_f32(u.x >> 16);
+  out[2] = bf16_bits_to_f32(u.y & 0xffffu);
+  out[3] = bf16_bits_to_f32(u.y >> 16);
+#endif
+}
+
+__device__ __forceinline__ void store_x4(io_t* p, const float (&v)[4]) {
+#if RESBM_IO_F32_BUILD
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+#else
+  bf16x4 h;
+  h[0] = to_bf16(v[0]); h[1] = to_bf16(v[1]); h[2] = to_bf16(v[2]); h[3] = to_bf16(v[3]);
+  *reinterpret_cast<uint2*>(p) = __builtin_bit_cast(uint2, h);
+#endif
+}
+
+// Activation function and its derivative (float32).
+__device__ __forceinline__ float act_phi(float a, int act) {
+  return act == 1 ? a / (1.0f + expf(-a)) : a;
+}
+__device__ __forceinline__ float act_dphi(float a, int act) {
+  if (act != 1) return 1.0f;
+  float s = 1.0f / (1.0f + expf(-a));
+  return s * (1.0f + a * (1.0f - s));
+}
+
+}  // namespace resbm

@@ -114,18 +114,28 @@ def _grad(rng: np.random.Generator, T: int, n: int) -> torch.Tensor:
     return out
 
 
-def make_inputs(T: int, n: int, r: int, dist: str = "normal", seed: int = 0,
-                grads: bool = True) -> dict[str, torch.Tensor]:
-    """Draw one boundary's inputs on the host.
-
-    Returns CPU tensors ``x_attn, z, g_zt, g_id`` (bf16, ``[T][n]``), ``W_e``
-    (fp32 ``[n][r]``, N(0, 1/n)) and ``W_d`` (fp32 ``[r][n]``, N(0, 1/r)), plus
-    ``meta`` describing structural draws (outlier channels, token scales).
-    """
-    if T < 0 or n <= 0 or r <= 0:
-        raise ValueError("T must be >= 0 and n, r positive")
+def _streams(seed: int) -> list[np.random.Generator]:
     ss = np.random.SeedSequence(seed).spawn(7)
-    rngs = [np.random.Generator(np.random.PCG64(s)) for s in ss]
+    return [np.random.Generator(np.random.PCG64(s)) for s in ss]
+
+
+def make_weights(n: int, r: int, seed: int = 0) -> dict[str, torch.Tensor]:
+    """The weights make_inputs would draw for (n, r, seed): W_e ~ N(0, 1/n) fp32
+    ``[n][r]`` and W_d ~ N(0, 1/r) fp32 ``[r][n]``."""
+    rngs = _streams(seed)
+    return {
+        "W_e": torch.from_numpy((rngs[2].standard_normal((n, r)) / np.sqrt(n)).astype(np.float32)),
+        "W_d": torch.from_numpy((rngs[3].standard_normal((r, n)) / np.sqrt(r)).astype(np.float32)),
+    }
+
+
+def make_activations(T: int, n: int, dist: str = "normal", seed: int = 0,
+                     grads: bool = True) -> dict:
+    """The activations and upstream gradients make_inputs would draw (they do
+    not depend on r): ``x_attn, z, g_zt, g_id`` bf16 ``[T][n]`` plus ``meta``."""
+    if T < 0 or n <= 0:
+        raise ValueError("T must be >= 0 and n positive")
+    rngs = _streams(seed)
     struct_rng = rngs[6]
     struct: dict = {}
     if dist == "outliers":
@@ -133,13 +143,9 @@ def make_inputs(T: int, n: int, r: int, dist: str = "normal", seed: int = 0,
         struct["channels"] = np.sort(struct_rng.choice(n, size=k, replace=False))
     elif dist == "token_lognormal":
         struct["token_scale"] = np.exp(0.5 * struct_rng.standard_normal(T))
-    out = {
+    out: dict = {
         "x_attn": _activation(rngs[0], T, n, dist, struct),
         "z": _activation(rngs[1], T, n, dist, struct),
-        "W_e": torch.from_numpy(
-            (rngs[2].standard_normal((n, r)) / np.sqrt(n)).astype(np.float32)),
-        "W_d": torch.from_numpy(
-            (rngs[3].standard_normal((r, n)) / np.sqrt(r)).astype(np.float32)),
     }
     if grads:
         out["g_zt"] = _grad(rngs[4], T, n)
@@ -147,8 +153,24 @@ def make_inputs(T: int, n: int, r: int, dist: str = "normal", seed: int = 0,
     meta = {"dist": dist, "seed": seed}
     if "channels" in struct:
         meta["outlier_channels"] = struct["channels"].tolist()
-        meta["outliers_in_skip"] = int(np.sum(struct["channels"] < r))
     out["meta"] = meta
+    return out
+
+
+def make_inputs(T: int, n: int, r: int, dist: str = "normal", seed: int = 0,
+                grads: bool = True) -> dict:
+    """Draw one boundary's inputs on the host.
+
+    Returns CPU tensors ``x_attn, z, g_zt, g_id`` (bf16, ``[T][n]``), ``W_e``
+    (fp32 ``[n][r]``, N(0, 1/n)) and ``W_d`` (fp32 ``[r][n]``, N(0, 1/r)), plus
+    ``meta`` describing structural draws (outlier channels).
+    """
+    if r <= 0:
+        raise ValueError("r must be positive")
+    out = make_activations(T, n, dist, seed, grads)
+    out.update(make_weights(n, r, seed))
+    if "outlier_channels" in out["meta"]:
+        out["meta"]["outliers_in_skip"] = int(sum(c < r for c in out["meta"]["outlier_channels"]))
     return out
 
 

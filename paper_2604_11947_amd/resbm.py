@@ -1,0 +1,204 @@
+"""ctypes binding of ``libresbm`` -- the C ABI declared in ``include/resbm.h``.
+
+Argument marshalling only: torch tensors supply device pointers, row strides
+and the current HIP stream; every step of the module runs in the library's
+kernels.  A missing library raises ``LibraryNotBuilt``; nothing falls back to
+another implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from . import build as _build
+
+ACT_IDENTITY = 0
+ACT_SILU = 1
+IO_BF16 = 0
+IO_F32 = 1
+
+OK = 0
+E_NULL = -1
+E_SHAPE = -2
+E_ALIGN = -3
+E_WORKSPACE = -4
+E_ACT = -5
+E_HIP = -6
+E_ALIAS = -7
+
+# (name, restype, argtypes) of every exported symbol
+_i64, _i32, _p, _sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+SIGNATURES = [
+    ("resbm_encode_fwd", _i32, [_i64, _i32, _i32, _i32, _p, _i64, _p, _i64, _p, _p, _p, _p, _sz, _p]),
+    ("resbm_decode_fwd", _i32, [_i64, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _sz, _p]),
+    ("resbm_decode_bwd", _i32, [_i64, _i32, _i32, _p, _p, _p, _i64, _p, _i64, _p, _p, _i32, _p, _sz, _p]),
+    ("resbm_encode_bwd", _i32, [_i64, _i32, _i32, _i32, _p, _i64, _p, _p, _p, _p, _i64, _p, _i64, _p, _i32,
+                                _p, _sz, _p]),
+    ("resbm_workspace_bytes", _sz, [_i64, _i32, _i32]),
+    ("resbm_io_dtype", _i32, []),
+    ("resbm_strerror", ctypes.c_char_p, [_i32]),
+]
+
+
+class LibraryNotBuilt(RuntimeError):
+    pass
+
+
+class ResbmError(RuntimeError):
+    def __init__(self, op: str, status: int, message: str):
+        super().__init__(f"{op}: status {status}: {message}")
+        self.status = status
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _ld(t: torch.Tensor, rows: int, cols: int, name: str) -> int:
+    if t.dim() != 2 or t.shape[0] != rows or t.shape[1] != cols:
+        raise ValueError(f"{name}: expected shape ({rows}, {cols}), got {tuple(t.shape)}")
+    if rows > 1 and cols > 0 and t.stride(1) != 1:
+        raise ValueError(f"{name}: rows must be contiguous")
+    return t.stride(0) if rows > 1 else max(t.stride(0), cols)
+
+
+def _packed(t: torch.Tensor, rows: int, cols: int, name: str) -> None:
+    if t.dim() != 2 or t.shape[0] != rows or t.shape[1] != cols or not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous ({rows}, {cols}) tensor, got {tuple(t.shape)}")
+
+
+def _dtype(t, dtype, name):
+    if t is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+
+
+def _stream(stream, ref: torch.Tensor):
+    if stream is None:
+        stream = torch.cuda.current_stream(ref.device)
+    return ctypes.c_void_p(getattr(stream, "cuda_stream", stream))
+
+
+class Library:
+    """One loaded variant of the library ("bf16" or "f32")."""
+
+    def __init__(self, variant: str = "bf16"):
+        path = _build.lib_path(variant)
+        if not os.path.exists(path):
+            raise LibraryNotBuilt(f"{path} is missing; run `python -m paper_2604_11947_amd.build`")
+        self.path = path
+        self.cdll = ctypes.CDLL(path)
+        for name, res, args in SIGNATURES:
+            fn = getattr(self.cdll, name)
+            fn.restype = res
+            fn.argtypes = args
+        self.io_code = int(self.cdll.resbm_io_dtype())
+        self.io_dtype = torch.bfloat16 if self.io_code == IO_BF16 else torch.float32
+
+    # ------------------------------------------------------------ helpers
+    def workspace_bytes(self, T: int, n: int, r: int) -> int:
+        return int(self.cdll.resbm_workspace_bytes(T, n, r))
+
+    def strerror(self, status: int) -> str:
+        return self.cdll.resbm_strerror(status).decode()
+
+    def workspace(self, T: int, n: int, r: int, device) -> torch.Tensor:
+        nbytes = self.workspace_bytes(T, n, r)
+        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        off = (-buf.data_ptr()) % 256
+        return buf[off:off + nbytes]
+
+    def _check(self, op: str, status: int) -> None:
+        if status != OK:
+            raise ResbmError(op, status, self.strerror(status))
+
+    # ------------------------------------------------------------ ops
+    def encode_fwd(self, x_attn, z, W_e, b, a_save=None, act=ACT_SILU, ws=None, stream=None):
+        T = z.shape[0]
+        n, r = W_e.shape
+        io = self.io_dtype
+        for t, nm in ((x_attn, "x_attn"), (z, "z"), (b, "b")):
+            _dtype(t, io, nm)
+        _dtype(W_e, torch.float32, "W_e")
+        _dtype(a_save, torch.float32, "a_save")
+        ld_x, ld_z = _ld(x_attn, T, n, "x_attn"), _ld(z, T, n, "z")
+        _packed(b, T, r, "b")
+        _packed(W_e, n, r, "W_e")
+        if a_save is not None:
+            _packed(a_save, T, r, "a_save")
+        if ws is None:
+            ws = self.workspace(T, n, r, z.device)
+        st = self.cdll.resbm_encode_fwd(T, n, r, act, _ptr(x_attn), ld_x, _ptr(z), ld_z, _ptr(W_e), _ptr(b),
+                                        _ptr(a_save), _ptr(ws), ws.numel(), _stream(stream, z))
+        self._check("resbm_encode_fwd", st)
+
+    def decode_fwd(self, b, W_d, z_tilde, add_identity=False, ws=None, stream=None):
+        T = b.shape[0]
+        r, n = W_d.shape
+        _dtype(b, self.io_dtype, "b")
+        _dtype(z_tilde, self.io_dtype, "z_tilde")
+        _dtype(W_d, torch.float32, "W_d")
+        _packed(b, T, r, "b")
+        _packed(W_d, r, n, "W_d")
+        ld = _ld(z_tilde, T, n, "z_tilde")
+        nbytes = 0 if ws is None else ws.numel()
+        st = self.cdll.resbm_decode_fwd(T, n, r, int(bool(add_identity)), _ptr(b), _ptr(W_d), _ptr(z_tilde), ld,
+                                        _ptr(ws), nbytes, _stream(stream, b))
+        self._check("resbm_decode_fwd", st)
+
+    def decode_bwd(self, b, W_d, g_zt, g_id, g_b, dW_d, accumulate=False, ws=None, stream=None):
+        T = b.shape[0]
+        r, n = W_d.shape
+        io = self.io_dtype
+        for t, nm in ((b, "b"), (g_zt, "g_zt"), (g_id, "g_id"), (g_b, "g_b")):
+            _dtype(t, io, nm)
+        _dtype(W_d, torch.float32, "W_d")
+        _dtype(dW_d, torch.float32, "dW_d")
+        _packed(b, T, r, "b")
+        _packed(g_b, T, r, "g_b")
+        _packed(W_d, r, n, "W_d")
+        _packed(dW_d, r, n, "dW_d")
+        ld_g = _ld(g_zt, T, n, "g_zt")
+        ld_i = _ld(g_id, T, n, "g_id") if g_id is not None else 0
+        if ws is None:
+            ws = self.workspace(T, n, r, g_zt.device)
+        st = self.cdll.resbm_decode_bwd(T, n, r, _ptr(b), _ptr(W_d), _ptr(g_zt), ld_g, _ptr(g_id), ld_i, _ptr(g_b),
+                                        _ptr(dW_d), int(bool(accumulate)), _ptr(ws), ws.numel(),
+                                        _stream(stream, g_zt))
+        self._check("resbm_decode_bwd", st)
+
+    def encode_bwd(self, z, W_e, a_save, g_b, g_z, dW_e, g_x=None, act=ACT_SILU, accumulate=False, ws=None,
+                   stream=None):
+        T = z.shape[0]
+        n, r = W_e.shape
+        io = self.io_dtype
+        for t, nm in ((z, "z"), (g_b, "g_b"), (g_z, "g_z"), (g_x, "g_x")):
+            _dtype(t, io, nm)
+        _dtype(W_e, torch.float32, "W_e")
+        _dtype(a_save, torch.float32, "a_save")
+        _dtype(dW_e, torch.float32, "dW_e")
+        ld_z = _ld(z, T, n, "z")
+        ld_gz = _ld(g_z, T, n, "g_z")
+        ld_gx = _ld(g_x, T, n, "g_x") if g_x is not None else 0
+        _packed(W_e, n, r, "W_e")
+        _packed(g_b, T, r, "g_b")
+        _packed(dW_e, n, r, "dW_e")
+        if a_save is not None:
+            _packed(a_save, T, r, "a_save")
+        if ws is None:
+            ws = self.workspace(T, n, r, z.device)
+        st = self.cdll.resbm_encode_bwd(T, n, r, act, _ptr(z), ld_z, _ptr(W_e), _ptr(a_save), _ptr(g_b), _ptr(g_z),
+                                        ld_gz, _ptr(g_x), ld_gx, _ptr(dW_e), int(bool(accumulate)), _ptr(ws),
+                                        ws.numel(), _stream(stream, z))
+        self._check("resbm_encode_bwd", st)
+
+
+_LOADED: dict[str, Library] = {}
+
+
+def library(variant: str = "bf16") -> Library:
+    """The loaded library variant ("bf16" = libresbm.so, "f32" = libresbm_f32.so)."""
+    if variant not in _LOADED:
+        _LOADED[variant] = Library(variant)
+    return _LOADED[variant]

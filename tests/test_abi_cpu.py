@@ -1,0 +1,202 @@
+"""Host-side checks of the C ABI: exports, workspace sizing, validation.
+
+Every call here is rejected by host validation before any HIP call (or is a
+pure host query), so these run without a GPU.  They use fake device addresses
+and are therefore skipped where a GPU is visible.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+import torch
+
+from paper_2604_11947_amd import build as B
+from paper_2604_11947_amd import resbm as R
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "resbm.h")
+
+
+@pytest.fixture(scope="module", params=["bf16", "f32"])
+def lib(request):
+    if not os.path.exists(B.lib_path(request.param)):
+        B.build_all()
+    return R.Library(request.param)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(resbm_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_four_ops_and_helpers():
+    names = declared_functions()
+    for op in ("resbm_encode_fwd", "resbm_decode_fwd", "resbm_decode_bwd", "resbm_encode_bwd",
+               "resbm_workspace_bytes", "resbm_io_dtype", "resbm_strerror"):
+        assert op in names
+    assert sorted(n for n, _, _ in R.SIGNATURES) == names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", lib.path], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (resbm_\w+)$", out, flags=re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib.cdll, name)
+
+
+def test_io_dtype(lib):
+    want = R.IO_BF16 if lib.path.endswith("libresbm.so") else R.IO_F32
+    assert lib.io_code == want
+
+
+def test_strerror(lib):
+    for st in (0, -1, -2, -3, -4, -5, -6, -7):
+        assert lib.strerror(st) and lib.strerror(st) != "unknown status"
+    assert lib.strerror(-99) == "unknown status"
+
+
+def test_workspace_bytes(lib):
+    assert lib.workspace_bytes(1024, 100, 32) == 0          # n % 64
+    assert lib.workspace_bytes(1024, 512, 6) == 0           # r % 4
+    assert lib.workspace_bytes(1024, 512, 260) == 0         # r > 256
+    assert lib.workspace_bytes(1024, 64, 128) == 0          # r > n
+    assert lib.workspace_bytes(-1, 512, 32) == 0
+    prev = 0
+    for T in (1, 31, 32, 1000, 16384, 65536, 1 << 20):
+        w = lib.workspace_bytes(T, 4096, 32)
+        assert w % 256 == 0 and w >= prev
+        prev = w
+    # headline shape: bounded by a modest fraction of its 4 x 128 MiB streams
+    assert lib.workspace_bytes(16384, 4096, 32) <= 64 << 20
+
+
+def test_library_missing_raises(monkeypatch, tmp_path):
+    monkeypatch.setattr(B, "lib_path", lambda variant="bf16": str(tmp_path / "nope.so"))
+    with pytest.raises(R.LibraryNotBuilt):
+        R.Library("bf16")
+
+
+def test_product_never_imports_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2604_11947_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle\b", text, flags=re.M), f
+                assert "resbm_oracle" not in text, f
+
+
+# ---------------------------------------------------------------- validation
+needs_no_gpu = pytest.mark.skipif(torch.cuda.is_available(),
+                                  reason="fake device addresses; host validation is covered on CPU hosts")
+
+A = 0x10000000   # fake, 256-byte aligned addresses far apart
+T, N, RR = 64, 256, 32
+
+
+def enc_fwd_args(**over):
+    names = ["T", "n", "r", "act", "x", "ldx", "z", "ldz", "We", "b", "a", "ws", "wsb", "s"]
+    vals = [T, N, RR, 1, A, N, 2 * A, N, 3 * A, 4 * A, 5 * A, 6 * A, 1 << 30, None]
+    for k, v in over.items():
+        vals[names.index(k)] = v
+    return vals
+
+
+@needs_no_gpu
+@pytest.mark.parametrize("over,status", [
+    (dict(T=-1), R.E_SHAPE), (dict(n=100), R.E_SHAPE), (dict(n=0), R.E_SHAPE), (dict(r=0), R.E_SHAPE),
+    (dict(r=6), R.E_SHAPE), (dict(r=260), R.E_SHAPE), (dict(n=64, r=128, ldx=64, ldz=64), R.E_SHAPE),
+    (dict(act=2), R.E_ACT), (dict(x=None), R.E_NULL), (dict(z=None), R.E_NULL), (dict(We=None), R.E_NULL),
+    (dict(b=None), R.E_NULL), (dict(ws=None), R.E_NULL), (dict(ldx=N - 8), R.E_SHAPE),
+    (dict(ldz=N + 4), R.E_SHAPE), (dict(x=A + 8), R.E_ALIGN), (dict(z=2 * A + 2), R.E_ALIGN),
+    (dict(a=5 * A + 4), R.E_ALIGN), (dict(ws=6 * A + 128), R.E_ALIGN), (dict(wsb=1024), R.E_WORKSPACE),
+    (dict(b=2 * A + 64), R.E_ALIAS), (dict(a=A), R.E_ALIAS), (dict(ws=2 * A), R.E_ALIAS),
+])
+def test_encode_fwd_validation(lib, over, status):
+    assert lib.cdll.resbm_encode_fwd(*enc_fwd_args(**over)) == status
+
+
+@needs_no_gpu
+def test_zero_tokens_needs_no_pointers(lib):
+    c = lib.cdll
+    assert c.resbm_encode_fwd(0, N, RR, 1, None, 0, None, 0, None, None, None, None, 0, None) == R.OK
+    assert c.resbm_decode_fwd(0, N, RR, 0, None, None, None, 0, None, 0, None) == R.OK
+    assert c.resbm_decode_bwd(0, N, RR, None, None, None, 0, None, 0, None, None, 0, None, 0, None) == R.OK
+    assert c.resbm_encode_bwd(0, N, RR, 1, None, 0, None, None, None, None, 0, None, 0, None, 0, None, 0,
+                              None) == R.OK
+    # shape rules still apply at T = 0
+    assert c.resbm_decode_fwd(0, 100, RR, 0, None, None, None, 0, None, 0, None) == R.E_SHAPE
+
+
+@needs_no_gpu
+def test_decode_fwd_validation(lib):
+    c = lib.cdll
+    ok = [T, N, RR, 0, A, 2 * A, 3 * A, N, None, 0, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm_decode_fwd(*a)
+
+    assert call(4, None) == R.E_NULL
+    assert call(5, None) == R.E_NULL
+    assert call(6, None) == R.E_NULL
+    assert call(7, N - 8) == R.E_SHAPE
+    assert call(4, A + 2) == R.E_ALIGN
+    assert call(6, A) == R.E_ALIAS          # z_tilde over b
+    assert call(1, 96) == R.E_SHAPE
+
+
+@needs_no_gpu
+def test_decode_bwd_validation(lib):
+    c = lib.cdll
+    ws = lib.workspace_bytes(T, N, RR)
+    ok = [T, N, RR, A, 2 * A, 3 * A, N, 4 * A, N, 5 * A, 6 * A, 0, 7 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm_decode_bwd(*a)
+
+    assert call(3, None) == R.E_NULL
+    assert call(5, None) == R.E_NULL
+    assert call(9, None) == R.E_NULL
+    assert call(10, None) == R.E_NULL
+    assert call(12, None) == R.E_NULL
+    assert call(13, 256) == R.E_WORKSPACE
+    assert call(8, N - 8) == R.E_SHAPE       # g_id leading dimension
+    assert call(7, 4 * A + 8) == R.E_ALIGN
+    assert call(9, 3 * A) == R.E_ALIAS       # g_b over g_zt
+    assert call(10, 2 * A) == R.E_ALIAS      # dW_d over W_d
+    assert call(12, 3 * A + 256) == R.E_ALIAS
+
+
+@needs_no_gpu
+def test_encode_bwd_validation(lib):
+    c = lib.cdll
+    ws = lib.workspace_bytes(T, N, RR)
+    ok = [T, N, RR, 1, A, N, 2 * A, 3 * A, 4 * A, 5 * A, N, 6 * A, N, 7 * A, 0, 8 * A, ws, None]
+
+    def call(**kw):
+        names = ["T", "n", "r", "act", "z", "ldz", "We", "a", "gb", "gz", "ldgz", "gx", "ldgx", "dWe", "acc",
+                 "ws", "wsb", "s"]
+        a = list(ok)
+        for k, v in kw.items():
+            a[names.index(k)] = v
+        return c.resbm_encode_bwd(*a)
+
+    assert call(a=None) == R.E_ACT            # SiLU needs a_save
+    assert call(act=5) == R.E_ACT
+    assert call(z=None) == R.E_NULL
+    assert call(gz=None) == R.E_NULL
+    assert call(dWe=None) == R.E_NULL
+    assert call(gx=5 * A, ldgx=N + 8) == R.E_ALIAS   # fused g_x needs the same ld
+    assert call(gz=A) == R.E_ALIAS
+    assert call(gx=A) == R.E_ALIAS
+    assert call(ldgx=N - 8) == R.E_SHAPE
+    assert call(wsb=256) == R.E_WORKSPACE
+    assert call(gb=4 * A + 4) == R.E_ALIGN
