@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--sets", type=int, default=4, help="rotating input/output copies")
     p.add_argument("--act", default="silu", choices=["silu", "identity"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-op-events", action="store_true", help="time whole steps only")
+    p.add_argument("--copy-probe-mib", type=int, default=256,
+                   help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
     p.add_argument("--cpu-tokens", type=int, default=None, help="tokens in the CPU oracle sample")
     return p.parse_args()
 
@@ -153,6 +156,24 @@ def main():
         if ev is not None:
             ev[4].record()
 
+    copy_gbs = None
+    if args.copy_probe_mib > 0:
+        # plain copy of known size: reference for achievable bandwidth and for
+        # scaling the FETCH_SIZE / WRITE_SIZE counters
+        nel = args.copy_probe_mib * 2**20 // 2
+        src = torch.empty(nel, dtype=torch.bfloat16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(5):
+            dst.copy_(src)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_gbs = 2 * nel * 2 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+        del src, dst
+
     for i in range(args.warmup):
         step(sets[i % len(sets)])
     torch.cuda.synchronize()
@@ -164,7 +185,7 @@ def main():
     wall0 = time.perf_counter()
     start.record()
     for i in range(args.steps):
-        step(sets[i % len(sets)], events[i])
+        step(sets[i % len(sets)], None if args.no_op_events else events[i])
     stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -173,11 +194,12 @@ def main():
 
     op_ms = {}
     for k, nm in enumerate(OPS):
-        op_ms[nm] = sum(e[k].elapsed_time(e[k + 1]) for e in events) / args.steps
+        op_ms[nm] = (float("nan") if args.no_op_events
+                     else sum(e[k].elapsed_time(e[k + 1]) for e in events) / args.steps)
     ob = op_bytes(T, n, r)
     total_bytes = sum(ob.values())
     gbs = total_bytes / (ms_step * 1e-3) / 1e9
-    dom = max(OPS, key=lambda k: op_ms[k])
+    dom = "encode_bwd" if args.no_op_events else max(OPS, key=lambda k: op_ms[k])
     dom_gbs = ob[dom] / (op_ms[dom] * 1e-3) / 1e9
 
     out = {
@@ -199,6 +221,7 @@ def main():
         "hbm_gbps": gbs,
         "hbm_frac": gbs / HBM_PEAK_GBS,
         "bytes_per_step": total_bytes,
+        "copy_probe_gbps": copy_gbs,
         "ops": {k: {"ms": op_ms[k], "gbps": ob[k] / (op_ms[k] * 1e-3) / 1e9, "bytes": ob[k]} for k in OPS},
         "roofline": {"bound": "hbm", "op": dom, "achieved": dom_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dom_gbs / HBM_PEAK_GBS, "traffic": None},

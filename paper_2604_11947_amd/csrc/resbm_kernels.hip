@@ -6,18 +6,26 @@
 // (bf16 payload).  The backward kernels are the adjoints of these maps.
 //
 // Work split (T tokens, hidden n, rank r; every streaming tensor is T x n):
-//   encode_fwd  a = z W_e over n: waves own token tiles and walk n; blockIdx.y
-//               splits n, and a second kernel adds the splits in a fixed order,
-//               then applies phi, the skip and the bf16 rounding.
+//   encode_fwd  a = z W_e: a block owns a token tile; its waves split the
+//               n-contraction and add their partial sums in LDS in wave order
+//               before phi, the skip and the bf16 rounding.
 //   decode_fwd  z~ = b W_d: waves own column strips (W_d held in registers) and
-//               walk tokens, writing full 16-byte rows.
-//   decode_bwd  one pass over g_z~ gives g_b (contraction over n, per-block
-//               partial) and dW_d (contraction over tokens, per-block partial);
-//               the token-major tile is transposed through LDS for the latter.
-//   encode_bwd  one pass reads z and writes g_z; g_h = g_b phi'(a) is formed
-//               once per 32-token step in LDS; dW_e partials as in decode_bwd.
-// Partial sums are added by small reduction kernels in index order, so every
-// result is reproducible bit for bit.
+//               walk tokens, writing 64 contiguous bytes per row per store.
+//   decode_bwd  one pass over g_z~ gives g_b (contraction over n; the 8 waves'
+//               column partials meet in LDS, one barrier per 32-token step) and
+//               dW_d (contraction over tokens, accumulated in registers); the
+//               token-major tiles are read back transposed from LDS.
+//   encode_bwd  one pass reads z and writes g_z; g_h = g_b phi'(a) comes from a
+//               small prologue kernel in the two fragment orders the matrix cores
+//               want; dW_e accumulates in registers and meets once per block.
+// Every partial sum is added in a fixed order, so results are reproducible bit
+// for bit.
+//
+// Streaming tensors are accessed through buffer descriptors: the hardware range
+// check returns zeros for loads and drops stores outside a descriptor, so token
+// tails and padding need no branches inside the loops, and every loop keeps two
+// register sets in flight (the next step's loads are issued before the current
+// step's math), which lets the compiler place each memory wait at its use.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -29,11 +37,225 @@
 
 namespace resbm {
 
+// ---------------------------------------------------------------- buffer access
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kOOB = 0xFFFFFFF0u;        // a byte offset outside every descriptor
+constexpr int64_t kMaxRange = 0xFFFFF000ll;   // descriptor ranges are clamped below kOOB
+constexpr int kEs = (int)sizeof(io_t);
+
+// Raw buffer descriptor over [base, base + bytes): gfx9-family dword 3, no stride.
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const uint32_t nb = bytes <= 0 ? 0u : (bytes > kMaxRange ? (uint32_t)kMaxRange : (uint32_t)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nb, 0x00020000);
+}
+__device__ __forceinline__ uint4 bld16(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ uint2 bld8(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+__device__ __forceinline__ void bst16(rsrc_t r, uint32_t off, uint4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, v), r, off, 0, 0);
+}
+__device__ __forceinline__ void bst8(rsrc_t r, uint32_t off, uint2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, v), r, off, 0, 0);
+}
+
+// Byte extent of rows [0, rows) of a row-major matrix with n used columns.
+__device__ __forceinline__ int64_t rows_bytes(int64_t rows, int n, int64_t ld, int es) {
+  return rows > 0 ? ((rows - 1) * ld + n) * es : 0;
+}
+
+// 8 consecutive I/O elements at byte offset off.
+__device__ __forceinline__ XFrag bld_x8(rsrc_t r, uint32_t off) {
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+  const uint4 a = bld16(r, off), b = bld16(r, off == kOOB ? kOOB : off + 16);
+  f.v[0] = __builtin_bit_cast(float, a.x); f.v[1] = __builtin_bit_cast(float, a.y);
+  f.v[2] = __builtin_bit_cast(float, a.z); f.v[3] = __builtin_bit_cast(float, a.w);
+  f.v[4] = __builtin_bit_cast(float, b.x); f.v[5] = __builtin_bit_cast(float, b.y);
+  f.v[6] = __builtin_bit_cast(float, b.z); f.v[7] = __builtin_bit_cast(float, b.w);
+#else
+  f.v = __builtin_bit_cast(bf16x8, bld16(r, off));
+#endif
+  return f;
+}
+
+// 4 consecutive I/O elements at byte offset off, widened to float.
+__device__ __forceinline__ void bld_x4(rsrc_t r, uint32_t off, float (&out)[4]) {
+#if RESBM_IO_F32_BUILD
+  const uint4 a = bld16(r, off);
+  out[0] = __builtin_bit_cast(float, a.x); out[1] = __builtin_bit_cast(float, a.y);
+  out[2] = __builtin_bit_cast(float, a.z); out[3] = __builtin_bit_cast(float, a.w);
+#else
+  const uint2 u = bld8(r, off);
+  out[0] = bf16_bits_to_f32(u.x & 0xffffu);
+  out[1] = bf16_bits_to_f32(u.x >> 16);
+  out[2] = bf16_bits_to_f32(u.y & 0xffffu);
+  out[3] = bf16_bits_to_f32(u.y >> 16);
+#endif
+}
+
+// Rounds and stores CNT (4 or 8) consecutive values at byte offset off.
+template <int CNT>
+__device__ __forceinline__ void bst_n(rsrc_t r, uint32_t off, const float* v) {
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int q = 0; q < CNT / 4; ++q)
+    bst16(r, off == kOOB ? kOOB : off + 16 * q,
+          make_uint4(__builtin_bit_cast(uint32_t, v[4 * q]), __builtin_bit_cast(uint32_t, v[4 * q + 1]),
+                     __builtin_bit_cast(uint32_t, v[4 * q + 2]), __builtin_bit_cast(uint32_t, v[4 * q + 3])));
+#else
+  if constexpr (CNT == 8) {
+    bf16x8 h;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = to_bf16(v[e]);
+    bst16(r, off, __builtin_bit_cast(uint4, h));
+  } else {
+    bf16x4 h;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = to_bf16(v[e]);
+    bst8(r, off, __builtin_bit_cast(uint2, h));
+  }
+#endif
+}
+
+// 8 consecutive elements m[row][kb .. kb + 8) of a packed matrix with r columns
+// (payload, wire gradient), zeros at columns >= r; r % 4 == 0, so a lane gets 8,
+// 4 or 0 of them.  `row_off` is the row's byte offset in the descriptor (or kOOB).
+__device__ __forceinline__ XFrag bld_r8(rsrc_t m, uint32_t row_off, int r, int kb) {
+  const bool lo = kb < r, hi = kb + 4 < r;
+  const uint32_t olo = (row_off == kOOB || !lo) ? kOOB : row_off + kb * kEs;
+  const uint32_t ohi = (row_off == kOOB || !hi) ? kOOB : row_off + (kb + 4) * kEs;
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+  const uint4 a = bld16(m, olo), b = bld16(m, ohi);
+  f.v[0] = __builtin_bit_cast(float, a.x); f.v[1] = __builtin_bit_cast(float, a.y);
+  f.v[2] = __builtin_bit_cast(float, a.z); f.v[3] = __builtin_bit_cast(float, a.w);
+  f.v[4] = __builtin_bit_cast(float, b.x); f.v[5] = __builtin_bit_cast(float, b.y);
+  f.v[6] = __builtin_bit_cast(float, b.z); f.v[7] = __builtin_bit_cast(float, b.w);
+#else
+  const uint2 a = bld8(m, olo), b = bld8(m, ohi);
+  f.v = __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+#endif
+  return f;
+}
+
+// Split (weight-like) fragment f of a fragment-ordered buffer: per fragment and
+// lane 2 x 16 bytes (hi, lo bf16 in the bf16 build; 8 floats in the f32 build).
+__device__ __forceinline__ SFrag bld_sfrag(rsrc_t r, int64_t f, int l) {
+  SFrag s;
+#if RESBM_IO_F32_BUILD
+  const uint32_t o = (uint32_t)((f * 64 + l) * 32);
+  const uint4 a = bld16(r, o), b = bld16(r, o + 16);
+  s.v[0] = __builtin_bit_cast(float, a.x); s.v[1] = __builtin_bit_cast(float, a.y);
+  s.v[2] = __builtin_bit_cast(float, a.z); s.v[3] = __builtin_bit_cast(float, a.w);
+  s.v[4] = __builtin_bit_cast(float, b.x); s.v[5] = __builtin_bit_cast(float, b.y);
+  s.v[6] = __builtin_bit_cast(float, b.z); s.v[7] = __builtin_bit_cast(float, b.w);
+#else
+  s.hi = __builtin_bit_cast(bf16x8, bld16(r, (uint32_t)(((f * 2 + 0) * 64 + l) * 16)));
+  s.lo = __builtin_bit_cast(bf16x8, bld16(r, (uint32_t)(((f * 2 + 1) * 64 + l) * 16)));
+#endif
+  return s;
+}
+constexpr int kSFragBytes = 2048;  // one split fragment for the 64 lanes
+
+__device__ __forceinline__ void store_sfrag(void* __restrict__ base, int64_t f, int l, const float (&w)[8]) {
+#if RESBM_IO_F32_BUILD
+  float4* out = reinterpret_cast<float4*>(base) + (f * 64 + l) * 2;
+  out[0] = make_float4(w[0], w[1], w[2], w[3]);
+  out[1] = make_float4(w[4], w[5], w[6], w[7]);
+#else
+  SFrag s = sfrag_from(w);
+  uint4* out = reinterpret_cast<uint4*>(base);
+  out[(f * 2 + 0) * 64 + l] = __builtin_bit_cast(uint4, s.hi);
+  out[(f * 2 + 1) * 64 + l] = __builtin_bit_cast(uint4, s.lo);
+#endif
+}
+
+// ---------------------------------------------------------------- LDS helpers
+// Orders this wave's LDS accesses: waits for its outstanding LDS operations and
+// keeps the compiler from moving memory accesses across.  Sufficient for LDS
+// regions that only this wave touches.
+__device__ __forceinline__ void wave_lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Index of this wave in its block, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// Column permutation of a 32-row x WC-column token tile staged in LDS: rows 8
+// apart (read together by the transposed fragment loads) land on different
+// banks.  The XOR only flips column bits inside whole 32- or 64-column blocks,
+// so 8-element chunks stay contiguous and a column never leaves its row.
+template <int WC>
+__device__ __forceinline__ int tile_col(int row, int col) {
+  if constexpr (WC % 64 == 0) return col ^ (((row >> 3) & 3) << 4);
+  else if constexpr (WC % 32 == 0) return col ^ (((row >> 3) & 1) << 4);
+  else return col;
+}
+
+// Stores 8 consecutive elements at (row, col) of a WC-wide tile (col % 8 == 0).
+template <int WC>
+__device__ __forceinline__ void tile_put8(io_t* tile, int row, int col, const XFrag& v) {
+  io_t* d = tile + row * WC + tile_col<WC>(row, col);
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int e = 0; e < 8; ++e) d[e] = v.v[e];
+#else
+  *reinterpret_cast<uint4*>(d) = __builtin_bit_cast(uint4, v.v);
+#endif
+}
+
+// Transposed fragment from a row-major 32 x WC tile in LDS: lane (row16, grp)
+// receives tile[8 grp + e][c0 + row16], e = 0..7, i.e. the operand of a
+// contraction over the 32 rows (tokens) of the tile.
+// bf16: two ds_read_b64_tr_b16.  Within a 16-lane group that instruction hands
+// lane i element i % 4 of the 8-byte chunks addressed by group lanes 4 e + i / 4,
+// e = 0..3; so group lane j addresses row 8 grp + 4 h + j / 4, columns
+// c0 + 4 (j % 4) .. + 3, and lane i collects 4 consecutive rows of column c0 + i.
+template <int WC>
+__device__ __forceinline__ XFrag tr_frag(const io_t* tile, int c0, int row16, int grp) {
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int row = 8 * grp + e;
+    f.v[e] = tile[row * WC + tile_col<WC>(row, c0 + row16)];
+  }
+#else
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  s16x4 h[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int row = 8 * grp + 4 * q + (row16 >> 2);
+    const io_t* p = tile + row * WC + tile_col<WC>(row, c0 + 4 * (row16 & 3));
+    h[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+  }
+  f.v = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){h[0][0], h[0][1], h[0][2], h[0][3],
+                                                                               h[1][0], h[1][1], h[1][2], h[1][3]});
+#endif
+  return f;
+}
+
+// Output-column permutation of the "expand" contractions (decode_fwd, the g_z
+// part of encode_bwd).  A wave's A operand covers 16*CT columns starting at c0;
+// row i of column tile ct stands for column
+//     c0 + 32 (ct / 2) + W grp + 4 (ct % 2) + i % 4,   grp = i / 4, W = 8 (CT >= 2) or 4,
+// so that lane group grp ends up holding runs of W consecutive columns and the
+// four lane groups of one token cover 4W contiguous columns per store.
+template <int CT>
+__device__ __forceinline__ int expand_col(int c0, int ct, int i) {
+  constexpr int W = CT >= 2 ? 8 : 4;
+  return c0 + 32 * (ct >> 1) + W * (i >> 2) + 4 * (ct & 1) + (i & 3);
+}
+
 // ============================================================ encode forward
-// Fragment-ordered copy of W_e for the A operand of a = z W_e:
+// Fragment-ordered hi/lo copy of W_e for the A operand of a = z W_e:
 // fragment f = ks * NT + nt, lane (row16, grp) holds W_e[32 ks + 8 grp + e][16 nt + row16].
-__global__ __launch_bounds__(256) void k_enc_fwd_prep(const float* __restrict__ W_e, int n,
-                                                      int r, int NT, void* __restrict__ wf) {
+__global__ __launch_bounds__(256) void k_enc_fwd_prep(const float* __restrict__ W_e, int n, int r, int NT,
+                                                      void* __restrict__ wf) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t total = (int64_t)(n / 32) * NT * 64;
   if (gid >= total) return;
@@ -49,61 +271,35 @@ __global__ __launch_bounds__(256) void k_enc_fwd_prep(const float* __restrict__ 
     const int k = ks * 32 + grp * 8 + e;
     w[e] = col < r ? W_e[(int64_t)k * r + col] : 0.0f;
   }
-#if RESBM_IO_F32_BUILD
-  float4* out = reinterpret_cast<float4*>(wf) + (f * 64 + l) * 2;
-  out[0] = make_float4(w[0], w[1], w[2], w[3]);
-  out[1] = make_float4(w[4], w[5], w[6], w[7]);
-#else
-  SFrag s = sfrag_from(w);
-  uint4* out = reinterpret_cast<uint4*>(wf);
-  out[(f * 2 + 0) * 64 + l] = __builtin_bit_cast(uint4, s.hi);
-  out[(f * 2 + 1) * 64 + l] = __builtin_bit_cast(uint4, s.lo);
-#endif
+  store_sfrag(wf, f, l, w);
 }
 
-__device__ __forceinline__ SFrag load_wfrag(const void* __restrict__ wf, int64_t f, int l) {
-  SFrag s;
-#if RESBM_IO_F32_BUILD
-  const float4* p = reinterpret_cast<const float4*>(wf) + (f * 64 + l) * 2;
-  float4 a = p[0], b = p[1];
-  s.v[0] = a.x; s.v[1] = a.y; s.v[2] = a.z; s.v[3] = a.w;
-  s.v[4] = b.x; s.v[5] = b.y; s.v[6] = b.z; s.v[7] = b.w;
-#else
-  const uint4* p = reinterpret_cast<const uint4*>(wf);
-  s.hi = __builtin_bit_cast(bf16x8, p[(f * 2 + 0) * 64 + l]);
-  s.lo = __builtin_bit_cast(bf16x8, p[(f * 2 + 1) * 64 + l]);
-#endif
-  return s;
-}
+// a = z W_e for 16*MT tokens per block; wave w takes k-steps [w nks / KW, (w+1) nks / KW).
+template <int NT, int MT, int KW>
+__global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, int act,
+                                                     const io_t* __restrict__ x_attn, int64_t ld_x,
+                                                     const io_t* __restrict__ z, int64_t ld_z,
+                                                     const void* __restrict__ wf, io_t* __restrict__ b,
+                                                     float* __restrict__ a_save) {
+  constexpr int U = NT <= 2 ? 2 : 1;    // k-steps per pipeline stage
+  constexpr bool PW = NT <= 4;          // W_e fragments travel with the stage
+  constexpr int NW = PW ? NT : 1;
+  constexpr int TOK = 16 * MT;
+  constexpr int RPT = 16 * NT;
+  __shared__ __attribute__((aligned(16))) float s_red[KW][TOK][RPT + 4];
 
-// Final encoder epilogue for 4 consecutive columns j0..j0+3 of token t:
-// a_save = a; b = x_attn[t, j0:j0+4] + phi(a), rounded once.
-__device__ __forceinline__ void enc_fwd_epilogue(int64_t t, int j0, int r, int act, const float (&a)[4],
-                                                 const io_t* __restrict__ x_attn, int64_t ld_x,
-                                                 io_t* __restrict__ b, float* __restrict__ a_save) {
-  if (a_save) *reinterpret_cast<float4*>(a_save + t * r + j0) = make_float4(a[0], a[1], a[2], a[3]);
-  float x[4];
-  load_x4(x_attn + t * ld_x + j0, x);
-  float o[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) o[v] = x[v] + act_phi(a[v], act);
-  store_x4(b + t * r + j0, o);
-}
-
-// a = z W_e over the k-steps [s*kspl, min(nks, (s+1)*kspl)), 16*MT tokens per wave.
-template <int NT, int MT>
-__global__ __launch_bounds__(256) void k_enc_fwd(int64_t T, int n, int r, int RP, int act,
-                                                 const io_t* __restrict__ x_attn, int64_t ld_x,
-                                                 const io_t* __restrict__ z, int64_t ld_z,
-                                                 const void* __restrict__ wf, io_t* __restrict__ b,
-                                                 float* __restrict__ a_save, float* __restrict__ part,
-                                                 int S, int kspl) {
-  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = threadIdx.x >> 6;
-  const int64_t tok0 = ((int64_t)blockIdx.x * 4 + wave) * (16 * MT);
-  const int s = blockIdx.y;
+  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+  const int64_t tok0 = (int64_t)blockIdx.x * TOK;
   const int nks = n / 32;
-  const int ks0 = s * kspl;
-  const int ks1 = min(nks, ks0 + kspl);
+  const int ks0 = wave * nks / KW;
+  const int ks1 = (wave + 1) * nks / KW;
+
+  // rows at or beyond T fall outside the descriptor (ld >= n)
+  const rsrc_t zr = make_rsrc(z + tok0 * ld_z, rows_bytes(min((int64_t)TOK, T - tok0), n, ld_z, kEs));
+  const rsrc_t wr = make_rsrc(wf, (int64_t)nks * NT * kSFragBytes);
+  uint32_t zoff[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) zoff[mt] = (uint32_t)(((16 * mt + row16) * ld_z + 8 * grp) * kEs);
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -111,128 +307,86 @@ __global__ __launch_bounds__(256) void k_enc_fwd(int64_t T, int n, int r, int RP
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const io_t* zrow[MT];
-  bool ok[MT];
+  XFrag za[U][MT], zb[U][MT];
+  SFrag wa[U][NW], wb[U][NW];
+  auto load = [&](XFrag (&zz)[U][MT], SFrag (&ww)[U][NW], int ks) {
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int64_t t = tok0 + 16 * mt + row16;
-    ok[mt] = t < T;
-    zrow[mt] = z + (ok[mt] ? t : 0) * ld_z + grp * 8;
-  }
-
-  XFrag cur[MT], nxt[MT];
+    for (int u = 0; u < U; ++u) {
+      const int k = ks + u;  // k >= ks1 is loaded (in range or zero) but never used
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-    cur[mt] = (ok[mt] && ks0 < ks1) ? load_x8(zrow[mt] + ks0 * 32) : xfrag_zero();
-
-  for (int ks = ks0; ks < ks1; ++ks) {
-    const bool more = ks + 1 < ks1;
+      for (int mt = 0; mt < MT; ++mt) zz[u][mt] = bld_x8(zr, zoff[mt] + (uint32_t)(k * 32 * kEs));
+      if constexpr (PW) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-      nxt[mt] = (ok[mt] && more) ? load_x8(zrow[mt] + (ks + 1) * 32) : xfrag_zero();
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const SFrag w = load_wfrag(wf, (int64_t)ks * NT + nt, l);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, cur[mt], acc[mt][nt]);
-    }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) cur[mt] = nxt[mt];
-  }
-
-  // acc[mt][nt][v] = a[tok0 + 16 mt + row16][16 nt + 4 grp + v]
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int64_t t = tok0 + 16 * mt + row16;
-    if (!ok[mt]) continue;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int j0 = nt * 16 + grp * 4;
-      if (j0 >= r) continue;
-      if (S == 1) {
-        float a[4] = {acc[mt][nt][0], acc[mt][nt][1], acc[mt][nt][2], acc[mt][nt][3]};
-        enc_fwd_epilogue(t, j0, r, act, a, x_attn, ld_x, b, a_save);
-      } else {
-        *reinterpret_cast<float4*>(part + ((int64_t)s * T + t) * RP + j0) =
-            make_float4(acc[mt][nt][0], acc[mt][nt][1], acc[mt][nt][2], acc[mt][nt][3]);
+        for (int nt = 0; nt < NT; ++nt) ww[u][nt] = bld_sfrag(wr, (int64_t)k * NT + nt, l);
       }
     }
-  }
-}
+  };
+  auto compute = [&](const XFrag (&zz)[U][MT], const SFrag (&ww)[U][NW], int ks) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (ks + u >= ks1) break;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        SFrag w;
+        if constexpr (PW) w = ww[u][nt];
+        else w = bld_sfrag(wr, (int64_t)(ks + u) * NT + nt, l);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, zz[u][mt], acc[mt][nt]);
+      }
+    }
+  };
 
-// Adds the S split-n partials of a in split order, then the epilogue.
-__global__ __launch_bounds__(256) void k_enc_fwd_fin(int64_t T, int r, int RP, int act,
-                                                     const io_t* __restrict__ x_attn, int64_t ld_x,
-                                                     const float* __restrict__ part, int S,
-                                                     io_t* __restrict__ b, float* __restrict__ a_save) {
-  const int nq = r / 4;
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (gid >= T * nq) return;
-  const int64_t t = gid / nq;
-  const int j0 = (int)(gid % nq) * 4;
-  float a[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < S; ++s) {
-    const float4 p = *reinterpret_cast<const float4*>(part + ((int64_t)s * T + t) * RP + j0);
-    a[0] += p.x; a[1] += p.y; a[2] += p.z; a[3] += p.w;
+  load(za, wa, ks0);
+  for (int ks = ks0; ks < ks1; ks += 2 * U) {
+    load(zb, wb, ks + U);
+    compute(za, wa, ks);
+    load(za, wa, ks + 2 * U);
+    compute(zb, wb, ks + U);
   }
-  enc_fwd_epilogue(t, j0, r, act, a, x_attn, ld_x, b, a_save);
+
+  // acc[mt][nt][v] = partial a[tok0 + 16 mt + row16][16 nt + 4 grp + v]
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      *reinterpret_cast<float4*>(&s_red[wave][16 * mt + row16][16 * nt + 4 * grp]) =
+          make_float4(acc[mt][nt][0], acc[mt][nt][1], acc[mt][nt][2], acc[mt][nt][3]);
+  __syncthreads();
+
+  // Sum the KW partials in wave order, then a_save = a, b = x_attn[:, :r] + phi(a).
+  constexpr int Q = RPT / 4;
+  for (int idx = threadIdx.x; idx < TOK * Q; idx += KW * 64) {
+    const int tt = idx / Q;
+    const int j0 = (idx % Q) * 4;
+    const int64_t t = tok0 + tt;
+    if (t >= T || j0 >= r) continue;
+    float a[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < KW; ++w) {
+      const float4 p = *reinterpret_cast<const float4*>(&s_red[w][tt][j0]);
+      a[0] += p.x; a[1] += p.y; a[2] += p.z; a[3] += p.w;
+    }
+    if (a_save) *reinterpret_cast<float4*>(a_save + t * r + j0) = make_float4(a[0], a[1], a[2], a[3]);
+    float x[4];
+    load_x4(x_attn + t * ld_x + j0, x);
+    float o[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) o[v] = x[v] + act_phi(a[v], act);
+    store_x4(b + t * r + j0, o);
+  }
 }
 
 // ============================================================ decode forward
-// 8 consecutive payload elements b[t][kb .. kb+8) with zeros at k >= r.
-__device__ __forceinline__ XFrag load_payload8(const io_t* __restrict__ b, int64_t t, int r, int kb, bool ok) {
-  if (!ok || kb >= r) return xfrag_zero();
-  const io_t* p = b + t * r + kb;
-#if RESBM_IO_F32_BUILD
-  XFrag f = xfrag_zero();
-  float4 a = *reinterpret_cast<const float4*>(p);
-  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
-  if (kb + 8 <= r) {
-    float4 c = *reinterpret_cast<const float4*>(p + 4);
-    f.v[4] = c.x; f.v[5] = c.y; f.v[6] = c.z; f.v[7] = c.w;
-  }
-  return f;
-#else
-  if (kb + 8 <= r && (r & 7) == 0) return load_x8(p);
-  uint2 lo = *reinterpret_cast<const uint2*>(p);
-  uint2 hi = kb + 8 <= r ? *reinterpret_cast<const uint2*>(p + 4) : make_uint2(0, 0);
-  XFrag f;
-  f.v = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-  return f;
-#endif
-}
-
-// Stores cnt = 4*CT consecutive values (16-byte aligned when cnt >= 8 for bf16).
-template <int CNT>
-__device__ __forceinline__ void store_row(io_t* __restrict__ p, const float (&v)[CNT]) {
-#if RESBM_IO_F32_BUILD
-#pragma unroll
-  for (int q = 0; q < CNT / 4; ++q)
-    *reinterpret_cast<float4*>(p + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
-#else
-  if constexpr (CNT >= 8) {
-#pragma unroll
-    for (int q = 0; q < CNT / 8; ++q) {
-      bf16x8 h;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) h[e] = to_bf16(v[8 * q + e]);
-      *reinterpret_cast<uint4*>(p + 8 * q) = __builtin_bit_cast(uint4, h);
-    }
-  } else {
-    float w[4] = {v[0], v[1], v[2], v[3]};
-    store_x4(p, w);
-  }
-#endif
-}
-
-// z~ = b W_d (+ b I_{r x n}).  A wave owns columns [c0, c0 + 16 CT) with the
-// A-operand row i of column tile ct mapped to column c0 + 4 CT (i / 4) + 4 ct + i % 4,
-// so that lane (row16, grp) ends up holding 4 CT consecutive columns of token row16.
-template <int KS, int CT>
-__global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r, int add_id,
+// z~ = b W_d (+ b I_{r x n} when ADD).  A wave owns columns [c0, c0 + 16 CT) (see
+// expand_col) and walks the token range [blockIdx.y tpg, ...) 16 tokens at a time.
+template <int KS, int CT, bool ADD>
+__global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
                                                  const io_t* __restrict__ b, const float* __restrict__ W_d,
                                                  io_t* __restrict__ zt, int64_t ld_zt, int tpg) {
-  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = threadIdx.x >> 6;
+  constexpr int W = CT >= 2 ? 8 : 4;      // consecutive columns per lane run
+  constexpr int NH = CT >= 2 ? CT / 2 : 1;  // runs per lane
+  constexpr int NI = ADD ? NH * W / 4 : 1;  // 4-column identity chunks per lane
+  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   const int strip = blockIdx.x * 4 + wave;
   const int c0 = strip * 16 * CT;
   if (c0 >= n) return;  // whole strips only: n % 64 == 0 and 16 CT divides 64
@@ -242,7 +396,7 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r, int ad
   for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
-      const int col = c0 + 4 * CT * (row16 >> 2) + 4 * ct + (row16 & 3);
+      const int col = expand_col<CT>(c0, ct, row16);
       float w[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -253,79 +407,88 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r, int ad
     }
 
   const int64_t t_begin = (int64_t)blockIdx.y * tpg;
-  const int64_t t_end = min(T, t_begin + tpg);
-  const int cl = c0 + 4 * CT * grp;  // first column held by this lane
+  const int64_t rows = min((int64_t)tpg, T - t_begin);
+  const rsrc_t br = make_rsrc(b + t_begin * r, rows * r * kEs);
+  const rsrc_t zr = make_rsrc(zt + t_begin * ld_zt, rows_bytes(rows, n, ld_zt, kEs));
+  const int cl = c0 + W * grp;  // first column of this lane's run 0
 
-  XFrag cur[KS], nxt[KS];
-  {
-    const int64_t t = t_begin + row16;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) cur[ks] = load_payload8(b, t, r, ks * 32 + grp * 8, t < t_end);
-  }
-  for (int64_t tt = t_begin; tt < t_end; tt += 16) {
+  struct Tile {
+    XFrag p[KS];
+    float id[NI][4];  // reading A: b[t][column chunk] below r, zeros elsewhere
+  };
+  auto load = [&](Tile& x, int64_t tt) {  // tt: tile start relative to t_begin
     const int64_t t = tt + row16;
-    const bool ok = t < t_end;
-    {
-      const int64_t tn = t + 16;
+    const uint32_t ro = (uint32_t)(t * r * kEs);  // rows >= `rows` are out of range
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) nxt[ks] = load_payload8(b, tn, r, ks * 32 + grp * 8, tn < t_end);
+    for (int ks = 0; ks < KS; ++ks) x.p[ks] = bld_r8(br, ro, r, ks * 32 + grp * 8);
+    if constexpr (ADD) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int cb = cl + 32 * (i / (W / 4)) + 4 * (i % (W / 4));
+        bld_x4(br, cb < r ? (uint32_t)((t * r + cb) * kEs) : kOOB, x.id[i]);
+      }
     }
+  };
+  auto compute = [&](const Tile& x, int64_t tt) {
     f32x4 acc[CT];
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_sx(wfr[ks][ct], cur[ks], acc[ct]);
-    if (ok) {
-      float v[4 * CT];
+      for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_sx(wfr[ks][ct], x.p[ks], acc[ct]);
+    const int64_t t = tt + row16;
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
+    for (int h = 0; h < NH; ++h) {
+      float v[W];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[4 * ct + q] = acc[ct][q];
-      if (add_id && cl < r) {
+      for (int q = 0; q < W / 4; ++q)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          const int cb = cl + 4 * ct;
-          if (cb < r) {
-            float x[4];
-            load_x4(b + t * r + cb, x);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) v[4 * ct + q] += x[q];
-          }
+        for (int e = 0; e < 4; ++e) {
+          v[4 * q + e] = acc[2 * h + q][e];
+          if constexpr (ADD) v[4 * q + e] += x.id[h * (W / 4) + q][e];
         }
-      }
-      store_row<4 * CT>(zt + t * ld_zt + cl, v);
+      bst_n<W>(zr, (uint32_t)((t * ld_zt + cl + 32 * h) * kEs), v);
     }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) cur[ks] = nxt[ks];
+  };
+
+  Tile xa, xb;
+  load(xa, 0);
+  for (int64_t tt = 0; tt < rows; tt += 32) {
+    load(xb, tt + 16);
+    compute(xa, tt);
+    load(xa, tt + 32);
+    compute(xb, tt + 16);  // past the range: loads were zeros, stores are dropped
   }
 }
 
 // ============================================================ decode backward
-// LDS pitches (elements) chosen to spread the transposed 2-byte reads over banks.
-constexpr int kDbWaves = 8;
-constexpr int kDbWC = 64;                 // columns per wave
-constexpr int kDbGzPitch = kDbWC + 8;     // s_gz row pitch
-constexpr int kBtPitch = 32 + 8;          // transposed payload / g_h row pitch
-
-// One pass over g_z~ for token range [tg*TB, ...) and columns [cg*512, cg*512 + 512),
-// j-tiles [16 jt0, 16 (jt0 + JT)) of r:
-//   gbp[cg][t][j]  = sum_{c in block} g_z~[t][c] W_d[j][c]
-//   dwp[tg][j][c]  = sum_{t in block} b[t][j] g_z~[t][c]
+// One pass over g_z~ for the token range [tg TB, ...), columns [cg 512, cg 512 + 512)
+// and j-tiles [16 jt0, 16 (jt0 + JT)) of r:
+//   gbp[cg][t][j] = sum over the block's columns of g_z~[t][c] W_d[j][c]
+//   dwp[tg][j][c] = sum over the block's tokens of b[t][j] g_z~[t][c]
+// Per 32-token step: each wave takes its 64 columns of g_z~ into registers (one
+// step ahead), forms its g_b partial with W_d held in registers, stages the tile
+// in its own LDS and reads it back transposed for dW_d; the step's payload rows
+// are staged once per block (double-buffered) and read transposed too.  The 8
+// waves' g_b partials meet in LDS behind the one barrier of the step.
 template <int JT>
-__global__ __launch_bounds__(512) void k_dec_bwd(int64_t T, int n, int r, int RP,
-                                                 const io_t* __restrict__ b, const float* __restrict__ W_d,
-                                                 const io_t* __restrict__ g_zt, int64_t ld_g,
-                                                 float* __restrict__ gbp, float* __restrict__ dwp, int TB) {
+__global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int r, int RP,
+                                                           const io_t* __restrict__ b,
+                                                           const float* __restrict__ W_d,
+                                                           const io_t* __restrict__ g_zt, int64_t ld_g,
+                                                           float* __restrict__ gbp, float* __restrict__ dwp,
+                                                           int TB) {
   constexpr int KSW = kDbWC / 32;  // 32-column steps per wave
   constexpr int CTW = kDbWC / 16;  // 16-column tiles per wave
   constexpr int JW = JT * 16;      // j values per pass
-  __shared__ __attribute__((aligned(16))) io_t s_gz[kDbWaves][32][kDbGzPitch];
-  __shared__ __attribute__((aligned(16))) io_t s_bT[JW][kBtPitch];
-  __shared__ __attribute__((aligned(16))) float s_gb[kDbWaves][32][JW];
+  constexpr int NBUF = JT <= 2 ? 2 : 1;  // double-buffered partials: one barrier per step
+  constexpr int BQ = JW / 8;       // 16-byte payload chunks per token row
+  __shared__ __attribute__((aligned(16))) io_t s_gz[kDbWaves][32 * kDbWC];
+  __shared__ __attribute__((aligned(16))) io_t s_b[2][32 * JW];
+  __shared__ __attribute__((aligned(16))) float s_gb[NBUF][kDbWaves][32][JW + 4];
 
-  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = threadIdx.x >> 6;
+  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   const int cg = blockIdx.x, tg = blockIdx.y;
   const int jt0 = blockIdx.z * JT;
   const int wc0 = cg * (kDbWaves * kDbWC) + wave * kDbWC;
@@ -359,86 +522,89 @@ __global__ __launch_bounds__(512) void k_dec_bwd(int64_t T, int n, int r, int RP
   const int64_t t_begin = (int64_t)tg * TB;
   const int64_t t_end = min(T, t_begin + TB);
 
-  for (int64_t t0 = t_begin; t0 < t_end; t0 += 32) {
-    // 1. g_z~ rows of this step: gz[th][ks] = g_z~[t0 + 16 th + row16][wc0 + 32 ks + 8 grp + e]
+  // payload rows of one step: threads [0, 32 BQ) each carry one 16-byte chunk
+  const bool bthr = threadIdx.x < 32 * BQ;
+  const int btt = bthr ? threadIdx.x / BQ : 0, bch = threadIdx.x % BQ;
+  const uint32_t gz_lane = (uint32_t)((row16 * ld_g + wc0 + 8 * grp) * kEs);
+
+  struct Step {
     XFrag gz[2][KSW];
+    XFrag bp;
+  };
+  // loads of the step at t0 (rows beyond t_end read as zeros)
+  auto load = [&](Step& s, int64_t t0) {
+    const int64_t rows = t_end - t0;
+    const rsrc_t gr = make_rsrc(g_zt + t0 * ld_g, won ? rows_bytes(min((int64_t)32, rows), n, ld_g, kEs) : 0);
 #pragma unroll
-    for (int th = 0; th < 2; ++th) {
-      const int64_t t = t0 + 16 * th + row16;
-      const bool ok = won && t < t_end;
+    for (int th = 0; th < 2; ++th)
 #pragma unroll
       for (int ks = 0; ks < KSW; ++ks)
-        gz[th][ks] = ok ? load_x8(g_zt + t * ld_g + wc0 + 32 * ks + 8 * grp) : xfrag_zero();
-    }
-    // 2. payload transposed into LDS: s_bT[jj][tt] = b[t0 + tt][16 jt0 + jj]
-    for (int idx = threadIdx.x; idx < 32 * JW; idx += kDbWaves * 64) {
-      const int tt = idx / JW, jj = idx % JW;
-      const int64_t t = t0 + tt;
-      const int j = 16 * jt0 + jj;
-      s_bT[jj][tt] = (t < t_end && j < r) ? b[t * r + j] : f32_to_io(0.0f);
-    }
-    // 3. g_b partial over this wave's 64 columns: D[j][t]
+        s.gz[th][ks] = bld_x8(gr, gz_lane + (uint32_t)((16 * th * ld_g + 32 * ks) * kEs));
+    const rsrc_t br = make_rsrc(b + t0 * r, min((int64_t)32, rows) * r * kEs);
+    s.bp = bld_r8(br, bthr ? (uint32_t)(btt * r * kEs) : kOOB, r, 16 * jt0 + 8 * bch);
+  };
+
+  // one step: math on `cur` (its payload rows already in s_b[bbuf]); the payload
+  // rows of the next step (`nxt`) go to the other buffer before the barrier
+  auto step = [&](const Step& cur, const Step& nxt, int64_t t0, int gbuf, int bbuf) {
+    // g_b partial over this wave's 64 columns: D[j][t]
 #pragma unroll
     for (int th = 0; th < 2; ++th)
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KSW; ++ks) acc = mma_sx(wdf[jt][ks], gz[th][ks], acc);
-        *reinterpret_cast<float4*>(&s_gb[wave][16 * th + row16][16 * jt + 4 * grp]) =
+        for (int ks = 0; ks < KSW; ++ks) acc = mma_sx(wdf[jt][ks], cur.gz[th][ks], acc);
+        *reinterpret_cast<float4*>(&s_gb[gbuf][wave][16 * th + row16][16 * jt + 4 * grp]) =
             make_float4(acc[0], acc[1], acc[2], acc[3]);
       }
-    // 4. stage the wave's tile row-major for the transposed reads
+    // stage the wave's tile row-major, read it back transposed for dW_d
+    wave_lds_fence();
 #pragma unroll
     for (int th = 0; th < 2; ++th)
 #pragma unroll
-      for (int ks = 0; ks < KSW; ++ks) {
-#if RESBM_IO_F32_BUILD
-        float* d = &s_gz[wave][16 * th + row16][32 * ks + 8 * grp];
+      for (int ks = 0; ks < KSW; ++ks)
+        tile_put8<kDbWC>(s_gz[wave], 16 * th + row16, 32 * ks + 8 * grp, cur.gz[th][ks]);
+    wave_lds_fence();
+    // dW_d: D[c][j] = sum_t g_z~[t][c] b[t][j], A = g_z~^T, B = b^T (both transposed from LDS)
+    XFrag bt[JT];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) d[e] = gz[th][ks].v[e];
-#else
-        *reinterpret_cast<uint4*>(&s_gz[wave][16 * th + row16][32 * ks + 8 * grp]) =
-            __builtin_bit_cast(uint4, gz[th][ks].v);
-#endif
-      }
-    __syncthreads();
-
-    // 5. dW_d: D[c][j] = sum_t g_z~[t][c] b[t][j], A = g_z~^T (LDS), B = b^T (LDS)
+    for (int jt = 0; jt < JT; ++jt) bt[jt] = tr_frag<JW>(s_b[bbuf], 16 * jt, row16, grp);
 #pragma unroll
     for (int ct = 0; ct < CTW; ++ct) {
-      XFrag a;
+      const XFrag a = tr_frag<kDbWC>(s_gz[wave], 16 * ct, row16, grp);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-#if RESBM_IO_F32_BUILD
-        a.v[e] = s_gz[wave][8 * grp + e][16 * ct + row16];
-#else
-        a.v[e] = s_gz[wave][8 * grp + e][16 * ct + row16];
-#endif
-      }
-#pragma unroll
-      for (int jt = 0; jt < JT; ++jt) {
-        XFrag bb;
-#if RESBM_IO_F32_BUILD
-#pragma unroll
-        for (int e = 0; e < 8; ++e) bb.v[e] = s_bT[16 * jt + row16][8 * grp + e];
-#else
-        bb.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&s_bT[16 * jt + row16][8 * grp]));
-#endif
-        dw[ct][jt] = mma_xx(a, bb, dw[ct][jt]);
-      }
+      for (int jt = 0; jt < JT; ++jt) dw[ct][jt] = mma_xx(a, bt[jt], dw[ct][jt]);
     }
-    // 6. sum the 8 waves' g_b partials in wave order and store this block's partial
+    if (bthr) tile_put8<JW>(s_b[bbuf ^ 1], btt, 8 * bch, nxt.bp);  // last read before the previous barrier
+
+    __syncthreads();  // s_gb[gbuf] and s_b[bbuf ^ 1] complete
+    // sum the 8 waves' g_b partials in wave order; rows past t_end are dropped by the descriptor
+    const rsrc_t pr = make_rsrc(gbp + ((int64_t)cg * T + t0) * RP, (t_end - t0) * RP * 4);
     for (int idx = threadIdx.x; idx < 32 * JW; idx += kDbWaves * 64) {
       const int tt = idx / JW, jj = idx % JW;
-      const int64_t t = t0 + tt;
       const int j = 16 * jt0 + jj;
       float s = 0.0f;
 #pragma unroll
-      for (int w = 0; w < kDbWaves; ++w) s += s_gb[w][tt][jj];
-      if (t < t_end && j < r) gbp[((int64_t)cg * T + t) * RP + j] = s;
+      for (int w = 0; w < kDbWaves; ++w) s += s_gb[gbuf][w][tt][jj];
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, s), pr,
+                                            j < r ? (uint32_t)((tt * RP + j) * 4) : kOOB, 0, 0);
     }
-    __syncthreads();
+    if constexpr (NBUF == 1) __syncthreads();  // the single buffer is refilled next step
+  };
+
+  Step sa, sb;
+  load(sa, t_begin);
+  if (bthr) tile_put8<JW>(s_b[0], btt, 8 * bch, sa.bp);
+  __syncthreads();
+  int gbuf = 0;
+  for (int64_t t0 = t_begin; t0 < t_end; t0 += 64) {
+    load(sb, t0 + 32);
+    step(sa, sb, t0, gbuf, 0);
+    gbuf = (gbuf + 1) % NBUF;
+    load(sa, t0 + 64);
+    step(sb, sa, t0 + 32, gbuf, 1);  // past t_end: zeros in, nothing out
+    gbuf = (gbuf + 1) % NBUF;
   }
 
   // dw[ct][jt][v] = dW_d partial [16 (jt0 + jt) + row16][wc0 + 16 ct + 4 grp + v]
@@ -455,8 +621,10 @@ __global__ __launch_bounds__(512) void k_dec_bwd(int64_t T, int n, int r, int RP
   }
 }
 
-// g_b = sum_cg gbp[cg] + g_id[:, :r]  (rounded once), then
-// dW_d (+)= sum_tg dwp[tg]; blocks [0, nb_gb) do the first part.
+// Blocks [0, nb_gb): g_b = sum_cg gbp[cg] + g_id[:, :r], rounded once.
+// Blocks [nb_gb, ...): dW_d (+)= sum_tg dwp[tg]; a block covers 64 four-column
+// groups, its 4 thread quarters sum consecutive quarters of the token groups and
+// the quarters are added in order.
 __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, int RP,
                                                      const float* __restrict__ gbp, int ncg,
                                                      const io_t* __restrict__ g_id, int64_t ld_gid,
@@ -464,6 +632,7 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
                                                      const float* __restrict__ dwp, int ntg,
                                                      float* __restrict__ dW_d, int accumulate,
                                                      int64_t nb_gb) {
+  __shared__ float4 s_q[4][64];
   if ((int64_t)blockIdx.x < nb_gb) {
     const int nq = r / 4;
     const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -482,71 +651,134 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
       for (int v = 0; v < 4; ++v) s[v] += x[v];
     }
     store_x4(g_b + t * r + j0, s);
-  } else {
-    const int nq = n / 4;
-    const int64_t gid = ((int64_t)blockIdx.x - nb_gb) * 256 + threadIdx.x;
-    if (gid >= (int64_t)r * nq) return;
-    const int j = (int)(gid / nq);
-    const int c0 = (int)(gid % nq) * 4;
-    float4 s = accumulate ? *reinterpret_cast<const float4*>(dW_d + (int64_t)j * n + c0)
-                          : make_float4(0.f, 0.f, 0.f, 0.f);
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int g = 0; g < ntg; ++g) {
+    return;
+  }
+  const int nq = n / 4;
+  const int q = threadIdx.x >> 6;
+  const int64_t cidx = ((int64_t)blockIdx.x - nb_gb) * 64 + (threadIdx.x & 63);
+  const bool ok = cidx < (int64_t)r * nq;
+  const int j = ok ? (int)(cidx / nq) : 0;
+  const int c0 = ok ? (int)(cidx % nq) * 4 : 0;
+  const int g0 = q * ntg / 4, g1 = (q + 1) * ntg / 4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (ok) {
+    for (int g = g0; g < g1; ++g) {
       const float4 p = *reinterpret_cast<const float4*>(dwp + ((int64_t)g * RP + j) * n + c0);
       acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
     }
-    s.x += acc.x; s.y += acc.y; s.z += acc.z; s.w += acc.w;
+  }
+  s_q[q][threadIdx.x & 63] = acc;
+  __syncthreads();
+  if (q == 0 && ok) {
+    float4 s = accumulate ? *reinterpret_cast<const float4*>(dW_d + (int64_t)j * n + c0)
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 tot = s_q[0][threadIdx.x];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      const float4 p = s_q[k][threadIdx.x];
+      tot.x += p.x; tot.y += p.y; tot.z += p.z; tot.w += p.w;
+    }
+    s.x += tot.x; s.y += tot.y; s.z += tot.z; s.w += tot.w;
     *reinterpret_cast<float4*>(dW_d + (int64_t)j * n + c0) = s;
   }
 }
 
 // ============================================================ encode backward
-// One pass for token range [tg*TB, ...) and columns [cg*64*CT, ...):
-//   g_z[t][c] = sum_j g_h[t][j] W_e[c][j]          (written, + g_b when fused with g_x)
-//   dwp[tg][c][j] = sum_t z[t][c] g_h[t][j]
-// with g_h = g_b * phi'(a_save) formed per 32-token step in LDS (row-major and
-// transposed, as hi/lo split fragments).
-template <int KS, int NT, int CT>
-__global__ __launch_bounds__(256) void k_enc_bwd(int64_t T, int n, int r, int RP, int act,
-                                                 const io_t* __restrict__ z, int64_t ld_z,
-                                                 const float* __restrict__ W_e, const float* __restrict__ a_save,
-                                                 const io_t* __restrict__ g_b,
-                                                 io_t* __restrict__ g_z, int64_t ld_gz,
-                                                 io_t* __restrict__ g_x, int64_t ld_gx, int gx_fused,
-                                                 float* __restrict__ dwp, int TB) {
-  constexpr int W = 4;
-  constexpr int WC = 16 * CT;          // columns per wave
-  constexpr int KP = 32 * KS;          // r padded for the contraction over r
-  constexpr int RPT = 16 * NT;         // r padded to output tiles
-  constexpr int GP = KP + 8;           // row-major g_h pitch
-  constexpr int ZP = WC + 8;           // z tile pitch
-#if RESBM_IO_F32_BUILD
-  __shared__ __attribute__((aligned(16))) float s_ghr[32][GP];
-  __shared__ __attribute__((aligned(16))) float s_ght[RPT][kBtPitch];
-#else
-  __shared__ __attribute__((aligned(16))) __bf16 s_ghr[2][32][GP];      // [hi/lo][t][j]
-  __shared__ __attribute__((aligned(16))) __bf16 s_ght[2][RPT][kBtPitch];  // [hi/lo][j][t]
-#endif
-  __shared__ __attribute__((aligned(16))) io_t s_z[W][32][ZP];
+// g_h = g_b phi'(a) is formed once per token by k_enc_bwd_prep and stored in the
+// two fragment orders the main kernel consumes:
+//   row order  (B operand of g_z):  fragment (tile16 KS + ks), lane (row16, grp) holds
+//                                   g_h[16 tile16 + row16][32 ks + 8 grp + e]
+//   transposed (A operand of dW_e): fragment (step32 NT + jt), lane (row16, grp) holds
+//                                   g_h[32 step32 + 8 grp + e][16 jt + row16]
+// (hi, lo) bf16 pairs in the bf16 build, 8 floats in the f32 build; tokens at or
+// beyond T hold zeros.
 
-  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = threadIdx.x >> 6;
-  const int cg = blockIdx.x, tg = blockIdx.y;
-  const int wc0 = (cg * W + wave) * WC;
-  const bool won = wc0 < n;  // n % 64 == 0 and WC divides 64
+// One block per 32-token step: g_h into both fragment orders, and
+// g_x[t][0:r] += g_b[t][0:r] (rounded once) when g_x is given.
+template <int KS, int NT>
+__global__ __launch_bounds__(256) void k_enc_bwd_prep(int64_t T, int r, int act, const float* __restrict__ a_save,
+                                                      const io_t* __restrict__ g_b, io_t* __restrict__ g_x,
+                                                      int64_t ld_gx, void* __restrict__ ghr,
+                                                      void* __restrict__ ght) {
+  constexpr int KP = 32 * KS;
+  __shared__ float s_gh[32][KP + 1];
+  const int64_t step = blockIdx.x;
+  const int64_t t0 = step * 32;
+  for (int idx = threadIdx.x; idx < 32 * KP; idx += 256) {
+    const int tt = idx / KP, j = idx % KP;
+    const int64_t t = t0 + tt;
+    float g = 0.0f;
+    if (t < T && j < r) {
+      const float gb = io_to_f32(g_b[t * r + j]);
+      g = a_save ? gb * act_dphi(a_save[t * r + j], act) : gb;
+      if (g_x) {
+        io_t* px = g_x + t * ld_gx + j;
+        *px = f32_to_io(io_to_f32(*px) + gb);
+      }
+    }
+    s_gh[tt][j] = g;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < (2 * KS + NT) * 64; idx += 256) {
+    const int l = idx & 63, f = idx >> 6, row16 = l & 15, grp = l >> 4;
+    float w[8];
+    if (f < 2 * KS) {
+      const int th = f / KS, ks = f % KS;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[e] = s_gh[16 * th + row16][32 * ks + 8 * grp + e];
+      store_sfrag(ghr, (2 * step + th) * KS + ks, l, w);
+    } else {
+      const int jt = f - 2 * KS;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[e] = s_gh[8 * grp + e][16 * jt + row16];
+      store_sfrag(ght, step * NT + jt, l, w);
+    }
+  }
+}
 
-  // W_e as the A operand of g_z: lane (row16, grp) holds W_e[col][32 ks + 8 grp + e],
-  // col = wc0 + 4 CT (row16 / 4) + 4 ct + row16 % 4.
+// EW waves of a block share the columns [cb 16 CT, (cb + 1) 16 CT) and take
+// turns over the 32-token steps of the token range [tg TB, ...):
+//   g_z[t][c] = sum_j g_h[t][j] W_e[c][j]      (+ g_b[t][c] for c < r when fused with g_x)
+//   dW_e partial [tg][c][j] = sum_t z[t][c] g_h[t][j]
+// The step's z tile is transposed through wave-private LDS; the EW partial dW_e
+// meet in LDS once at the end.
+template <int KS, int NT, int CT, int EW, bool FUSED>
+__global__ __launch_bounds__(EW * 64) void k_enc_bwd(int64_t T, int n, int r, int RP,
+                                                     const io_t* __restrict__ z, int64_t ld_z,
+                                                     const float* __restrict__ W_e,
+                                                     const void* __restrict__ ghr, const void* __restrict__ ght,
+                                                     int64_t nsteps, const io_t* __restrict__ g_b,
+                                                     io_t* __restrict__ g_z, int64_t ld_gz,
+                                                     float* __restrict__ dwp, int TB) {
+  constexpr int WC = 16 * CT;            // columns of the block
+  constexpr int RPT = 16 * NT;
+  constexpr int W = CT >= 2 ? 8 : 4;     // consecutive g_z columns per lane run
+  constexpr int NH = CT >= 2 ? CT / 2 : 1;
+  constexpr int ZQ = WC / 16;            // 16-byte z chunks per lane per step
+  constexpr bool PF = KS <= 2;           // g_h fragments travel with the step (r <= 64)
+  constexpr int NI = FUSED ? NH * W / 4 : 1;  // 4-column g_b chunks per lane and token half
+  constexpr int WAVE_LDS = 32 * WC * (int)sizeof(io_t);
+  constexpr int RED_LDS = EW * WC * (RPT + 4) * 4;
+  constexpr int LDS = EW * WAVE_LDS > RED_LDS ? EW * WAVE_LDS : RED_LDS;
+  __shared__ __attribute__((aligned(16))) char smem[LDS];
+
+  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+  const int cb = blockIdx.x, tg = blockIdx.y;
+  const int wc0 = cb * WC;
+  io_t* s_z = reinterpret_cast<io_t*>(smem + wave * WAVE_LDS);
+
+  // W_e as the A operand of g_z: lane (row16, grp) holds W_e[col][32 ks + 8 grp + e], col = expand_col.
   SFrag wef[KS][CT];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
-      const int col = wc0 + 4 * CT * (row16 >> 2) + 4 * ct + (row16 & 3);
+      const int col = expand_col<CT>(wc0, ct, row16);
       float w[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int j = ks * 32 + grp * 8 + e;
-        w[e] = (won && j < r) ? W_e[(int64_t)col * r + j] : 0.0f;
+        w[e] = j < r ? W_e[(int64_t)col * r + j] : 0.0f;
       }
       wef[ks][ct] = sfrag_from(w);
     }
@@ -559,132 +791,135 @@ __global__ __launch_bounds__(256) void k_enc_bwd(int64_t T, int n, int r, int RP
 
   const int64_t t_begin = (int64_t)tg * TB;
   const int64_t t_end = min(T, t_begin + TB);
-  const int cl = wc0 + 4 * CT * grp;  // first g_z column held by this lane
+  const rsrc_t rr = make_rsrc(ghr, nsteps * 2 * KS * kSFragBytes);
+  const rsrc_t tr = make_rsrc(ght, nsteps * NT * kSFragBytes);
 
-  for (int64_t t0 = t_begin; t0 < t_end; t0 += 32) {
-    // 1. g_h for 32 tokens x KP, both layouts
-    for (int idx = threadIdx.x; idx < 32 * KP; idx += W * 64) {
-      const int tt = idx / KP, j = idx % KP;
-      const int64_t t = t0 + tt;
-      float gh = 0.0f;
-      if (t < t_end && j < r) {
-        const float gb = io_to_f32(g_b[t * r + j]);
-        const float d = a_save ? act_dphi(a_save[t * r + j], act) : 1.0f;
-        gh = gb * d;
-        if (g_x && !gx_fused && cg == 0) {
-          io_t* px = g_x + t * ld_gx + j;
-          *px = f32_to_io(io_to_f32(*px) + gb);
-        }
-      }
-#if RESBM_IO_F32_BUILD
-      s_ghr[tt][j] = gh;
-      if (j < RPT) s_ght[j][tt] = gh;
-#else
-      __bf16 h, lo;
-      split_hi_lo(gh, h, lo);
-      s_ghr[0][tt][j] = h;
-      s_ghr[1][tt][j] = lo;
-      if (j < RPT) {
-        s_ght[0][j][tt] = h;
-        s_ght[1][j][tt] = lo;
-      }
-#endif
-    }
-    // 2. this wave's z tile, 32 tokens x WC columns, row-major into LDS
+  struct Step {
+    XFrag zz[ZQ];
+    SFrag gr[PF ? 2 : 1][PF ? KS : 1];
+    SFrag gt[PF ? NT : 1];
+    float gb[2][NI][4];  // fused g_x: g_b[t][column chunk] below r, zeros elsewhere
+  };
+  auto load = [&](Step& s, int64_t t0) {
+    const int64_t rows = min((int64_t)32, t_end - t0);
+    const rsrc_t zr = make_rsrc(z + t0 * ld_z + wc0, rows_bytes(rows, WC, ld_z, kEs));
+    if constexpr (FUSED) {
+      const rsrc_t gbr = make_rsrc(g_b + t0 * r, rows * r * kEs);
 #pragma unroll
-    for (int q = 0; q < WC / 16; ++q) {
+      for (int th = 0; th < 2; ++th)
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int cc = wc0 + 32 * (i / (W / 4)) + W * grp + 4 * (i % (W / 4));
+          bld_x4(gbr, cc < r ? (uint32_t)(((16 * th + row16) * r + cc) * kEs) : kOOB, s.gb[th][i]);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < ZQ; ++q) {
       const int idx = l + 64 * q;
       const int tt = idx / (WC / 8), ch = idx % (WC / 8);
-      const int64_t t = t0 + tt;
-      XFrag v = (won && t < t_end) ? load_x8(z + t * ld_z + wc0 + 8 * ch) : xfrag_zero();
-#if RESBM_IO_F32_BUILD
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s_z[wave][tt][8 * ch + e] = v.v[e];
-#else
-      *reinterpret_cast<uint4*>(&s_z[wave][tt][8 * ch]) = __builtin_bit_cast(uint4, v.v);
-#endif
+      s.zz[q] = bld_x8(zr, (uint32_t)((tt * ld_z + 8 * ch) * kEs));
     }
-    __syncthreads();
-
-    // 3. g_z for two 16-token halves: D[c][t] = sum_j W_e[c][j] g_h[t][j]
-    if (won) {
+    if constexpr (PF) {
+      const int64_t si = t0 / 32;  // past the last step: out of range, zeros
 #pragma unroll
-      for (int th = 0; th < 2; ++th) {
-        f32x4 acc[CT];
+      for (int th = 0; th < 2; ++th)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ks = 0; ks < KS; ++ks) s.gr[th][ks] = bld_sfrag(rr, (2 * si + th) * KS + ks, l);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          SFrag g;
-#if RESBM_IO_F32_BUILD
+      for (int jt = 0; jt < NT; ++jt) s.gt[jt] = bld_sfrag(tr, si * NT + jt, l);
+    }
+  };
+  auto step = [&](const Step& s, int64_t t0) {
+    const int64_t si = t0 / 32;
+    const int64_t rows = min((int64_t)32, t_end - t0);
+    const rsrc_t gzr = make_rsrc(g_z + t0 * ld_gz, rows_bytes(rows, n, ld_gz, kEs));
+    // g_z for the two 16-token halves: D[c][t] = sum_j W_e[c][j] g_h[t][j]
 #pragma unroll
-          for (int e = 0; e < 8; ++e) g.v[e] = s_ghr[16 * th + row16][32 * ks + 8 * grp + e];
-#else
-          g.hi = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&s_ghr[0][16 * th + row16][32 * ks + 8 * grp]));
-          g.lo = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&s_ghr[1][16 * th + row16][32 * ks + 8 * grp]));
-#endif
+    for (int th = 0; th < 2; ++th) {
+      f32x4 acc[CT];
 #pragma unroll
-          for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_ss(wef[ks][ct], g, acc[ct]);
+      for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        SFrag g;
+        if constexpr (PF) g = s.gr[th][ks];
+        else g = bld_sfrag(rr, (2 * si + th) * KS + ks, l);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_ss(wef[ks][ct], g, acc[ct]);
+      }
+      const int tt = 16 * th + row16;
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        float v[W];
+#pragma unroll
+        for (int q = 0; q < W / 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[4 * q + e] = acc[2 * h + q][e];
+        const int cc = wc0 + 32 * h + W * grp;
+        if constexpr (FUSED) {
+#pragma unroll
+          for (int q = 0; q < W / 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[4 * q + e] += s.gb[th][h * (W / 4) + q][e];
         }
-        const int64_t t = t0 + 16 * th + row16;
-        if (t < t_end) {
-          float v[4 * CT];
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) v[4 * ct + q] = acc[ct][q];
-          if (gx_fused && cl < r) {
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) {
-              const int cb = cl + 4 * ct;
-              if (cb < r) {
-                float x[4];
-                load_x4(g_b + t * r + cb, x);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) v[4 * ct + q] += x[q];
-              }
-            }
-          }
-          store_row<4 * CT>(g_z + t * ld_gz + cl, v);
-        }
+        bst_n<W>(gzr, (uint32_t)((tt * ld_gz + cc) * kEs), v);
       }
     }
 
-    // 4. dW_e: D[j][c] = sum_t g_h[t][j] z[t][c], A = g_h^T (LDS), B = z^T (LDS)
+    // stage the z tile in this wave's LDS and read it back transposed
+    wave_lds_fence();
+#pragma unroll
+    for (int q = 0; q < ZQ; ++q) {
+      const int idx = l + 64 * q;
+      tile_put8<WC>(s_z, idx / (WC / 8), 8 * (idx % (WC / 8)), s.zz[q]);
+    }
+    wave_lds_fence();
+    // dW_e: D[j][c] = sum_t g_h[t][j] z[t][c], A = g_h^T (fragments), B = z^T (LDS)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
-      XFrag zb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) zb.v[e] = s_z[wave][8 * grp + e][16 * ct + row16];
+      const XFrag zb = tr_frag<WC>(s_z, 16 * ct, row16, grp);
 #pragma unroll
       for (int jt = 0; jt < NT; ++jt) {
         SFrag g;
-#if RESBM_IO_F32_BUILD
-#pragma unroll
-        for (int e = 0; e < 8; ++e) g.v[e] = s_ght[16 * jt + row16][8 * grp + e];
-#else
-        g.hi = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&s_ght[0][16 * jt + row16][8 * grp]));
-        g.lo = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&s_ght[1][16 * jt + row16][8 * grp]));
-#endif
+        if constexpr (PF) g = s.gt[jt];
+        else g = bld_sfrag(tr, si * NT + jt, l);
         dw[ct][jt] = mma_sx(g, zb, dw[ct][jt]);
       }
     }
-    __syncthreads();
+  };
+
+  const int64_t stride = 32 * EW;
+  Step sa, sb;
+  int64_t t0 = t_begin + 32 * wave;
+  load(sa, t0);
+  for (; t0 < t_end; t0 += 2 * stride) {
+    load(sb, t0 + stride);
+    step(sa, t0);
+    load(sa, t0 + 2 * stride);
+    step(sb, t0 + stride);  // past t_end: zeros in, nothing out
   }
 
-  // dw[ct][jt][v] = dW_e partial [wc0 + 16 ct + row16][16 jt + 4 grp + v]
-  if (won) {
+  // dw[ct][jt][v] = partial dW_e[wc0 + 16 ct + row16][16 jt + 4 grp + v]; add the EW waves in order
+  __syncthreads();  // every wave is done with its staging area
+  float (*s_red)[WC][RPT + 4] = reinterpret_cast<float (*)[WC][RPT + 4]>(smem);
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-      const int c = wc0 + 16 * ct + row16;
+  for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-      for (int jt = 0; jt < NT; ++jt) {
-        const int j0 = 16 * jt + 4 * grp;
-        if (j0 >= r) continue;
-        *reinterpret_cast<float4*>(dwp + ((int64_t)tg * n + c) * RP + j0) =
-            make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
-      }
+    for (int jt = 0; jt < NT; ++jt)
+      *reinterpret_cast<float4*>(&s_red[wave][16 * ct + row16][16 * jt + 4 * grp]) =
+          make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
+  __syncthreads();
+  constexpr int Q = RPT / 4;
+  for (int idx = threadIdx.x; idx < WC * Q; idx += EW * 64) {
+    const int c = idx / Q, j0 = (idx % Q) * 4;
+    if (j0 >= r) continue;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int w = 0; w < EW; ++w) {
+      const float4 p = *reinterpret_cast<const float4*>(&s_red[w][c][j0]);
+      s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
     }
+    *reinterpret_cast<float4*>(dwp + ((int64_t)tg * n + wc0 + c) * RP + j0) = s;
   }
 }
 
@@ -748,20 +983,22 @@ bool ld_ok(int64_t ld, int n) { return ld >= n && ld % 8 == 0; }
 
 template <int NT>
 void launch_enc_fwd(const Plan& p, int act, const io_t* x, int64_t ld_x, const io_t* z, int64_t ld_z,
-                    const void* wf, io_t* b, float* a_save, float* part, hipStream_t st) {
-  constexpr int MT = NT <= 2 ? 4 : (NT <= 4 ? 2 : 1);
-  dim3 grid(p.ef_nblk, p.ef_S);
-  hipLaunchKernelGGL((k_enc_fwd<NT, MT>), grid, dim3(256), 0, st, p.T, p.n, p.r, p.RP, act, x, ld_x, z,
-                     ld_z, wf, b, a_save, part, p.ef_S, p.ef_kspl);
+                    const void* wf, io_t* b, float* a_save, hipStream_t st) {
+  constexpr int MT = ef_mt(NT);
+  constexpr int KW = ef_kw(NT);
+  hipLaunchKernelGGL((k_enc_fwd<NT, MT, KW>), dim3(p.ef_nblk), dim3(KW * 64), 0, st, p.T, p.n, p.r, act, x, ld_x,
+                     z, ld_z, wf, b, a_save);
 }
 
 template <int KS>
 void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, io_t* zt, int64_t ld,
                     hipStream_t st) {
-  constexpr int CT = KS <= 2 ? 4 : (KS <= 4 ? 2 : 1);
+  constexpr int CT = df_ct(KS);
   dim3 grid(p.df_nwg, p.df_ngrp);
-  hipLaunchKernelGGL((k_dec_fwd<KS, CT>), grid, dim3(256), 0, st, p.T, p.n, p.r, add_id, b, W_d, zt, ld,
-                     p.df_tpg);
+  if (add_id)
+    hipLaunchKernelGGL((k_dec_fwd<KS, CT, true>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, W_d, zt, ld, p.df_tpg);
+  else
+    hipLaunchKernelGGL((k_dec_fwd<KS, CT, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, W_d, zt, ld, p.df_tpg);
 }
 
 template <int JT>
@@ -774,13 +1011,24 @@ void launch_dec_bwd(const Plan& p, const io_t* b, const float* W_d, const io_t* 
 
 template <int NT>
 void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const float* W_e, const float* a_save,
-                    const io_t* g_b, io_t* g_z, int64_t ld_gz, io_t* g_x, int64_t ld_gx, int fused, float* dwp,
+                    const io_t* g_b, io_t* g_z, int64_t ld_gz, io_t* g_x, int64_t ld_gx, int fused, char* ws,
                     hipStream_t st) {
   constexpr int KS = (NT + 1) / 2;
-  constexpr int CT = KS <= 2 ? 4 : (KS <= 4 ? 2 : 1);
-  dim3 grid(p.eb_ncg, p.eb_ntg);
-  hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT>), grid, dim3(256), 0, st, p.T, p.n, p.r, p.RP, act, z, ld_z, W_e,
-                     a_save, g_b, g_z, ld_gz, g_x, ld_gx, fused, dwp, p.eb_TB);
+  constexpr int CT = eb_ct(KS);
+  constexpr int EW = eb_ew(NT);
+  void* ghr = ws + p.eb_ghr_off;
+  void* ght = ws + p.eb_ght_off;
+  const unsigned nsteps = (unsigned)ceil_div(p.T, 32);
+  hipLaunchKernelGGL((k_enc_bwd_prep<KS, NT>), dim3(nsteps), dim3(256), 0, st, p.T, p.r, act, a_save, g_b,
+                     fused ? nullptr : g_x, ld_gx, ghr, ght);
+  dim3 grid(p.eb_ncb, p.eb_ntg);
+  float* dwp = (float*)(ws + p.eb_dwp_off);
+  if (fused)
+    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, EW, true>), grid, dim3(EW * 64), 0, st, p.T, p.n, p.r, p.RP, z, ld_z,
+                       W_e, (const void*)ghr, (const void*)ght, (int64_t)nsteps, g_b, g_z, ld_gz, dwp, p.eb_TB);
+  else
+    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, EW, false>), grid, dim3(EW * 64), 0, st, p.T, p.n, p.r, p.RP, z, ld_z,
+                       W_e, (const void*)ghr, (const void*)ght, (int64_t)nsteps, g_b, g_z, ld_gz, dwp, p.eb_TB);
 }
 
 #define RESBM_DISPATCH_NT(NTV, CALL) \
@@ -833,20 +1081,14 @@ int32_t resbm_encode_fwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   hipStream_t s = (hipStream_t)stream;
   char* w = (char*)ws;
   void* wf = w + p.ef_wf_off;
-  float* part = (float*)(w + p.ef_part_off);
   const int64_t nprep = (int64_t)(n / 32) * p.NT * 64;
   hipLaunchKernelGGL(k_enc_fwd_prep, dim3((unsigned)ceil_div(nprep, 256)), dim3(256), 0, s, W_e, n, r, p.NT, wf);
   const io_t* X = (const io_t*)x_attn;
   const io_t* Z = (const io_t*)z;
   io_t* B = (io_t*)b;
-#define CALL(NTV) launch_enc_fwd<NTV>(p, act, X, ld_x, Z, ld_z, wf, B, a_save, part, s)
+#define CALL(NTV) launch_enc_fwd<NTV>(p, act, X, ld_x, Z, ld_z, wf, B, a_save, s)
   RESBM_DISPATCH_NT(p.NT, CALL)
 #undef CALL
-  if (p.ef_S > 1) {
-    const int64_t nth = T * (r / 4);
-    hipLaunchKernelGGL(k_enc_fwd_fin, dim3((unsigned)ceil_div(nth, 256)), dim3(256), 0, s, T, r, p.RP, act, X,
-                       ld_x, (const float*)part, p.ef_S, B, a_save);
-  }
   return launch_status();
 }
 
@@ -906,7 +1148,7 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r, const void* b, const f
   float* dwp = (float*)(w + p.db_dwp_off);
   const io_t* B = (const io_t*)b;
   const io_t* G = (const io_t*)g_zt;
-  switch (p.db_JT) {
+  switch (p.db_jt) {
     case 1: launch_dec_bwd<1>(p, B, W_d, G, ld_gzt, gbp, dwp, s); break;
     case 2: launch_dec_bwd<2>(p, B, W_d, G, ld_gzt, gbp, dwp, s); break;
     case 3: launch_dec_bwd<3>(p, B, W_d, G, ld_gzt, gbp, dwp, s); break;
@@ -914,7 +1156,7 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r, const void* b, const f
     default: return RESBM_E_SHAPE;
   }
   const int64_t nb_gb = ceil_div(T * (r / 4), 256);
-  const int64_t nb_dw = ceil_div((int64_t)r * (n / 4), 256);
+  const int64_t nb_dw = ceil_div((int64_t)r * (n / 4), 64);
   hipLaunchKernelGGL(k_dec_bwd_fin, dim3((unsigned)(nb_gb + nb_dw)), dim3(256), 0, s, T, n, r, p.RP,
                      (const float*)gbp, p.db_ncg, (const io_t*)g_id, ld_gid, (io_t*)g_b, (const float*)dwp,
                      p.db_ntg, dW_d, accumulate, nb_gb);
@@ -958,7 +1200,7 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   io_t* GZ = (io_t*)g_z;
   io_t* GX = (io_t*)g_x;
   const float* AS = act == RESBM_ACT_SILU ? a_save : nullptr;
-#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, GX, ld_gx, fused, dwp, s)
+#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, GX, ld_gx, fused, (char*)ws, s)
   RESBM_DISPATCH_NT(p.NT, CALL)
 #undef CALL
   const int64_t nth = (int64_t)n * (r / 4);
