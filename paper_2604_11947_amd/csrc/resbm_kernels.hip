@@ -684,88 +684,133 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
 }
 
 // ============================================================ encode backward
-// g_h = g_b phi'(a) is formed once per token by k_enc_bwd_prep and stored in the
-// two fragment orders the main kernel consumes:
-//   row order  (B operand of g_z):  fragment (tile16 KS + ks), lane (row16, grp) holds
-//                                   g_h[16 tile16 + row16][32 ks + 8 grp + e]
-//   transposed (A operand of dW_e): fragment (step32 NT + jt), lane (row16, grp) holds
-//                                   g_h[32 step32 + 8 grp + e][16 jt + row16]
-// (hi, lo) bf16 pairs in the bf16 build, 8 floats in the f32 build; tokens at or
-// beyond T hold zeros.
+// A block has CW x TW waves.  Wave (cw, tw) owns the 16 CT columns starting at
+// bc0 + cw 16 CT and, in every block step of 32 TW tokens, the 32 tokens
+// starting at t0 + 32 tw.  Per block step:
+//   1. the block forms g_h = g_b phi'(a) for the step's tokens in LDS, in split
+//      form, with zeros in the columns r .. 32 KS,
+//   2. each wave stages its 32-token tile of z in wave-private LDS,
+//   3. g_z[t][c] = sum_j g_h[t][j] W_e[c][j]: A = W_e fragments held in
+//      registers, B = g_h rows from LDS; stored from the accumulators
+//      (+ g_b[t][c] for c < r when g_x is g_z),
+//   4. dW_e[c][j] += sum_t z[t][c] g_h[t][j]: A = g_h^T and B = z^T, both read
+//      transposed from LDS, accumulated in registers over the token group.
+// All waves of a block read the same z rows at once, 32 CT x CW contiguous
+// bytes of each, and the block shares one copy of g_h.  The TW partial dW_e of
+// a column slice are added in LDS in wave order; k_enc_bwd_fin adds the token
+// groups in order.
 
-// One block per 32-token step: g_h into both fragment orders, and
-// g_x[t][0:r] += g_b[t][0:r] (rounded once) when g_x is given.
-template <int KS, int NT>
-__global__ __launch_bounds__(256) void k_enc_bwd_prep(int64_t T, int r, int act, const float* __restrict__ a_save,
-                                                      const io_t* __restrict__ g_b, io_t* __restrict__ g_x,
-                                                      int64_t ld_gx, void* __restrict__ ghr,
-                                                      void* __restrict__ ght) {
-  constexpr int KP = 32 * KS;
-  __shared__ float s_gh[32][KP + 1];
-  const int64_t step = blockIdx.x;
-  const int64_t t0 = step * 32;
-  for (int idx = threadIdx.x; idx < 32 * KP; idx += 256) {
-    const int tt = idx / KP, j = idx % KP;
-    const int64_t t = t0 + tt;
-    float g = 0.0f;
-    if (t < T && j < r) {
-      const float gb = io_to_f32(g_b[t * r + j]);
-      g = a_save ? gb * act_dphi(a_save[t * r + j], act) : gb;
-      if (g_x) {
-        io_t* px = g_x + t * ld_gx + j;
-        *px = f32_to_io(io_to_f32(*px) + gb);
-      }
-    }
-    s_gh[tt][j] = g;
-  }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < (2 * KS + NT) * 64; idx += 256) {
-    const int l = idx & 63, f = idx >> 6, row16 = l & 15, grp = l >> 4;
-    float w[8];
-    if (f < 2 * KS) {
-      const int th = f / KS, ks = f % KS;
+// Split g_h tile of TS tokens x RPS columns: bf16 build: hi and lo planes;
+// f32 build: one float plane.
+template <int TS, int RPS>
+struct GhTile {
+#if RESBM_IO_F32_BUILD
+  float v[TS][RPS];
+#else
+  __bf16 hi[TS][RPS];
+  __bf16 lo[TS][RPS];
+#endif
+};
+
+template <int TS, int RPS>
+__device__ __forceinline__ void gh_put4(GhTile<TS, RPS>& t, int row, int col, const float (&g)[4]) {
+#if RESBM_IO_F32_BUILD
+  *reinterpret_cast<float4*>(&t.v[row][col]) = make_float4(g[0], g[1], g[2], g[3]);
+#else
+  bf16x4 h, l;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) w[e] = s_gh[16 * th + row16][32 * ks + 8 * grp + e];
-      store_sfrag(ghr, (2 * step + th) * KS + ks, l, w);
-    } else {
-      const int jt = f - 2 * KS;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) w[e] = s_gh[8 * grp + e][16 * jt + row16];
-      store_sfrag(ght, step * NT + jt, l, w);
-    }
+  for (int e = 0; e < 4; ++e) {
+    __bf16 a, b;
+    split_hi_lo(g[e], a, b);
+    h[e] = a;
+    l[e] = b;
   }
+  *reinterpret_cast<uint2*>(&t.hi[row][col]) = __builtin_bit_cast(uint2, h);
+  *reinterpret_cast<uint2*>(&t.lo[row][col]) = __builtin_bit_cast(uint2, l);
+#endif
 }
 
-// EW waves of a block share the columns [cb 16 CT, (cb + 1) 16 CT) and take
-// turns over the 32-token steps of the token range [tg TB, ...):
-//   g_z[t][c] = sum_j g_h[t][j] W_e[c][j]      (+ g_b[t][c] for c < r when fused with g_x)
-//   dW_e partial [tg][c][j] = sum_t z[t][c] g_h[t][j]
-// The step's z tile is transposed through wave-private LDS; the EW partial dW_e
-// meet in LDS once at the end.
-template <int KS, int NT, int CT, int EW, bool FUSED>
-__global__ __launch_bounds__(EW * 64) void k_enc_bwd(int64_t T, int n, int r, int RP,
-                                                     const io_t* __restrict__ z, int64_t ld_z,
-                                                     const float* __restrict__ W_e,
-                                                     const void* __restrict__ ghr, const void* __restrict__ ght,
-                                                     int64_t nsteps, const io_t* __restrict__ g_b,
-                                                     io_t* __restrict__ g_z, int64_t ld_gz,
-                                                     float* __restrict__ dwp, int TB) {
-  constexpr int WC = 16 * CT;            // columns of the block
-  constexpr int RPT = 16 * NT;
-  constexpr int W = CT >= 2 ? 8 : 4;     // consecutive g_z columns per lane run
+// g_h[row][col .. col + 8) as the B operand of g_z (k = j).
+template <int TS, int RPS>
+__device__ __forceinline__ SFrag gh_row(const GhTile<TS, RPS>& t, int row, int col) {
+  SFrag f;
+#if RESBM_IO_F32_BUILD
+  const float4 a = *reinterpret_cast<const float4*>(&t.v[row][col]);
+  const float4 b = *reinterpret_cast<const float4*>(&t.v[row][col + 4]);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+#else
+  f.hi = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&t.hi[row][col]));
+  f.lo = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&t.lo[row][col]));
+#endif
+  return f;
+}
+
+// Transposed 16-bit fragment from a row-major plane with PITCH elements per row:
+// lane (row16, grp) receives plane[row0 + 8 grp + e][c0 + row16], e = 0..7
+// (two ds_read_b64_tr_b16, addressed as in tr_frag).
+template <int PITCH>
+__device__ __forceinline__ bf16x8 tr_plane(const __bf16* plane, int row0, int c0, int row16, int grp) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  s16x4 h[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int row = row0 + 8 * grp + 4 * q + (row16 >> 2);
+    const __bf16* p = plane + row * PITCH + c0 + 4 * (row16 & 3);
+    h[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+  }
+  return __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){h[0][0], h[0][1], h[0][2], h[0][3],
+                                                                               h[1][0], h[1][1], h[1][2], h[1][3]});
+}
+
+// g_h[row0 + 8 grp + e][c0 + row16] as the A operand of dW_e (k = t).
+template <int TS, int RPS>
+__device__ __forceinline__ SFrag gh_tr(const GhTile<TS, RPS>& t, int row0, int c0, int row16, int grp) {
+  SFrag f;
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f.v[e] = t.v[row0 + 8 * grp + e][c0 + row16];
+#else
+  f.hi = tr_plane<RPS>(&t.hi[0][0], row0, c0, row16, grp);
+  f.lo = tr_plane<RPS>(&t.lo[0][0], row0, c0, row16, grp);
+#endif
+  return f;
+}
+
+template <int KS, int NT, int CT, int CW, int TW, int PD, bool FUSED>
+__global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int r, int RP, int silu,
+                                                          const io_t* __restrict__ z, int64_t ld_z,
+                                                          const float* __restrict__ W_e,
+                                                          const float* __restrict__ a_save,
+                                                          const io_t* __restrict__ g_b, io_t* __restrict__ g_z,
+                                                          int64_t ld_gz, float* __restrict__ dwp, int TB) {
+  constexpr int EW = CW * TW, NTH = EW * 64;
+  constexpr int WC = 16 * CT, BC = CW * WC;
+  constexpr int TS = 32 * TW;
+  constexpr int KP = 32 * KS, RPT = 16 * NT, RPS = KP + 8;
+  constexpr int W = CT >= 2 ? 8 : 4;       // consecutive g_z columns per lane run
   constexpr int NH = CT >= 2 ? CT / 2 : 1;
-  constexpr int ZQ = WC / 16;            // 16-byte z chunks per lane per step
-  constexpr bool PF = KS <= 2;           // g_h fragments travel with the step (r <= 64)
-  constexpr int NI = FUSED ? NH * W / 4 : 1;  // 4-column g_b chunks per lane and token half
-  constexpr int WAVE_LDS = 32 * WC * (int)sizeof(io_t);
-  constexpr int RED_LDS = EW * WC * (RPT + 4) * 4;
-  constexpr int LDS = EW * WAVE_LDS > RED_LDS ? EW * WAVE_LDS : RED_LDS;
+  constexpr int ZQ = WC / 16;              // 8-element z chunks per lane per step
+  constexpr int GQ = TS * KP / 4;          // 4-column chunks of the g_h tile
+  constexpr int NCH = (GQ + NTH - 1) / NTH;
+  constexpr int GH_BYTES = (int)sizeof(GhTile<TS, RPS>);
+  constexpr int GB_BYTES = FUSED ? TS * RPT * 4 : 0;
+  constexpr int Z_BYTES = 32 * WC * (int)sizeof(io_t);
+  constexpr int MAIN_LDS = 2 * GH_BYTES + 2 * GB_BYTES + EW * Z_BYTES;
+  constexpr int RED_LDS = (TW - 1) * BC * (RPT + 4) * 4;
+  constexpr int LDS = MAIN_LDS > RED_LDS ? MAIN_LDS : RED_LDS;
   __shared__ __attribute__((aligned(16))) char smem[LDS];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
-  const int cb = blockIdx.x, tg = blockIdx.y;
-  const int wc0 = cb * WC;
-  io_t* s_z = reinterpret_cast<io_t*>(smem + wave * WAVE_LDS);
+  const int cw = wave % CW, tw = wave / CW;
+  const int wc0 = blockIdx.x * BC + cw * WC;
+  const bool on = wc0 < n;  // whole waves fall inside or outside [0, n): n % 64 == 0, WC | 64
+  const int tg = blockIdx.y;
+  const int64_t t_begin = (int64_t)tg * TB;
+  const int64_t t_end = min(T, t_begin + TB);
+  GhTile<TS, RPS>* s_gh = reinterpret_cast<GhTile<TS, RPS>*>(smem);
+  float (*s_gb)[TS][RPT] = reinterpret_cast<float (*)[TS][RPT]>(smem + 2 * GH_BYTES);
+  io_t* s_z = reinterpret_cast<io_t*>(smem + 2 * GH_BYTES + 2 * GB_BYTES + wave * Z_BYTES);
 
   // W_e as the A operand of g_z: lane (row16, grp) holds W_e[col][32 ks + 8 grp + e], col = expand_col.
   SFrag wef[KS][CT];
@@ -778,7 +823,7 @@ __global__ __launch_bounds__(EW * 64) void k_enc_bwd(int64_t T, int n, int r, in
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int j = ks * 32 + grp * 8 + e;
-        w[e] = j < r ? W_e[(int64_t)col * r + j] : 0.0f;
+        w[e] = (on && j < r) ? W_e[(int64_t)col * r + j] : 0.0f;
       }
       wef[ks][ct] = sfrag_from(w);
     }
@@ -789,51 +834,78 @@ __global__ __launch_bounds__(EW * 64) void k_enc_bwd(int64_t T, int n, int r, in
 #pragma unroll
     for (int jt = 0; jt < NT; ++jt) dw[ct][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int64_t t_begin = (int64_t)tg * TB;
-  const int64_t t_end = min(T, t_begin + TB);
-  const rsrc_t rr = make_rsrc(ghr, nsteps * 2 * KS * kSFragBytes);
-  const rsrc_t tr = make_rsrc(ght, nsteps * NT * kSFragBytes);
-
-  struct Step {
-    XFrag zz[ZQ];
-    SFrag gr[PF ? 2 : 1][PF ? KS : 1];
-    SFrag gt[PF ? NT : 1];
-    float gb[2][NI][4];  // fused g_x: g_b[t][column chunk] below r, zeros elsewhere
+  // g_h inputs of one block step: chunk q = threadIdx + i NTH covers token q / (KP / 4),
+  // columns 4 (q % (KP / 4)) .. + 3 (zeros at or beyond r and past the token range).
+  struct Gin {
+    float gb[NCH][4];
+    float a[NCH][4];
   };
-  auto load = [&](Step& s, int64_t t0) {
-    const int64_t rows = min((int64_t)32, t_end - t0);
-    const rsrc_t zr = make_rsrc(z + t0 * ld_z + wc0, rows_bytes(rows, WC, ld_z, kEs));
-    if constexpr (FUSED) {
-      const rsrc_t gbr = make_rsrc(g_b + t0 * r, rows * r * kEs);
+  auto load_gin = [&](Gin& g, int64_t t0) {
+    const int64_t rows = min((int64_t)TS, t_end - t0);
+    const rsrc_t gbr = make_rsrc(g_b + t0 * r, rows * r * kEs);
+    const rsrc_t ar = make_rsrc(silu ? a_save + t0 * r : a_save, silu ? rows * r * 4 : 0);
 #pragma unroll
-      for (int th = 0; th < 2; ++th)
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          const int cc = wc0 + 32 * (i / (W / 4)) + W * grp + 4 * (i % (W / 4));
-          bld_x4(gbr, cc < r ? (uint32_t)(((16 * th + row16) * r + cc) * kEs) : kOOB, s.gb[th][i]);
-        }
+    for (int i = 0; i < NCH; ++i) {
+      const int q = threadIdx.x + i * NTH;
+      const int tt = q / (KP / 4), j0 = 4 * (q % (KP / 4));
+      const bool ok = q < GQ && j0 < r;
+      bld_x4(gbr, ok ? (uint32_t)((tt * r + j0) * kEs) : kOOB, g.gb[i]);
+      if (silu) {
+        const uint4 v = bld16(ar, ok ? (uint32_t)((tt * r + j0) * 4) : kOOB);
+        g.a[i][0] = __builtin_bit_cast(float, v.x);
+        g.a[i][1] = __builtin_bit_cast(float, v.y);
+        g.a[i][2] = __builtin_bit_cast(float, v.z);
+        g.a[i][3] = __builtin_bit_cast(float, v.w);
+      }
     }
+  };
+  auto put_gh = [&](const Gin& g, int buf) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int q = threadIdx.x + i * NTH;
+      if (GQ % NTH == 0 || q < GQ) {
+        const int tt = q / (KP / 4), j0 = 4 * (q % (KP / 4));
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = silu ? g.gb[i][e] * act_dphi(g.a[i][e], 1) : g.gb[i][e];
+        gh_put4(s_gh[buf], tt, j0, v);
+        if constexpr (FUSED) {
+          if (j0 < RPT)
+            *reinterpret_cast<float4*>(&s_gb[buf][tt][j0]) = make_float4(g.gb[i][0], g.gb[i][1], g.gb[i][2],
+                                                                          g.gb[i][3]);
+        }
+      }
+    }
+  };
+  auto load_z = [&](XFrag (&zz)[ZQ], int64_t t0w) {
+    const int64_t rows = min((int64_t)32, t_end - t0w);
+    const rsrc_t zr = make_rsrc(z + t0w * ld_z + wc0, on ? rows_bytes(rows, WC, ld_z, kEs) : 0);
 #pragma unroll
     for (int q = 0; q < ZQ; ++q) {
       const int idx = l + 64 * q;
       const int tt = idx / (WC / 8), ch = idx % (WC / 8);
-      s.zz[q] = bld_x8(zr, (uint32_t)((tt * ld_z + 8 * ch) * kEs));
-    }
-    if constexpr (PF) {
-      const int64_t si = t0 / 32;  // past the last step: out of range, zeros
-#pragma unroll
-      for (int th = 0; th < 2; ++th)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) s.gr[th][ks] = bld_sfrag(rr, (2 * si + th) * KS + ks, l);
-#pragma unroll
-      for (int jt = 0; jt < NT; ++jt) s.gt[jt] = bld_sfrag(tr, si * NT + jt, l);
+      zz[q] = bld_x8(zr, (uint32_t)((tt * ld_z + 8 * ch) * kEs));
     }
   };
-  auto step = [&](const Step& s, int64_t t0) {
-    const int64_t si = t0 / 32;
-    const int64_t rows = min((int64_t)32, t_end - t0);
-    const rsrc_t gzr = make_rsrc(g_z + t0 * ld_gz, rows_bytes(rows, n, ld_gz, kEs));
+
+  auto body = [&](int64_t s, XFrag (&zz)[ZQ], Gin& gin) {
+    const int buf = (int)(s & 1);
+    const int64_t t0 = t_begin + s * TS;
+    const int64_t t0w = t0 + 32 * tw;
+    put_gh(gin, buf);
+    load_gin(gin, t0 + TS);
+    wave_lds_fence();  // the previous step's transposed reads of s_z are complete
+#pragma unroll
+    for (int q = 0; q < ZQ; ++q) {
+      const int idx = l + 64 * q;
+      tile_put8<WC>(s_z, idx / (WC / 8), 8 * (idx % (WC / 8)), zz[q]);
+    }
+    load_z(zz, t0w + PD * TS);
+    __syncthreads();  // g_h of this step is complete; the buffer written next step is free
+
     // g_z for the two 16-token halves: D[c][t] = sum_j W_e[c][j] g_h[t][j]
+    const int64_t rows = min((int64_t)32, t_end - t0w);
+    const rsrc_t gzr = make_rsrc(g_z + t0w * ld_gz, rows_bytes(rows, n, ld_gz, kEs));
 #pragma unroll
     for (int th = 0; th < 2; ++th) {
       f32x4 acc[CT];
@@ -841,9 +913,7 @@ __global__ __launch_bounds__(EW * 64) void k_enc_bwd(int64_t T, int n, int r, in
       for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        SFrag g;
-        if constexpr (PF) g = s.gr[th][ks];
-        else g = bld_sfrag(rr, (2 * si + th) * KS + ks, l);
+        const SFrag g = gh_row(s_gh[buf], 32 * tw + 16 * th + row16, 32 * ks + 8 * grp);
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_ss(wef[ks][ct], g, acc[ct]);
       }
@@ -857,76 +927,97 @@ __global__ __launch_bounds__(EW * 64) void k_enc_bwd(int64_t T, int n, int r, in
           for (int e = 0; e < 4; ++e) v[4 * q + e] = acc[2 * h + q][e];
         const int cc = wc0 + 32 * h + W * grp;
         if constexpr (FUSED) {
+          if (wc0 < r) {
 #pragma unroll
-          for (int q = 0; q < W / 4; ++q)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[4 * q + e] += s.gb[th][h * (W / 4) + q][e];
+            for (int e = 0; e < W; ++e)
+              if (cc + e < r) v[e] += s_gb[buf][32 * tw + tt][cc + e];
+          }
         }
-        bst_n<W>(gzr, (uint32_t)((tt * ld_gz + cc) * kEs), v);
+        bst_n<W>(gzr, on ? (uint32_t)((tt * ld_gz + cc) * kEs) : kOOB, v);
       }
     }
 
-    // stage the z tile in this wave's LDS and read it back transposed
-    wave_lds_fence();
+    // dW_e: D[j][c] = sum_t g_h[t][j] z[t][c], A = g_h^T, B = z^T
+    XFrag zb[CT];
 #pragma unroll
-    for (int q = 0; q < ZQ; ++q) {
-      const int idx = l + 64 * q;
-      tile_put8<WC>(s_z, idx / (WC / 8), 8 * (idx % (WC / 8)), s.zz[q]);
-    }
-    wave_lds_fence();
-    // dW_e: D[j][c] = sum_t g_h[t][j] z[t][c], A = g_h^T (fragments), B = z^T (LDS)
+    for (int ct = 0; ct < CT; ++ct) zb[ct] = tr_frag<WC>(s_z, 16 * ct, row16, grp);
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-      const XFrag zb = tr_frag<WC>(s_z, 16 * ct, row16, grp);
+    for (int jt = 0; jt < NT; ++jt) {
+      const SFrag g = gh_tr(s_gh[buf], 32 * tw, 16 * jt, row16, grp);
 #pragma unroll
-      for (int jt = 0; jt < NT; ++jt) {
-        SFrag g;
-        if constexpr (PF) g = s.gt[jt];
-        else g = bld_sfrag(tr, si * NT + jt, l);
-        dw[ct][jt] = mma_sx(g, zb, dw[ct][jt]);
-      }
+      for (int ct = 0; ct < CT; ++ct) dw[ct][jt] = mma_sx(g, zb[ct], dw[ct][jt]);
     }
   };
 
-  const int64_t stride = 32 * EW;
-  Step sa, sb;
-  int64_t t0 = t_begin + 32 * wave;
-  load(sa, t0);
-  for (; t0 < t_end; t0 += 2 * stride) {
-    load(sb, t0 + stride);
-    step(sa, t0);
-    load(sa, t0 + 2 * stride);
-    step(sb, t0 + stride);  // past t_end: zeros in, nothing out
+  const int64_t nsb = (t_end - t_begin + TS - 1) / TS;
+  Gin gin;
+  XFrag z0[ZQ], z1[ZQ];
+  load_gin(gin, t_begin);
+  load_z(z0, t_begin + 32 * tw);
+  if constexpr (PD == 2) load_z(z1, t_begin + TS + 32 * tw);
+  for (int64_t s = 0; s < nsb; s += 2) {
+    body(s, z0, gin);
+    if (s + 1 < nsb) {
+      if constexpr (PD == 2) body(s + 1, z1, gin);
+      else body(s + 1, z0, gin);
+    }
   }
 
-  // dw[ct][jt][v] = partial dW_e[wc0 + 16 ct + row16][16 jt + 4 grp + v]; add the EW waves in order
-  __syncthreads();  // every wave is done with its staging area
-  float (*s_red)[WC][RPT + 4] = reinterpret_cast<float (*)[WC][RPT + 4]>(smem);
+  // dw[ct][jt][v] = partial dW_e[wc0 + 16 ct + row16][16 jt + 4 grp + v]
+  if constexpr (TW > 1) {
+    __syncthreads();  // the reduction area overlaps the step buffers
+    float (*s_red)[BC][RPT + 4] = reinterpret_cast<float (*)[BC][RPT + 4]>(smem);
+    if (tw > 0) {
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int jt = 0; jt < NT; ++jt)
+          *reinterpret_cast<float4*>(&s_red[tw - 1][cw * WC + 16 * ct + row16][16 * jt + 4 * grp]) =
+              make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
+    }
+    __syncthreads();
+    if (tw > 0) return;
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int jt = 0; jt < NT; ++jt)
+#pragma unroll
+        for (int u = 0; u < TW - 1; ++u) {
+          const float4 p = *reinterpret_cast<const float4*>(&s_red[u][cw * WC + 16 * ct + row16][16 * jt + 4 * grp]);
+          dw[ct][jt][0] += p.x; dw[ct][jt][1] += p.y; dw[ct][jt][2] += p.z; dw[ct][jt][3] += p.w;
+        }
+  }
+  if (!on) return;
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
     for (int jt = 0; jt < NT; ++jt)
-      *reinterpret_cast<float4*>(&s_red[wave][16 * ct + row16][16 * jt + 4 * grp]) =
+      *reinterpret_cast<float4*>(dwp + ((int64_t)tg * n + wc0 + 16 * ct + row16) * RP + 16 * jt + 4 * grp) =
           make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
-  __syncthreads();
-  constexpr int Q = RPT / 4;
-  for (int idx = threadIdx.x; idx < WC * Q; idx += EW * 64) {
-    const int c = idx / Q, j0 = (idx % Q) * 4;
-    if (j0 >= r) continue;
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int w = 0; w < EW; ++w) {
-      const float4 p = *reinterpret_cast<const float4*>(&s_red[w][c][j0]);
-      s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
-    }
-    *reinterpret_cast<float4*>(dwp + ((int64_t)tg * n + wc0 + c) * RP + j0) = s;
-  }
 }
 
-// dW_e (+)= sum_tg dwp[tg] in token-group order.
-__global__ __launch_bounds__(256) void k_enc_bwd_fin(int n, int r, int RP, const float* __restrict__ dwp,
-                                                     int ntg, float* __restrict__ dW_e, int accumulate) {
+// dW_e (+)= sum_tg dwp[tg] in token-group order (blocks [0, nb_dw)), and
+// g_x[t][0:r] += g_b[t][0:r], rounded once (the remaining blocks, when g_x is
+// given apart from g_z).
+__global__ __launch_bounds__(256) void k_enc_bwd_fin(int64_t T, int n, int r, int RP,
+                                                     const float* __restrict__ dwp, int ntg,
+                                                     float* __restrict__ dW_e, int accumulate, int64_t nb_dw,
+                                                     const io_t* __restrict__ g_b, io_t* __restrict__ g_x,
+                                                     int64_t ld_gx) {
   const int nq = r / 4;
+  if ((int64_t)blockIdx.x >= nb_dw) {
+    const int64_t gid = ((int64_t)blockIdx.x - nb_dw) * 256 + threadIdx.x;
+    if (gid >= T * nq) return;
+    const int64_t t = gid / nq;
+    const int j0 = (int)(gid % nq) * 4;
+    float gb[4], x[4];
+    load_x4(g_b + t * r + j0, gb);
+    load_x4(g_x + t * ld_gx + j0, x);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) x[v] += gb[v];
+    store_x4(g_x + t * ld_gx + j0, x);
+    return;
+  }
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= (int64_t)n * nq) return;
   const int c = (int)(gid / nq);
@@ -1011,24 +1102,17 @@ void launch_dec_bwd(const Plan& p, const io_t* b, const float* W_d, const io_t* 
 
 template <int NT>
 void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const float* W_e, const float* a_save,
-                    const io_t* g_b, io_t* g_z, int64_t ld_gz, io_t* g_x, int64_t ld_gx, int fused, char* ws,
-                    hipStream_t st) {
+                    const io_t* g_b, io_t* g_z, int64_t ld_gz, int fused, float* dwp, hipStream_t st) {
   constexpr int KS = (NT + 1) / 2;
-  constexpr int CT = eb_ct(KS);
-  constexpr int EW = eb_ew(NT);
-  void* ghr = ws + p.eb_ghr_off;
-  void* ght = ws + p.eb_ght_off;
-  const unsigned nsteps = (unsigned)ceil_div(p.T, 32);
-  hipLaunchKernelGGL((k_enc_bwd_prep<KS, NT>), dim3(nsteps), dim3(256), 0, st, p.T, p.r, act, a_save, g_b,
-                     fused ? nullptr : g_x, ld_gx, ghr, ght);
+  constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS), PD = eb_pd(KS);
   dim3 grid(p.eb_ncb, p.eb_ntg);
-  float* dwp = (float*)(ws + p.eb_dwp_off);
+  const int silu = act == RESBM_ACT_SILU;
   if (fused)
-    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, EW, true>), grid, dim3(EW * 64), 0, st, p.T, p.n, p.r, p.RP, z, ld_z,
-                       W_e, (const void*)ghr, (const void*)ght, (int64_t)nsteps, g_b, g_z, ld_gz, dwp, p.eb_TB);
+    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, PD, true>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
+                       p.RP, silu, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, dwp, p.eb_TB);
   else
-    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, EW, false>), grid, dim3(EW * 64), 0, st, p.T, p.n, p.r, p.RP, z, ld_z,
-                       W_e, (const void*)ghr, (const void*)ght, (int64_t)nsteps, g_b, g_z, ld_gz, dwp, p.eb_TB);
+    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, PD, false>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
+                       p.RP, silu, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, dwp, p.eb_TB);
 }
 
 #define RESBM_DISPATCH_NT(NTV, CALL) \
@@ -1198,14 +1282,14 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   const io_t* Z = (const io_t*)z;
   const io_t* GB = (const io_t*)g_b;
   io_t* GZ = (io_t*)g_z;
-  io_t* GX = (io_t*)g_x;
   const float* AS = act == RESBM_ACT_SILU ? a_save : nullptr;
-#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, GX, ld_gx, fused, (char*)ws, s)
+#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, s)
   RESBM_DISPATCH_NT(p.NT, CALL)
 #undef CALL
-  const int64_t nth = (int64_t)n * (r / 4);
-  hipLaunchKernelGGL(k_enc_bwd_fin, dim3((unsigned)ceil_div(nth, 256)), dim3(256), 0, s, n, r, p.RP,
-                     (const float*)dwp, p.eb_ntg, dW_e, accumulate);
+  const int64_t nb_dw = ceil_div((int64_t)n * (r / 4), 256);
+  const int64_t nb_gx = (g_x && !fused) ? ceil_div(T * (r / 4), 256) : 0;
+  hipLaunchKernelGGL(k_enc_bwd_fin, dim3((unsigned)(nb_dw + nb_gx)), dim3(256), 0, s, T, n, r, p.RP,
+                     (const float*)dwp, p.eb_ntg, dW_e, accumulate, nb_dw, GB, (io_t*)g_x, ld_gx);
   return launch_status();
 }
 

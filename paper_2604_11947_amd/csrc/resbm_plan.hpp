@@ -13,8 +13,8 @@
 #ifndef RESBM_DB_WG_PER_CU
 #define RESBM_DB_WG_PER_CU 1
 #endif
-#ifndef RESBM_EB_WAVES_PER_CU
-#define RESBM_EB_WAVES_PER_CU 8
+#ifndef RESBM_EB_BLOCKS_PER_CU
+#define RESBM_EB_BLOCKS_PER_CU 1
 #endif
 #ifndef RESBM_EF_MT_SMALL_R
 #define RESBM_EF_MT_SMALL_R 4
@@ -37,11 +37,13 @@ constexpr int kDbWaves = 8;
 constexpr int kDbWC = 64;
 constexpr int db_jt(int NT) { return NT < 4 ? NT : 4; }
 
-// ---- encode_bwd: EW waves share 16*CT columns and take turns over 32-token steps.
-// Workspace: dW_e partials, then g_h in row-fragment order (KS fragments of
-// 2 x 16 bytes per lane per 16 tokens), then in transposed order (NT per 32 tokens).
+// ---- encode_bwd: blocks of CW x TW waves; a wave owns 16*CT columns, a block
+// step covers 32*TW tokens; PD block steps of z are in flight per wave.
+// Workspace: the dW_e partials of the token groups.
 constexpr int eb_ct(int KS) { return KS <= 1 ? 4 : (KS <= 2 ? 2 : 1); }
-constexpr int eb_ew(int) { return 4; }
+constexpr int eb_cw(int) { return 4; }
+constexpr int eb_tw(int KS) { return KS <= 2 ? 2 : 1; }
+constexpr int eb_pd(int KS) { return KS <= 2 ? 2 : 1; }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
@@ -62,8 +64,8 @@ struct Plan {
   int db_jt, db_njg, db_ncg, db_TB, db_ntg;
   size_t db_gbp_off, db_dwp_off, db_ws;
 
-  int eb_ct, eb_ew, eb_ncb, eb_TB, eb_ntg;
-  size_t eb_dwp_off, eb_ghr_off, eb_ght_off, eb_ws;
+  int eb_ct, eb_bc, eb_ncb, eb_TB, eb_ntg;
+  size_t eb_dwp_off, eb_ws;
 
   size_t ws_total;
 };
@@ -114,23 +116,17 @@ inline Plan make_plan(int64_t T, int n, int r) {
 
   // ---- encode_bwd: dW_e partials per token group
   p.eb_ct = eb_ct(p.KS);
-  p.eb_ew = eb_ew(p.NT);
-  p.eb_ncb = n / (16 * p.eb_ct);
+  p.eb_bc = eb_cw(p.KS) * 16 * p.eb_ct;
+  p.eb_ncb = (int)ceil_div(n, p.eb_bc);
   {
-    const int64_t nstep = ceil_div(Tm, 32);
-    const int64_t wpb = p.eb_ew;
-    const int64_t g = clamp64(ceil_div((int64_t)RESBM_EB_WAVES_PER_CU * kNumCU, (int64_t)p.eb_ncb * wpb), 1,
-                              ceil_div(nstep, wpb));
-    p.eb_TB = (int)(32 * ceil_div(nstep, g));
+    const int64_t ts = 32 * eb_tw(p.KS);
+    const int64_t nstep = ceil_div(Tm, ts);
+    const int64_t g = clamp64(ceil_div((int64_t)RESBM_EB_BLOCKS_PER_CU * kNumCU, p.eb_ncb), 1, nstep);
+    p.eb_TB = (int)(ts * ceil_div(nstep, g));
     p.eb_ntg = (int)ceil_div(Tm, p.eb_TB);
   }
   p.eb_dwp_off = 0;
-  {
-    const size_t nsteps = (size_t)ceil_div(Tm, 32);
-    p.eb_ghr_off = align_ws((size_t)p.eb_ntg * n * p.RP * 4);
-    p.eb_ght_off = p.eb_ghr_off + align_ws(nsteps * p.KS * 4096);
-    p.eb_ws = p.eb_ght_off + align_ws(nsteps * p.NT * 2048);
-  }
+  p.eb_ws = align_ws((size_t)p.eb_ntg * n * p.RP * 4);
 
   size_t m = p.ef_ws;
   if (p.db_ws > m) m = p.db_ws;
