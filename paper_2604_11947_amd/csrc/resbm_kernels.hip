@@ -123,6 +123,16 @@ __device__ __forceinline__ void bst_n(rsrc_t r, uint32_t off, const float* v) {
 #endif
 }
 
+// Stores 8 consecutive I/O elements read from LDS at src (16-byte aligned).
+__device__ __forceinline__ void bst_x8(rsrc_t r, uint32_t off, const io_t* src) {
+#if RESBM_IO_F32_BUILD
+  bst16(r, off, *reinterpret_cast<const uint4*>(src));
+  bst16(r, off == kOOB ? kOOB : off + 16, *reinterpret_cast<const uint4*>(src + 4));
+#else
+  bst16(r, off, *reinterpret_cast<const uint4*>(src));
+#endif
+}
+
 // 8 consecutive elements m[row][kb .. kb + 8) of a packed matrix with r columns
 // (payload, wire gradient), zeros at columns >= r; r % 4 == 0, so a lane gets 8,
 // 4 or 0 of them.  `row_off` is the row's byte offset in the descriptor (or kOOB).
@@ -777,7 +787,7 @@ __device__ __forceinline__ SFrag gh_tr(const GhTile<TS, RPS>& t, int row0, int c
   return f;
 }
 
-template <int KS, int NT, int CT, int CW, int TW, int PD, bool FUSED>
+template <int KS, int NT, int CT, int CW, int TW, bool SG, bool FUSED>
 __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int r, int RP, int silu,
                                                           const io_t* __restrict__ z, int64_t ld_z,
                                                           const float* __restrict__ W_e,
@@ -799,6 +809,7 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   constexpr int MAIN_LDS = 2 * GH_BYTES + 2 * GB_BYTES + EW * Z_BYTES;
   constexpr int RED_LDS = (TW - 1) * BC * (RPT + 4) * 4;
   constexpr int LDS = MAIN_LDS > RED_LDS ? MAIN_LDS : RED_LDS;
+  constexpr int STORES = SG ? ZQ * (kEs == 2 ? 1 : 2) : 2 * NH * (kEs == 2 ? 1 : W / 4);  // g_z stores per step
   __shared__ __attribute__((aligned(16))) char smem[LDS];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
@@ -840,6 +851,8 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
     float gb[NCH][4];
     float a[NCH][4];
   };
+  // Any memory operation that is never waited for; used to prime the wait counter.
+  const rsrc_t nowhere = make_rsrc(g_z, 0);
   auto load_gin = [&](Gin& g, int64_t t0) {
     const int64_t rows = min((int64_t)TS, t_end - t0);
     const rsrc_t gbr = make_rsrc(g_b + t0 * r, rows * r * kEs);
@@ -867,7 +880,7 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
         const int tt = q / (KP / 4), j0 = 4 * (q % (KP / 4));
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = silu ? g.gb[i][e] * act_dphi(g.a[i][e], 1) : g.gb[i][e];
+        for (int e = 0; e < 4; ++e) v[e] = silu ? g.gb[i][e] * silu_grad(g.a[i][e]) : g.gb[i][e];
         gh_put4(s_gh[buf], tt, j0, v);
         if constexpr (FUSED) {
           if (j0 < RPT)
@@ -888,24 +901,40 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
     }
   };
 
+  // One block step.  zz and gin hold this step's z tile and g_h inputs and are
+  // reloaded with those of the step after next.
   auto body = [&](int64_t s, XFrag (&zz)[ZQ], Gin& gin) {
     const int buf = (int)(s & 1);
     const int64_t t0 = t_begin + s * TS;
     const int64_t t0w = t0 + 32 * tw;
     put_gh(gin, buf);
-    load_gin(gin, t0 + TS);
-    wave_lds_fence();  // the previous step's transposed reads of s_z are complete
+    load_gin(gin, t0 + 2 * TS);
+    wave_lds_fence();  // the previous step's reads of s_z are complete
 #pragma unroll
     for (int q = 0; q < ZQ; ++q) {
       const int idx = l + 64 * q;
       tile_put8<WC>(s_z, idx / (WC / 8), 8 * (idx % (WC / 8)), zz[q]);
     }
-    load_z(zz, t0w + PD * TS);
+    load_z(zz, t0w + 2 * TS);
     __syncthreads();  // g_h of this step is complete; the buffer written next step is free
+
+    // dW_e: D[j][c] = sum_t g_h[t][j] z[t][c], A = g_h^T, B = z^T
+    {
+      XFrag zb[CT];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) zb[ct] = tr_frag<WC>(s_z, 16 * ct, row16, grp);
+#pragma unroll
+      for (int jt = 0; jt < NT; ++jt) {
+        const SFrag g = gh_tr(s_gh[buf], 32 * tw, 16 * jt, row16, grp);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) dw[ct][jt] = mma_sx(g, zb[ct], dw[ct][jt]);
+      }
+    }
 
     // g_z for the two 16-token halves: D[c][t] = sum_j W_e[c][j] g_h[t][j]
     const int64_t rows = min((int64_t)32, t_end - t0w);
     const rsrc_t gzr = make_rsrc(g_z + t0w * ld_gz, rows_bytes(rows, n, ld_gz, kEs));
+    if constexpr (SG) wave_lds_fence();  // the transposed reads of s_z above are complete
 #pragma unroll
     for (int th = 0; th < 2; ++th) {
       f32x4 acc[CT];
@@ -925,42 +954,57 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
         for (int q = 0; q < W / 4; ++q)
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[4 * q + e] = acc[2 * h + q][e];
-        const int cc = wc0 + 32 * h + W * grp;
+        const int cc = 32 * h + W * grp;  // column within the wave's slice
         if constexpr (FUSED) {
           if (wc0 < r) {
 #pragma unroll
             for (int e = 0; e < W; ++e)
-              if (cc + e < r) v[e] += s_gb[buf][32 * tw + tt][cc + e];
+              if (wc0 + cc + e < r) v[e] += s_gb[buf][32 * tw + tt][wc0 + cc + e];
           }
         }
-        bst_n<W>(gzr, on ? (uint32_t)((tt * ld_gz + cc) * kEs) : kOOB, v);
+        if constexpr (SG) {
+          // round into the wave's tile; written out row by row below
+          io_t o[W];
+#pragma unroll
+          for (int e = 0; e < W; ++e) o[e] = f32_to_io(v[e]);
+          io_t* d = s_z + tt * WC + tile_col<WC>(tt, cc);
+#pragma unroll
+          for (int e = 0; e < W; ++e) d[e] = o[e];
+        } else {
+          bst_n<W>(gzr, on ? (uint32_t)((tt * ld_gz + wc0 + cc) * kEs) : kOOB, v);
+        }
       }
     }
-
-    // dW_e: D[j][c] = sum_t g_h[t][j] z[t][c], A = g_h^T, B = z^T
-    XFrag zb[CT];
+    if constexpr (SG) {
+      wave_lds_fence();
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) zb[ct] = tr_frag<WC>(s_z, 16 * ct, row16, grp);
-#pragma unroll
-    for (int jt = 0; jt < NT; ++jt) {
-      const SFrag g = gh_tr(s_gh[buf], 32 * tw, 16 * jt, row16, grp);
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) dw[ct][jt] = mma_sx(g, zb[ct], dw[ct][jt]);
+      for (int q = 0; q < ZQ; ++q) {
+        const int idx = l + 64 * q;
+        const int tt = idx / (WC / 8), c8 = 8 * (idx % (WC / 8));
+        const io_t* src = s_z + tt * WC + tile_col<WC>(tt, c8);
+        bst_x8(gzr, on ? (uint32_t)((tt * ld_gz + wc0 + c8) * kEs) : kOOB, src);
+      }
     }
   };
 
+  // The z tiles and g_h inputs of two steps are in flight at all times.  The
+  // compiler places the waits of the loop from the memory operations it sees in
+  // flight when the loop is entered, so the prologue issues as many as one
+  // iteration leaves behind (the stores of two steps go nowhere).
   const int64_t nsb = (t_end - t_begin + TS - 1) / TS;
-  Gin gin;
+  Gin ga, gb;
   XFrag z0[ZQ], z1[ZQ];
-  load_gin(gin, t_begin);
+  load_gin(ga, t_begin);
   load_z(z0, t_begin + 32 * tw);
-  if constexpr (PD == 2) load_z(z1, t_begin + TS + 32 * tw);
+#pragma unroll
+  for (int q = 0; q < STORES + 8; ++q) bst16(nowhere, kOOB - 16 * q, make_uint4(0, 0, 0, 0));
+  load_gin(gb, t_begin + TS);
+  load_z(z1, t_begin + TS + 32 * tw);
+#pragma unroll
+  for (int q = 0; q < STORES + 8; ++q) bst16(nowhere, kOOB - 16 * q, make_uint4(0, 0, 0, 0));
   for (int64_t s = 0; s < nsb; s += 2) {
-    body(s, z0, gin);
-    if (s + 1 < nsb) {
-      if constexpr (PD == 2) body(s + 1, z1, gin);
-      else body(s + 1, z0, gin);
-    }
+    body(s, z0, ga);
+    if (s + 1 < nsb) body(s + 1, z1, gb);
   }
 
   // dw[ct][jt][v] = partial dW_e[wc0 + 16 ct + row16][16 jt + 4 grp + v]
@@ -1104,14 +1148,15 @@ template <int NT>
 void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const float* W_e, const float* a_save,
                     const io_t* g_b, io_t* g_z, int64_t ld_gz, int fused, float* dwp, hipStream_t st) {
   constexpr int KS = (NT + 1) / 2;
-  constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS), PD = eb_pd(KS);
+  constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS);
+  constexpr bool SG = eb_sg(KS);
   dim3 grid(p.eb_ncb, p.eb_ntg);
   const int silu = act == RESBM_ACT_SILU;
   if (fused)
-    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, PD, true>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
+    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, SG, true>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
                        p.RP, silu, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, dwp, p.eb_TB);
   else
-    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, PD, false>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
+    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, SG, false>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
                        p.RP, silu, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, dwp, p.eb_TB);
 }
 

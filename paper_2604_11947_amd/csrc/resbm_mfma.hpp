@@ -206,4 +206,11 @@ __device__ __forceinline__ float act_dphi(float a, int act) {
   return s * (1.0f + a * (1.0f - s));
 }
 
+// SiLU'(a) = s (1 + a (1 - s)), s = 1 / (1 + e^-a), with a hardware reciprocal
+// (1 ulp) in place of the division.
+__device__ __forceinline__ float silu_grad(float a) {
+  const float s = __builtin_amdgcn_rcpf(1.0f + expf(-a));
+  return s * (1.0f + a * (1.0f - s));
+}
+
 }  // namespace resbm

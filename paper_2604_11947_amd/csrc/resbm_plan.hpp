@@ -38,12 +38,15 @@ constexpr int kDbWC = 64;
 constexpr int db_jt(int NT) { return NT < 4 ? NT : 4; }
 
 // ---- encode_bwd: blocks of CW x TW waves; a wave owns 16*CT columns, a block
-// step covers 32*TW tokens; PD block steps of z are in flight per wave.
+// step covers 32*TW tokens; SG: g_z leaves through LDS in whole row segments.
 // Workspace: the dW_e partials of the token groups.
 constexpr int eb_ct(int KS) { return KS <= 1 ? 4 : (KS <= 2 ? 2 : 1); }
 constexpr int eb_cw(int) { return 4; }
 constexpr int eb_tw(int KS) { return KS <= 2 ? 2 : 1; }
-constexpr int eb_pd(int KS) { return KS <= 2 ? 2 : 1; }
+#ifndef RESBM_EB_STAGE_GZ
+#define RESBM_EB_STAGE_GZ 1
+#endif
+constexpr bool eb_sg(int) { return RESBM_EB_STAGE_GZ != 0; }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
