@@ -133,6 +133,19 @@ __device__ __forceinline__ void bst_x8(rsrc_t r, uint32_t off, const io_t* src) 
 #endif
 }
 
+// Stores the 8 elements of an exact fragment at byte offset off.
+__device__ __forceinline__ void bst_frag(rsrc_t r, uint32_t off, const XFrag& f) {
+#if RESBM_IO_F32_BUILD
+  bst16(r, off, make_uint4(__builtin_bit_cast(uint32_t, f.v[0]), __builtin_bit_cast(uint32_t, f.v[1]),
+                           __builtin_bit_cast(uint32_t, f.v[2]), __builtin_bit_cast(uint32_t, f.v[3])));
+  bst16(r, off == kOOB ? kOOB : off + 16,
+        make_uint4(__builtin_bit_cast(uint32_t, f.v[4]), __builtin_bit_cast(uint32_t, f.v[5]),
+                   __builtin_bit_cast(uint32_t, f.v[6]), __builtin_bit_cast(uint32_t, f.v[7])));
+#else
+  bst16(r, off, __builtin_bit_cast(uint4, f.v));
+#endif
+}
+
 // 8 consecutive elements m[row][kb .. kb + 8) of a packed matrix with r columns
 // (payload, wire gradient), zeros at columns >= r; r % 4 == 0, so a lane gets 8,
 // 4 or 0 of them.  `row_off` is the row's byte offset in the descriptor (or kOOB).
@@ -156,18 +169,18 @@ __device__ __forceinline__ XFrag bld_r8(rsrc_t m, uint32_t row_off, int r, int k
 
 // Split (weight-like) fragment f of a fragment-ordered buffer: per fragment and
 // lane 2 x 16 bytes (hi, lo bf16 in the bf16 build; 8 floats in the f32 build).
-__device__ __forceinline__ SFrag bld_sfrag(rsrc_t r, int64_t f, int l) {
+__device__ __forceinline__ SFrag bld_sfrag(rsrc_t r, int64_t f, int l, bool ok = true) {
   SFrag s;
 #if RESBM_IO_F32_BUILD
-  const uint32_t o = (uint32_t)((f * 64 + l) * 32);
-  const uint4 a = bld16(r, o), b = bld16(r, o + 16);
+  const uint32_t o = ok ? (uint32_t)((f * 64 + l) * 32) : kOOB;
+  const uint4 a = bld16(r, o), b = bld16(r, ok ? o + 16 : kOOB);
   s.v[0] = __builtin_bit_cast(float, a.x); s.v[1] = __builtin_bit_cast(float, a.y);
   s.v[2] = __builtin_bit_cast(float, a.z); s.v[3] = __builtin_bit_cast(float, a.w);
   s.v[4] = __builtin_bit_cast(float, b.x); s.v[5] = __builtin_bit_cast(float, b.y);
   s.v[6] = __builtin_bit_cast(float, b.z); s.v[7] = __builtin_bit_cast(float, b.w);
 #else
-  s.hi = __builtin_bit_cast(bf16x8, bld16(r, (uint32_t)(((f * 2 + 0) * 64 + l) * 16)));
-  s.lo = __builtin_bit_cast(bf16x8, bld16(r, (uint32_t)(((f * 2 + 1) * 64 + l) * 16)));
+  s.hi = __builtin_bit_cast(bf16x8, bld16(r, ok ? (uint32_t)(((f * 2 + 0) * 64 + l) * 16) : kOOB));
+  s.lo = __builtin_bit_cast(bf16x8, bld16(r, ok ? (uint32_t)(((f * 2 + 1) * 64 + l) * 16) : kOOB));
 #endif
   return s;
 }
@@ -195,15 +208,49 @@ __device__ __forceinline__ void wave_lds_fence() { asm volatile("s_waitcnt lgkmc
 // Index of this wave in its block, as a wave-uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-// Column permutation of a 32-row x WC-column token tile staged in LDS: rows 8
-// apart (read together by the transposed fragment loads) land on different
-// banks.  The XOR only flips column bits inside whole 32- or 64-column blocks,
-// so 8-element chunks stay contiguous and a column never leaves its row.
+// The value v, opaque to the optimizer.  Used for the first index of the
+// streaming loops, which start before their range on zeroed registers: the
+// compiler then cannot peel the first iterations off the loop, which would
+// leave it fewer memory operations in flight at the loop entry than the loop
+// itself keeps, and so make it wait too early inside the loop.  32-bit on
+// purpose: this toolchain encodes a negative 64-bit constant moved into a scalar
+// register pair as a 32-bit literal, which the hardware zero-extends.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
+// Column permutation of a row-major tile with WC elements per row staged in
+// LDS.  The 8-element chunks of a row are permuted by an XOR with the row's
+// index among the rows that share a 256-byte bank window (16 / (WC / 8) rows in
+// the bf16 build), so that a wave touches distinct banks both when it copies
+// whole rows (8 lanes per 128 bytes, the layout of coalesced global accesses)
+// and when it reads one chunk from each of 16 rows (matrix-core fragments).
+// Chunks stay contiguous and never leave their row; WC whose chunk count is not
+// a power of two up to 8 is left as is.
 template <int WC>
 __device__ __forceinline__ int tile_col(int row, int col) {
-  if constexpr (WC % 64 == 0) return col ^ (((row >> 3) & 3) << 4);
-  else if constexpr (WC % 32 == 0) return col ^ (((row >> 3) & 1) << 4);
-  else return col;
+  constexpr int CPR = WC / 8;
+  if constexpr (CPR == 8 || CPR == 4 || CPR == 2) {
+    constexpr int RPW = 16 / CPR;
+    return ((((col >> 3) ^ (row / RPW)) & (CPR - 1)) << 3) | (col & 7);
+  } else {
+    return col;
+  }
+}
+
+// Loads 8 consecutive elements at (row, col) of a WC-wide tile (col % 8 == 0).
+template <int WC>
+__device__ __forceinline__ XFrag tile_get8(const io_t* tile, int row, int col) {
+  const io_t* p = tile + row * WC + tile_col<WC>(row, col);
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w; f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+#else
+  f.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+#endif
+  return f;
 }
 
 // Stores 8 consecutive elements at (row, col) of a WC-wide tile (col % 8 == 0).
@@ -296,20 +343,28 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
   constexpr int NW = PW ? NT : 1;
   constexpr int TOK = 16 * MT;
   constexpr int RPT = 16 * NT;
-  __shared__ __attribute__((aligned(16))) float s_red[KW][TOK][RPT + 4];
+  constexpr int SC = 32 * U;            // z columns per stage
+  constexpr int CPR = SC / 8;           // 8-element chunks per tile row
+  constexpr int NQ = TOK * CPR / 64;    // coalesced loads per lane per stage
+  constexpr int TILE = TOK * SC * (int)sizeof(io_t);
+  constexpr int RED = KW * TOK * (RPT + 4) * 4;
+  __shared__ __attribute__((aligned(16))) char smem[KW * TILE > RED ? KW * TILE : RED];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   const int64_t tok0 = (int64_t)blockIdx.x * TOK;
   const int nks = n / 32;
   const int ks0 = wave * nks / KW;
   const int ks1 = (wave + 1) * nks / KW;
+  io_t* s_z = reinterpret_cast<io_t*>(smem + wave * TILE);
 
   // rows at or beyond T fall outside the descriptor (ld >= n)
   const rsrc_t zr = make_rsrc(z + tok0 * ld_z, rows_bytes(min((int64_t)TOK, T - tok0), n, ld_z, kEs));
   const rsrc_t wr = make_rsrc(wf, (int64_t)nks * NT * kSFragBytes);
-  uint32_t zoff[MT];
+  // coalesced z loads: load q of a stage covers tile rows [q 64 / CPR, ...), CPR lanes per row
+  const int zch = l % CPR;
+  uint32_t zoff[NQ];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) zoff[mt] = (uint32_t)(((16 * mt + row16) * ld_z + 8 * grp) * kEs);
+  for (int q = 0; q < NQ; ++q) zoff[q] = (uint32_t)(((q * (64 / CPR) + l / CPR) * ld_z + 8 * zch) * kEs);
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -317,42 +372,64 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  XFrag za[U][MT], zb[U][MT];
+  // A stage is U k-steps (SC columns of z for the block's TOK tokens).  Stages
+  // outside [ks0, ks1) load zeros and add nothing.
+  XFrag za[NQ], zb[NQ];
   SFrag wa[U][NW], wb[U][NW];
-  auto load = [&](XFrag (&zz)[U][MT], SFrag (&ww)[U][NW], int ks) {
+  auto load = [&](XFrag (&zz)[NQ], SFrag (&ww)[U][NW], int ks) {
+    const int kz = ks + zch * 8 / 32;  // k-step of this lane's chunk
+    const bool zok = kz >= ks0 && kz < ks1;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = ks + u;  // k >= ks1 is loaded (in range or zero) but never used
+    for (int q = 0; q < NQ; ++q) zz[q] = bld_x8(zr, zok ? zoff[q] + (uint32_t)(ks * 32 * kEs) : kOOB);
+    if constexpr (PW) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) zz[u][mt] = bld_x8(zr, zoff[mt] + (uint32_t)(k * 32 * kEs));
-      if constexpr (PW) {
+      for (int u = 0; u < U; ++u) {
+        const int k = ks + u;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) ww[u][nt] = bld_sfrag(wr, (int64_t)k * NT + nt, l);
+        for (int nt = 0; nt < NT; ++nt) ww[u][nt] = bld_sfrag(wr, (int64_t)k * NT + nt, l, k >= ks0 && k < ks1);
       }
     }
   };
-  auto compute = [&](const XFrag (&zz)[U][MT], const SFrag (&ww)[U][NW], int ks) {
+  // stage the tile in the wave's LDS, read it back in fragment order
+  auto compute = [&](const XFrag (&zz)[NQ], const SFrag (&ww)[U][NW], int ks) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) tile_put8<SC>(s_z, q * (64 / CPR) + l / CPR, 8 * zch, zz[q]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (ks + u >= ks1) break;
+      const int k = ks + u;
+      XFrag f[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) f[mt] = tile_get8<SC>(s_z, 16 * mt + row16, 32 * u + 8 * grp);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         SFrag w;
         if constexpr (PW) w = ww[u][nt];
-        else w = bld_sfrag(wr, (int64_t)(ks + u) * NT + nt, l);
+        else w = bld_sfrag(wr, (int64_t)k * NT + nt, l, k >= ks0 && k < ks1);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, zz[u][mt], acc[mt][nt]);
+        for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, f[mt], acc[mt][nt]);
       }
     }
   };
 
-  load(za, wa, ks0);
-  for (int ks = ks0; ks < ks1; ks += 2 * U) {
-    load(zb, wb, ks + U);
+  // Every memory operation sits in one unconditional loop body (the loop starts
+  // two stages early on zeroed registers instead of after a prologue of loads),
+  // which lets the compiler place each wait at its exact distance.
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) za[q] = zb[q] = xfrag_zero();
+  if constexpr (PW) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) wa[u][nt] = wb[u][nt] = sfrag_zero();
+  }
+  for (int ks = opaque(ks0 - 2 * U); ks < ks1; ks += 2 * U) {
     compute(za, wa, ks);
     load(za, wa, ks + 2 * U);
     compute(zb, wb, ks + U);
+    load(zb, wb, ks + 3 * U);
   }
+  __syncthreads();  // the reduction area overlaps the tiles
+  float (*s_red)[TOK][RPT + 4] = reinterpret_cast<float (*)[TOK][RPT + 4]>(smem);
 
   // acc[mt][nt][v] = partial a[tok0 + 16 mt + row16][16 nt + 4 grp + v]
 #pragma unroll
@@ -396,7 +473,12 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
   constexpr int W = CT >= 2 ? 8 : 4;      // consecutive columns per lane run
   constexpr int NH = CT >= 2 ? CT / 2 : 1;  // runs per lane
   constexpr int NI = ADD ? NH * W / 4 : 1;  // 4-column identity chunks per lane
+  constexpr int WC = 16 * CT;               // columns of the wave
+  constexpr int CPR = WC / 8;               // 8-element chunks per output row
+  constexpr int NS = (16 * CPR + 63) / 64;  // coalesced stores per lane per tile
+  __shared__ __attribute__((aligned(16))) io_t s_out[4][16 * WC];
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+  io_t* tile = s_out[wave];
   const int strip = blockIdx.x * 4 + wave;
   const int c0 = strip * 16 * CT;
   if (c0 >= n) return;  // whole strips only: n % 64 == 0 and 16 CT divides 64
@@ -424,7 +506,11 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
 
   struct Tile {
     XFrag p[KS];
-    float id[NI][4];  // reading A: b[t][column chunk] below r, zeros elsewhere
+#if RESBM_IO_F32_BUILD
+    uint4 id[NI];  // reading A: b[t][column chunk] below r, zeros elsewhere (raw bits)
+#else
+    uint2 id[NI];
+#endif
   };
   auto load = [&](Tile& x, int64_t tt) {  // tt: tile start relative to t_begin
     const int64_t t = tt + row16;
@@ -435,7 +521,12 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int cb = cl + 32 * (i / (W / 4)) + 4 * (i % (W / 4));
-        bld_x4(br, cb < r ? (uint32_t)((t * r + cb) * kEs) : kOOB, x.id[i]);
+        const uint32_t o = cb < r ? (uint32_t)((t * r + cb) * kEs) : kOOB;
+#if RESBM_IO_F32_BUILD
+        x.id[i] = bld16(br, o);
+#else
+        x.id[i] = bld8(br, o);
+#endif
       }
     }
   };
@@ -452,23 +543,55 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
     for (int h = 0; h < NH; ++h) {
       float v[W];
 #pragma unroll
-      for (int q = 0; q < W / 4; ++q)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[4 * q + e] = acc[2 * h + q][e];
-          if constexpr (ADD) v[4 * q + e] += x.id[h * (W / 4) + q][e];
+      for (int q = 0; q < W / 4; ++q) {
+        float id[4] = {0.f, 0.f, 0.f, 0.f};  // reading A
+        if constexpr (ADD) {
+          const auto u = x.id[h * (W / 4) + q];
+#if RESBM_IO_F32_BUILD
+          id[0] = __builtin_bit_cast(float, u.x); id[1] = __builtin_bit_cast(float, u.y);
+          id[2] = __builtin_bit_cast(float, u.z); id[3] = __builtin_bit_cast(float, u.w);
+#else
+          id[0] = bf16_bits_to_f32(u.x & 0xffffu); id[1] = bf16_bits_to_f32(u.x >> 16);
+          id[2] = bf16_bits_to_f32(u.y & 0xffffu); id[3] = bf16_bits_to_f32(u.y >> 16);
+#endif
         }
-      bst_n<W>(zr, (uint32_t)((t * ld_zt + cl + 32 * h) * kEs), v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[4 * q + e] = ADD ? acc[2 * h + q][e] + id[e] : acc[2 * h + q][e];
+      }
+      // round into the wave's tile (row = token)
+      io_t* d = tile + row16 * WC + tile_col<WC>(row16, cl - c0 + 32 * h);
+#pragma unroll
+      for (int e = 0; e < W; ++e) d[e] = f32_to_io(v[e]);
+    }
+    // write the tile out row by row, 8 lanes per 128 bytes
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+      const int idx = l + 64 * q;
+      const int row = idx / CPR, c8 = 8 * (idx % CPR);
+      const XFrag o = tile_get8<WC>(tile, row < 16 ? row : 0, c8);
+      bst_frag(zr, (tt < 0 || row >= 16) ? kOOB : (uint32_t)(((tt + row) * ld_zt + c0 + c8) * kEs), o);
     }
   };
 
+  // Every memory operation sits in one unconditional loop body: the loop starts
+  // two (empty) tiles early on zeroed registers instead of after a prologue of
+  // loads, so the compiler can place each wait at its exact distance.
   Tile xa, xb;
-  load(xa, 0);
-  for (int64_t tt = 0; tt < rows; tt += 32) {
-    load(xb, tt + 16);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) xa.p[ks] = xb.p[ks] = xfrag_zero();
+  if constexpr (ADD) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) xa.id[i] = xb.id[i] = {};
+  }
+  // (the scheduling barriers keep the compiler from hoisting a tile's math
+  // above the loads issued before it, which would wait for those loads)
+  for (int64_t tt = opaque(-32); tt < rows; tt += 32) {
     compute(xa, tt);
     load(xa, tt + 32);
+    __builtin_amdgcn_sched_barrier(0);
     compute(xb, tt + 16);  // past the range: loads were zeros, stores are dropped
+    load(xb, tt + 48);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -477,11 +600,12 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
 // and j-tiles [16 jt0, 16 (jt0 + JT)) of r:
 //   gbp[cg][t][j] = sum over the block's columns of g_z~[t][c] W_d[j][c]
 //   dwp[tg][j][c] = sum over the block's tokens of b[t][j] g_z~[t][c]
-// Per 32-token step: each wave takes its 64 columns of g_z~ into registers (one
-// step ahead), forms its g_b partial with W_d held in registers, stages the tile
-// in its own LDS and reads it back transposed for dW_d; the step's payload rows
-// are staged once per block (double-buffered) and read transposed too.  The 8
-// waves' g_b partials meet in LDS behind the one barrier of the step.
+// Per 32-token step: each wave loads its 64 columns of g_z~ (two steps ahead,
+// 8 lanes per 128-byte row), stages the tile in its own LDS, reads it back in
+// fragment order for its g_b partial (W_d held in registers) and transposed
+// for dW_d; the step's payload rows are staged once per block (double-buffered)
+// and read transposed too.  The 8 waves' g_b partials meet in LDS behind the
+// one barrier of the step.
 template <int JT>
 __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int r, int RP,
                                                            const io_t* __restrict__ b,
@@ -535,47 +659,52 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
   // payload rows of one step: threads [0, 32 BQ) each carry one 16-byte chunk
   const bool bthr = threadIdx.x < 32 * BQ;
   const int btt = bthr ? threadIdx.x / BQ : 0, bch = threadIdx.x % BQ;
-  const uint32_t gz_lane = (uint32_t)((row16 * ld_g + wc0 + 8 * grp) * kEs);
+  // coalesced g_z~ loads: load q covers rows [8 q, 8 q + 8) of the step, 8 lanes per 128-byte row
+  const uint32_t gz_lane = (uint32_t)(((l >> 3) * ld_g + wc0 + 8 * (l & 7)) * kEs);
 
+  // Registers of step s: its g_z~ tile and the payload rows of step s + 1.
+  // Steps before 0 or past the range read zeros and store nothing.
   struct Step {
-    XFrag gz[2][KSW];
+    XFrag gz[4];
     XFrag bp;
   };
-  // loads of the step at t0 (rows beyond t_end read as zeros)
-  auto load = [&](Step& s, int64_t t0) {
-    const int64_t rows = t_end - t0;
-    const rsrc_t gr = make_rsrc(g_zt + t0 * ld_g, won ? rows_bytes(min((int64_t)32, rows), n, ld_g, kEs) : 0);
+  auto load = [&](Step& st, int64_t s) {
+    const int64_t t0 = t_begin + 32 * s;
+    const int64_t rows = s < 0 ? 0 : min((int64_t)32, t_end - t0);
+    const rsrc_t gr = make_rsrc(g_zt + t0 * ld_g, won ? rows_bytes(rows, n, ld_g, kEs) : 0);
 #pragma unroll
-    for (int th = 0; th < 2; ++th)
-#pragma unroll
-      for (int ks = 0; ks < KSW; ++ks)
-        s.gz[th][ks] = bld_x8(gr, gz_lane + (uint32_t)((16 * th * ld_g + 32 * ks) * kEs));
-    const rsrc_t br = make_rsrc(b + t0 * r, min((int64_t)32, rows) * r * kEs);
-    s.bp = bld_r8(br, bthr ? (uint32_t)(btt * r * kEs) : kOOB, r, 16 * jt0 + 8 * bch);
+    for (int q = 0; q < 4; ++q) st.gz[q] = bld_x8(gr, gz_lane + (uint32_t)(8 * q * ld_g * kEs));
+    const int64_t rows1 = s + 1 < 0 ? 0 : min((int64_t)32, t_end - t0 - 32);
+    const rsrc_t br = make_rsrc(b + (t0 + 32) * r, rows1 > 0 ? rows1 * r * kEs : 0);
+    st.bp = bld_r8(br, bthr ? (uint32_t)(btt * r * kEs) : kOOB, r, 16 * jt0 + 8 * bch);
   };
 
-  // one step: math on `cur` (its payload rows already in s_b[bbuf]); the payload
-  // rows of the next step (`nxt`) go to the other buffer before the barrier
-  auto step = [&](const Step& cur, const Step& nxt, int64_t t0, int gbuf, int bbuf) {
-    // g_b partial over this wave's 64 columns: D[j][t]
+  // One 32-token step; `st` is reloaded with the registers of step s + 2.
+  auto body = [&](Step& st, int64_t s) {
+    const int gbuf = NBUF == 2 ? (int)(s & 1) : 0;
+    const int bbuf = (int)(s & 1);
+    // stage the wave's tile row-major; the next step's payload rows go to the
+    // other buffer, last read before the previous barrier
+    wave_lds_fence();  // the previous step's reads of s_gz are complete
 #pragma unroll
-    for (int th = 0; th < 2; ++th)
+    for (int q = 0; q < 4; ++q) tile_put8<kDbWC>(s_gz[wave], 8 * q + (l >> 3), 8 * (l & 7), st.gz[q]);
+    if (bthr) tile_put8<JW>(s_b[bbuf ^ 1], btt, 8 * bch, st.bp);
+    load(st, s + 2);
+    // g_b partial over this wave's 64 columns: D[j][t], B = g_z~ rows in fragment order
+#pragma unroll
+    for (int th = 0; th < 2; ++th) {
+      XFrag f[KSW];
+#pragma unroll
+      for (int ks = 0; ks < KSW; ++ks) f[ks] = tile_get8<kDbWC>(s_gz[wave], 16 * th + row16, 32 * ks + 8 * grp);
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KSW; ++ks) acc = mma_sx(wdf[jt][ks], cur.gz[th][ks], acc);
+        for (int ks = 0; ks < KSW; ++ks) acc = mma_sx(wdf[jt][ks], f[ks], acc);
         *reinterpret_cast<float4*>(&s_gb[gbuf][wave][16 * th + row16][16 * jt + 4 * grp]) =
             make_float4(acc[0], acc[1], acc[2], acc[3]);
       }
-    // stage the wave's tile row-major, read it back transposed for dW_d
-    wave_lds_fence();
-#pragma unroll
-    for (int th = 0; th < 2; ++th)
-#pragma unroll
-      for (int ks = 0; ks < KSW; ++ks)
-        tile_put8<kDbWC>(s_gz[wave], 16 * th + row16, 32 * ks + 8 * grp, cur.gz[th][ks]);
-    wave_lds_fence();
+    }
     // dW_d: D[c][j] = sum_t g_z~[t][c] b[t][j], A = g_z~^T, B = b^T (both transposed from LDS)
     XFrag bt[JT];
 #pragma unroll
@@ -586,35 +715,37 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) dw[ct][jt] = mma_xx(a, bt[jt], dw[ct][jt]);
     }
-    if (bthr) tile_put8<JW>(s_b[bbuf ^ 1], btt, 8 * bch, nxt.bp);  // last read before the previous barrier
 
     __syncthreads();  // s_gb[gbuf] and s_b[bbuf ^ 1] complete
     // sum the 8 waves' g_b partials in wave order; rows past t_end are dropped by the descriptor
-    const rsrc_t pr = make_rsrc(gbp + ((int64_t)cg * T + t0) * RP, (t_end - t0) * RP * 4);
-    for (int idx = threadIdx.x; idx < 32 * JW; idx += kDbWaves * 64) {
+    const int64_t t0 = t_begin + 32 * s;
+    const rsrc_t pr = make_rsrc(gbp + ((int64_t)cg * T + t0) * RP, s < 0 ? 0 : (t_end - t0) * RP * 4);
+#pragma unroll
+    for (int idx0 = 0; idx0 < 32 * JW; idx0 += kDbWaves * 64) {
+      const int idx = idx0 + threadIdx.x;
       const int tt = idx / JW, jj = idx % JW;
       const int j = 16 * jt0 + jj;
-      float s = 0.0f;
+      float v = 0.0f;
 #pragma unroll
-      for (int w = 0; w < kDbWaves; ++w) s += s_gb[gbuf][w][tt][jj];
-      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, s), pr,
+      for (int w = 0; w < kDbWaves; ++w) v += s_gb[gbuf][w][tt][jj];
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), pr,
                                             j < r ? (uint32_t)((tt * RP + j) * 4) : kOOB, 0, 0);
     }
     if constexpr (NBUF == 1) __syncthreads();  // the single buffer is refilled next step
   };
 
+  // Every memory operation sits in one unconditional loop body: the loop starts
+  // three (empty) steps early on zeroed registers instead of after a prologue of
+  // loads, so the compiler can place each wait at its exact distance.  Step -1
+  // stages the payload rows of step 0.
+  const int64_t nsteps = (t_end - t_begin + 31) / 32;
   Step sa, sb;
-  load(sa, t_begin);
-  if (bthr) tile_put8<JW>(s_b[0], btt, 8 * bch, sa.bp);
-  __syncthreads();
-  int gbuf = 0;
-  for (int64_t t0 = t_begin; t0 < t_end; t0 += 64) {
-    load(sb, t0 + 32);
-    step(sa, sb, t0, gbuf, 0);
-    gbuf = (gbuf + 1) % NBUF;
-    load(sa, t0 + 64);
-    step(sb, sa, t0 + 32, gbuf, 1);  // past t_end: zeros in, nothing out
-    gbuf = (gbuf + 1) % NBUF;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) sa.gz[q] = sb.gz[q] = xfrag_zero();
+  sa.bp = sb.bp = xfrag_zero();
+  for (int64_t s = opaque(-3); s < nsteps; s += 2) {
+    body(sb, s);      // odd steps
+    body(sa, s + 1);  // even steps
   }
 
   // dw[ct][jt][v] = dW_d partial [16 (jt0 + jt) + row16][wc0 + 16 ct + 4 grp + v]
@@ -847,12 +978,16 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
 
   // g_h inputs of one block step: chunk q = threadIdx + i NTH covers token q / (KP / 4),
   // columns 4 (q % (KP / 4)) .. + 3 (zeros at or beyond r and past the token range).
+  // Raw loaded bits: converting at load time would make the compiler wait for
+  // the load right where it is issued.
   struct Gin {
-    float gb[NCH][4];
-    float a[NCH][4];
+#if RESBM_IO_F32_BUILD
+    uint4 gb[NCH];
+#else
+    uint2 gb[NCH];
+#endif
+    uint4 a[NCH];
   };
-  // Any memory operation that is never waited for; used to prime the wait counter.
-  const rsrc_t nowhere = make_rsrc(g_z, 0);
   auto load_gin = [&](Gin& g, int64_t t0) {
     const int64_t rows = min((int64_t)TS, t_end - t0);
     const rsrc_t gbr = make_rsrc(g_b + t0 * r, rows * r * kEs);
@@ -862,14 +997,12 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
       const int q = threadIdx.x + i * NTH;
       const int tt = q / (KP / 4), j0 = 4 * (q % (KP / 4));
       const bool ok = q < GQ && j0 < r;
-      bld_x4(gbr, ok ? (uint32_t)((tt * r + j0) * kEs) : kOOB, g.gb[i]);
-      if (silu) {
-        const uint4 v = bld16(ar, ok ? (uint32_t)((tt * r + j0) * 4) : kOOB);
-        g.a[i][0] = __builtin_bit_cast(float, v.x);
-        g.a[i][1] = __builtin_bit_cast(float, v.y);
-        g.a[i][2] = __builtin_bit_cast(float, v.z);
-        g.a[i][3] = __builtin_bit_cast(float, v.w);
-      }
+#if RESBM_IO_F32_BUILD
+      g.gb[i] = bld16(gbr, ok ? (uint32_t)((tt * r + j0) * kEs) : kOOB);
+#else
+      g.gb[i] = bld8(gbr, ok ? (uint32_t)((tt * r + j0) * kEs) : kOOB);
+#endif
+      g.a[i] = bld16(ar, ok ? (uint32_t)((tt * r + j0) * 4) : kOOB);  // zeros without SiLU
     }
   };
   auto put_gh = [&](const Gin& g, int buf) {
@@ -878,20 +1011,28 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
       const int q = threadIdx.x + i * NTH;
       if (GQ % NTH == 0 || q < GQ) {
         const int tt = q / (KP / 4), j0 = 4 * (q % (KP / 4));
-        float v[4];
+        float gbv[4], av[4], v[4];
+#if RESBM_IO_F32_BUILD
+        gbv[0] = __builtin_bit_cast(float, g.gb[i].x); gbv[1] = __builtin_bit_cast(float, g.gb[i].y);
+        gbv[2] = __builtin_bit_cast(float, g.gb[i].z); gbv[3] = __builtin_bit_cast(float, g.gb[i].w);
+#else
+        gbv[0] = bf16_bits_to_f32(g.gb[i].x & 0xffffu); gbv[1] = bf16_bits_to_f32(g.gb[i].x >> 16);
+        gbv[2] = bf16_bits_to_f32(g.gb[i].y & 0xffffu); gbv[3] = bf16_bits_to_f32(g.gb[i].y >> 16);
+#endif
+        av[0] = __builtin_bit_cast(float, g.a[i].x); av[1] = __builtin_bit_cast(float, g.a[i].y);
+        av[2] = __builtin_bit_cast(float, g.a[i].z); av[3] = __builtin_bit_cast(float, g.a[i].w);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = silu ? g.gb[i][e] * silu_grad(g.a[i][e]) : g.gb[i][e];
+        for (int e = 0; e < 4; ++e) v[e] = silu ? gbv[e] * silu_grad(av[e]) : gbv[e];
         gh_put4(s_gh[buf], tt, j0, v);
         if constexpr (FUSED) {
           if (j0 < RPT)
-            *reinterpret_cast<float4*>(&s_gb[buf][tt][j0]) = make_float4(g.gb[i][0], g.gb[i][1], g.gb[i][2],
-                                                                          g.gb[i][3]);
+            *reinterpret_cast<float4*>(&s_gb[buf][tt][j0]) = make_float4(gbv[0], gbv[1], gbv[2], gbv[3]);
         }
       }
     }
   };
   auto load_z = [&](XFrag (&zz)[ZQ], int64_t t0w) {
-    const int64_t rows = min((int64_t)32, t_end - t0w);
+    const int64_t rows = min((int64_t)32, t_end - t0w);  // <= 0 past the range: zeros
     const rsrc_t zr = make_rsrc(z + t0w * ld_z + wc0, on ? rows_bytes(rows, WC, ld_z, kEs) : 0);
 #pragma unroll
     for (int q = 0; q < ZQ; ++q) {
@@ -902,7 +1043,8 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   };
 
   // One block step.  zz and gin hold this step's z tile and g_h inputs and are
-  // reloaded with those of the step after next.
+  // reloaded with those of the step after next.  Steps outside [0, nsb) see
+  // zero inputs and store nothing.
   auto body = [&](int64_t s, XFrag (&zz)[ZQ], Gin& gin) {
     const int buf = (int)(s & 1);
     const int64_t t0 = t_begin + s * TS;
@@ -932,7 +1074,7 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
     }
 
     // g_z for the two 16-token halves: D[c][t] = sum_j W_e[c][j] g_h[t][j]
-    const int64_t rows = min((int64_t)32, t_end - t0w);
+    const int64_t rows = s < 0 ? 0 : min((int64_t)32, t_end - t0w);
     const rsrc_t gzr = make_rsrc(g_z + t0w * ld_gz, rows_bytes(rows, n, ld_gz, kEs));
     if constexpr (SG) wave_lds_fence();  // the transposed reads of s_z above are complete
 #pragma unroll
@@ -988,23 +1130,23 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   };
 
   // The z tiles and g_h inputs of two steps are in flight at all times.  The
-  // compiler places the waits of the loop from the memory operations it sees in
-  // flight when the loop is entered, so the prologue issues as many as one
-  // iteration leaves behind (the stores of two steps go nowhere).
+  // loop starts two (empty) steps early with zeroed registers instead of a
+  // prologue of loads, and runs an even number of steps, so that every memory
+  // operation sits inside one unconditional loop body and the compiler can
+  // place each wait at its exact distance.
   const int64_t nsb = (t_end - t_begin + TS - 1) / TS;
   Gin ga, gb;
   XFrag z0[ZQ], z1[ZQ];
-  load_gin(ga, t_begin);
-  load_z(z0, t_begin + 32 * tw);
 #pragma unroll
-  for (int q = 0; q < STORES + 8; ++q) bst16(nowhere, kOOB - 16 * q, make_uint4(0, 0, 0, 0));
-  load_gin(gb, t_begin + TS);
-  load_z(z1, t_begin + TS + 32 * tw);
+  for (int i = 0; i < NCH; ++i) {
+    ga.gb[i] = gb.gb[i] = {};
+    ga.a[i] = gb.a[i] = make_uint4(0, 0, 0, 0);
+  }
 #pragma unroll
-  for (int q = 0; q < STORES + 8; ++q) bst16(nowhere, kOOB - 16 * q, make_uint4(0, 0, 0, 0));
-  for (int64_t s = 0; s < nsb; s += 2) {
+  for (int q = 0; q < ZQ; ++q) z0[q] = z1[q] = xfrag_zero();
+  for (int64_t s = opaque(-2); s < nsb; s += 2) {
     body(s, z0, ga);
-    if (s + 1 < nsb) body(s + 1, z1, gb);
+    body(s + 1, z1, gb);
   }
 
   // dw[ct][jt][v] = partial dW_e[wc0 + 16 ct + row16][16 jt + 4 grp + v]
