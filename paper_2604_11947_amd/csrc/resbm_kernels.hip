@@ -296,6 +296,41 @@ __device__ __forceinline__ XFrag tr_frag(const io_t* tile, int c0, int row16, in
   return f;
 }
 
+// Column permutation of a block-wide row-major tile (WIDE elements per row, a
+// multiple of 128): the 8-element chunk index is XORed with the row's low four
+// bits, which keeps rows written whole (64 lanes x 16 bytes, the layout of
+// 1 KiB-contiguous global loads) conflict-free and spreads one chunk read from
+// 16 rows (matrix-core fragments) over all banks.
+__device__ __forceinline__ int wide_col(int row, int col) {
+  return ((((col >> 3) ^ row) & 15) | ((col >> 3) & ~15)) << 3 | (col & 7);
+}
+
+// Transposed fragment from a block-wide tile (see wide_col): lane (row16, grp)
+// receives tile[row0 + 8 grp + e][c0 + row16], e = 0..7 (addressed as tr_frag).
+template <int WIDE>
+__device__ __forceinline__ XFrag tr_frag_wide(const io_t* tile, int row0, int c0, int row16, int grp) {
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int row = row0 + 8 * grp + e;
+    f.v[e] = tile[row * WIDE + wide_col(row, c0 + row16)];
+  }
+#else
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  s16x4 h[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int row = row0 + 8 * grp + 4 * q + (row16 >> 2);
+    const io_t* p = tile + row * WIDE + wide_col(row, c0 + 4 * (row16 & 3));
+    h[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+  }
+  f.v = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){h[0][0], h[0][1], h[0][2], h[0][3],
+                                                                               h[1][0], h[1][1], h[1][2], h[1][3]});
+#endif
+  return f;
+}
+
 // Output-column permutation of the "expand" contractions (decode_fwd, the g_z
 // part of encode_bwd).  A wave's A operand covers 16*CT columns starting at c0;
 // row i of column tile ct stands for column
@@ -331,7 +366,7 @@ __global__ __launch_bounds__(256) void k_enc_fwd_prep(const float* __restrict__ 
   store_sfrag(wf, f, l, w);
 }
 
-// a = z W_e for 16*MT tokens per block; wave w takes k-steps [w nks / KW, (w+1) nks / KW).
+// a = z W_e for 16*MT tokens per block; the KW waves take interleaved stages of the n-contraction.
 template <int NT, int MT, int KW>
 __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, int act,
                                                      const io_t* __restrict__ x_attn, int64_t ld_x,
@@ -353,8 +388,7 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   const int64_t tok0 = (int64_t)blockIdx.x * TOK;
   const int nks = n / 32;
-  const int ks0 = wave * nks / KW;
-  const int ks1 = (wave + 1) * nks / KW;
+  const int nst = (nks + KW * U - 1) / (KW * U);  // stages; stage i of wave w: k-steps (i KW + w) U + u
   io_t* s_z = reinterpret_cast<io_t*>(smem + wave * TILE);
 
   // rows at or beyond T fall outside the descriptor (ld >= n)
@@ -372,13 +406,24 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // A stage is U k-steps (SC columns of z for the block's TOK tokens).  Stages
-  // outside [ks0, ks1) load zeros and add nothing.
+  // A stage is U k-steps (SC columns of z for the block's TOK tokens).  The
+  // waves of a block take adjacent stages, so that together they read KW SC
+  // contiguous columns of each row at a time.  Stages before 0 or past n load
+  // zeros and add nothing.
   XFrag za[NQ], zb[NQ];
   SFrag wa[U][NW], wb[U][NW];
-  auto load = [&](XFrag (&zz)[NQ], SFrag (&ww)[U][NW], int ks) {
+  // blocks start at different stages (rotating through all of them), so that
+  // concurrently running blocks read different column ranges
+#if RESBM_XCD_SPREAD
+  const int srot = (int)(blockIdx.x % (unsigned)nst);
+#else
+  const int srot = 0;
+#endif
+  auto stage_k = [&](int i) { const int ir = i + srot < nst ? i + srot : i + srot - nst; return (ir * KW + wave) * U; };
+  auto load = [&](XFrag (&zz)[NQ], SFrag (&ww)[U][NW], int i) {
+    const int ks = i < 0 || i >= nst ? nks : stage_k(i);
     const int kz = ks + zch * 8 / 32;  // k-step of this lane's chunk
-    const bool zok = kz >= ks0 && kz < ks1;
+    const bool zok = i >= 0 && kz < nks;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) zz[q] = bld_x8(zr, zok ? zoff[q] + (uint32_t)(ks * 32 * kEs) : kOOB);
     if constexpr (PW) {
@@ -386,12 +431,13 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
       for (int u = 0; u < U; ++u) {
         const int k = ks + u;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) ww[u][nt] = bld_sfrag(wr, (int64_t)k * NT + nt, l, k >= ks0 && k < ks1);
+        for (int nt = 0; nt < NT; ++nt) ww[u][nt] = bld_sfrag(wr, (int64_t)k * NT + nt, l, i >= 0 && k < nks);
       }
     }
   };
   // stage the tile in the wave's LDS, read it back in fragment order
-  auto compute = [&](const XFrag (&zz)[NQ], const SFrag (&ww)[U][NW], int ks) {
+  auto compute = [&](const XFrag (&zz)[NQ], const SFrag (&ww)[U][NW], int i) {
+    const int ks = i < 0 || i >= nst ? nks : stage_k(i);
 #pragma unroll
     for (int q = 0; q < NQ; ++q) tile_put8<SC>(s_z, q * (64 / CPR) + l / CPR, 8 * zch, zz[q]);
 #pragma unroll
@@ -404,7 +450,7 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
       for (int nt = 0; nt < NT; ++nt) {
         SFrag w;
         if constexpr (PW) w = ww[u][nt];
-        else w = bld_sfrag(wr, (int64_t)k * NT + nt, l, k >= ks0 && k < ks1);
+        else w = bld_sfrag(wr, (int64_t)k * NT + nt, l, i >= 0 && k < nks);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, f[mt], acc[mt][nt]);
       }
@@ -422,11 +468,11 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) wa[u][nt] = wb[u][nt] = sfrag_zero();
   }
-  for (int ks = opaque(ks0 - 2 * U); ks < ks1; ks += 2 * U) {
-    compute(za, wa, ks);
-    load(za, wa, ks + 2 * U);
-    compute(zb, wb, ks + U);
-    load(zb, wb, ks + 3 * U);
+  for (int i = opaque(-2); i < nst; i += 2) {
+    compute(za, wa, i);
+    load(za, wa, i + 2);
+    compute(zb, wb, i + 1);
+    load(zb, wb, i + 3);
   }
   __syncthreads();  // the reduction area overlaps the tiles
   float (*s_red)[TOK][RPT + 4] = reinterpret_cast<float (*)[TOK][RPT + 4]>(smem);
@@ -480,6 +526,7 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   io_t* tile = s_out[wave];
   const int strip = blockIdx.x * 4 + wave;
+  const int tgi = blockIdx.y;
   const int c0 = strip * 16 * CT;
   if (c0 >= n) return;  // whole strips only: n % 64 == 0 and 16 CT divides 64
 
@@ -498,7 +545,7 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
       wfr[ks][ct] = sfrag_from(w);
     }
 
-  const int64_t t_begin = (int64_t)blockIdx.y * tpg;
+  const int64_t t_begin = (int64_t)tgi * tpg;
   const int64_t rows = min((int64_t)tpg, T - t_begin);
   const rsrc_t br = make_rsrc(b + t_begin * r, rows * r * kEs);
   const rsrc_t zr = make_rsrc(zt + t_begin * ld_zt, rows_bytes(rows, n, ld_zt, kEs));
@@ -600,12 +647,13 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
 // and j-tiles [16 jt0, 16 (jt0 + JT)) of r:
 //   gbp[cg][t][j] = sum over the block's columns of g_z~[t][c] W_d[j][c]
 //   dwp[tg][j][c] = sum over the block's tokens of b[t][j] g_z~[t][c]
-// Per 32-token step: each wave loads its 64 columns of g_z~ (two steps ahead,
-// 8 lanes per 128-byte row), stages the tile in its own LDS, reads it back in
-// fragment order for its g_b partial (W_d held in registers) and transposed
-// for dW_d; the step's payload rows are staged once per block (double-buffered)
-// and read transposed too.  The 8 waves' g_b partials meet in LDS behind the
-// one barrier of the step.
+// Per 32-token step the block loads its 32 x 512 tile of g_z~ cooperatively,
+// one 1 KiB row segment per load instruction (wave w: rows 4 w .. 4 w + 3, two
+// steps ahead), into a block-wide LDS tile; after the step's barrier each wave
+// reads its 64 columns back in fragment order for its g_b partial (W_d held in
+// registers) and transposed for dW_d.  The payload rows of a step are staged
+// once per block.  The 8 waves' g_b partials of a step are added in wave order
+// behind the next step's barrier.
 template <int JT>
 __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int r, int RP,
                                                            const io_t* __restrict__ b,
@@ -615,17 +663,25 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
                                                            int TB) {
   constexpr int KSW = kDbWC / 32;  // 32-column steps per wave
   constexpr int CTW = kDbWC / 16;  // 16-column tiles per wave
+  constexpr int BW = kDbWaves * kDbWC;  // block columns (one 1 KiB bf16 row segment)
   constexpr int JW = JT * 16;      // j values per pass
-  constexpr int NBUF = JT <= 2 ? 2 : 1;  // double-buffered partials: one barrier per step
+  constexpr int NBUF = JT <= 2 ? 2 : 1;                 // g_b partial buffers
+  constexpr int GZB = RESBM_IO_F32_BUILD ? 1 : 2;       // g_z~ tile buffers
   constexpr int BQ = JW / 8;       // 16-byte payload chunks per token row
-  __shared__ __attribute__((aligned(16))) io_t s_gz[kDbWaves][32 * kDbWC];
+  constexpr int RPW = 32 / kDbWaves;  // tile rows loaded per wave
+  __shared__ __attribute__((aligned(16))) io_t s_gz[GZB][32 * BW];
   __shared__ __attribute__((aligned(16))) io_t s_b[2][32 * JW];
   __shared__ __attribute__((aligned(16))) float s_gb[NBUF][kDbWaves][32][JW + 4];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+#if RESBM_XCD_SPREAD
+  const int tg = blockIdx.x, cg = blockIdx.y;  // token groups vary fastest: every XCD sees every column group
+#else
   const int cg = blockIdx.x, tg = blockIdx.y;
+#endif
   const int jt0 = blockIdx.z * JT;
-  const int wc0 = cg * (kDbWaves * kDbWC) + wave * kDbWC;
+  const int bc0 = cg * BW;
+  const int wc0 = bc0 + wave * kDbWC;
   const bool won = wc0 < n;  // n % 64 == 0: a wave's 64 columns are all in or all out
 
   // W_d as the A operand of g_b: lane (row16, grp) holds W_d[16 (jt0 + jt) + row16][wc0 + 32 ks + 8 grp + e].
@@ -659,21 +715,23 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
   // payload rows of one step: threads [0, 32 BQ) each carry one 16-byte chunk
   const bool bthr = threadIdx.x < 32 * BQ;
   const int btt = bthr ? threadIdx.x / BQ : 0, bch = threadIdx.x % BQ;
-  // coalesced g_z~ loads: load q covers rows [8 q, 8 q + 8) of the step, 8 lanes per 128-byte row
-  const uint32_t gz_lane = (uint32_t)(((l >> 3) * ld_g + wc0 + 8 * (l & 7)) * kEs);
+  // g_z~ loads: lane l takes columns bc0 + 8 l .. + 8 of rows RPW wave + q (outside [0, n): zeros)
+  const bool lon = bc0 + 8 * l < n;
+  const uint32_t gz_lane = (uint32_t)((RPW * wave * ld_g + bc0 + 8 * l) * kEs);
 
-  // Registers of step s: its g_z~ tile and the payload rows of step s + 1.
+  // Registers of step s: its tile rows and the payload rows of step s + 1.
   // Steps before 0 or past the range read zeros and store nothing.
   struct Step {
-    XFrag gz[4];
+    XFrag gz[RPW];
     XFrag bp;
   };
   auto load = [&](Step& st, int64_t s) {
     const int64_t t0 = t_begin + 32 * s;
     const int64_t rows = s < 0 ? 0 : min((int64_t)32, t_end - t0);
-    const rsrc_t gr = make_rsrc(g_zt + t0 * ld_g, won ? rows_bytes(rows, n, ld_g, kEs) : 0);
+    const rsrc_t gr = make_rsrc(g_zt + t0 * ld_g, rows_bytes(rows, n, ld_g, kEs));
 #pragma unroll
-    for (int q = 0; q < 4; ++q) st.gz[q] = bld_x8(gr, gz_lane + (uint32_t)(8 * q * ld_g * kEs));
+    for (int q = 0; q < RPW; ++q)
+      st.gz[q] = bld_x8(gr, lon ? gz_lane + (uint32_t)(q * ld_g * kEs) : kOOB);
     const int64_t rows1 = s + 1 < 0 ? 0 : min((int64_t)32, t_end - t0 - 32);
     const rsrc_t br = make_rsrc(b + (t0 + 32) * r, rows1 > 0 ? rows1 * r * kEs : 0);
     st.bp = bld_r8(br, bthr ? (uint32_t)(btt * r * kEs) : kOOB, r, 16 * jt0 + 8 * bch);
@@ -681,69 +739,89 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
 
   // One 32-token step; `st` is reloaded with the registers of step s + 2.
   auto body = [&](Step& st, int64_t s) {
-    const int gbuf = NBUF == 2 ? (int)(s & 1) : 0;
-    const int bbuf = (int)(s & 1);
-    // stage the wave's tile row-major; the next step's payload rows go to the
-    // other buffer, last read before the previous barrier
-    wave_lds_fence();  // the previous step's reads of s_gz are complete
+    const int tb = GZB == 2 ? (int)(s & 1) : 0;
+    const int gcur = NBUF == 2 ? (int)(s & 1) : 0, gprev = NBUF == 2 ? (int)((s + 1) & 1) : 0;
+    io_t* tile = s_gz[tb];
+    if constexpr (GZB == 1) __syncthreads();  // the previous step's readers of the single tile are done
 #pragma unroll
-    for (int q = 0; q < 4; ++q) tile_put8<kDbWC>(s_gz[wave], 8 * q + (l >> 3), 8 * (l & 7), st.gz[q]);
-    if (bthr) tile_put8<JW>(s_b[bbuf ^ 1], btt, 8 * bch, st.bp);
+    for (int q = 0; q < RPW; ++q) {
+      const int row = RPW * wave + q;
+      io_t* d = tile + row * BW + wide_col(row, 8 * l);
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = st.gz[q].v[e];
+#else
+      *reinterpret_cast<uint4*>(d) = __builtin_bit_cast(uint4, st.gz[q].v);
+#endif
+    }
+    __syncthreads();  // the step's tile, its payload rows and the previous step's partials are complete
+    // the next step's payload rows go to the other buffer (its readers passed this barrier)
+    if (bthr) tile_put8<JW>(s_b[(s + 1) & 1], btt, 8 * bch, st.bp);
     load(st, s + 2);
+    // add the previous step's 8 partials of g_b in wave order; rows outside the range are dropped
+    {
+      const int64_t t0 = t_begin + 32 * (s - 1);
+      const rsrc_t pr = make_rsrc(gbp + ((int64_t)cg * T + t0) * RP, s - 1 < 0 ? 0 : (t_end - t0) * RP * 4);
+#pragma unroll
+      for (int idx0 = 0; idx0 < 32 * JW; idx0 += kDbWaves * 64) {
+        const int idx = idx0 + threadIdx.x;
+        const int tt = idx / JW, jj = idx % JW;
+        const int j = 16 * jt0 + jj;
+        float v = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kDbWaves; ++w) v += s_gb[gprev][w][tt][jj];
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), pr,
+                                              j < r ? (uint32_t)((tt * RP + j) * 4) : kOOB, 0, 0);
+      }
+    }
+    if constexpr (NBUF == 1) __syncthreads();  // the single partial buffer is refilled below
     // g_b partial over this wave's 64 columns: D[j][t], B = g_z~ rows in fragment order
 #pragma unroll
     for (int th = 0; th < 2; ++th) {
       XFrag f[KSW];
 #pragma unroll
-      for (int ks = 0; ks < KSW; ++ks) f[ks] = tile_get8<kDbWC>(s_gz[wave], 16 * th + row16, 32 * ks + 8 * grp);
+      for (int ks = 0; ks < KSW; ++ks) {
+        const int row = 16 * th + row16;
+        const io_t* p = tile + row * BW + wide_col(row, wave * kDbWC + 32 * ks + 8 * grp);
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[ks].v[e] = p[e];
+#else
+        f[ks].v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+#endif
+      }
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KSW; ++ks) acc = mma_sx(wdf[jt][ks], f[ks], acc);
-        *reinterpret_cast<float4*>(&s_gb[gbuf][wave][16 * th + row16][16 * jt + 4 * grp]) =
+        *reinterpret_cast<float4*>(&s_gb[gcur][wave][16 * th + row16][16 * jt + 4 * grp]) =
             make_float4(acc[0], acc[1], acc[2], acc[3]);
       }
     }
     // dW_d: D[c][j] = sum_t g_z~[t][c] b[t][j], A = g_z~^T, B = b^T (both transposed from LDS)
     XFrag bt[JT];
 #pragma unroll
-    for (int jt = 0; jt < JT; ++jt) bt[jt] = tr_frag<JW>(s_b[bbuf], 16 * jt, row16, grp);
+    for (int jt = 0; jt < JT; ++jt) bt[jt] = tr_frag<JW>(s_b[s & 1], 16 * jt, row16, grp);
 #pragma unroll
     for (int ct = 0; ct < CTW; ++ct) {
-      const XFrag a = tr_frag<kDbWC>(s_gz[wave], 16 * ct, row16, grp);
+      const XFrag a = tr_frag_wide<BW>(tile, 0, wave * kDbWC + 16 * ct, row16, grp);
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) dw[ct][jt] = mma_xx(a, bt[jt], dw[ct][jt]);
     }
-
-    __syncthreads();  // s_gb[gbuf] and s_b[bbuf ^ 1] complete
-    // sum the 8 waves' g_b partials in wave order; rows past t_end are dropped by the descriptor
-    const int64_t t0 = t_begin + 32 * s;
-    const rsrc_t pr = make_rsrc(gbp + ((int64_t)cg * T + t0) * RP, s < 0 ? 0 : (t_end - t0) * RP * 4);
-#pragma unroll
-    for (int idx0 = 0; idx0 < 32 * JW; idx0 += kDbWaves * 64) {
-      const int idx = idx0 + threadIdx.x;
-      const int tt = idx / JW, jj = idx % JW;
-      const int j = 16 * jt0 + jj;
-      float v = 0.0f;
-#pragma unroll
-      for (int w = 0; w < kDbWaves; ++w) v += s_gb[gbuf][w][tt][jj];
-      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), pr,
-                                            j < r ? (uint32_t)((tt * RP + j) * 4) : kOOB, 0, 0);
-    }
-    if constexpr (NBUF == 1) __syncthreads();  // the single buffer is refilled next step
   };
 
   // Every memory operation sits in one unconditional loop body: the loop starts
   // three (empty) steps early on zeroed registers instead of after a prologue of
-  // loads, so the compiler can place each wait at its exact distance.  Step -1
-  // stages the payload rows of step 0.
+  // loads, so the compiler can place each wait at its exact distance, and runs
+  // one step past the range to add the last step's partials.  Step -1 stages
+  // the payload rows of step 0.
   const int64_t nsteps = (t_end - t_begin + 31) / 32;
   Step sa, sb;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) sa.gz[q] = sb.gz[q] = xfrag_zero();
+  for (int q = 0; q < RPW; ++q) sa.gz[q] = sb.gz[q] = xfrag_zero();
   sa.bp = sb.bp = xfrag_zero();
-  for (int64_t s = opaque(-3); s < nsteps; s += 2) {
+  for (int64_t s = opaque(-3); s <= nsteps; s += 2) {
     body(sb, s);      // odd steps
     body(sa, s + 1);  // even steps
   }
@@ -945,9 +1023,13 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   const int cw = wave % CW, tw = wave / CW;
-  const int wc0 = blockIdx.x * BC + cw * WC;
+#if RESBM_XCD_SPREAD
+  const int cbi = blockIdx.y, tg = blockIdx.x;  // token groups vary fastest: every XCD sees every column block
+#else
+  const int cbi = blockIdx.x, tg = blockIdx.y;
+#endif
+  const int wc0 = cbi * BC + cw * WC;
   const bool on = wc0 < n;  // whole waves fall inside or outside [0, n): n % 64 == 0, WC | 64
-  const int tg = blockIdx.y;
   const int64_t t_begin = (int64_t)tg * TB;
   const int64_t t_end = min(T, t_begin + TB);
   GhTile<TS, RPS>* s_gh = reinterpret_cast<GhTile<TS, RPS>*>(smem);
@@ -1281,7 +1363,11 @@ void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, 
 template <int JT>
 void launch_dec_bwd(const Plan& p, const io_t* b, const float* W_d, const io_t* g, int64_t ld, float* gbp,
                     float* dwp, hipStream_t st) {
+#if RESBM_XCD_SPREAD
+  dim3 grid(p.db_ntg, p.db_ncg, p.db_njg);
+#else
   dim3 grid(p.db_ncg, p.db_ntg, p.db_njg);
+#endif
   hipLaunchKernelGGL((k_dec_bwd<JT>), grid, dim3(512), 0, st, p.T, p.n, p.r, p.RP, b, W_d, g, ld, gbp, dwp,
                      p.db_TB);
 }
@@ -1292,7 +1378,11 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
   constexpr int KS = (NT + 1) / 2;
   constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS);
   constexpr bool SG = eb_sg(KS);
+#if RESBM_XCD_SPREAD
+  dim3 grid(p.eb_ntg, p.eb_ncb);
+#else
   dim3 grid(p.eb_ncb, p.eb_ntg);
+#endif
   const int silu = act == RESBM_ACT_SILU;
   if (fused)
     hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, SG, true>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,

@@ -20,6 +20,15 @@
 #define RESBM_EF_MT_SMALL_R 4
 #endif
 
+// The hardware hands consecutive blocks of a grid to the 8 XCDs in turn.  The
+// streaming kernels that read (encode_fwd, decode_bwd, encode_bwd) put the
+// token dimension first, so that each XCD sees every column range rather than
+// one narrow column strip of every row, and encode_fwd rotates the starting
+// column stage by block.
+#ifndef RESBM_XCD_SPREAD
+#define RESBM_XCD_SPREAD 1
+#endif
+
 namespace resbm {
 
 constexpr int kNumCU = 256;          // MI355X compute units (8 XCDs x 32)
@@ -41,8 +50,14 @@ constexpr int db_jt(int NT) { return NT < 4 ? NT : 4; }
 // step covers 32*TW tokens; SG: g_z leaves through LDS in whole row segments.
 // Workspace: the dW_e partials of the token groups.
 constexpr int eb_ct(int KS) { return KS <= 1 ? 4 : (KS <= 2 ? 2 : 1); }
-constexpr int eb_cw(int) { return 4; }
-constexpr int eb_tw(int KS) { return KS <= 2 ? 2 : 1; }
+#ifndef RESBM_EB_CW
+#define RESBM_EB_CW 4
+#endif
+constexpr int eb_cw(int) { return RESBM_EB_CW; }
+#ifndef RESBM_EB_TW
+#define RESBM_EB_TW 2
+#endif
+constexpr int eb_tw(int KS) { return KS <= 2 ? RESBM_EB_TW : 1; }
 #ifndef RESBM_EB_STAGE_GZ
 #define RESBM_EB_STAGE_GZ 1
 #endif
