@@ -2,14 +2,16 @@
 
 A step is the whole hot path over one batch: resbm_encode_fwd, resbm_decode_fwd,
 resbm_decode_bwd, resbm_encode_bwd on T tokens of width n at rank r, all on
-torch's current HIP stream, inputs resident in HBM.  Consecutive steps rotate
-over several copies of the inputs and outputs so that no step finds its
-streams in the 256 MB Infinity Cache left behind by the previous one.
+one HIP stream, inputs resident in HBM.  Consecutive steps rotate over several
+copies of the inputs and outputs so that no step finds its streams in the
+256 MB Infinity Cache left behind by the previous one; the library's scratch
+workspace is one buffer shared by all steps, as a caller would keep it.
 
-Prints one JSON line: tokens/s (value), algorithmic HBM GB/s and its fraction
-of the 8 TB/s peak, per-op times from HIP events recorded inside the timed
-steps, the roofline entry of the dominant op, and the CPU oracle timed on a
-bounded sample of the same workload.
+The step is timed twice: captured in a HIP graph per input copy and replayed
+(the reported value; a graph removes the host's launch gaps between the ops),
+and launched eagerly with HIP events between the ops (per-op times, the
+roofline entry of the dominant op).  Prints one JSON line, with the CPU oracle
+timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -47,10 +49,119 @@ def parse():
     p.add_argument("--act", default="silu", choices=["silu", "identity"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-op-events", action="store_true", help="time whole steps only")
-    p.add_argument("--copy-probe-mib", type=int, default=256,
+    p.add_argument("--copy-probe-mib", type=int, default=COPY_PROBE_MIB,
                    help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
     p.add_argument("--cpu-tokens", type=int, default=None, help="tokens in the CPU oracle sample")
+    p.add_argument("--no-graph", action="store_true", help="report the eager launches instead of graph replays")
+    p.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                   help="write profiles/ summaries from rocprofv3 output of this script (no GPU work)")
+    p.add_argument("--commands", nargs=3, default=None, help="the three rocprofv3 commands, recorded in the summaries")
     return p.parse_args()
+
+
+KERNEL_OP = (("k_enc_fwd", "encode_fwd"), ("k_dec_fwd", "decode_fwd"), ("k_dec_bwd", "decode_bwd"),
+             ("k_enc_bwd", "encode_bwd"))
+
+
+def kernel_op(name: str):
+    """The boundary op a kernel name belongs to (prologue and finishing kernels included)."""
+    import re
+    base = re.sub(r"\(.*", "", name)
+    for key, op in KERNEL_OP:
+        if key in base or key.replace("_", "") in base.replace("_", ""):
+            return op
+    return None
+
+
+def summarize_profiles(trace_dir: str, fetch_dir: str, write_dir: str, name: str, commands) -> None:
+    """Kernel-time statistics of a traced bench run and per-op HBM traffic from FETCH_SIZE /
+    WRITE_SIZE runs, scaled by what the same counters read for the plain device copy."""
+    import glob
+    import re
+    import sqlite3
+
+    def db(d):
+        f = sorted(glob.glob(os.path.join(d, "**", "*results.db"), recursive=True))
+        if not f:
+            raise SystemExit(f"no rocprofv3 database under {d}")
+        return sqlite3.connect(f[0])
+
+    def short(k):
+        return re.sub(r"\(.*", "", k).replace("void ", "")
+
+    rows = list(db(trace_dir).execute("select name, end - start from kernels"))
+    stats = {}
+    for k, dur in rows:
+        stats.setdefault(short(k), []).append(dur / 1000.0)
+
+    def counter(d, cname):
+        out = {}
+        for k, cn, v in db(d).execute("select kernel_name, counter_name, value from counters_collection"):
+            if cn == cname:
+                out.setdefault(short(k), []).append(v)
+        return {k: sum(v) / len(v) for k, v in out.items()}
+
+    fetch, write = counter(fetch_dir, "FETCH_SIZE"), counter(write_dir, "WRITE_SIZE")
+    copy_bytes = None
+    for k in fetch:
+        if "copyBuffer" in k or "copy" in k.lower():
+            copy_bytes = COPY_PROBE_MIB * 2**20
+            f_fetch = copy_bytes / (fetch[k] * 1024)
+            f_write = copy_bytes / (write[k] * 1024)
+            break
+    if copy_bytes is None:
+        raise SystemExit("the runs hold no plain copy kernel to calibrate the counters")
+    ops = {}
+    for k in fetch:
+        op = kernel_op(k)
+        if op is None or k not in write:
+            continue
+        e = ops.setdefault(op, {"kernels": {}, "hbm_bytes": 0.0})
+        b = fetch[k] * 1024 * f_fetch + write[k] * 1024 * f_write
+        e["kernels"][k] = {"fetch_kib": fetch[k], "write_kib": write[k], "hbm_bytes": b}
+        e["hbm_bytes"] += b
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    rec = {"workload": name, "source_sha256": source_digest(), "fetch_scale": f_fetch, "write_scale": f_write,
+           "calibration": f"plain device copy of {COPY_PROBE_MIB} MiB", "commands": commands, "ops": ops}
+    with open(os.path.join(ROOT, "profiles", f"traffic_{name}.json"), "w") as fh:
+        json.dump(rec, fh, indent=1)
+    lines = [f"# rocprofv3 kernel trace, workload {name}", "", "command:", f"    {commands[0] if commands else '?'}", "",
+             f"{'kernel':60s} {'calls':>6s} {'avg us':>9s} {'min us':>9s} {'max us':>9s}"]
+    for k, v in sorted(stats.items(), key=lambda kv: -sum(kv[1])):
+        lines.append(f"{k[:60]:60s} {len(v):6d} {sum(v) / len(v):9.2f} {min(v):9.2f} {max(v):9.2f}")
+    lines += ["", "HBM traffic per call (FETCH_SIZE x %.3f + WRITE_SIZE x %.3f, calibrated on a plain copy):"
+              % (f_fetch, f_write)]
+    for op, e in ops.items():
+        lines.append(f"    {op:12s} {e['hbm_bytes'] / 1e6:10.1f} MB")
+    if commands:
+        lines += ["", "counter commands:", f"    {commands[1]}", f"    {commands[2]}"]
+    with open(os.path.join(ROOT, "profiles", f"kernels_{name}.txt"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def source_digest() -> str:
+    """sha256 over the kernel sources; HBM traffic measured on other sources is not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("resbm_kernels.hip", "resbm_plan.hpp", "resbm_mfma.hpp"):
+        with open(os.path.join(ROOT, "paper_2604_11947_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(name: str, op: str):
+    """HBM bytes per call of `op` on workload `name` from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE scaled by the plain-copy calibration), if it was taken
+    on the current kernel sources; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{name}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_sha256") != source_digest():
+        return None
+    return rec.get("ops", {}).get(op, {}).get("hbm_bytes")
 
 
 def cpu_baseline(d: dict, r: int, act: int, tokens: int, min_seconds: float = 10.0) -> dict:
@@ -98,8 +209,15 @@ def cpu_baseline(d: dict, r: int, act: int, tokens: int, min_seconds: float = 10
                       f"{len(os.sched_getaffinity(0))} host cores visible"}
 
 
+COPY_PROBE_MIB = 256
+
+
 def main():
     args = parse()
+    if args.summarize_profiles:
+        from paper_2604_11947_amd import inputs as I
+        summarize_profiles(*args.summarize_profiles, args.workload or I.HEADLINE, args.commands)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): this build runs the "
               f"boundary module on a single MI355X; across GPUs it would shard by tokens", file=sys.stderr)
@@ -124,6 +242,7 @@ def main():
     d = I.make_inputs(T, n, r, w.dist, w.seed)
     t_gen = time.perf_counter() - t_gen
     io = lib.io_dtype
+    ws = lib.workspace(T, n, r, dev)
     sets = []
     for _ in range(max(1, args.sets)):
         s = {k: d[k].to(dev) for k in ("x_attn", "z", "W_e", "W_d", "g_zt", "g_id")}
@@ -135,7 +254,6 @@ def main():
             gz=torch.empty(T, n, dtype=io, device=dev),
             dWd=torch.empty(r, n, dtype=torch.float32, device=dev),
             dWe=torch.empty(n, r, dtype=torch.float32, device=dev),
-            ws=lib.workspace(T, n, r, dev),
         )
         sets.append(s)
     torch.cuda.synchronize()
@@ -143,16 +261,16 @@ def main():
     def step(s, ev=None):
         if ev is not None:
             ev[0].record()
-        lib.encode_fwd(s["x_attn"], s["z"], s["W_e"], s["b"], s["a"], act=act, ws=s["ws"])
+        lib.encode_fwd(s["x_attn"], s["z"], s["W_e"], s["b"], s["a"], act=act, ws=ws)
         if ev is not None:
             ev[1].record()
-        lib.decode_fwd(s["b"], s["W_d"], s["zt"], ws=s["ws"])
+        lib.decode_fwd(s["b"], s["W_d"], s["zt"], ws=ws)
         if ev is not None:
             ev[2].record()
-        lib.decode_bwd(s["b"], s["W_d"], s["g_zt"], s["g_id"], s["gb"], s["dWd"], ws=s["ws"])
+        lib.decode_bwd(s["b"], s["W_d"], s["g_zt"], s["g_id"], s["gb"], s["dWd"], ws=ws)
         if ev is not None:
             ev[3].record()
-        lib.encode_bwd(s["z"], s["W_e"], s["a"], s["gb"], s["gz"], s["dWe"], act=act, ws=s["ws"])
+        lib.encode_bwd(s["z"], s["W_e"], s["a"], s["gb"], s["gz"], s["dWe"], act=act, ws=ws)
         if ev is not None:
             ev[4].record()
 
@@ -178,6 +296,7 @@ def main():
         step(sets[i % len(sets)])
     torch.cuda.synchronize()
 
+    # eager launches, HIP events between the ops (on the stream the ops run on)
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
@@ -189,8 +308,30 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms_total = start.elapsed_time(stop)
-    ms_step = ms_total / args.steps
+    ms_eager = start.elapsed_time(stop) / args.steps
+
+    # the same steps as HIP graph replays, one graph per input copy
+    ms_graph = None
+    if not args.no_graph:
+        graphs = []
+        for s in sets:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(s)
+            graphs.append(g)
+        for i in range(args.warmup):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        wall0 = time.perf_counter()
+        g0.record()
+        for i in range(args.steps):
+            graphs[i % len(graphs)].replay()
+        g1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        ms_graph = g0.elapsed_time(g1) / args.steps
+    ms_step = ms_graph if ms_graph is not None else ms_eager
 
     op_ms = {}
     for k, nm in enumerate(OPS):
@@ -202,6 +343,7 @@ def main():
     dom = "encode_bwd" if args.no_op_events else max(OPS, key=lambda k: op_ms[k])
     dom_gbs = ob[dom] / (op_ms[dom] * 1e-3) / 1e9
 
+    traffic = measured_traffic(name, dom)
     out = {
         "metric": "tokens/s and achieved HBM GB/s (% peak), ResBM fwd+bwd, n=4096 r=32",
         "value": T / (ms_step * 1e-3),
@@ -210,6 +352,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "timing": "hip graph replay" if ms_graph is not None else "eager launches",
+        "ms_per_step_eager": ms_eager,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -224,7 +368,7 @@ def main():
         "copy_probe_gbps": copy_gbs,
         "ops": {k: {"ms": op_ms[k], "gbps": ob[k] / (op_ms[k] * 1e-3) / 1e9, "bytes": ob[k]} for k in OPS},
         "roofline": {"bound": "hbm", "op": dom, "achieved": dom_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": dom_gbs / HBM_PEAK_GBS, "traffic": None},
+                     "frac": dom_gbs / HBM_PEAK_GBS, "traffic": traffic},
         "wall_s_timed": wall,
         "input_gen_s": t_gen,
     }
