@@ -346,9 +346,10 @@ __device__ __forceinline__ int expand_col(int c0, int ct, int i) {
 // ============================================================ encode forward
 // Fragment-ordered hi/lo copy of W_e for the A operand of a = z W_e:
 // fragment f = ks * NT + nt, lane (row16, grp) holds W_e[32 ks + 8 grp + e][16 nt + row16].
-__global__ __launch_bounds__(256) void k_enc_fwd_prep(const float* __restrict__ W_e, int n, int r, int NT,
-                                                      void* __restrict__ wf) {
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+// One wave per block, so that the few fragments spread over many compute units.
+__global__ __launch_bounds__(64) void k_enc_fwd_prep(const float* __restrict__ W_e, int n, int r, int NT,
+                                                     void* __restrict__ wf) {
+  const int64_t gid = (int64_t)blockIdx.x * 64 + threadIdx.x;
   const int64_t total = (int64_t)(n / 32) * NT * 64;
   if (gid >= total) return;
   const int l = (int)(gid & 63);
@@ -366,39 +367,45 @@ __global__ __launch_bounds__(256) void k_enc_fwd_prep(const float* __restrict__ 
   store_sfrag(wf, f, l, w);
 }
 
-// a = z W_e for 16*MT tokens per block; the KW waves take interleaved stages of the n-contraction.
+// a = z W_e for 16*MT tokens per block.  A stage covers KW * SC columns of the
+// n-contraction: the block loads its TOK x (KW SC) tile cooperatively, whole
+// row segments per load instruction (1 KiB at r <= 32), into a block-wide LDS
+// tile; after the stage's barrier wave w contracts columns [w SC, (w + 1) SC)
+// of it, with the W_e fragments of those rows from the prologue kernel.
 template <int NT, int MT, int KW>
 __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, int act,
                                                      const io_t* __restrict__ x_attn, int64_t ld_x,
                                                      const io_t* __restrict__ z, int64_t ld_z,
                                                      const void* __restrict__ wf, io_t* __restrict__ b,
                                                      float* __restrict__ a_save) {
-  constexpr int U = NT <= 2 ? 2 : 1;    // k-steps per pipeline stage
+  constexpr int U = NT <= 2 ? 2 : 1;    // k-steps per wave and stage
   constexpr bool PW = NT <= 4;          // W_e fragments travel with the stage
   constexpr int NW = PW ? NT : 1;
   constexpr int TOK = 16 * MT;
   constexpr int RPT = 16 * NT;
-  constexpr int SC = 32 * U;            // z columns per stage
-  constexpr int CPR = SC / 8;           // 8-element chunks per tile row
-  constexpr int NQ = TOK * CPR / 64;    // coalesced loads per lane per stage
-  constexpr int TILE = TOK * SC * (int)sizeof(io_t);
+  constexpr int SC = 32 * U;            // z columns per wave and stage
+  constexpr int BC = KW * SC;           // z columns per stage (tile row)
+  constexpr int LPR = BC / 8;           // lanes per tile row in the cooperative loads
+  constexpr int NQ = TOK * LPR / (64 * KW);  // cooperative loads per lane per stage
+  constexpr int ZB = RESBM_IO_F32_BUILD ? 1 : 2;  // tile buffers
+  constexpr int TILE = TOK * BC * (int)sizeof(io_t);
   constexpr int RED = KW * TOK * (RPT + 4) * 4;
-  __shared__ __attribute__((aligned(16))) char smem[KW * TILE > RED ? KW * TILE : RED];
+  static_assert(TOK * LPR % (64 * KW) == 0, "tile rows must split evenly over the waves");
+  __shared__ __attribute__((aligned(16))) char smem[ZB * TILE > RED ? ZB * TILE : RED];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   const int64_t tok0 = (int64_t)blockIdx.x * TOK;
   const int nks = n / 32;
-  const int nst = (nks + KW * U - 1) / (KW * U);  // stages; stage i of wave w: k-steps (i KW + w) U + u
-  io_t* s_z = reinterpret_cast<io_t*>(smem + wave * TILE);
+  const int nst = (n + BC - 1) / BC;  // stages
 
   // rows at or beyond T fall outside the descriptor (ld >= n)
   const rsrc_t zr = make_rsrc(z + tok0 * ld_z, rows_bytes(min((int64_t)TOK, T - tok0), n, ld_z, kEs));
   const rsrc_t wr = make_rsrc(wf, (int64_t)nks * NT * kSFragBytes);
-  // coalesced z loads: load q of a stage covers tile rows [q 64 / CPR, ...), CPR lanes per row
-  const int zch = l % CPR;
-  uint32_t zoff[NQ];
+  // cooperative load q of this lane: tile row zrow[q], columns zc .. zc + 8 of the stage
+  const int zc = 8 * (l % LPR);
+  int zrow[NQ];
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) zoff[q] = (uint32_t)(((q * (64 / CPR) + l / CPR) * ld_z + 8 * zch) * kEs);
+  for (int q = 0; q < NQ; ++q) zrow[q] = (wave * NQ * 64 + q * 64 + l) / LPR;
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -406,60 +413,78 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // A stage is U k-steps (SC columns of z for the block's TOK tokens).  The
-  // waves of a block take adjacent stages, so that together they read KW SC
-  // contiguous columns of each row at a time.  Stages before 0 or past n load
-  // zeros and add nothing.
-  XFrag za[NQ], zb[NQ];
-  SFrag wa[U][NW], wb[U][NW];
-  // blocks start at different stages (rotating through all of them), so that
-  // concurrently running blocks read different column ranges
-#if RESBM_XCD_SPREAD
+  // Blocks start at different stages (rotating through all of them), so that
+  // concurrently running blocks read different column ranges.  Stages before 0
+  // or past the last load zeros and add nothing.
   const int srot = (int)(blockIdx.x % (unsigned)nst);
-#else
-  const int srot = 0;
-#endif
-  auto stage_k = [&](int i) { const int ir = i + srot < nst ? i + srot : i + srot - nst; return (ir * KW + wave) * U; };
-  auto load = [&](XFrag (&zz)[NQ], SFrag (&ww)[U][NW], int i) {
-    const int ks = i < 0 || i >= nst ? nks : stage_k(i);
-    const int kz = ks + zch * 8 / 32;  // k-step of this lane's chunk
-    const bool zok = i >= 0 && kz < nks;
+  auto stage_col = [&](int i) {  // first column of stage i, or n outside [0, nst)
+    if (i < 0 || i >= nst) return n;
+    const int ir = i + srot < nst ? i + srot : i + srot - nst;
+    return ir * BC;
+  };
+  auto load_z = [&](XFrag (&zz)[NQ], int i) {
+    const int c = stage_col(i) + zc;
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) zz[q] = bld_x8(zr, zok ? zoff[q] + (uint32_t)(ks * 32 * kEs) : kOOB);
+    for (int q = 0; q < NQ; ++q) zz[q] = bld_x8(zr, c < n ? (uint32_t)((zrow[q] * ld_z + c) * kEs) : kOOB);
+  };
+  auto load_w = [&](SFrag (&ww)[U][NW], int i) {
     if constexpr (PW) {
+      const int ks = (stage_col(i) + wave * SC) / 32;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int k = ks + u;
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) ww[u][nt] = bld_sfrag(wr, (int64_t)k * NT + nt, l, i >= 0 && k < nks);
-      }
+        for (int nt = 0; nt < NT; ++nt) ww[u][nt] = bld_sfrag(wr, (int64_t)(ks + u) * NT + nt, l, ks + u < nks);
     }
   };
-  // stage the tile in the wave's LDS, read it back in fragment order
-  auto compute = [&](const XFrag (&zz)[NQ], const SFrag (&ww)[U][NW], int i) {
-    const int ks = i < 0 || i >= nst ? nks : stage_k(i);
+
+  // One stage; zz / ww are reloaded with the z rows / W_e fragments of stage i + 2.
+  auto body = [&](XFrag (&zz)[NQ], SFrag (&ww)[U][NW], int i) {
+    io_t* tile = reinterpret_cast<io_t*>(smem + (ZB == 2 ? (i & 1) : 0) * TILE);
+    if constexpr (ZB == 1) __syncthreads();  // the previous stage's readers of the single tile are done
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) tile_put8<SC>(s_z, q * (64 / CPR) + l / CPR, 8 * zch, zz[q]);
+    for (int q = 0; q < NQ; ++q) {
+      io_t* d = tile + zrow[q] * BC + wide_col(zrow[q], zc);
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = zz[q].v[e];
+#else
+      *reinterpret_cast<uint4*>(d) = __builtin_bit_cast(uint4, zz[q].v);
+#endif
+    }
+    load_z(zz, i + 2);
+    __syncthreads();  // the stage's tile is complete; the other buffer's readers are done
+    const int ks = (stage_col(i) + wave * SC) / 32;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = ks + u;
       XFrag f[MT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) f[mt] = tile_get8<SC>(s_z, 16 * mt + row16, 32 * u + 8 * grp);
+      for (int mt = 0; mt < MT; ++mt) {
+        const int row = 16 * mt + row16;
+        const io_t* p = tile + row * BC + wide_col(row, wave * SC + 32 * u + 8 * grp);
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[mt].v[e] = p[e];
+#else
+        f[mt].v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+#endif
+      }
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         SFrag w;
         if constexpr (PW) w = ww[u][nt];
-        else w = bld_sfrag(wr, (int64_t)k * NT + nt, l, i >= 0 && k < nks);
+        else w = bld_sfrag(wr, (int64_t)(ks + u) * NT + nt, l, ks + u < nks);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, f[mt], acc[mt][nt]);
       }
     }
+    load_w(ww, i + 2);
   };
 
   // Every memory operation sits in one unconditional loop body (the loop starts
   // two stages early on zeroed registers instead of after a prologue of loads),
   // which lets the compiler place each wait at its exact distance.
+  XFrag za[NQ], zb[NQ];
+  SFrag wa[U][NW], wb[U][NW];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) za[q] = zb[q] = xfrag_zero();
   if constexpr (PW) {
@@ -469,10 +494,8 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
       for (int nt = 0; nt < NT; ++nt) wa[u][nt] = wb[u][nt] = sfrag_zero();
   }
   for (int i = opaque(-2); i < nst; i += 2) {
-    compute(za, wa, i);
-    load(za, wa, i + 2);
-    compute(zb, wb, i + 1);
-    load(zb, wb, i + 3);
+    body(za, wa, i);
+    body(zb, wb, i + 1);
   }
   __syncthreads();  // the reduction area overlaps the tiles
   float (*s_red)[TOK][RPT + 4] = reinterpret_cast<float (*)[TOK][RPT + 4]>(smem);
@@ -640,6 +663,24 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
     load(xb, tt + 48);
     __builtin_amdgcn_sched_barrier(0);
   }
+}
+
+// sum_{c < cnt} p[c stride .. + 4), added in order of c; the loads of eight
+// terms are issued together.
+__device__ __forceinline__ float4 sum_ordered4(const float* __restrict__ p, int64_t stride, int cnt) {
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = 0; c0 < cnt; c0 += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      v[k] = c0 + k < cnt ? *reinterpret_cast<const float4*>(p + (int64_t)(c0 + k) * stride)
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      s.x += v[k].x; s.y += v[k].y; s.z += v[k].z; s.w += v[k].w;
+    }
+  }
+  return s;
 }
 
 // ============================================================ decode backward
@@ -858,11 +899,8 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
     if (gid >= T * nq) return;
     const int64_t t = gid / nq;
     const int j0 = (int)(gid % nq) * 4;
-    float s[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < ncg; ++c) {
-      const float4 p = *reinterpret_cast<const float4*>(gbp + ((int64_t)c * T + t) * RP + j0);
-      s[0] += p.x; s[1] += p.y; s[2] += p.z; s[3] += p.w;
-    }
+    const float4 p = sum_ordered4(gbp + t * RP + j0, T * RP, ncg);
+    float s[4] = {p.x, p.y, p.z, p.w};
     if (g_id) {
       float x[4];
       load_x4(g_id + t * ld_gid + j0, x);
@@ -879,13 +917,8 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
   const int j = ok ? (int)(cidx / nq) : 0;
   const int c0 = ok ? (int)(cidx % nq) * 4 : 0;
   const int g0 = q * ntg / 4, g1 = (q + 1) * ntg / 4;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (ok) {
-    for (int g = g0; g < g1; ++g) {
-      const float4 p = *reinterpret_cast<const float4*>(dwp + ((int64_t)g * RP + j) * n + c0);
-      acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
-    }
-  }
+  const float4 acc = ok ? sum_ordered4(dwp + ((int64_t)g0 * RP + j) * n + c0, (int64_t)RP * n, g1 - g0)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
   s_q[q][threadIdx.x & 63] = acc;
   __syncthreads();
   if (q == 0 && ok) {
@@ -1264,14 +1297,16 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
           make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
 }
 
-// dW_e (+)= sum_tg dwp[tg] in token-group order (blocks [0, nb_dw)), and
-// g_x[t][0:r] += g_b[t][0:r], rounded once (the remaining blocks, when g_x is
-// given apart from g_z).
+// Blocks [0, nb_dw): dW_e (+)= sum_tg dwp[tg]; a block covers 64 four-column
+// groups, its 4 thread quarters sum consecutive quarters of the token groups and
+// the quarters are added in order.  Remaining blocks (when g_x is given apart
+// from g_z): g_x[t][0:r] += g_b[t][0:r], rounded once.
 __global__ __launch_bounds__(256) void k_enc_bwd_fin(int64_t T, int n, int r, int RP,
                                                      const float* __restrict__ dwp, int ntg,
                                                      float* __restrict__ dW_e, int accumulate, int64_t nb_dw,
                                                      const io_t* __restrict__ g_b, io_t* __restrict__ g_x,
                                                      int64_t ld_gx) {
+  __shared__ float4 s_q[4][64];
   const int nq = r / 4;
   if ((int64_t)blockIdx.x >= nb_dw) {
     const int64_t gid = ((int64_t)blockIdx.x - nb_dw) * 256 + threadIdx.x;
@@ -1286,19 +1321,28 @@ __global__ __launch_bounds__(256) void k_enc_bwd_fin(int64_t T, int n, int r, in
     store_x4(g_x + t * ld_gx + j0, x);
     return;
   }
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (gid >= (int64_t)n * nq) return;
-  const int c = (int)(gid / nq);
-  const int j0 = (int)(gid % nq) * 4;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int g = 0; g < ntg; ++g) {
-    const float4 p = *reinterpret_cast<const float4*>(dwp + ((int64_t)g * n + c) * RP + j0);
-    acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
+  const int q = threadIdx.x >> 6;
+  const int64_t cidx = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
+  const bool ok = cidx < (int64_t)n * nq;
+  const int c = ok ? (int)(cidx / nq) : 0;
+  const int j0 = ok ? (int)(cidx % nq) * 4 : 0;
+  const int g0 = q * ntg / 4, g1 = (q + 1) * ntg / 4;
+  const float4 acc = ok ? sum_ordered4(dwp + ((int64_t)g0 * n + c) * RP + j0, (int64_t)n * RP, g1 - g0)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+  s_q[q][threadIdx.x & 63] = acc;
+  __syncthreads();
+  if (q == 0 && ok) {
+    float4 s = accumulate ? *reinterpret_cast<const float4*>(dW_e + (int64_t)c * r + j0)
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 tot = s_q[0][threadIdx.x];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      const float4 p = s_q[k][threadIdx.x];
+      tot.x += p.x; tot.y += p.y; tot.z += p.z; tot.w += p.w;
+    }
+    s.x += tot.x; s.y += tot.y; s.z += tot.z; s.w += tot.w;
+    *reinterpret_cast<float4*>(dW_e + (int64_t)c * r + j0) = s;
   }
-  float4 s = accumulate ? *reinterpret_cast<const float4*>(dW_e + (int64_t)c * r + j0)
-                        : make_float4(0.f, 0.f, 0.f, 0.f);
-  s.x += acc.x; s.y += acc.y; s.z += acc.z; s.w += acc.w;
-  *reinterpret_cast<float4*>(dW_e + (int64_t)c * r + j0) = s;
 }
 
 }  // namespace resbm
@@ -1443,7 +1487,7 @@ int32_t resbm_encode_fwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   char* w = (char*)ws;
   void* wf = w + p.ef_wf_off;
   const int64_t nprep = (int64_t)(n / 32) * p.NT * 64;
-  hipLaunchKernelGGL(k_enc_fwd_prep, dim3((unsigned)ceil_div(nprep, 256)), dim3(256), 0, s, W_e, n, r, p.NT, wf);
+  hipLaunchKernelGGL(k_enc_fwd_prep, dim3((unsigned)ceil_div(nprep, 64)), dim3(64), 0, s, W_e, n, r, p.NT, wf);
   const io_t* X = (const io_t*)x_attn;
   const io_t* Z = (const io_t*)z;
   io_t* B = (io_t*)b;
@@ -1563,7 +1607,7 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
 #define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, s)
   RESBM_DISPATCH_NT(p.NT, CALL)
 #undef CALL
-  const int64_t nb_dw = ceil_div((int64_t)n * (r / 4), 256);
+  const int64_t nb_dw = ceil_div((int64_t)n * (r / 4), 64);
   const int64_t nb_gx = (g_x && !fused) ? ceil_div(T * (r / 4), 256) : 0;
   hipLaunchKernelGGL(k_enc_bwd_fin, dim3((unsigned)(nb_dw + nb_gx)), dim3(256), 0, s, T, n, r, p.RP,
                      (const float*)dwp, p.eb_ntg, dW_e, accumulate, nb_dw, GB, (io_t*)g_x, ld_gx);

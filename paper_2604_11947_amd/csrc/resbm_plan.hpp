@@ -21,10 +21,10 @@
 #endif
 
 // The hardware hands consecutive blocks of a grid to the 8 XCDs in turn.  The
-// streaming kernels that read (encode_fwd, decode_bwd, encode_bwd) put the
-// token dimension first, so that each XCD sees every column range rather than
-// one narrow column strip of every row, and encode_fwd rotates the starting
-// column stage by block.
+// streaming kernels with 2-D grids (decode_bwd, encode_bwd) put the token
+// dimension first, so that each XCD sees every column range rather than one
+// narrow column strip of every row; encode_fwd blocks start their walk over
+// the columns at rotated stages.
 #ifndef RESBM_XCD_SPREAD
 #define RESBM_XCD_SPREAD 1
 #endif
