@@ -858,6 +858,12 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
   // one step past the range to add the last step's partials.  Step -1 stages
   // the payload rows of step 0.
   const int64_t nsteps = (t_end - t_begin + 31) / 32;
+  // The first (empty) step reads payload buffer 1 before any step has filled
+  // it; LDS starts with whatever the previous kernel left, and a NaN or Inf
+  // there would survive the product with the zero tile.  Both buffers start at
+  // zero (ordered before those reads by the first step's barrier).
+  for (int i = threadIdx.x; i < (int)(sizeof(s_b) / 16); i += kDbWaves * 64)
+    reinterpret_cast<uint4*>(&s_b[0][0])[i] = make_uint4(0, 0, 0, 0);
   Step sa, sb;
 #pragma unroll
   for (int q = 0; q < RPW; ++q) sa.gz[q] = sb.gz[q] = xfrag_zero();

@@ -55,10 +55,17 @@ def errors(gpu: np.ndarray, ref: np.ndarray, bf16_output: bool) -> dict:
     return {"rms": rms, "raw": raw / scale, "disc": disc / scale, "finite": bool(np.all(np.isfinite(gpu)))}
 
 
-def check(name: str, gpu, ref: np.ndarray, bf16_output: bool, bound: float = BF16_BOUND) -> dict:
+def check(name: str, gpu, ref: np.ndarray, bf16_output: bool, bound: float = BF16_BOUND,
+          scale: float | None = None) -> dict:
+    """Assert max error <= bound x RMS(ref) (x ``scale`` instead of RMS(ref) when given)."""
     g = f64(gpu) if isinstance(gpu, torch.Tensor) else gpu
     e = errors(g, ref, bf16_output)
-    say(f"    {name:10s} rms={e['rms']:.3e} raw={e['raw']:.2e} disc={e['disc']:.2e}")
+    if scale is not None and e["rms"] > 0:
+        k = e["rms"] / scale
+        e["raw"] *= k
+        e["disc"] *= k
+    say(f"    {name:10s} rms={e['rms']:.3e} raw={e['raw']:.2e} disc={e['disc']:.2e}"
+        + (f" (vs abs-sum rms {scale:.3e})" if scale is not None else ""))
     assert e["finite"], f"{name}: non-finite values"
     assert e["disc"] <= bound, f"{name}: max err {e['disc']:.3e} RMS > {bound}"
     return e
