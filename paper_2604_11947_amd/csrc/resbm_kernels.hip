@@ -51,17 +51,38 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
   const uint32_t nb = bytes <= 0 ? 0u : (bytes > kMaxRange ? (uint32_t)kMaxRange : (uint32_t)bytes);
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nb, 0x00020000);
 }
+// Cache policy of the T x n streams, read or written once per op: non-temporal
+// loads, and non-temporal device-scope stores (streamed out instead of left
+// dirty in the caches for the next kernel to write back).  Everything reused
+// (weights, payload rows, partial sums) keeps the default policy.
+// (gfx950 cache-policy operand bits: 1 = sc0, 2 = nt, 16 = sc1; measured on the
+// four-op step: loads nt and stores nt|sc1 took it from ~196 to ~178 us, the
+// gain being mostly the next kernel's reads no longer competing with
+// write-backs of the previous kernel's output.)
+#ifndef RESBM_LD_STREAM
+#define RESBM_LD_STREAM 2   // nt
+#endif
+#ifndef RESBM_ST_STREAM
+#define RESBM_ST_STREAM 18  // nt | sc1
+#endif
+constexpr int kLdStream = RESBM_LD_STREAM;
+constexpr int kStStream = RESBM_ST_STREAM;
+
+template <int POL = 0>
 __device__ __forceinline__ uint4 bld16(rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, POL));
 }
+template <int POL = 0>
 __device__ __forceinline__ uint2 bld8(rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, POL));
 }
+template <int POL = 0>
 __device__ __forceinline__ void bst16(rsrc_t r, uint32_t off, uint4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, v), r, off, 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, v), r, off, 0, POL);
 }
+template <int POL = 0>
 __device__ __forceinline__ void bst8(rsrc_t r, uint32_t off, uint2 v) {
-  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, v), r, off, 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, v), r, off, 0, POL);
 }
 
 // Byte extent of rows [0, rows) of a row-major matrix with n used columns.
@@ -69,17 +90,17 @@ __device__ __forceinline__ int64_t rows_bytes(int64_t rows, int n, int64_t ld, i
   return rows > 0 ? ((rows - 1) * ld + n) * es : 0;
 }
 
-// 8 consecutive I/O elements at byte offset off.
+// 8 consecutive I/O elements of a streamed T x n matrix at byte offset off.
 __device__ __forceinline__ XFrag bld_x8(rsrc_t r, uint32_t off) {
   XFrag f;
 #if RESBM_IO_F32_BUILD
-  const uint4 a = bld16(r, off), b = bld16(r, off == kOOB ? kOOB : off + 16);
+  const uint4 a = bld16<kLdStream>(r, off), b = bld16<kLdStream>(r, off == kOOB ? kOOB : off + 16);
   f.v[0] = __builtin_bit_cast(float, a.x); f.v[1] = __builtin_bit_cast(float, a.y);
   f.v[2] = __builtin_bit_cast(float, a.z); f.v[3] = __builtin_bit_cast(float, a.w);
   f.v[4] = __builtin_bit_cast(float, b.x); f.v[5] = __builtin_bit_cast(float, b.y);
   f.v[6] = __builtin_bit_cast(float, b.z); f.v[7] = __builtin_bit_cast(float, b.w);
 #else
-  f.v = __builtin_bit_cast(bf16x8, bld16(r, off));
+  f.v = __builtin_bit_cast(bf16x8, bld16<kLdStream>(r, off));
 #endif
   return f;
 }
@@ -99,13 +120,14 @@ __device__ __forceinline__ void bld_x4(rsrc_t r, uint32_t off, float (&out)[4]) 
 #endif
 }
 
-// Rounds and stores CNT (4 or 8) consecutive values at byte offset off.
+// Rounds and stores CNT (4 or 8) consecutive values of a streamed T x n matrix
+// at byte offset off.
 template <int CNT>
 __device__ __forceinline__ void bst_n(rsrc_t r, uint32_t off, const float* v) {
 #if RESBM_IO_F32_BUILD
 #pragma unroll
   for (int q = 0; q < CNT / 4; ++q)
-    bst16(r, off == kOOB ? kOOB : off + 16 * q,
+    bst16<kStStream>(r, off == kOOB ? kOOB : off + 16 * q,
           make_uint4(__builtin_bit_cast(uint32_t, v[4 * q]), __builtin_bit_cast(uint32_t, v[4 * q + 1]),
                      __builtin_bit_cast(uint32_t, v[4 * q + 2]), __builtin_bit_cast(uint32_t, v[4 * q + 3])));
 #else
@@ -113,36 +135,37 @@ __device__ __forceinline__ void bst_n(rsrc_t r, uint32_t off, const float* v) {
     bf16x8 h;
 #pragma unroll
     for (int e = 0; e < 8; ++e) h[e] = to_bf16(v[e]);
-    bst16(r, off, __builtin_bit_cast(uint4, h));
+    bst16<kStStream>(r, off, __builtin_bit_cast(uint4, h));
   } else {
     bf16x4 h;
 #pragma unroll
     for (int e = 0; e < 4; ++e) h[e] = to_bf16(v[e]);
-    bst8(r, off, __builtin_bit_cast(uint2, h));
+    bst8<kStStream>(r, off, __builtin_bit_cast(uint2, h));
   }
 #endif
 }
 
-// Stores 8 consecutive I/O elements read from LDS at src (16-byte aligned).
+// Stores 8 consecutive I/O elements read from LDS at src (16-byte aligned) into
+// a streamed T x n matrix.
 __device__ __forceinline__ void bst_x8(rsrc_t r, uint32_t off, const io_t* src) {
 #if RESBM_IO_F32_BUILD
-  bst16(r, off, *reinterpret_cast<const uint4*>(src));
-  bst16(r, off == kOOB ? kOOB : off + 16, *reinterpret_cast<const uint4*>(src + 4));
+  bst16<kStStream>(r, off, *reinterpret_cast<const uint4*>(src));
+  bst16<kStStream>(r, off == kOOB ? kOOB : off + 16, *reinterpret_cast<const uint4*>(src + 4));
 #else
-  bst16(r, off, *reinterpret_cast<const uint4*>(src));
+  bst16<kStStream>(r, off, *reinterpret_cast<const uint4*>(src));
 #endif
 }
 
-// Stores the 8 elements of an exact fragment at byte offset off.
+// Stores the 8 elements of an exact fragment into a streamed T x n matrix.
 __device__ __forceinline__ void bst_frag(rsrc_t r, uint32_t off, const XFrag& f) {
 #if RESBM_IO_F32_BUILD
-  bst16(r, off, make_uint4(__builtin_bit_cast(uint32_t, f.v[0]), __builtin_bit_cast(uint32_t, f.v[1]),
+  bst16<kStStream>(r, off, make_uint4(__builtin_bit_cast(uint32_t, f.v[0]), __builtin_bit_cast(uint32_t, f.v[1]),
                            __builtin_bit_cast(uint32_t, f.v[2]), __builtin_bit_cast(uint32_t, f.v[3])));
-  bst16(r, off == kOOB ? kOOB : off + 16,
+  bst16<kStStream>(r, off == kOOB ? kOOB : off + 16,
         make_uint4(__builtin_bit_cast(uint32_t, f.v[4]), __builtin_bit_cast(uint32_t, f.v[5]),
                    __builtin_bit_cast(uint32_t, f.v[6]), __builtin_bit_cast(uint32_t, f.v[7])));
 #else
-  bst16(r, off, __builtin_bit_cast(uint4, f.v));
+  bst16<kStStream>(r, off, __builtin_bit_cast(uint4, f.v));
 #endif
 }
 
