@@ -437,9 +437,12 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Blocks start at different stages (rotating through all of them), so that
-  // concurrently running blocks read different column ranges.  Stages before 0
-  // or past the last load zeros and add nothing.
-  const int srot = (int)(blockIdx.x % (unsigned)nst);
+  // concurrently running blocks read different column ranges.  Consecutive
+  // blocks go to the 8 XCDs in turn, so the rotation steps every 8 blocks: the
+  // blocks sharing an XCD start at different stages (stepping with every block
+  // put all of an XCD's blocks on one column range; 2-3 us slower).  Stages
+  // before 0 or past the last load zeros and add nothing.
+  const int srot = (int)((blockIdx.x / 8u) % (unsigned)nst);
   auto stage_col = [&](int i) {  // first column of stage i, or n outside [0, nst)
     if (i < 0 || i >= nst) return n;
     const int ir = i + srot < nst ? i + srot : i + srot - nst;
@@ -789,13 +792,16 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
     XFrag gz[RPW];
     XFrag bp;
   };
-  auto load = [&](Step& st, int64_t s) {
+  auto load_gz = [&](Step& st, int64_t s) {
     const int64_t t0 = t_begin + 32 * s;
     const int64_t rows = s < 0 ? 0 : min((int64_t)32, t_end - t0);
     const rsrc_t gr = make_rsrc(g_zt + t0 * ld_g, rows_bytes(rows, n, ld_g, kEs));
 #pragma unroll
     for (int q = 0; q < RPW; ++q)
       st.gz[q] = bld_x8(gr, lon ? gz_lane + (uint32_t)(q * ld_g * kEs) : kOOB);
+  };
+  auto load_bp = [&](Step& st, int64_t s) {
+    const int64_t t0 = t_begin + 32 * s;
     const int64_t rows1 = s + 1 < 0 ? 0 : min((int64_t)32, t_end - t0 - 32);
     const rsrc_t br = make_rsrc(b + (t0 + 32) * r, rows1 > 0 ? rows1 * r * kEs : 0);
     st.bp = bld_r8(br, bthr ? (uint32_t)(btt * r * kEs) : kOOB, r, 16 * jt0 + 8 * bch);
@@ -818,10 +824,11 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
       *reinterpret_cast<uint4*>(d) = __builtin_bit_cast(uint4, st.gz[q].v);
 #endif
     }
+    load_gz(st, s + 2);  // in flight across the barrier
     __syncthreads();  // the step's tile, its payload rows and the previous step's partials are complete
     // the next step's payload rows go to the other buffer (its readers passed this barrier)
     if (bthr) tile_put8<JW>(s_b[(s + 1) & 1], btt, 8 * bch, st.bp);
-    load(st, s + 2);
+    load_bp(st, s + 2);
     // add the previous step's 8 partials of g_b in wave order; rows outside the range are dropped
     {
       const int64_t t0 = t_begin + 32 * (s - 1);
