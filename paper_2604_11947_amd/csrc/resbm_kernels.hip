@@ -558,19 +558,26 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
   }
 }
 
-// ============================================================ decode forward
-// z~ = b W_d (+ b I_{r x n} when ADD).  A wave owns columns [c0, c0 + 16 CT) (see
-// expand_col) and walks the token range [blockIdx.y tpg, ...) 16 tokens at a time.
-template <int KS, int CT, bool ADD>
-__global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
-                                                 const io_t* __restrict__ b, const float* __restrict__ W_d,
-                                                 io_t* __restrict__ zt, int64_t ld_zt, int tpg) {
-  constexpr int W = CT >= 2 ? 8 : 4;      // consecutive columns per lane run
+// ============================================================ expand contractions
+// out = in W (+ idsrc I_{r x n} when ADD), an r-wide input times an r x n map:
+//   decode_fwd (GZ = false): z~ = b W_d (+ b I_{r x n}, reading A); in = b, W = W_d [r][n];
+//   encode_bwd (GZ = true):  g_z = g_h W_e^T (+ g_b I_{r x n} when g_x is g_z);
+//     in = g_h as hi and lo bf16 planes [T][r] (one fp32 plane in the fp32 build),
+//     W = W_e [n][r].
+// A wave owns columns [c0, c0 + 16 CT) (see expand_col) and walks the token range
+// [blockIdx.y tpg, ...) 16 tokens at a time.
+template <int KS, int CT, bool ADD, bool GZ>
+__global__ __launch_bounds__(256) void k_expand(int64_t T, int n, int r,
+                                                const io_t* __restrict__ in, const io_t* __restrict__ in_lo,
+                                                const io_t* __restrict__ idsrc, const float* __restrict__ W,
+                                                io_t* __restrict__ out, int64_t ld_out, int tpg) {
+  constexpr int W8 = CT >= 2 ? 8 : 4;       // consecutive columns per lane run
   constexpr int NH = CT >= 2 ? CT / 2 : 1;  // runs per lane
-  constexpr int NI = ADD ? NH * W / 4 : 1;  // 4-column identity chunks per lane
+  constexpr int NI = ADD ? NH * W8 / 4 : 1;  // 4-column identity chunks per lane
   constexpr int WC = 16 * CT;               // columns of the wave
   constexpr int CPR = WC / 8;               // 8-element chunks per output row
   constexpr int NS = (16 * CPR + 63) / 64;  // coalesced stores per lane per tile
+  constexpr bool LO = GZ && !RESBM_IO_F32_BUILD;  // a second (lo) input plane
   __shared__ __attribute__((aligned(16))) io_t s_out[4][16 * WC];
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   io_t* tile = s_out[wave];
@@ -579,6 +586,7 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
   const int c0 = strip * 16 * CT;
   if (c0 >= n) return;  // whole strips only: n % 64 == 0 and 16 CT divides 64
 
+  // the map as the A operand: lane (row16, grp) holds W(k = 32 ks + 8 grp + e, column)
   SFrag wfr[KS][CT];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
@@ -589,21 +597,24 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int k = ks * 32 + grp * 8 + e;
-        w[e] = k < r ? W_d[(int64_t)k * n + col] : 0.0f;
+        w[e] = k < r ? (GZ ? W[(int64_t)col * r + k] : W[(int64_t)k * n + col]) : 0.0f;
       }
       wfr[ks][ct] = sfrag_from(w);
     }
 
   const int64_t t_begin = (int64_t)tgi * tpg;
   const int64_t rows = min((int64_t)tpg, T - t_begin);
-  const rsrc_t br = make_rsrc(b + t_begin * r, rows * r * kEs);
-  const rsrc_t zr = make_rsrc(zt + t_begin * ld_zt, rows_bytes(rows, n, ld_zt, kEs));
-  const int cl = c0 + W * grp;  // first column of this lane's run 0
+  const rsrc_t br = make_rsrc(in + t_begin * r, rows * r * kEs);
+  const rsrc_t lr = make_rsrc(LO ? in_lo + t_begin * r : in, LO ? rows * r * kEs : 0);
+  const rsrc_t ir = make_rsrc(idsrc + t_begin * r, ADD ? rows * r * kEs : 0);
+  const rsrc_t zr = make_rsrc(out + t_begin * ld_out, rows_bytes(rows, n, ld_out, kEs));
+  const int cl = c0 + W8 * grp;  // first column of this lane's run 0
 
   struct Tile {
     XFrag p[KS];
+    XFrag q[LO ? KS : 1];  // lo plane
 #if RESBM_IO_F32_BUILD
-    uint4 id[NI];  // reading A: b[t][column chunk] below r, zeros elsewhere (raw bits)
+    uint4 id[NI];  // idsrc[t][column chunk] below r, zeros elsewhere (raw bits)
 #else
     uint2 id[NI];
 #endif
@@ -612,16 +623,19 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
     const int64_t t = tt + row16;
     const uint32_t ro = (uint32_t)(t * r * kEs);  // rows >= `rows` are out of range
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) x.p[ks] = bld_r8(br, ro, r, ks * 32 + grp * 8);
+    for (int ks = 0; ks < KS; ++ks) {
+      x.p[ks] = bld_r8(br, ro, r, ks * 32 + grp * 8);
+      if constexpr (LO) x.q[ks] = bld_r8(lr, ro, r, ks * 32 + grp * 8);
+    }
     if constexpr (ADD) {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        const int cb = cl + 32 * (i / (W / 4)) + 4 * (i % (W / 4));
+        const int cb = cl + 32 * (i / (W8 / 4)) + 4 * (i % (W8 / 4));
         const uint32_t o = cb < r ? (uint32_t)((t * r + cb) * kEs) : kOOB;
 #if RESBM_IO_F32_BUILD
-        x.id[i] = bld16(br, o);
+        x.id[i] = bld16(ir, o);
 #else
-        x.id[i] = bld8(br, o);
+        x.id[i] = bld8(ir, o);
 #endif
       }
     }
@@ -631,18 +645,32 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+    for (int ks = 0; ks < KS; ++ks) {
+      if constexpr (GZ) {
+        SFrag g;  // the split input
+#if RESBM_IO_F32_BUILD
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_sx(wfr[ks][ct], x.p[ks], acc[ct]);
+        for (int e = 0; e < 8; ++e) g.v[e] = x.p[ks].v[e];
+#else
+        g.hi = x.p[ks].v;
+        g.lo = x.q[ks].v;
+#endif
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_ss(wfr[ks][ct], g, acc[ct]);
+      } else {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_sx(wfr[ks][ct], x.p[ks], acc[ct]);
+      }
+    }
     const int64_t t = tt + row16;
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
-      float v[W];
+      float v[W8];
 #pragma unroll
-      for (int q = 0; q < W / 4; ++q) {
-        float id[4] = {0.f, 0.f, 0.f, 0.f};  // reading A
+      for (int q = 0; q < W8 / 4; ++q) {
+        float id[4] = {0.f, 0.f, 0.f, 0.f};
         if constexpr (ADD) {
-          const auto u = x.id[h * (W / 4) + q];
+          const auto u = x.id[h * (W8 / 4) + q];
 #if RESBM_IO_F32_BUILD
           id[0] = __builtin_bit_cast(float, u.x); id[1] = __builtin_bit_cast(float, u.y);
           id[2] = __builtin_bit_cast(float, u.z); id[3] = __builtin_bit_cast(float, u.w);
@@ -657,15 +685,16 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
       // round into the wave's tile (row = token)
       io_t* d = tile + row16 * WC + tile_col<WC>(row16, cl - c0 + 32 * h);
 #pragma unroll
-      for (int e = 0; e < W; ++e) d[e] = f32_to_io(v[e]);
+      for (int e = 0; e < W8; ++e) d[e] = f32_to_io(v[e]);
     }
+    (void)t;
     // write the tile out row by row, 8 lanes per 128 bytes
 #pragma unroll
     for (int q = 0; q < NS; ++q) {
       const int idx = l + 64 * q;
       const int row = idx / CPR, c8 = 8 * (idx % CPR);
       const XFrag o = tile_get8<WC>(tile, row < 16 ? row : 0, c8);
-      bst_frag(zr, (tt < 0 || row >= 16) ? kOOB : (uint32_t)(((tt + row) * ld_zt + c0 + c8) * kEs), o);
+      bst_frag(zr, (tt < 0 || row >= 16) ? kOOB : (uint32_t)(((tt + row) * ld_out + c0 + c8) * kEs), o);
     }
   };
 
@@ -675,6 +704,10 @@ __global__ __launch_bounds__(256) void k_dec_fwd(int64_t T, int n, int r,
   Tile xa, xb;
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) xa.p[ks] = xb.p[ks] = xfrag_zero();
+  if constexpr (LO) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) xa.q[ks] = xb.q[ks] = xfrag_zero();
+  }
   if constexpr (ADD) {
 #pragma unroll
     for (int i = 0; i < NI; ++i) xa.id[i] = xb.id[i] = {};
@@ -972,16 +1005,18 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
 }
 
 // ============================================================ encode backward
-// A block has CW x TW waves.  Wave (cw, tw) owns the 16 CT columns starting at
-// bc0 + cw 16 CT and, in every block step of 32 TW tokens, the 32 tokens
-// starting at t0 + 32 tw.  Per block step:
+// Two streams, one kernel each: k_enc_bwd reads z for dW_e, k_expand (GZ)
+// writes g_z; a read-only and a write-only pass each run closer to their own
+// bandwidth ceilings than one pass that does both.
+//
+// k_enc_bwd: a block has CW x TW waves.  Wave (cw, tw) owns the 16 CT columns
+// starting at bc0 + cw 16 CT and, in every block step of 32 TW tokens, the 32
+// tokens starting at t0 + 32 tw.  Per block step:
 //   1. the block forms g_h = g_b phi'(a) for the step's tokens in LDS, in split
-//      form, with zeros in the columns r .. 32 KS,
+//      form, with zeros in the columns r .. 32 KS (the blocks of column block 0
+//      also write it out, split, for k_expand),
 //   2. each wave stages its 32-token tile of z in wave-private LDS,
-//   3. g_z[t][c] = sum_j g_h[t][j] W_e[c][j]: A = W_e fragments held in
-//      registers, B = g_h rows from LDS; stored from the accumulators
-//      (+ g_b[t][c] for c < r when g_x is g_z),
-//   4. dW_e[c][j] += sum_t z[t][c] g_h[t][j]: A = g_h^T and B = z^T, both read
+//   3. dW_e[c][j] += sum_t z[t][c] g_h[t][j]: A = g_h^T and B = z^T, both read
 //      transposed from LDS, accumulated in registers over the token group.
 // All waves of a block read the same z rows at once, 32 CT x CW contiguous
 // bytes of each, and the block shares one copy of g_h.  The TW partial dW_e of
@@ -1065,29 +1100,25 @@ __device__ __forceinline__ SFrag gh_tr(const GhTile<TS, RPS>& t, int row0, int c
   return f;
 }
 
-template <int KS, int NT, int CT, int CW, int TW, bool SG, bool FUSED>
+template <int KS, int NT, int CT, int CW, int TW>
 __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int r, int RP, int silu,
                                                           const io_t* __restrict__ z, int64_t ld_z,
-                                                          const float* __restrict__ W_e,
                                                           const float* __restrict__ a_save,
-                                                          const io_t* __restrict__ g_b, io_t* __restrict__ g_z,
-                                                          int64_t ld_gz, float* __restrict__ dwp, int TB) {
+                                                          const io_t* __restrict__ g_b, io_t* __restrict__ gh_hi,
+                                                          io_t* __restrict__ gh_lo, float* __restrict__ dwp,
+                                                          int TB) {
   constexpr int EW = CW * TW, NTH = EW * 64;
   constexpr int WC = 16 * CT, BC = CW * WC;
   constexpr int TS = 32 * TW;
   constexpr int KP = 32 * KS, RPT = 16 * NT, RPS = KP + 8;
-  constexpr int W = CT >= 2 ? 8 : 4;       // consecutive g_z columns per lane run
-  constexpr int NH = CT >= 2 ? CT / 2 : 1;
   constexpr int ZQ = WC / 16;              // 8-element z chunks per lane per step
   constexpr int GQ = TS * KP / 4;          // 4-column chunks of the g_h tile
   constexpr int NCH = (GQ + NTH - 1) / NTH;
   constexpr int GH_BYTES = (int)sizeof(GhTile<TS, RPS>);
-  constexpr int GB_BYTES = FUSED ? TS * RPT * 4 : 0;
   constexpr int Z_BYTES = 32 * WC * (int)sizeof(io_t);
-  constexpr int MAIN_LDS = 2 * GH_BYTES + 2 * GB_BYTES + EW * Z_BYTES;
+  constexpr int MAIN_LDS = 2 * GH_BYTES + EW * Z_BYTES;
   constexpr int RED_LDS = (TW - 1) * BC * (RPT + 4) * 4;
   constexpr int LDS = MAIN_LDS > RED_LDS ? MAIN_LDS : RED_LDS;
-  constexpr int STORES = SG ? ZQ * (kEs == 2 ? 1 : 2) : 2 * NH * (kEs == 2 ? 1 : W / 4);  // g_z stores per step
   __shared__ __attribute__((aligned(16))) char smem[LDS];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
@@ -1102,24 +1133,7 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   const int64_t t_begin = (int64_t)tg * TB;
   const int64_t t_end = min(T, t_begin + TB);
   GhTile<TS, RPS>* s_gh = reinterpret_cast<GhTile<TS, RPS>*>(smem);
-  float (*s_gb)[TS][RPT] = reinterpret_cast<float (*)[TS][RPT]>(smem + 2 * GH_BYTES);
-  io_t* s_z = reinterpret_cast<io_t*>(smem + 2 * GH_BYTES + 2 * GB_BYTES + wave * Z_BYTES);
-
-  // W_e as the A operand of g_z: lane (row16, grp) holds W_e[col][32 ks + 8 grp + e], col = expand_col.
-  SFrag wef[KS][CT];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-      const int col = expand_col<CT>(wc0, ct, row16);
-      float w[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int j = ks * 32 + grp * 8 + e;
-        w[e] = (on && j < r) ? W_e[(int64_t)col * r + j] : 0.0f;
-      }
-      wef[ks][ct] = sfrag_from(w);
-    }
+  io_t* s_z = reinterpret_cast<io_t*>(smem + 2 * GH_BYTES + wave * Z_BYTES);
 
   f32x4 dw[CT][NT];
 #pragma unroll
@@ -1156,7 +1170,14 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
       g.a[i] = bld16(ar, ok ? (uint32_t)((tt * r + j0) * 4) : kOOB);  // zeros without SiLU
     }
   };
-  auto put_gh = [&](const Gin& g, int buf) {
+  // g_h of one block step into LDS (split); the blocks of column block 0 also
+  // write it to gh_hi / gh_lo for the g_z kernel (other blocks: empty range).
+  auto put_gh = [&](const Gin& g, int buf, int64_t s, int64_t t0) {
+    const int64_t grows = (cbi == 0 && s >= 0) ? min((int64_t)TS, t_end - t0) : 0;
+    const rsrc_t ghr = make_rsrc(gh_hi + t0 * r, grows * r * kEs);
+#if !RESBM_IO_F32_BUILD
+    const rsrc_t glr = make_rsrc(gh_lo + t0 * r, grows * r * kEs);
+#endif
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const int q = threadIdx.x + i * NTH;
@@ -1175,10 +1196,22 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = silu ? gbv[e] * silu_grad(av[e]) : gbv[e];
         gh_put4(s_gh[buf], tt, j0, v);
-        if constexpr (FUSED) {
-          if (j0 < RPT)
-            *reinterpret_cast<float4*>(&s_gb[buf][tt][j0]) = make_float4(gbv[0], gbv[1], gbv[2], gbv[3]);
+        const uint32_t go = j0 < r ? (uint32_t)((tt * r + j0) * kEs) : kOOB;
+#if RESBM_IO_F32_BUILD
+        bst16(ghr, go, make_uint4(__builtin_bit_cast(uint32_t, v[0]), __builtin_bit_cast(uint32_t, v[1]),
+                                  __builtin_bit_cast(uint32_t, v[2]), __builtin_bit_cast(uint32_t, v[3])));
+#else
+        bf16x4 h, lo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          __bf16 a, b;
+          split_hi_lo(v[e], a, b);
+          h[e] = a;
+          lo[e] = b;
         }
+        bst8(ghr, go, __builtin_bit_cast(uint2, h));
+        bst8(glr, go, __builtin_bit_cast(uint2, lo));
+#endif
       }
     }
   };
@@ -1200,7 +1233,7 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
     const int buf = (int)(s & 1);
     const int64_t t0 = t_begin + s * TS;
     const int64_t t0w = t0 + 32 * tw;
-    put_gh(gin, buf);
+    put_gh(gin, buf, s, t0);
     load_gin(gin, t0 + 2 * TS);
     wave_lds_fence();  // the previous step's reads of s_z are complete
 #pragma unroll
@@ -1224,60 +1257,6 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
       }
     }
 
-    // g_z for the two 16-token halves: D[c][t] = sum_j W_e[c][j] g_h[t][j]
-    const int64_t rows = s < 0 ? 0 : min((int64_t)32, t_end - t0w);
-    const rsrc_t gzr = make_rsrc(g_z + t0w * ld_gz, rows_bytes(rows, n, ld_gz, kEs));
-    if constexpr (SG) wave_lds_fence();  // the transposed reads of s_z above are complete
-#pragma unroll
-    for (int th = 0; th < 2; ++th) {
-      f32x4 acc[CT];
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const SFrag g = gh_row(s_gh[buf], 32 * tw + 16 * th + row16, 32 * ks + 8 * grp);
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_ss(wef[ks][ct], g, acc[ct]);
-      }
-      const int tt = 16 * th + row16;
-#pragma unroll
-      for (int h = 0; h < NH; ++h) {
-        float v[W];
-#pragma unroll
-        for (int q = 0; q < W / 4; ++q)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[4 * q + e] = acc[2 * h + q][e];
-        const int cc = 32 * h + W * grp;  // column within the wave's slice
-        if constexpr (FUSED) {
-          if (wc0 < r) {
-#pragma unroll
-            for (int e = 0; e < W; ++e)
-              if (wc0 + cc + e < r) v[e] += s_gb[buf][32 * tw + tt][wc0 + cc + e];
-          }
-        }
-        if constexpr (SG) {
-          // round into the wave's tile; written out row by row below
-          io_t o[W];
-#pragma unroll
-          for (int e = 0; e < W; ++e) o[e] = f32_to_io(v[e]);
-          io_t* d = s_z + tt * WC + tile_col<WC>(tt, cc);
-#pragma unroll
-          for (int e = 0; e < W; ++e) d[e] = o[e];
-        } else {
-          bst_n<W>(gzr, on ? (uint32_t)((tt * ld_gz + wc0 + cc) * kEs) : kOOB, v);
-        }
-      }
-    }
-    if constexpr (SG) {
-      wave_lds_fence();
-#pragma unroll
-      for (int q = 0; q < ZQ; ++q) {
-        const int idx = l + 64 * q;
-        const int tt = idx / (WC / 8), c8 = 8 * (idx % (WC / 8));
-        const io_t* src = s_z + tt * WC + tile_col<WC>(tt, c8);
-        bst_x8(gzr, on ? (uint32_t)((tt * ld_gz + wc0 + c8) * kEs) : kOOB, src);
-      }
-    }
   };
 
   // The z tiles and g_h inputs of two steps are in flight at all times.  The
@@ -1435,9 +1414,11 @@ void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, 
   constexpr int CT = df_ct(KS);
   dim3 grid(p.df_nwg, p.df_ngrp);
   if (add_id)
-    hipLaunchKernelGGL((k_dec_fwd<KS, CT, true>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, W_d, zt, ld, p.df_tpg);
+    hipLaunchKernelGGL((k_expand<KS, CT, true, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt,
+                       ld, p.df_tpg);
   else
-    hipLaunchKernelGGL((k_dec_fwd<KS, CT, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, W_d, zt, ld, p.df_tpg);
+    hipLaunchKernelGGL((k_expand<KS, CT, false, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt,
+                       ld, p.df_tpg);
 }
 
 template <int JT>
@@ -1454,22 +1435,27 @@ void launch_dec_bwd(const Plan& p, const io_t* b, const float* W_d, const io_t* 
 
 template <int NT>
 void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const float* W_e, const float* a_save,
-                    const io_t* g_b, io_t* g_z, int64_t ld_gz, int fused, float* dwp, hipStream_t st) {
+                    const io_t* g_b, io_t* g_z, int64_t ld_gz, int fused, float* dwp, io_t* gh_hi, io_t* gh_lo,
+                    hipStream_t st) {
   constexpr int KS = (NT + 1) / 2;
   constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS);
-  constexpr bool SG = eb_sg(KS);
 #if RESBM_XCD_SPREAD
   dim3 grid(p.eb_ntg, p.eb_ncb);
 #else
   dim3 grid(p.eb_ncb, p.eb_ntg);
 #endif
   const int silu = act == RESBM_ACT_SILU;
+  hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r, p.RP, silu, z,
+                     ld_z, a_save, g_b, gh_hi, gh_lo, dwp, p.eb_TB);
+  // g_z = g_h W_e^T (+ g_b I_{r x n} when g_x is g_z): the expand kernel of decode_fwd on the split g_h
+  constexpr int GCT = df_ct(KS);
+  dim3 ggrid(p.df_nwg, p.df_ngrp);
   if (fused)
-    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, SG, true>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
-                       p.RP, silu, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, dwp, p.eb_TB);
+    hipLaunchKernelGGL((k_expand<KS, GCT, true, true>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b,
+                       W_e, g_z, ld_gz, p.df_tpg);
   else
-    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW, SG, false>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r,
-                       p.RP, silu, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, dwp, p.eb_TB);
+    hipLaunchKernelGGL((k_expand<KS, GCT, false, true>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b,
+                       W_e, g_z, ld_gz, p.df_tpg);
 }
 
 #define RESBM_DISPATCH_NT(NTV, CALL) \
@@ -1636,11 +1622,13 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
     return RESBM_E_ALIAS;
   hipStream_t s = (hipStream_t)stream;
   float* dwp = (float*)((char*)ws + p.eb_dwp_off);
+  io_t* gh_hi = (io_t*)((char*)ws + p.eb_gh_off);
+  io_t* gh_lo = gh_hi + (RESBM_IO_F32_BUILD ? 0 : T * r);  // bf16 build: hi and lo planes
   const io_t* Z = (const io_t*)z;
   const io_t* GB = (const io_t*)g_b;
   io_t* GZ = (io_t*)g_z;
   const float* AS = act == RESBM_ACT_SILU ? a_save : nullptr;
-#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, s)
+#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, gh_hi, gh_lo, s)
   RESBM_DISPATCH_NT(p.NT, CALL)
 #undef CALL
   const int64_t nb_dw = ceil_div((int64_t)n * (r / 4), 64);

@@ -47,8 +47,8 @@ constexpr int kDbWC = 64;
 constexpr int db_jt(int NT) { return NT < 4 ? NT : 4; }
 
 // ---- encode_bwd: blocks of CW x TW waves; a wave owns 16*CT columns, a block
-// step covers 32*TW tokens; SG: g_z leaves through LDS in whole row segments.
-// Workspace: the dW_e partials of the token groups.
+// step covers 32*TW tokens (g_z is written by the decode_fwd expand kernel).
+// Workspace: the dW_e partials of the token groups, then g_h (split) for g_z.
 constexpr int eb_ct(int KS) { return KS <= 1 ? 4 : (KS <= 2 ? 2 : 1); }
 #ifndef RESBM_EB_CW
 #define RESBM_EB_CW 4
@@ -58,10 +58,6 @@ constexpr int eb_cw(int) { return RESBM_EB_CW; }
 #define RESBM_EB_TW 2
 #endif
 constexpr int eb_tw(int KS) { return KS <= 2 ? RESBM_EB_TW : 1; }
-#ifndef RESBM_EB_STAGE_GZ
-#define RESBM_EB_STAGE_GZ 1
-#endif
-constexpr bool eb_sg(int) { return RESBM_EB_STAGE_GZ != 0; }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
@@ -83,7 +79,7 @@ struct Plan {
   size_t db_gbp_off, db_dwp_off, db_ws;
 
   int eb_ct, eb_bc, eb_ncb, eb_TB, eb_ntg;
-  size_t eb_dwp_off, eb_ws;
+  size_t eb_dwp_off, eb_gh_off, eb_ws;
 
   size_t ws_total;
 };
@@ -144,7 +140,8 @@ inline Plan make_plan(int64_t T, int n, int r) {
     p.eb_ntg = (int)ceil_div(Tm, p.eb_TB);
   }
   p.eb_dwp_off = 0;
-  p.eb_ws = align_ws((size_t)p.eb_ntg * n * p.RP * 4);
+  p.eb_gh_off = align_ws((size_t)p.eb_ntg * n * p.RP * 4);
+  p.eb_ws = p.eb_gh_off + align_ws((size_t)Tm * r * 4);  // g_h, split into two bf16 planes (or one fp32)
 
   size_t m = p.ef_ws;
   if (p.db_ws > m) m = p.db_ws;
