@@ -59,14 +59,18 @@ def parse():
     return p.parse_args()
 
 
-KERNEL_OP = (("k_enc_fwd", "encode_fwd"), ("k_dec_fwd", "decode_fwd"), ("k_dec_bwd", "decode_bwd"),
-             ("k_enc_bwd", "encode_bwd"))
+KERNEL_OP = (("k_enc_fwd", "encode_fwd"), ("k_dec_bwd", "decode_bwd"), ("k_enc_bwd", "encode_bwd"))
 
 
 def kernel_op(name: str):
-    """The boundary op a kernel name belongs to (prologue and finishing kernels included)."""
+    """The boundary op a kernel name belongs to (prologue and finishing kernels included).
+    The expand kernel serves decode_fwd (last template flag false) and the g_z pass of
+    encode_bwd (true)."""
     import re
     base = re.sub(r"\(.*", "", name)
+    if "k_expand" in base:
+        gz = base.rstrip().endswith("true>") or re.search(r"k_expandI(?:Li\d+E){2}Lb[01]ELb1E", base) is not None
+        return "encode_bwd" if gz else "decode_fwd"
     for key, op in KERNEL_OP:
         if key in base or key.replace("_", "") in base.replace("_", ""):
             return op

@@ -581,8 +581,15 @@ __global__ __launch_bounds__(256) void k_expand(int64_t T, int n, int r,
   __shared__ __attribute__((aligned(16))) io_t s_out[4][16 * WC];
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
   io_t* tile = s_out[wave];
+#if RESBM_DF_TOKEN_FASTEST
+  // token groups vary fastest: the blocks of one token group share an XCD and
+  // its L2 holds their input rows once
+  const int strip = blockIdx.y * 4 + wave;
+  const int tgi = blockIdx.x;
+#else
   const int strip = blockIdx.x * 4 + wave;
   const int tgi = blockIdx.y;
+#endif
   const int c0 = strip * 16 * CT;
   if (c0 >= n) return;  // whole strips only: n % 64 == 0 and 16 CT divides 64
 
@@ -782,7 +789,7 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
   const int jt0 = blockIdx.z * JT;
   const int bc0 = cg * BW;
   const int wc0 = bc0 + wave * kDbWC;
-  const bool won = wc0 < n;  // n % 64 == 0: a wave's 64 columns are all in or all out
+  const bool won = wc0 < n;  // n % 64 == 0: a wave's columns lie in [0, n) in whole runs of 64
 
   // W_d as the A operand of g_b: lane (row16, grp) holds W_d[16 (jt0 + jt) + row16][wc0 + 32 ks + 8 grp + e].
   SFrag wdf[JT][KSW];
@@ -792,7 +799,7 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
     for (int ks = 0; ks < KSW; ++ks) {
       const int j = 16 * (jt0 + jt) + row16;
       float w[8];
-      if (won && j < r) {
+      if (wc0 + 32 * ks + 8 * grp < n && j < r) {
         const float4* p = reinterpret_cast<const float4*>(W_d + (int64_t)j * n + wc0 + 32 * ks + 8 * grp);
         const float4 a = p[0], c = p[1];
         w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w; w[4] = c.x; w[5] = c.y; w[6] = c.z; w[7] = c.w;
@@ -944,8 +951,9 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
       if (j >= r) continue;
 #pragma unroll
       for (int ct = 0; ct < CTW; ++ct)
-        *reinterpret_cast<float4*>(dwp + ((int64_t)tg * RP + j) * n + wc0 + 16 * ct + 4 * grp) =
-            make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
+        if (wc0 + 16 * ct < n)
+          *reinterpret_cast<float4*>(dwp + ((int64_t)tg * RP + j) * n + wc0 + 16 * ct + 4 * grp) =
+              make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
     }
   }
 }
@@ -1412,7 +1420,11 @@ template <int KS>
 void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, io_t* zt, int64_t ld,
                     hipStream_t st) {
   constexpr int CT = df_ct(KS);
+#if RESBM_DF_TOKEN_FASTEST
+  dim3 grid(p.df_ngrp, p.df_nwg);
+#else
   dim3 grid(p.df_nwg, p.df_ngrp);
+#endif
   if (add_id)
     hipLaunchKernelGGL((k_expand<KS, CT, true, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt,
                        ld, p.df_tpg);
@@ -1429,8 +1441,8 @@ void launch_dec_bwd(const Plan& p, const io_t* b, const float* W_d, const io_t* 
 #else
   dim3 grid(p.db_ncg, p.db_ntg, p.db_njg);
 #endif
-  hipLaunchKernelGGL((k_dec_bwd<JT>), grid, dim3(512), 0, st, p.T, p.n, p.r, p.RP, b, W_d, g, ld, gbp, dwp,
-                     p.db_TB);
+  hipLaunchKernelGGL((k_dec_bwd<JT>), grid, dim3(kDbWaves * 64), 0, st, p.T, p.n, p.r, p.RP, b, W_d, g, ld, gbp,
+                     dwp, p.db_TB);
 }
 
 template <int NT>
@@ -1449,7 +1461,11 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
                      ld_z, a_save, g_b, gh_hi, gh_lo, dwp, p.eb_TB);
   // g_z = g_h W_e^T (+ g_b I_{r x n} when g_x is g_z): the expand kernel of decode_fwd on the split g_h
   constexpr int GCT = df_ct(KS);
+#if RESBM_DF_TOKEN_FASTEST
+  dim3 ggrid(p.df_ngrp, p.df_nwg);
+#else
   dim3 ggrid(p.df_nwg, p.df_ngrp);
+#endif
   if (fused)
     hipLaunchKernelGGL((k_expand<KS, GCT, true, true>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b,
                        W_e, g_z, ld_gz, p.df_tpg);

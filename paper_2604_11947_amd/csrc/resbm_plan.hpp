@@ -8,7 +8,7 @@
 
 // Launch-shape targets, in waves (or workgroups) per compute unit.
 #ifndef RESBM_DF_WAVES_PER_CU
-#define RESBM_DF_WAVES_PER_CU 8
+#define RESBM_DF_WAVES_PER_CU 4
 #endif
 #ifndef RESBM_DB_WG_PER_CU
 #define RESBM_DB_WG_PER_CU 1
@@ -28,6 +28,9 @@
 #ifndef RESBM_XCD_SPREAD
 #define RESBM_XCD_SPREAD 1
 #endif
+#ifndef RESBM_DF_TOKEN_FASTEST
+#define RESBM_DF_TOKEN_FASTEST 1
+#endif
 
 namespace resbm {
 
@@ -36,14 +39,20 @@ constexpr size_t kWsAlign = 256;
 
 // ---- encode_fwd: a block owns 16*MT tokens; its KW waves split the n-contraction.
 constexpr int ef_mt(int NT) { return NT <= 2 ? RESBM_EF_MT_SMALL_R : (NT <= 4 ? 2 : 1); }
-constexpr int ef_kw(int NT) { return 8 * 16 * ef_mt(NT) * (16 * NT + 4) * 4 <= 73728 ? 8 : 4; }
+#ifndef RESBM_EF_KW
+#define RESBM_EF_KW 4
+#endif
+constexpr int ef_kw(int NT) { return 8 * 16 * ef_mt(NT) * (16 * NT + 4) * 4 <= 73728 ? RESBM_EF_KW : 4; }
 
 // ---- decode_fwd: a wave owns 16*CT columns and walks a token range.
 constexpr int df_ct(int KS) { return KS <= 2 ? 4 : (KS <= 4 ? 2 : 1); }
 
 // ---- decode_bwd: 8 waves x 64 columns per block, JT j-tiles (16 of r each) per pass.
-constexpr int kDbWaves = 8;
-constexpr int kDbWC = 64;
+#ifndef RESBM_DB_WAVES
+#define RESBM_DB_WAVES 8
+#endif
+constexpr int kDbWaves = RESBM_DB_WAVES;
+constexpr int kDbWC = 512 / kDbWaves;  // a block spans 512 columns (1 KiB of a bf16 row)
 constexpr int db_jt(int NT) { return NT < 4 ? NT : 4; }
 
 // ---- encode_bwd: blocks of CW x TW waves; a wave owns 16*CT columns, a block
