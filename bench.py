@@ -42,8 +42,10 @@ def op_bytes(T: int, n: int, r: int) -> dict:
 def parse():
     p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=200)
+    # the GPU reaches its steady clocks only after ~20 ms of this load; 200 steps
+    # (~35 ms, untimed) get it there (10 steps left the timed steps ~6 % slower)
+    p.add_argument("--warmup", type=int, default=200)
     p.add_argument("--workload", default=None, help="workload name (default: the headline n=4096 r=32)")
     p.add_argument("--sets", type=int, default=4, help="rotating input/output copies")
     p.add_argument("--act", default="silu", choices=["silu", "identity"])
