@@ -558,179 +558,6 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
   }
 }
 
-// ============================================================ expand contractions
-// out = in W (+ idsrc I_{r x n} when ADD), an r-wide input times an r x n map:
-//   decode_fwd (GZ = false): z~ = b W_d (+ b I_{r x n}, reading A); in = b, W = W_d [r][n];
-//   encode_bwd (GZ = true):  g_z = g_h W_e^T (+ g_b I_{r x n} when g_x is g_z);
-//     in = g_h as hi and lo bf16 planes [T][r] (one fp32 plane in the fp32 build),
-//     W = W_e [n][r].
-// A wave owns columns [c0, c0 + 16 CT) (see expand_col) and walks the token range
-// [blockIdx.y tpg, ...) 16 tokens at a time.
-template <int KS, int CT, bool ADD, bool GZ>
-__global__ __launch_bounds__(256) void k_expand(int64_t T, int n, int r,
-                                                const io_t* __restrict__ in, const io_t* __restrict__ in_lo,
-                                                const io_t* __restrict__ idsrc, const float* __restrict__ W,
-                                                io_t* __restrict__ out, int64_t ld_out, int tpg) {
-  constexpr int W8 = CT >= 2 ? 8 : 4;       // consecutive columns per lane run
-  constexpr int NH = CT >= 2 ? CT / 2 : 1;  // runs per lane
-  constexpr int NI = ADD ? NH * W8 / 4 : 1;  // 4-column identity chunks per lane
-  constexpr int WC = 16 * CT;               // columns of the wave
-  constexpr int CPR = WC / 8;               // 8-element chunks per output row
-  constexpr int NS = (16 * CPR + 63) / 64;  // coalesced stores per lane per tile
-  constexpr bool LO = GZ && !RESBM_IO_F32_BUILD;  // a second (lo) input plane
-  __shared__ __attribute__((aligned(16))) io_t s_out[4][16 * WC];
-  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
-  io_t* tile = s_out[wave];
-#if RESBM_DF_TOKEN_FASTEST
-  // token groups vary fastest: the blocks of one token group share an XCD and
-  // its L2 holds their input rows once
-  const int strip = blockIdx.y * 4 + wave;
-  const int tgi = blockIdx.x;
-#else
-  const int strip = blockIdx.x * 4 + wave;
-  const int tgi = blockIdx.y;
-#endif
-  const int c0 = strip * 16 * CT;
-  if (c0 >= n) return;  // whole strips only: n % 64 == 0 and 16 CT divides 64
-
-  // the map as the A operand: lane (row16, grp) holds W(k = 32 ks + 8 grp + e, column)
-  SFrag wfr[KS][CT];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-      const int col = expand_col<CT>(c0, ct, row16);
-      float w[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int k = ks * 32 + grp * 8 + e;
-        w[e] = k < r ? (GZ ? W[(int64_t)col * r + k] : W[(int64_t)k * n + col]) : 0.0f;
-      }
-      wfr[ks][ct] = sfrag_from(w);
-    }
-
-  const int64_t t_begin = (int64_t)tgi * tpg;
-  const int64_t rows = min((int64_t)tpg, T - t_begin);
-  const rsrc_t br = make_rsrc(in + t_begin * r, rows * r * kEs);
-  const rsrc_t lr = make_rsrc(LO ? in_lo + t_begin * r : in, LO ? rows * r * kEs : 0);
-  const rsrc_t ir = make_rsrc(idsrc + t_begin * r, ADD ? rows * r * kEs : 0);
-  const rsrc_t zr = make_rsrc(out + t_begin * ld_out, rows_bytes(rows, n, ld_out, kEs));
-  const int cl = c0 + W8 * grp;  // first column of this lane's run 0
-
-  struct Tile {
-    XFrag p[KS];
-    XFrag q[LO ? KS : 1];  // lo plane
-#if RESBM_IO_F32_BUILD
-    uint4 id[NI];  // idsrc[t][column chunk] below r, zeros elsewhere (raw bits)
-#else
-    uint2 id[NI];
-#endif
-  };
-  auto load = [&](Tile& x, int64_t tt) {  // tt: tile start relative to t_begin
-    const int64_t t = tt + row16;
-    const uint32_t ro = (uint32_t)(t * r * kEs);  // rows >= `rows` are out of range
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      x.p[ks] = bld_r8(br, ro, r, ks * 32 + grp * 8);
-      if constexpr (LO) x.q[ks] = bld_r8(lr, ro, r, ks * 32 + grp * 8);
-    }
-    if constexpr (ADD) {
-#pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        const int cb = cl + 32 * (i / (W8 / 4)) + 4 * (i % (W8 / 4));
-        const uint32_t o = cb < r ? (uint32_t)((t * r + cb) * kEs) : kOOB;
-#if RESBM_IO_F32_BUILD
-        x.id[i] = bld16(ir, o);
-#else
-        x.id[i] = bld8(ir, o);
-#endif
-      }
-    }
-  };
-  auto compute = [&](const Tile& x, int64_t tt) {
-    f32x4 acc[CT];
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if constexpr (GZ) {
-        SFrag g;  // the split input
-#if RESBM_IO_F32_BUILD
-#pragma unroll
-        for (int e = 0; e < 8; ++e) g.v[e] = x.p[ks].v[e];
-#else
-        g.hi = x.p[ks].v;
-        g.lo = x.q[ks].v;
-#endif
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_ss(wfr[ks][ct], g, acc[ct]);
-      } else {
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_sx(wfr[ks][ct], x.p[ks], acc[ct]);
-      }
-    }
-    const int64_t t = tt + row16;
-#pragma unroll
-    for (int h = 0; h < NH; ++h) {
-      float v[W8];
-#pragma unroll
-      for (int q = 0; q < W8 / 4; ++q) {
-        float id[4] = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (ADD) {
-          const auto u = x.id[h * (W8 / 4) + q];
-#if RESBM_IO_F32_BUILD
-          id[0] = __builtin_bit_cast(float, u.x); id[1] = __builtin_bit_cast(float, u.y);
-          id[2] = __builtin_bit_cast(float, u.z); id[3] = __builtin_bit_cast(float, u.w);
-#else
-          id[0] = bf16_bits_to_f32(u.x & 0xffffu); id[1] = bf16_bits_to_f32(u.x >> 16);
-          id[2] = bf16_bits_to_f32(u.y & 0xffffu); id[3] = bf16_bits_to_f32(u.y >> 16);
-#endif
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[4 * q + e] = ADD ? acc[2 * h + q][e] + id[e] : acc[2 * h + q][e];
-      }
-      // round into the wave's tile (row = token)
-      io_t* d = tile + row16 * WC + tile_col<WC>(row16, cl - c0 + 32 * h);
-#pragma unroll
-      for (int e = 0; e < W8; ++e) d[e] = f32_to_io(v[e]);
-    }
-    (void)t;
-    // write the tile out row by row, 8 lanes per 128 bytes
-#pragma unroll
-    for (int q = 0; q < NS; ++q) {
-      const int idx = l + 64 * q;
-      const int row = idx / CPR, c8 = 8 * (idx % CPR);
-      const XFrag o = tile_get8<WC>(tile, row < 16 ? row : 0, c8);
-      bst_frag(zr, (tt < 0 || row >= 16) ? kOOB : (uint32_t)(((tt + row) * ld_out + c0 + c8) * kEs), o);
-    }
-  };
-
-  // Every memory operation sits in one unconditional loop body: the loop starts
-  // two (empty) tiles early on zeroed registers instead of after a prologue of
-  // loads, so the compiler can place each wait at its exact distance.
-  Tile xa, xb;
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) xa.p[ks] = xb.p[ks] = xfrag_zero();
-  if constexpr (LO) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) xa.q[ks] = xb.q[ks] = xfrag_zero();
-  }
-  if constexpr (ADD) {
-#pragma unroll
-    for (int i = 0; i < NI; ++i) xa.id[i] = xb.id[i] = {};
-  }
-  // (the scheduling barriers keep the compiler from hoisting a tile's math
-  // above the loads issued before it, which would wait for those loads)
-  for (int64_t tt = opaque(-32); tt < rows; tt += 32) {
-    compute(xa, tt);
-    load(xa, tt + 32);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(xb, tt + 16);  // past the range: loads were zeros, stores are dropped
-    load(xb, tt + 48);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-}
-
 // sum_{c < cnt} p[c stride .. + 4), added in order of c; the loads of eight
 // terms are issued together.
 __device__ __forceinline__ float4 sum_ordered4(const float* __restrict__ p, int64_t stride, int cnt) {
@@ -1320,19 +1147,21 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
           make_float4(dw[ct][jt][0], dw[ct][jt][1], dw[ct][jt][2], dw[ct][jt][3]);
 }
 
-// Blocks [0, nb_dw): dW_e (+)= sum_tg dwp[tg]; a block covers 64 four-column
+// Finishing work of encode_bwd, one 256-thread block per call (bid = its index):
+// blocks [0, nb_dw): dW_e (+)= sum_tg dwp[tg]; a block covers 64 four-column
 // groups, its 4 thread quarters sum consecutive quarters of the token groups and
 // the quarters are added in order.  Remaining blocks (when g_x is given apart
-// from g_z): g_x[t][0:r] += g_b[t][0:r], rounded once.
-__global__ __launch_bounds__(256) void k_enc_bwd_fin(int64_t T, int n, int r, int RP,
-                                                     const float* __restrict__ dwp, int ntg,
-                                                     float* __restrict__ dW_e, int accumulate, int64_t nb_dw,
-                                                     const io_t* __restrict__ g_b, io_t* __restrict__ g_x,
-                                                     int64_t ld_gx) {
+// from g_z): g_x[t][0:r] += g_b[t][0:r], rounded once.  These blocks ride along
+// with the g_z pass (extra blocks of its launch), whose stream they do not touch.
+__device__ __forceinline__ void enc_bwd_fin_block(int64_t bid, int64_t T, int n, int r, int RP,
+                                                  const float* __restrict__ dwp, int ntg,
+                                                  float* __restrict__ dW_e, int accumulate, int64_t nb_dw,
+                                                  const io_t* __restrict__ g_b, io_t* __restrict__ g_x,
+                                                  int64_t ld_gx) {
   __shared__ float4 s_q[4][64];
   const int nq = r / 4;
-  if ((int64_t)blockIdx.x >= nb_dw) {
-    const int64_t gid = ((int64_t)blockIdx.x - nb_dw) * 256 + threadIdx.x;
+  if (bid >= nb_dw) {
+    const int64_t gid = (bid - nb_dw) * 256 + threadIdx.x;
     if (gid >= T * nq) return;
     const int64_t t = gid / nq;
     const int j0 = (int)(gid % nq) * 4;
@@ -1345,7 +1174,7 @@ __global__ __launch_bounds__(256) void k_enc_bwd_fin(int64_t T, int n, int r, in
     return;
   }
   const int q = threadIdx.x >> 6;
-  const int64_t cidx = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
+  const int64_t cidx = bid * 64 + (threadIdx.x & 63);
   const bool ok = cidx < (int64_t)n * nq;
   const int c = ok ? (int)(cidx / nq) : 0;
   const int j0 = ok ? (int)(cidx % nq) * 4 : 0;
@@ -1365,6 +1194,203 @@ __global__ __launch_bounds__(256) void k_enc_bwd_fin(int64_t T, int n, int r, in
     }
     s.x += tot.x; s.y += tot.y; s.z += tot.z; s.w += tot.w;
     *reinterpret_cast<float4*>(dW_e + (int64_t)c * r + j0) = s;
+  }
+}
+
+// ============================================================ expand contractions
+// out = in W (+ idsrc I_{r x n} when ADD), an r-wide input times an r x n map:
+//   decode_fwd (GZ = false): z~ = b W_d (+ b I_{r x n}, reading A); in = b, W = W_d [r][n];
+//   encode_bwd (GZ = true):  g_z = g_h W_e^T (+ g_b I_{r x n} when g_x is g_z);
+//     in = g_h as hi and lo bf16 planes [T][r] (one fp32 plane in the fp32 build),
+//     W = W_e [n][r].
+// A wave owns columns [c0, c0 + 16 CT) (see expand_col) and walks the token range
+// [blockIdx.y tpg, ...) 16 tokens at a time.
+// Finishing work that rides along with the g_z pass (GZ): the dW_e partial sums
+// and a separate g_x update, in extra rows of the grid (see enc_bwd_fin_block).
+struct FinArgs {
+  int RP;
+  const float* dwp;
+  int ntg;
+  float* dW_e;
+  int accumulate;
+  int64_t nb_dw, nb_all;
+  const io_t* g_b;
+  io_t* g_x;
+  int64_t ld_gx;
+};
+
+template <int KS, int CT, bool ADD, bool GZ>
+__global__ __launch_bounds__(256) void k_expand(int64_t T, int n, int r,
+                                                const io_t* __restrict__ in, const io_t* __restrict__ in_lo,
+                                                const io_t* __restrict__ idsrc, const float* __restrict__ W,
+                                                io_t* __restrict__ out, int64_t ld_out, int tpg, int main_y,
+                                                FinArgs fin) {
+  if constexpr (GZ) {
+    if ((int)blockIdx.y >= main_y) {  // a finishing block
+      const int64_t bid = (int64_t)(blockIdx.y - main_y) * gridDim.x + blockIdx.x;
+      if (bid < fin.nb_all)
+        enc_bwd_fin_block(bid, T, n, r, fin.RP, fin.dwp, fin.ntg, fin.dW_e, fin.accumulate, fin.nb_dw, fin.g_b,
+                          fin.g_x, fin.ld_gx);
+      return;
+    }
+  }
+  constexpr int W8 = CT >= 2 ? 8 : 4;       // consecutive columns per lane run
+  constexpr int NH = CT >= 2 ? CT / 2 : 1;  // runs per lane
+  constexpr int NI = ADD ? NH * W8 / 4 : 1;  // 4-column identity chunks per lane
+  constexpr int WC = 16 * CT;               // columns of the wave
+  constexpr int CPR = WC / 8;               // 8-element chunks per output row
+  constexpr int NS = (16 * CPR + 63) / 64;  // coalesced stores per lane per tile
+  constexpr bool LO = GZ && !RESBM_IO_F32_BUILD;  // a second (lo) input plane
+  __shared__ __attribute__((aligned(16))) io_t s_out[4][16 * WC];
+  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+  io_t* tile = s_out[wave];
+#if RESBM_DF_TOKEN_FASTEST
+  // token groups vary fastest: the blocks of one token group share an XCD and
+  // its L2 holds their input rows once
+  const int strip = blockIdx.y * 4 + wave;
+  const int tgi = blockIdx.x;
+#else
+  const int strip = blockIdx.x * 4 + wave;
+  const int tgi = blockIdx.y;
+#endif
+  const int c0 = strip * 16 * CT;
+  if (c0 >= n) return;  // whole strips only: n % 64 == 0 and 16 CT divides 64
+
+  // the map as the A operand: lane (row16, grp) holds W(k = 32 ks + 8 grp + e, column)
+  SFrag wfr[KS][CT];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      const int col = expand_col<CT>(c0, ct, row16);
+      float w[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = ks * 32 + grp * 8 + e;
+        w[e] = k < r ? (GZ ? W[(int64_t)col * r + k] : W[(int64_t)k * n + col]) : 0.0f;
+      }
+      wfr[ks][ct] = sfrag_from(w);
+    }
+
+  const int64_t t_begin = (int64_t)tgi * tpg;
+  const int64_t rows = min((int64_t)tpg, T - t_begin);
+  const rsrc_t br = make_rsrc(in + t_begin * r, rows * r * kEs);
+  const rsrc_t lr = make_rsrc(LO ? in_lo + t_begin * r : in, LO ? rows * r * kEs : 0);
+  const rsrc_t ir = make_rsrc(idsrc + t_begin * r, ADD ? rows * r * kEs : 0);
+  const rsrc_t zr = make_rsrc(out + t_begin * ld_out, rows_bytes(rows, n, ld_out, kEs));
+  const int cl = c0 + W8 * grp;  // first column of this lane's run 0
+
+  struct Tile {
+    XFrag p[KS];
+    XFrag q[LO ? KS : 1];  // lo plane
+#if RESBM_IO_F32_BUILD
+    uint4 id[NI];  // idsrc[t][column chunk] below r, zeros elsewhere (raw bits)
+#else
+    uint2 id[NI];
+#endif
+  };
+  auto load = [&](Tile& x, int64_t tt) {  // tt: tile start relative to t_begin
+    const int64_t t = tt + row16;
+    const uint32_t ro = (uint32_t)(t * r * kEs);  // rows >= `rows` are out of range
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      x.p[ks] = bld_r8(br, ro, r, ks * 32 + grp * 8);
+      if constexpr (LO) x.q[ks] = bld_r8(lr, ro, r, ks * 32 + grp * 8);
+    }
+    if constexpr (ADD) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int cb = cl + 32 * (i / (W8 / 4)) + 4 * (i % (W8 / 4));
+        const uint32_t o = cb < r ? (uint32_t)((t * r + cb) * kEs) : kOOB;
+#if RESBM_IO_F32_BUILD
+        x.id[i] = bld16(ir, o);
+#else
+        x.id[i] = bld8(ir, o);
+#endif
+      }
+    }
+  };
+  auto compute = [&](const Tile& x, int64_t tt) {
+    f32x4 acc[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if constexpr (GZ) {
+        SFrag g;  // the split input
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+        for (int e = 0; e < 8; ++e) g.v[e] = x.p[ks].v[e];
+#else
+        g.hi = x.p[ks].v;
+        g.lo = x.q[ks].v;
+#endif
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_ss(wfr[ks][ct], g, acc[ct]);
+      } else {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = mma_sx(wfr[ks][ct], x.p[ks], acc[ct]);
+      }
+    }
+    const int64_t t = tt + row16;
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      float v[W8];
+#pragma unroll
+      for (int q = 0; q < W8 / 4; ++q) {
+        float id[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (ADD) {
+          const auto u = x.id[h * (W8 / 4) + q];
+#if RESBM_IO_F32_BUILD
+          id[0] = __builtin_bit_cast(float, u.x); id[1] = __builtin_bit_cast(float, u.y);
+          id[2] = __builtin_bit_cast(float, u.z); id[3] = __builtin_bit_cast(float, u.w);
+#else
+          id[0] = bf16_bits_to_f32(u.x & 0xffffu); id[1] = bf16_bits_to_f32(u.x >> 16);
+          id[2] = bf16_bits_to_f32(u.y & 0xffffu); id[3] = bf16_bits_to_f32(u.y >> 16);
+#endif
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[4 * q + e] = ADD ? acc[2 * h + q][e] + id[e] : acc[2 * h + q][e];
+      }
+      // round into the wave's tile (row = token)
+      io_t* d = tile + row16 * WC + tile_col<WC>(row16, cl - c0 + 32 * h);
+#pragma unroll
+      for (int e = 0; e < W8; ++e) d[e] = f32_to_io(v[e]);
+    }
+    (void)t;
+    // write the tile out row by row, 8 lanes per 128 bytes
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+      const int idx = l + 64 * q;
+      const int row = idx / CPR, c8 = 8 * (idx % CPR);
+      const XFrag o = tile_get8<WC>(tile, row < 16 ? row : 0, c8);
+      bst_frag(zr, (tt < 0 || row >= 16) ? kOOB : (uint32_t)(((tt + row) * ld_out + c0 + c8) * kEs), o);
+    }
+  };
+
+  // Every memory operation sits in one unconditional loop body: the loop starts
+  // two (empty) tiles early on zeroed registers instead of after a prologue of
+  // loads, so the compiler can place each wait at its exact distance.
+  Tile xa, xb;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) xa.p[ks] = xb.p[ks] = xfrag_zero();
+  if constexpr (LO) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) xa.q[ks] = xb.q[ks] = xfrag_zero();
+  }
+  if constexpr (ADD) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) xa.id[i] = xb.id[i] = {};
+  }
+  // (the scheduling barriers keep the compiler from hoisting a tile's math
+  // above the loads issued before it, which would wait for those loads)
+  for (int64_t tt = opaque(-32); tt < rows; tt += 32) {
+    compute(xa, tt);
+    load(xa, tt + 32);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(xb, tt + 16);  // past the range: loads were zeros, stores are dropped
+    load(xb, tt + 48);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -1425,12 +1451,13 @@ void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, 
 #else
   dim3 grid(p.df_nwg, p.df_ngrp);
 #endif
+  const FinArgs none{};
   if (add_id)
     hipLaunchKernelGGL((k_expand<KS, CT, true, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt,
-                       ld, p.df_tpg);
+                       ld, p.df_tpg, (int)grid.y, none);
   else
     hipLaunchKernelGGL((k_expand<KS, CT, false, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt,
-                       ld, p.df_tpg);
+                       ld, p.df_tpg, (int)grid.y, none);
 }
 
 template <int JT>
@@ -1448,7 +1475,7 @@ void launch_dec_bwd(const Plan& p, const io_t* b, const float* W_d, const io_t* 
 template <int NT>
 void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const float* W_e, const float* a_save,
                     const io_t* g_b, io_t* g_z, int64_t ld_gz, int fused, float* dwp, io_t* gh_hi, io_t* gh_lo,
-                    hipStream_t st) {
+                    FinArgs fin, hipStream_t st) {
   constexpr int KS = (NT + 1) / 2;
   constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS);
 #if RESBM_XCD_SPREAD
@@ -1466,12 +1493,15 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
 #else
   dim3 ggrid(p.df_nwg, p.df_ngrp);
 #endif
+  // the finishing blocks follow in extra grid rows (dispatched after the g_z blocks, run beside them)
+  const int main_y = (int)ggrid.y;
+  ggrid.y += (unsigned)ceil_div(fin.nb_all, (int64_t)ggrid.x);
   if (fused)
     hipLaunchKernelGGL((k_expand<KS, GCT, true, true>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b,
-                       W_e, g_z, ld_gz, p.df_tpg);
+                       W_e, g_z, ld_gz, p.df_tpg, main_y, fin);
   else
     hipLaunchKernelGGL((k_expand<KS, GCT, false, true>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b,
-                       W_e, g_z, ld_gz, p.df_tpg);
+                       W_e, g_z, ld_gz, p.df_tpg, main_y, fin);
 }
 
 #define RESBM_DISPATCH_NT(NTV, CALL) \
@@ -1644,13 +1674,12 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   const io_t* GB = (const io_t*)g_b;
   io_t* GZ = (io_t*)g_z;
   const float* AS = act == RESBM_ACT_SILU ? a_save : nullptr;
-#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, gh_hi, gh_lo, s)
-  RESBM_DISPATCH_NT(p.NT, CALL)
-#undef CALL
   const int64_t nb_dw = ceil_div((int64_t)n * (r / 4), 64);
   const int64_t nb_gx = (g_x && !fused) ? ceil_div(T * (r / 4), 256) : 0;
-  hipLaunchKernelGGL(k_enc_bwd_fin, dim3((unsigned)(nb_dw + nb_gx)), dim3(256), 0, s, T, n, r, p.RP,
-                     (const float*)dwp, p.eb_ntg, dW_e, accumulate, nb_dw, GB, (io_t*)g_x, ld_gx);
+  const FinArgs fin{p.RP, dwp, p.eb_ntg, dW_e, accumulate, nb_dw, nb_dw + nb_gx, GB, (io_t*)g_x, ld_gx};
+#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, gh_hi, gh_lo, fin, s)
+  RESBM_DISPATCH_NT(p.NT, CALL)
+#undef CALL
   return launch_status();
 }
 
