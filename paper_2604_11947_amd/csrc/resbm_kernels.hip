@@ -700,16 +700,23 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
     {
       const int64_t t0 = t_begin + 32 * (s - 1);
       const rsrc_t pr = make_rsrc(gbp + ((int64_t)cg * T + t0) * RP, s - 1 < 0 ? 0 : (t_end - t0) * RP * 4);
+      // four consecutive j per thread (r % 4 == 0: all four in range or none)
 #pragma unroll
-      for (int idx0 = 0; idx0 < 32 * JW; idx0 += kDbWaves * 64) {
+      for (int idx0 = 0; idx0 < 32 * JW / 4; idx0 += kDbWaves * 64) {
         const int idx = idx0 + threadIdx.x;
-        const int tt = idx / JW, jj = idx % JW;
+        const int tt = idx / (JW / 4), jj = 4 * (idx % (JW / 4));
         const int j = 16 * jt0 + jj;
-        float v = 0.0f;
+        if (32 * JW / 4 % (kDbWaves * 64) == 0 || idx < 32 * JW / 4) {
+          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int w = 0; w < kDbWaves; ++w) v += s_gb[gprev][w][tt][jj];
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), pr,
-                                              j < r ? (uint32_t)((tt * RP + j) * 4) : kOOB, 0, 0);
+          for (int w = 0; w < kDbWaves; ++w) {
+            const float4 p = *reinterpret_cast<const float4*>(&s_gb[gprev][w][tt][jj]);
+            v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+          }
+          bst16(pr, j < r ? (uint32_t)((tt * RP + j) * 4) : kOOB,
+                make_uint4(__builtin_bit_cast(uint32_t, v.x), __builtin_bit_cast(uint32_t, v.y),
+                           __builtin_bit_cast(uint32_t, v.z), __builtin_bit_cast(uint32_t, v.w)));
+        }
       }
     }
     if constexpr (NBUF == 1) __syncthreads();  // the single partial buffer is refilled below

@@ -206,10 +206,11 @@ __device__ __forceinline__ float act_dphi(float a, int act) {
   return s * (1.0f + a * (1.0f - s));
 }
 
-// SiLU'(a) = s (1 + a (1 - s)), s = 1 / (1 + e^-a), with a hardware reciprocal
-// (1 ulp) in place of the division.
+// SiLU'(a) = s (1 + a (1 - s)), s = 1 / (1 + e^-a) = 1 / (1 + 2^(-a log2 e)),
+// with the hardware exp2 and reciprocal (about 1 ulp each) in place of expf and
+// a division; exp2 overflowing to inf gives s = 0, underflowing gives s = 1.
 __device__ __forceinline__ float silu_grad(float a) {
-  const float s = __builtin_amdgcn_rcpf(1.0f + expf(-a));
+  const float s = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-a * 1.44269504088896341f));
   return s * (1.0f + a * (1.0f - s));
 }
 
