@@ -855,15 +855,15 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
 // starting at bc0 + cw 16 CT and, in every block step of 32 TW tokens, the 32
 // tokens starting at t0 + 32 tw.  Per block step:
 //   1. the block forms g_h = g_b phi'(a) for the step's tokens in LDS, in split
-//      form, with zeros in the columns r .. 32 KS (the blocks of column block 0
-//      also write it out, split, for k_expand),
-//   2. each wave stages its 32-token tile of z in wave-private LDS,
+//      form, with zeros in the columns r .. 32 KS (each column block also writes
+//      its share of the rows out, split, for k_expand),
+//   2. the block loads the step's 32 TW x 16 CT CW tile of z cooperatively,
+//      whole row segments per load instruction, into a double-buffered LDS tile,
 //   3. dW_e[c][j] += sum_t z[t][c] g_h[t][j]: A = g_h^T and B = z^T, both read
 //      transposed from LDS, accumulated in registers over the token group.
-// All waves of a block read the same z rows at once, 32 CT x CW contiguous
-// bytes of each, and the block shares one copy of g_h.  The TW partial dW_e of
-// a column slice are added in LDS in wave order; k_enc_bwd_fin adds the token
-// groups in order.
+// One barrier per step covers the tile and g_h.  The TW partial dW_e of a
+// column slice are added in LDS in wave order; the finishing blocks add the
+// token groups in order.
 
 // Split g_h tile of TS tokens x RPS columns: bf16 build: hi and lo planes;
 // f32 build: one float plane.
@@ -953,12 +953,18 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   constexpr int WC = 16 * CT, BC = CW * WC;
   constexpr int TS = 32 * TW;
   constexpr int KP = 32 * KS, RPT = 16 * NT, RPS = KP + 8;
-  constexpr int ZQ = WC / 16;              // 8-element z chunks per lane per step
   constexpr int GQ = TS * KP / 4;          // 4-column chunks of the g_h tile
   constexpr int NCH = (GQ + NTH - 1) / NTH;
   constexpr int GH_BYTES = (int)sizeof(GhTile<TS, RPS>);
-  constexpr int Z_BYTES = 32 * WC * (int)sizeof(io_t);
-  constexpr int MAIN_LDS = 2 * GH_BYTES + EW * Z_BYTES;
+  constexpr int Z_BYTES = TS * BC * (int)sizeof(io_t);  // block tile of one step
+  constexpr int MAIN_LDS = 2 * GH_BYTES + 2 * Z_BYTES;
+  constexpr int LPR = BC / 8;                 // lanes per tile row
+  constexpr int NQ = TS * LPR / NTH;          // cooperative loads per lane and step
+  static_assert(TS * LPR % NTH == 0 && 64 % LPR == 0, "tile rows must split evenly over the block");
+  // wide_col needs rows of a multiple of 128 elements; narrower tiles (one
+  // token wave) use tile_col, whose rows hold 8 chunks
+  constexpr bool kWideZ = BC % 128 == 0;
+  static_assert(kWideZ || (TW == 1 && BC / 8 == 8), "narrow z tiles hold 32 rows of 8 chunks");
   constexpr int RED_LDS = (TW - 1) * BC * (RPT + 4) * 4;
   constexpr int LDS = MAIN_LDS > RED_LDS ? MAIN_LDS : RED_LDS;
   __shared__ __attribute__((aligned(16))) char smem[LDS];
@@ -967,15 +973,23 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   const int cw = wave % CW, tw = wave / CW;
 #if RESBM_XCD_SPREAD
   const int cbi = blockIdx.y, tg = blockIdx.x;  // token groups vary fastest: every XCD sees every column block
+  const int ncb = gridDim.y;
 #else
   const int cbi = blockIdx.x, tg = blockIdx.y;
+  const int ncb = gridDim.x;
 #endif
   const int wc0 = cbi * BC + cw * WC;
   const bool on = wc0 < n;  // whole waves fall inside or outside [0, n): n % 64 == 0, WC | 64
   const int64_t t_begin = (int64_t)tg * TB;
   const int64_t t_end = min(T, t_begin + TB);
   GhTile<TS, RPS>* s_gh = reinterpret_cast<GhTile<TS, RPS>*>(smem);
-  io_t* s_z = reinterpret_cast<io_t*>(smem + 2 * GH_BYTES + wave * Z_BYTES);
+  io_t* s_zb = reinterpret_cast<io_t*>(smem + 2 * GH_BYTES);
+  const int bc0 = cbi * BC;
+  const int bcv = min(BC, n - bc0);  // valid columns of the block (a multiple of 64, or <= 0)
+  const int zc = 8 * (l % LPR);
+  int zrow[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) zrow[q] = (wave * NQ * 64 + q * 64 + l) / LPR;
 
   f32x4 dw[CT][NT];
 #pragma unroll
@@ -1012,10 +1026,12 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
       g.a[i] = bld16(ar, ok ? (uint32_t)((tt * r + j0) * 4) : kOOB);  // zeros without SiLU
     }
   };
-  // g_h of one block step into LDS (split); the blocks of column block 0 also
-  // write it to gh_hi / gh_lo for the g_z kernel (other blocks: empty range).
+  // g_h of one block step into LDS (split).  Every column block forms the same
+  // g_h; row tt of the step also goes to gh_hi / gh_lo for the g_z kernel from
+  // column block tt mod ncb (one writer per row), which spreads those writes
+  // over the grid.
   auto put_gh = [&](const Gin& g, int buf, int64_t s, int64_t t0) {
-    const int64_t grows = (cbi == 0 && s >= 0) ? min((int64_t)TS, t_end - t0) : 0;
+    const int64_t grows = s >= 0 ? min((int64_t)TS, t_end - t0) : 0;
     const rsrc_t ghr = make_rsrc(gh_hi + t0 * r, grows * r * kEs);
 #if !RESBM_IO_F32_BUILD
     const rsrc_t glr = make_rsrc(gh_lo + t0 * r, grows * r * kEs);
@@ -1038,7 +1054,7 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = silu ? gbv[e] * silu_grad(av[e]) : gbv[e];
         gh_put4(s_gh[buf], tt, j0, v);
-        const uint32_t go = j0 < r ? (uint32_t)((tt * r + j0) * kEs) : kOOB;
+        const uint32_t go = j0 < r && tt % ncb == cbi ? (uint32_t)((tt * r + j0) * kEs) : kOOB;
 #if RESBM_IO_F32_BUILD
         bst16(ghr, go, make_uint4(__builtin_bit_cast(uint32_t, v[0]), __builtin_bit_cast(uint32_t, v[1]),
                                   __builtin_bit_cast(uint32_t, v[2]), __builtin_bit_cast(uint32_t, v[3])));
@@ -1057,40 +1073,44 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
       }
     }
   };
-  auto load_z = [&](XFrag (&zz)[ZQ], int64_t t0w) {
-    const int64_t rows = min((int64_t)32, t_end - t0w);  // <= 0 past the range: zeros
-    const rsrc_t zr = make_rsrc(z + t0w * ld_z + wc0, on ? rows_bytes(rows, WC, ld_z, kEs) : 0);
+  auto load_z = [&](XFrag (&zz)[NQ], int64_t t0) {
+    const int64_t rows = min((int64_t)TS, t_end - t0);  // <= 0 past the range: zeros
+    const rsrc_t zr = make_rsrc(z + t0 * ld_z + bc0, bcv > 0 ? rows_bytes(rows, bcv, ld_z, kEs) : 0);
 #pragma unroll
-    for (int q = 0; q < ZQ; ++q) {
-      const int idx = l + 64 * q;
-      const int tt = idx / (WC / 8), ch = idx % (WC / 8);
-      zz[q] = bld_x8(zr, (uint32_t)((tt * ld_z + 8 * ch) * kEs));
-    }
+    for (int q = 0; q < NQ; ++q)
+      zz[q] = bld_x8(zr, zc < bcv ? (uint32_t)((zrow[q] * ld_z + zc) * kEs) : kOOB);
   };
 
   // One block step.  zz and gin hold this step's z tile and g_h inputs and are
   // reloaded with those of the step after next.  Steps outside [0, nsb) see
   // zero inputs and store nothing.
-  auto body = [&](int64_t s, XFrag (&zz)[ZQ], Gin& gin) {
+  auto body = [&](int64_t s, XFrag (&zz)[NQ], Gin& gin) {
     const int buf = (int)(s & 1);
     const int64_t t0 = t_begin + s * TS;
-    const int64_t t0w = t0 + 32 * tw;
+    io_t* tile = s_zb + buf * (TS * BC);
     put_gh(gin, buf, s, t0);
     load_gin(gin, t0 + 2 * TS);
-    wave_lds_fence();  // the previous step's reads of s_z are complete
+    // this buffer's readers (two steps back) passed the previous step's barrier
 #pragma unroll
-    for (int q = 0; q < ZQ; ++q) {
-      const int idx = l + 64 * q;
-      tile_put8<WC>(s_z, idx / (WC / 8), 8 * (idx % (WC / 8)), zz[q]);
+    for (int q = 0; q < NQ; ++q) {
+      io_t* d = tile + zrow[q] * BC + (kWideZ ? wide_col(zrow[q], zc) : tile_col<BC>(zrow[q], zc));
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = zz[q].v[e];
+#else
+      *reinterpret_cast<uint4*>(d) = __builtin_bit_cast(uint4, zz[q].v);
+#endif
     }
-    load_z(zz, t0w + 2 * TS);
-    __syncthreads();  // g_h of this step is complete; the buffer written next step is free
+    load_z(zz, t0 + 2 * TS);
+    __syncthreads();  // g_h and the z tile of this step are complete
 
     // dW_e: D[j][c] = sum_t g_h[t][j] z[t][c], A = g_h^T, B = z^T
     {
       XFrag zb[CT];
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct) zb[ct] = tr_frag<WC>(s_z, 16 * ct, row16, grp);
+      for (int ct = 0; ct < CT; ++ct)
+        zb[ct] = kWideZ ? tr_frag_wide<BC>(tile, 32 * tw, cw * WC + 16 * ct, row16, grp)
+                        : tr_frag<BC>(tile, cw * WC + 16 * ct, row16, grp);
 #pragma unroll
       for (int jt = 0; jt < NT; ++jt) {
         const SFrag g = gh_tr(s_gh[buf], 32 * tw, 16 * jt, row16, grp);
@@ -1108,14 +1128,14 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   // place each wait at its exact distance.
   const int64_t nsb = (t_end - t_begin + TS - 1) / TS;
   Gin ga, gb;
-  XFrag z0[ZQ], z1[ZQ];
+  XFrag z0[NQ], z1[NQ];
 #pragma unroll
   for (int i = 0; i < NCH; ++i) {
     ga.gb[i] = gb.gb[i] = {};
     ga.a[i] = gb.a[i] = make_uint4(0, 0, 0, 0);
   }
 #pragma unroll
-  for (int q = 0; q < ZQ; ++q) z0[q] = z1[q] = xfrag_zero();
+  for (int q = 0; q < NQ; ++q) z0[q] = z1[q] = xfrag_zero();
   for (int64_t s = opaque(-2); s < nsb; s += 2) {
     body(s, z0, ga);
     body(s + 1, z1, gb);
