@@ -4,3 +4,4 @@ Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
 import this package; the product path never does.
 """
 from .resbm_oracle import *  # noqa: F401,F403
+from . import muon_oracle  # noqa: F401

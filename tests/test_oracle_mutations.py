@@ -66,3 +66,71 @@ def test_pin_rejects_planted_mistake(monkeypatch, name, bad, pin):
     monkeypatch.setattr(O, name, bad)
     with pytest.raises(AssertionError):
         pin()
+
+
+# ------------------------------------------------ optimizer-side oracle (Muon)
+from oracle import muon_oracle as MU  # noqa: E402
+import test_muon_oracle_pins as MP  # noqa: E402
+
+
+def _ns_no_quintic_term(U, steps=5, coeffs=MU.NS_QUINTIC, eps=MU.NS_EPS):
+    a, b, c = coeffs
+    tall = U.shape[0] > U.shape[1]
+    X = U.T if tall else U
+    X = X / (np.sqrt(np.sum(X * X)) + eps)
+    for _ in range(steps):
+        X = a * X + b * (X @ X.T) @ X
+    return X.T if tall else X
+
+
+def _ns_max_norm(U, steps=5, coeffs=MU.NS_QUINTIC, eps=MU.NS_EPS):
+    a, b, c = coeffs
+    tall = U.shape[0] > U.shape[1]
+    X = U.T if tall else U
+    X = X / (np.abs(X).max() + eps)
+    with np.errstate(all="ignore"):  # the wrong normalisation can diverge
+        for _ in range(steps):
+            A = X @ X.T
+            X = a * X + (b * A + c * (A @ A)) @ X
+    return X.T if tall else X
+
+
+def _muon_no_momentum_factor(W, G, M, lr, momentum, weight_decay=0.0, scale=None, nesterov=False, steps=5,
+                             coeffs=MU.NS_QUINTIC, eps=MU.NS_EPS):
+    scale = MU.default_scale(*np.shape(W)) if scale is None else scale
+    M_new = MU.to_f32(np.asarray(M) + G)
+    U = G + momentum * M_new if nesterov else M_new
+    O = MU.newton_schulz(U, steps, coeffs, eps)
+    return MU.to_f32(W - lr * (scale * O + weight_decay * W)), M_new, O
+
+
+def _muon_nesterov_ignored(W, G, M, lr, momentum, weight_decay=0.0, scale=None, nesterov=False, steps=5,
+                           coeffs=MU.NS_QUINTIC, eps=MU.NS_EPS):
+    scale = MU.default_scale(*np.shape(W)) if scale is None else scale
+    M_new = MU.to_f32(momentum * np.asarray(M) + G)
+    O = MU.newton_schulz(M_new, steps, coeffs, eps)
+    return MU.to_f32(W - lr * (scale * O + weight_decay * W)), M_new, O
+
+
+def _spectrum_unsquared(W):
+    sigma = np.linalg.svd(np.asarray(W, dtype=np.float64), compute_uv=False)
+    return sigma, float(np.sum(sigma) / sigma[0]) if sigma.size and sigma[0] > 0 else 0.0
+
+
+MUON_MUTATIONS = [
+    ("newton_schulz", _ns_no_quintic_term,
+     lambda: MP.test_newton_schulz_acts_on_singular_values(64, 8, False, MU.NS_QUINTIC, 5)),
+    ("newton_schulz", _ns_max_norm,
+     lambda: MP.test_newton_schulz_acts_on_singular_values(40, 40, True, MU.NS_CUBIC, 7)),
+    ("muon_update", _muon_no_momentum_factor, MP.test_muon_update_momentum_recurrence_and_direction),
+    ("muon_update", _muon_nesterov_ignored, MP.test_muon_update_momentum_recurrence_and_direction),
+    ("spectrum", _spectrum_unsquared, lambda: MP.test_spectrum_of_built_matrices(90, 9)),
+]
+
+
+@pytest.mark.parametrize("name,bad,pin", MUON_MUTATIONS,
+                         ids=[f"{m[0]}:{m[1].__name__.lstrip('_')}" for m in MUON_MUTATIONS])
+def test_muon_pin_rejects_planted_mistake(monkeypatch, name, bad, pin):
+    monkeypatch.setattr(MU, name, bad)
+    with pytest.raises(AssertionError):
+        pin()
