@@ -54,7 +54,7 @@ extern "C" {
 #define RESBM_E_NULL       -1  /* a required pointer is NULL                    */
 #define RESBM_E_SHAPE      -2  /* T, n, r or a leading dimension breaks a rule  */
 #define RESBM_E_ALIGN      -3  /* a pointer is not aligned as required          */
-#define RESBM_E_WORKSPACE  -4  /* ws_bytes < resbm_workspace_bytes(T, n, r)     */
+#define RESBM_E_WORKSPACE  -4  /* ws_bytes below the op's workspace size         */
 #define RESBM_E_ACT        -5  /* unknown act, or SiLU backward without a_save  */
 #define RESBM_E_HIP        -6  /* a kernel launch failed                        */
 #define RESBM_E_ALIAS      -7  /* an output aliases an input it may not alias   */
@@ -144,8 +144,71 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act,
                          float* dW_e, int32_t accumulate,
                          void* ws, size_t ws_bytes, void* stream);
 
-/* Workspace bytes every op above needs for (T, n, r): the maximum over the
- * four ops, a multiple of 256.  Returns 0 when (n, r) break the shape rules. */
+/*
+ * Optimizer-side ops on one bottleneck weight (W_e, n x r, or W_d, r x n).
+ * Sec. 3.4 trains the bottleneck weights with Muon -- the gradient momentum of
+ * a weight matrix is orthogonalised by a Newton-Schulz iteration before the
+ * update -- and Sec. 4.1 uses it for every bottleneck model; App. B.1
+ * measures a bottleneck projection by its effective rank.  The paper prints
+ * neither the iteration nor its constants; the ops follow the Muon method it
+ * cites, with the constants as arguments.
+ *
+ * Shared conventions (in addition to the ones above):
+ *  - A p x q matrix is float32, row-major, contiguous, 4-byte aligned; with
+ *    s = min(p, q) and L = max(p, q): 1 <= s <= 256 (<= 128 for
+ *    resbm_spectrum) and L <= 2^20.
+ *  - ws holds at least resbm_matrix_workspace_bytes(p, q) bytes, 256-byte
+ *    aligned, not overlapping any argument.
+ *  - Arithmetic is float64 inside (float32 inputs widen exactly); every float32
+ *    output is rounded once, to nearest even.  Sums run in a fixed order, so
+ *    results are reproducible run to run.
+ *
+ * Newton-Schulz orthogonalisation, with X taken on the short side (X = U when
+ * p >= q, else U^T, so that A below is s x s):
+ *     X_0 = X / (||U||_F + 1e-7)
+ *     A = X^T X,  X <- a X + X (b A + c A^2)        (`steps` times)
+ * which is the wide form X_w <- a X_w + (b A + c A^2) X_w transposed.  It
+ * keeps U's singular vectors and maps each singular value sigma / ||U||_F
+ * through the scalar recurrence x <- a x + b x^3 + c x^5.  Muon's quintic is
+ * (a, b, c) = (3.4445, -4.7750, 2.0315) with 5 steps; (1.5, -0.5, 0) converges
+ * to the orthogonal polar factor.  steps is 0 .. 100; 0 returns X_0.
+ *  G  p x q input;  O  p x q output, must not overlap G.
+ */
+int32_t resbm_newton_schulz(int32_t p, int32_t q, const float* G, float* O,
+                            int32_t steps, double a, double b, double c,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One Muon step of a p x q weight (Sec. 3.4), in place:
+ *     M <- float32(momentum M + G)                      (when M != NULL)
+ *     U  = M, or G + momentum M with nesterov != 0      (U = G when M == NULL)
+ *     O  = Newton-Schulz(U; steps, a, b, c)             (as above)
+ *     W <- float32(W - lr (scale O + weight_decay W))
+ * `scale` matches the update's size to AdamW's; the cited method uses
+ * 0.2 sqrt(max(p, q)).  W, G and M must not overlap each other.
+ */
+int32_t resbm_muon_update(int32_t p, int32_t q, float* W, const float* G, float* M,
+                          double lr, double momentum, double weight_decay, double scale,
+                          int32_t nesterov, int32_t steps, double a, double b, double c,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Singular values and effective rank of a p x q matrix (App. B.1):
+ *     sigma[0 .. s)  singular values, descending (device float64 array)
+ *     r_eff[0]       = sum_i sigma_i^2 / max_i sigma_i^2  (0 for the zero matrix)
+ * Computed as the eigenvalues of the s x s Gram matrix (float64 Jacobi
+ * rotations); a singular value below ~1e-8 of the largest carries an absolute
+ * error near 1e-8 of the largest.
+ */
+int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, double* r_eff,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of the three ops above for a p x q matrix (a multiple of
+ * 256); 0 when (p, q) break the shape rules. */
+size_t resbm_matrix_workspace_bytes(int32_t p, int32_t q);
+
+/* Workspace bytes every module op above needs for (T, n, r): the maximum over
+ * the four ops, a multiple of 256.  Returns 0 when (n, r) break the shape rules. */
 size_t resbm_workspace_bytes(int64_t T, int32_t n, int32_t r);
 
 /* RESBM_IO_BF16 for libresbm.so, RESBM_IO_F32 for the validation build. */

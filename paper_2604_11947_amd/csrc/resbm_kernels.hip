@@ -1723,7 +1723,7 @@ const char* resbm_strerror(int32_t status) {
     case RESBM_E_NULL: return "a required pointer is NULL";
     case RESBM_E_SHAPE: return "T, n, r or a leading dimension breaks the shape rules";
     case RESBM_E_ALIGN: return "a pointer is not aligned as required";
-    case RESBM_E_WORKSPACE: return "workspace smaller than resbm_workspace_bytes(T, n, r)";
+    case RESBM_E_WORKSPACE: return "workspace smaller than the op requires";
     case RESBM_E_ACT: return "unknown activation, or SiLU backward without a_save";
     case RESBM_E_HIP: return "a HIP kernel launch failed";
     case RESBM_E_ALIAS: return "an output overlaps an input it may not alias";

@@ -1,0 +1,583 @@
+// resbm_matrix.hip -- optimizer-side kernels on the bottleneck weights, gfx950.
+//
+// Sec. 3.4 pairs the bottleneck weights with Muon: a weight matrix moves along
+// its gradient momentum orthogonalised by a Newton-Schulz iteration; Sec. 4.1
+// trains every bottleneck model that way.  App. B.1 measures a bottleneck
+// projection by its effective rank r_eff = sum sigma_i^2 / max sigma_i^2.
+// These matrices are n x r or r x n with r <= 256 -- a few MiB at most, tiny
+// next to the module's T x n streams -- so every kernel here is latency-bound:
+// the design keeps launches few, blocks busy for about a microsecond, and the
+// arithmetic in float64 (full vector rate on CDNA4), which costs nothing at
+// this size and keeps results within rounding of a float64 reference.
+//
+// Logical layout.  A p x q matrix is viewed as X (L x s), s = min(p, q),
+// L = max(p, q): the matrix itself when p >= q, its transpose otherwise.  X
+// lives in the workspace as float64, row-major [L][s4] (s4 = s rounded up to
+// a multiple of 4; the padding columns are zero and stay zero).  On the short
+// side one Newton-Schulz step is
+//     A = X^T X,   B = b A + c A^2,   X <- a X + X B,
+// the transpose of the wide-form step X_w <- a X_w + (b A + c A^2) X_w.
+//
+// Launches per call: k_mx_rows in load mode (float32 input, momentum, X and
+// the per-chunk partial Grams), then per step k_mx_reduce (partials -> A in
+// chunk order), k_mx_poly (B, and on the first step the Frobenius scale
+// kappa = 1 / (||U||_F + eps)), and k_mx_rows (X <- kappa (a X + X B) and the
+// partial Grams of the result; on the last step the float32 outputs instead).
+// No atomics and no waits between blocks: every sum has a fixed order, so
+// results are reproducible run to run.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "resbm.h"
+
+namespace resbm_mx {
+
+constexpr int kThreads = 256;
+constexpr int kMaxShort = 256;        // s <= 256
+constexpr int kMaxShortSpectrum = 128;  // the eigen-solver keeps s x s in LDS
+constexpr int64_t kMaxLong = 1 << 20;
+constexpr int kMaxSteps = 100;
+constexpr double kNsEps = 1e-7;       // added to ||U||_F before the division
+constexpr int kLdsDoubles = 17408;    // 136 KiB of LDS per block
+constexpr int kMaxSweeps = 60;
+
+enum Mode { kLoad = 0, kStep = 1, kOutO = 2, kOutW = 3 };
+
+struct Dims {
+  int L, s, s4;  // logical rows, short side, short side rounded up to 4
+  int tall;      // 1: X is the matrix; 0: X is its transpose
+  int q;         // columns (row stride) of the matrix as stored
+  int sub;       // rows per LDS sub-chunk of the row kernel
+  int ch;        // rows per block (a multiple of sub)
+  int nch;       // blocks of the row kernel = partial Grams per step
+  int b_lds;     // B fits LDS beside a sub-chunk
+};
+
+// Index of logical element (row l, column k) in the stored p x q matrix.
+__device__ __forceinline__ int64_t phys(const Dims& d, int64_t l, int k) {
+  return d.tall ? l * d.q + k : (int64_t)k * d.q + l;
+}
+
+// M <- float32(mu M + G); returns the matrix to orthogonalise, M or G + mu M.
+// Separate roundings in that order, so that the float32 momentum matches a
+// float64 reference bit for bit.
+__device__ __forceinline__ double momentum_step(float* m, double gv, double mu, int nesterov) {
+#pragma clang fp contract(off)
+  const float mn = (float)(mu * (double)*m + gv);
+  *m = mn;
+  return nesterov ? gv + mu * (double)mn : (double)mn;
+}
+
+// ---------------------------------------------------------------- rows
+// Block b owns logical rows [b ch, b ch + ch).
+//  kLoad: X = U from the float32 input (momentum applied first when given);
+//  kStep: X <- kappa (a X + X B);
+//  kOutO: out = float32(kappa (a X + X B)) in the stored layout;
+//  kOutW: out = float32(W - lr (scale X' + wd W)), X' = kappa (a X + X B).
+// kLoad and kStep then write the chunk's partial Gram part[b] = X^T X (rows of
+// the chunk only, s4 x s4).
+struct RowArgs {
+  double* X;
+  double* part;
+  const double* B;
+  const double* scal;  // scal[0] = kappa
+  double a;
+  const float* src;    // kLoad: gradient G
+  float* mom;          // kLoad: momentum buffer M or NULL
+  double mu;
+  int nesterov;
+  float* out;          // kOutO: O; kOutW: W (read and written)
+  double lr, scale, wd;
+};
+
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
+  __shared__ double s_mem[kLdsDoubles];
+  const int t = threadIdx.x;
+  const int s = d.s, s4 = d.s4;
+  const int64_t r0 = (int64_t)blockIdx.x * d.ch;
+  const int64_t r1 = r0 + d.ch < d.L ? r0 + d.ch : d.L;
+  if (r0 >= r1) return;  // uniform per block
+
+  if constexpr (MODE == kLoad) {
+    // logical rows of the chunk in order of the stored layout (coalesced reads)
+    const int rows = (int)(r1 - r0);
+    for (int64_t e = t; e < (int64_t)rows * s; e += kThreads) {
+      const int i = d.tall ? (int)(e / s) : (int)(e % rows);
+      const int k = d.tall ? (int)(e % s) : (int)(e / rows);
+      const int64_t pi = phys(d, r0 + i, k);
+      const double gv = (double)g.src[pi];
+      double u = gv;
+      if (g.mom) u = momentum_step(g.mom + pi, gv, g.mu, g.nesterov);
+      g.X[(r0 + i) * s4 + k] = u;
+    }
+    for (int e = t; e < rows * (s4 - s); e += kThreads)
+      g.X[(r0 + e / (s4 - s)) * s4 + s + e % (s4 - s)] = 0.0;
+  } else {
+    // X <- kappa (a X + X B), one sub-chunk of rows at a time through LDS
+    double* s_b = s_mem;
+    double* tile = s_mem + (d.b_lds ? s4 * s4 : 0);
+    const double* Bm = d.b_lds ? s_b : g.B;
+    if (d.b_lds) {
+      for (int e = t; e < s4 * s4; e += kThreads) s_b[e] = g.B[e];
+    }
+    const double kappa = g.scal[0];
+    const int ncg = s4 / 4;
+    const int nrg = kThreads / ncg > 0 ? kThreads / ncg : 1;
+    const int cg = t % ncg, rg = t / ncg;
+    for (int64_t t0 = r0; t0 < r1; t0 += d.sub) {
+      const int rows = (int)(r1 - t0 < d.sub ? r1 - t0 : d.sub);
+      for (int e = t; e < rows * s4; e += kThreads) tile[e] = g.X[t0 * s4 + e];
+      __syncthreads();
+      if (rg < nrg) {
+        for (int i = rg; i < rows; i += nrg) {
+          double acc[4] = {0.0, 0.0, 0.0, 0.0};
+          const double* xr = tile + i * s4;
+          for (int m = 0; m < s4; ++m) {
+            const double x = xr[m];
+            const double* br = Bm + m * s4 + 4 * cg;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[v] = fma(x, br[v], acc[v]);
+          }
+#pragma unroll
+          for (int v = 0; v < 4; ++v) g.X[(t0 + i) * s4 + 4 * cg + v] = kappa * fma(g.a, xr[4 * cg + v], acc[v]);
+        }
+      }
+      __syncthreads();  // the tile is reloaded next
+    }
+  }
+
+  if constexpr (MODE == kOutO || MODE == kOutW) {
+    __syncthreads();  // this block's rows of X are complete
+    const int rows = (int)(r1 - r0);
+    for (int64_t e = t; e < (int64_t)rows * s; e += kThreads) {
+      const int i = d.tall ? (int)(e / s) : (int)(e % rows);
+      const int k = d.tall ? (int)(e % s) : (int)(e / rows);
+      const int64_t pi = phys(d, r0 + i, k);
+      const double x = g.X[(r0 + i) * s4 + k];
+      if constexpr (MODE == kOutO) {
+        g.out[pi] = (float)x;
+      } else {
+        const double w = (double)g.out[pi];
+        g.out[pi] = (float)(w - g.lr * (g.scale * x + g.wd * w));
+      }
+    }
+    return;
+  } else {
+    // partial Gram of the chunk: part[b][i][j] = sum over its rows of X[l][i] X[l][j],
+    // 4 x 4 entry blocks per thread; row groups (small s4) are added in order
+    __syncthreads();  // this block's rows of X are complete
+    double* tile = s_mem;
+    double* red = s_mem + d.sub * s4;
+    const int nb4 = s4 / 4, nblk = nb4 * nb4;
+    const int R = nblk < kThreads ? kThreads / nblk : 1;
+    const int groups = nblk <= kThreads ? 1 : (nblk + 4 * kThreads - 1) / (4 * kThreads);
+    double* part = g.part + (int64_t)blockIdx.x * s4 * s4;
+    for (int grp = 0; grp < groups; ++grp) {
+      // this pass: blocks blk = t + kThreads (4 grp + u), u < 4 (large s4), or blk = t % nblk (small s4)
+      double acc[4][4][4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y) acc[u][x][y] = 0.0;
+      const int rgp = R > 1 ? t / nblk : 0;
+      for (int64_t t0 = r0; t0 < r1; t0 += d.sub) {
+        const int rows = (int)(r1 - t0 < d.sub ? r1 - t0 : d.sub);
+        for (int e = t; e < rows * s4; e += kThreads) tile[e] = g.X[t0 * s4 + e];
+        __syncthreads();
+        if (rgp < R) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int blk = R > 1 ? t % nblk : t + kThreads * (4 * grp + u);
+            if ((R > 1 && u > 0) || blk >= nblk) continue;
+            const int bi = blk / nb4, bj = blk % nb4;
+            for (int i = rgp; i < rows; i += R) {
+              const double* xr = tile + i * s4;
+              double xa[4], xb[4];
+#pragma unroll
+              for (int v = 0; v < 4; ++v) { xa[v] = xr[4 * bi + v]; xb[v] = xr[4 * bj + v]; }
+#pragma unroll
+              for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 4; ++y) acc[u][x][y] = fma(xa[x], xb[y], acc[u][x][y]);
+            }
+          }
+        }
+        __syncthreads();
+      }
+      if (R > 1) {
+        // row groups meet in LDS, added in group order
+        const int blk = t % nblk;
+        if (rgp < R) {
+#pragma unroll
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) red[(rgp * nblk + blk) * 16 + 4 * x + y] = acc[0][x][y];
+        }
+        __syncthreads();
+        if (t < nblk) {
+          const int bi = t / nb4, bj = t % nb4;
+#pragma unroll
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) {
+              double v = red[t * 16 + 4 * x + y];
+              for (int k = 1; k < R; ++k) v += red[(k * nblk + t) * 16 + 4 * x + y];
+              part[(4 * bi + x) * s4 + 4 * bj + y] = v;
+            }
+        }
+        __syncthreads();
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int blk = t + kThreads * (4 * grp + u);
+          if (blk >= nblk) continue;
+          const int bi = blk / nb4, bj = blk % nb4;
+#pragma unroll
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) part[(4 * bi + x) * s4 + 4 * bj + y] = acc[u][x][y];
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- reduce
+// A[e] = sum over chunks, in chunk order, of part[chunk][e].
+__global__ __launch_bounds__(kThreads) void k_mx_reduce(int ne, int nch, const double* part, double* A) {
+  const int e = blockIdx.x * kThreads + threadIdx.x;
+  if (e >= ne) return;
+  double v = 0.0;
+  int c = 0;
+  for (; c + 8 <= nch; c += 8) {
+    double p[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) p[k] = part[(int64_t)(c + k) * ne + e];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v += p[k];
+  }
+  for (; c < nch; ++c) v += part[(int64_t)c * ne + e];
+  A[e] = v;
+}
+
+// ---------------------------------------------------------------- poly
+// B = b Ah + c Ah^2 with Ah = kappa^2 A; kappa = 1 / (sqrt(trace A) + eps) on
+// the first step (X_0 = U / (||U||_F + eps)), else 1.  Block bx owns rows
+// [16 bx, 16 bx + 16) of B; block 0 publishes kappa for the row kernel.
+__global__ __launch_bounds__(kThreads) void k_mx_poly(int s4, const double* A, double* B, double* scal, int first,
+                                                      double cb, double cc) {
+  __shared__ double s_rows[16 * kMaxShort];
+  __shared__ double s_kappa;
+  const int t = threadIdx.x;
+  const int i0 = blockIdx.x * 16;
+  const int nr = s4 - i0 < 16 ? s4 - i0 : 16;
+  if (t == 0) {
+    double k = 1.0;
+    if (first) {
+      double tr = 0.0;
+      for (int i = 0; i < s4; ++i) tr += A[i * s4 + i];
+      k = 1.0 / (sqrt(tr) + kNsEps);
+    }
+    s_kappa = k;
+    if (blockIdx.x == 0) scal[0] = k;
+  }
+  for (int e = t; e < nr * s4; e += kThreads) s_rows[e] = A[(int64_t)i0 * s4 + e];
+  __syncthreads();
+  const double k2 = s_kappa * s_kappa, k4 = k2 * k2;
+  for (int e = t; e < nr * s4; e += kThreads) {
+    const int i = e / s4, j = e % s4;
+    double sq = 0.0;
+    for (int m = 0; m < s4; ++m) sq = fma(s_rows[i * s4 + m], A[m * s4 + j], sq);
+    B[(int64_t)(i0 + i) * s4 + j] = cb * k2 * s_rows[e] + cc * k4 * sq;
+  }
+}
+
+// ---------------------------------------------------------------- spectrum
+// Eigenvalues of the s x s Gram A (row stride s4) by cyclic Jacobi rotations in
+// round-robin order (s/2 disjoint pairs per round, all rotated at once), in
+// LDS, until the off-diagonal mass is below 1e-30 of the diagonal mass.
+// sigma[k] = sqrt(max(lambda, 0)) in descending order; r_eff = sum lambda^+ /
+// max lambda (0 for the zero matrix).
+__global__ __launch_bounds__(kThreads) void k_mx_eig(int s, int s4, const double* A, double* sigma,
+                                                     double* r_eff) {
+  __shared__ double M[kMaxShortSpectrum * kMaxShortSpectrum];
+  __shared__ double s_c[kMaxShortSpectrum / 2 + 1], s_s[kMaxShortSpectrum / 2 + 1];
+  __shared__ int s_p[kMaxShortSpectrum / 2 + 1], s_q[kMaxShortSpectrum / 2 + 1];
+  __shared__ double s_red[2][kThreads];
+  __shared__ int s_done;
+  const int t = threadIdx.x;
+  for (int e = t; e < s * s; e += kThreads) M[e] = A[(e / s) * s4 + e % s];
+  __syncthreads();
+  const int m = s + (s & 1);  // players; index s is the bye when s is odd
+  const int np = m / 2;
+  for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
+    double off = 0.0, dg = 0.0;
+    for (int e = t; e < s * s; e += kThreads) {
+      const double v = M[e] * M[e];
+      if (e / s == e % s) dg += v; else off += v;
+    }
+    s_red[0][t] = off;
+    s_red[1][t] = dg;
+    __syncthreads();
+    for (int w = kThreads / 2; w > 0; w >>= 1) {
+      if (t < w) {
+        s_red[0][t] += s_red[0][t + w];
+        s_red[1][t] += s_red[1][t + w];
+      }
+      __syncthreads();
+    }
+    if (t == 0) s_done = s_red[0][0] <= 1e-30 * s_red[1][0];
+    __syncthreads();
+    if (s_done) break;
+    for (int round = 0; round < m - 1; ++round) {
+      if (t < np) {
+        // circle method: player 0 fixed, players 1 .. m-1 rotate by one per round
+        const int a = t == 0 ? 0 : 1 + (t - 1 + round) % (m - 1);
+        const int b = 1 + (m - 2 - t + round) % (m - 1);
+        const int p = a < b ? a : b, q = a < b ? b : a;
+        double c = 1.0, sn = 0.0;
+        if (q < s && M[p * s + q] != 0.0) {
+          const double tau = (M[q * s + q] - M[p * s + p]) / (2.0 * M[p * s + q]);
+          const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + hypot(1.0, tau));
+          c = 1.0 / sqrt(1.0 + tt * tt);
+          sn = tt * c;
+        }
+        s_c[t] = c;
+        s_s[t] = sn;
+        s_p[t] = p;
+        s_q[t] = q < s ? q : -1;
+      }
+      __syncthreads();
+      for (int e = t; e < s * np; e += kThreads) {  // columns p, q of every row
+        const int i = e / np, k = e % np, q = s_q[k];
+        if (q < 0) continue;
+        const int p = s_p[k];
+        const double c = s_c[k], sn = s_s[k];
+        const double xp = M[i * s + p], xq = M[i * s + q];
+        M[i * s + p] = c * xp - sn * xq;
+        M[i * s + q] = sn * xp + c * xq;
+      }
+      __syncthreads();
+      for (int e = t; e < s * np; e += kThreads) {  // rows p, q of every column
+        const int k = e / s, j = e % s, q = s_q[k];
+        if (q < 0) continue;
+        const int p = s_p[k];
+        const double c = s_c[k], sn = s_s[k];
+        const double xp = M[p * s + j], xq = M[q * s + j];
+        M[p * s + j] = c * xp - sn * xq;
+        M[q * s + j] = sn * xp + c * xq;
+      }
+      __syncthreads();
+    }
+  }
+  // descending order by rank (ties by index)
+  for (int i = t; i < s; i += kThreads) {
+    const double li = M[i * s + i];
+    int rank = 0;
+    for (int j = 0; j < s; ++j) {
+      const double lj = M[j * s + j];
+      rank += (lj > li) || (lj == li && j < i);
+    }
+    sigma[rank] = sqrt(li > 0.0 ? li : 0.0);
+  }
+  if (t == 0) {
+    double tot = 0.0, top = 0.0;
+    for (int i = 0; i < s; ++i) {
+      const double l = M[i * s + i] > 0.0 ? M[i * s + i] : 0.0;
+      tot += l;
+      top = l > top ? l : top;
+    }
+    r_eff[0] = top > 0.0 ? tot / top : 0.0;
+  }
+}
+
+// ---------------------------------------------------------------- host
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+struct Plan {
+  Dims d;
+  size_t off_x, off_part, off_a, off_b, off_scal, bytes;
+};
+
+bool shape_ok(int64_t p, int64_t q, int max_short) {
+  const int64_t s = p < q ? p : q, L = p < q ? q : p;
+  return s >= 1 && s <= max_short && L <= kMaxLong;
+}
+
+Plan make_plan(int p, int q) {
+  Plan P{};
+  Dims& d = P.d;
+  d.tall = p >= q;
+  d.L = d.tall ? p : q;
+  d.s = d.tall ? q : p;
+  d.s4 = (d.s + 3) & ~3;
+  d.q = q;
+  d.b_lds = d.s4 * d.s4 <= 8192;
+  const int room = kLdsDoubles - (d.b_lds ? d.s4 * d.s4 : 0);
+  // the Gram pass also keeps up to 4096 doubles of row-group sums beside the tile
+  int sub = (room - 4096) / d.s4;
+  sub = sub > 512 ? 512 : sub;
+  sub = sub >= 16 ? sub & ~15 : (sub >= 1 ? sub : 1);
+  d.sub = sub;
+  // about 64 blocks, each row chunk a whole number of sub-chunks, partial
+  // Grams capped at 64 MiB
+  const int64_t cap = (int64_t)(64u << 20) / ((int64_t)d.s4 * d.s4 * 8);
+  int64_t nch = (d.L + 63) / 64;
+  nch = nch > 64 ? 64 : nch;
+  if (nch > cap) nch = cap > 0 ? cap : 1;
+  int64_t ch = (d.L + nch - 1) / nch;
+  ch = (ch + sub - 1) / sub * sub;
+  d.ch = (int)ch;
+  d.nch = (int)((d.L + ch - 1) / ch);
+  size_t off = 0;
+  P.off_x = off;
+  off += align256((size_t)d.L * d.s4 * 8);
+  P.off_part = off;
+  off += align256((size_t)d.nch * d.s4 * d.s4 * 8);
+  P.off_a = off;
+  off += align256((size_t)d.s4 * d.s4 * 8);
+  P.off_b = off;
+  off += align256((size_t)d.s4 * d.s4 * 8);
+  P.off_scal = off;
+  off += 256;
+  P.bytes = off;
+  return P;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+  return pa < pb + nb && pb < pa + na;
+}
+
+int32_t launch_status() { return hipGetLastError() == hipSuccess ? RESBM_OK : RESBM_E_HIP; }
+
+int32_t check_ws(const Plan& P, const void* ws, size_t ws_bytes) {
+  if (!ws) return RESBM_E_NULL;
+  if (!aligned(ws, 256)) return RESBM_E_ALIGN;
+  if (ws_bytes < P.bytes) return RESBM_E_WORKSPACE;
+  return RESBM_OK;
+}
+
+// Load, then `steps` Newton-Schulz steps (at least one launch set; steps == 0
+// runs one with coefficients (1, 0, 0), i.e. X_0 itself), the last one in
+// output mode MODE_OUT.
+template <int MODE_OUT>
+void run_ns(const Plan& P, char* ws, RowArgs g, int steps, double a, double b, double c, hipStream_t st) {
+  const Dims& d = P.d;
+  g.X = (double*)(ws + P.off_x);
+  g.part = (double*)(ws + P.off_part);
+  g.B = (const double*)(ws + P.off_b);
+  g.scal = (const double*)(ws + P.off_scal);
+  double* A = (double*)(ws + P.off_a);
+  double* B = (double*)(ws + P.off_b);
+  double* scal = (double*)(ws + P.off_scal);
+  const dim3 grid(d.nch), blk(kThreads);
+  hipLaunchKernelGGL(k_mx_rows<kLoad>, grid, blk, 0, st, d, g);
+  const int n = steps > 0 ? steps : 1;
+  if (steps == 0) { a = 1.0; b = 0.0; c = 0.0; }
+  const int ne = d.s4 * d.s4;
+  for (int i = 0; i < n; ++i) {
+    hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), blk, 0, st, ne, d.nch,
+                       (const double*)g.part, A);
+    hipLaunchKernelGGL(k_mx_poly, dim3((d.s4 + 15) / 16), blk, 0, st, d.s4, (const double*)A, B, scal, (int)(i == 0),
+                       b, c);
+    RowArgs gi = g;
+    gi.a = a;
+    if (i + 1 < n)
+      hipLaunchKernelGGL(k_mx_rows<kStep>, grid, blk, 0, st, d, gi);
+    else
+      hipLaunchKernelGGL(k_mx_rows<MODE_OUT>, grid, blk, 0, st, d, gi);
+  }
+}
+
+}  // namespace resbm_mx
+
+using namespace resbm_mx;
+
+extern "C" {
+
+size_t resbm_matrix_workspace_bytes(int32_t p, int32_t q) {
+  if (!shape_ok(p, q, kMaxShort)) return 0;
+  return make_plan(p, q).bytes;
+}
+
+int32_t resbm_newton_schulz(int32_t p, int32_t q, const float* G, float* O, int32_t steps, double a, double b,
+                            double c, void* ws, size_t ws_bytes, void* stream) {
+  if (!shape_ok(p, q, kMaxShort) || steps < 0 || steps > kMaxSteps) return RESBM_E_SHAPE;
+  if (!G || !O) return RESBM_E_NULL;
+  const Plan P = make_plan(p, q);
+  const int32_t w = check_ws(P, ws, ws_bytes);
+  if (w != RESBM_OK) return w;
+  if (!aligned(G, 4) || !aligned(O, 4)) return RESBM_E_ALIGN;
+  const size_t bm = (size_t)p * q * 4;
+  if (overlap(O, bm, G, bm) || overlap(ws, P.bytes, G, bm) || overlap(ws, P.bytes, O, bm)) return RESBM_E_ALIAS;
+  RowArgs g{};
+  g.src = G;
+  g.out = O;
+  run_ns<kOutO>(P, (char*)ws, g, steps, a, b, c, (hipStream_t)stream);
+  return launch_status();
+}
+
+int32_t resbm_muon_update(int32_t p, int32_t q, float* W, const float* G, float* M, double lr, double momentum,
+                          double weight_decay, double scale, int32_t nesterov, int32_t steps, double a, double b,
+                          double c, void* ws, size_t ws_bytes, void* stream) {
+  if (!shape_ok(p, q, kMaxShort) || steps < 0 || steps > kMaxSteps) return RESBM_E_SHAPE;
+  if (!W || !G) return RESBM_E_NULL;
+  const Plan P = make_plan(p, q);
+  const int32_t w = check_ws(P, ws, ws_bytes);
+  if (w != RESBM_OK) return w;
+  if (!aligned(W, 4) || !aligned(G, 4) || (M && !aligned(M, 4))) return RESBM_E_ALIGN;
+  const size_t bm = (size_t)p * q * 4;
+  if (overlap(W, bm, G, bm) || overlap(W, bm, M, bm) || overlap(G, bm, M, bm) || overlap(ws, P.bytes, W, bm) ||
+      overlap(ws, P.bytes, G, bm) || overlap(ws, P.bytes, M, bm))
+    return RESBM_E_ALIAS;
+  RowArgs g{};
+  g.src = G;
+  g.mom = M;
+  g.mu = momentum;
+  g.nesterov = nesterov ? 1 : 0;
+  g.out = W;
+  g.lr = lr;
+  g.scale = scale;
+  g.wd = weight_decay;
+  run_ns<kOutW>(P, (char*)ws, g, steps, a, b, c, (hipStream_t)stream);
+  return launch_status();
+}
+
+int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, double* r_eff, void* ws,
+                       size_t ws_bytes, void* stream) {
+  if (!shape_ok(p, q, kMaxShortSpectrum)) return RESBM_E_SHAPE;
+  if (!W || !sigma || !r_eff) return RESBM_E_NULL;
+  const Plan P = make_plan(p, q);
+  const int32_t w = check_ws(P, ws, ws_bytes);
+  if (w != RESBM_OK) return w;
+  if (!aligned(W, 4) || !aligned(sigma, 8) || !aligned(r_eff, 8)) return RESBM_E_ALIGN;
+  const size_t bm = (size_t)p * q * 4, bs = (size_t)P.d.s * 8;
+  if (overlap(sigma, bs, r_eff, 8) || overlap(ws, P.bytes, W, bm) || overlap(ws, P.bytes, sigma, bs) ||
+      overlap(ws, P.bytes, r_eff, 8) || overlap(sigma, bs, W, bm) || overlap(r_eff, 8, W, bm))
+    return RESBM_E_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  char* wsc = (char*)ws;
+  RowArgs g{};
+  g.X = (double*)(wsc + P.off_x);
+  g.part = (double*)(wsc + P.off_part);
+  g.src = W;
+  const Dims& d = P.d;
+  hipLaunchKernelGGL(k_mx_rows<kLoad>, dim3(d.nch), dim3(kThreads), 0, st, d, g);
+  const int ne = d.s4 * d.s4;
+  double* A = (double*)(wsc + P.off_a);
+  hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), dim3(kThreads), 0, st, ne, d.nch,
+                     (const double*)g.part, A);
+  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(kThreads), 0, st, d.s, d.s4, (const double*)A, sigma, r_eff);
+  return launch_status();
+}
+
+}  // extern "C"

@@ -191,3 +191,46 @@ def upstream_grad(T: int, n: int, seed: int) -> torch.Tensor:
 def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
     """Exact widening of a bf16/fp32 CPU tensor to a float64 NumPy array."""
     return t.to(torch.float64).numpy()
+
+
+# ---------------------------------------------------------------- bottleneck-weight matrices
+MATRIX_KINDS = ("gaussian", "powerlaw", "orthonormal", "rank1", "zero")
+
+
+def make_matrix(p: int, q: int, kind: str = "gaussian", seed: int = 0, scale: float = 1.0) -> torch.Tensor:
+    """A seeded float32 p x q matrix for the optimizer-side ops.
+
+    gaussian     N(0, scale^2) entries (a gradient or momentum draw);
+    powerlaw     U diag(sigma) V^T with random orthonormal U, V and
+                 sigma_i = scale (i + 1)^-1.5 (i < min(p, q)): a decaying
+                 spectrum down to ~1e-3 of the top at s = 128;
+    orthonormal  scale times orthonormal columns (rows if p < q): all singular
+                 values equal;
+    rank1        scale u v^T with Gaussian u, v;
+    zero         all zeros.
+    """
+    if p <= 0 or q <= 0:
+        raise ValueError("p and q must be positive")
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, p, q, MATRIX_KINDS.index(kind)])))
+    s, L = min(p, q), max(p, q)
+
+    def orth(rows, cols):
+        qm, rm = np.linalg.qr(rng.standard_normal((rows, cols)))
+        return qm * np.sign(np.diag(rm))
+
+    if kind == "gaussian":
+        m = scale * rng.standard_normal((p, q))
+    elif kind == "powerlaw":
+        sig = scale * (np.arange(s) + 1.0) ** -1.5
+        tall = orth(L, s) @ np.diag(sig) @ orth(s, s).T
+        m = tall if p >= q else tall.T
+    elif kind == "orthonormal":
+        tall = scale * orth(L, s)
+        m = tall if p >= q else tall.T
+    elif kind == "rank1":
+        m = scale * np.outer(rng.standard_normal(p), rng.standard_normal(q))
+    elif kind == "zero":
+        m = np.zeros((p, q))
+    else:
+        raise ValueError(f"unknown matrix kind {kind!r}")
+    return torch.from_numpy(np.ascontiguousarray(m).astype(np.float32))

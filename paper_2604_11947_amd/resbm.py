@@ -28,14 +28,22 @@ E_ACT = -5
 E_HIP = -6
 E_ALIAS = -7
 
+# Newton-Schulz coefficients of the Muon method the paper cites (Sec. 3.4)
+NS_QUINTIC = (3.4445, -4.7750, 2.0315)
+NS_CUBIC = (1.5, -0.5, 0.0)
+
 # (name, restype, argtypes) of every exported symbol
-_i64, _i32, _p, _sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+_i64, _i32, _p, _sz, _d = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_double
 SIGNATURES = [
     ("resbm_encode_fwd", _i32, [_i64, _i32, _i32, _i32, _p, _i64, _p, _i64, _p, _p, _p, _p, _sz, _p]),
     ("resbm_decode_fwd", _i32, [_i64, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _sz, _p]),
     ("resbm_decode_bwd", _i32, [_i64, _i32, _i32, _p, _p, _p, _i64, _p, _i64, _p, _p, _i32, _p, _sz, _p]),
     ("resbm_encode_bwd", _i32, [_i64, _i32, _i32, _i32, _p, _i64, _p, _p, _p, _p, _i64, _p, _i64, _p, _i32,
                                 _p, _sz, _p]),
+    ("resbm_newton_schulz", _i32, [_i32, _i32, _p, _p, _i32, _d, _d, _d, _p, _sz, _p]),
+    ("resbm_muon_update", _i32, [_i32, _i32, _p, _p, _p, _d, _d, _d, _d, _i32, _i32, _d, _d, _d, _p, _sz, _p]),
+    ("resbm_spectrum", _i32, [_i32, _i32, _p, _p, _p, _p, _sz, _p]),
+    ("resbm_matrix_workspace_bytes", _sz, [_i32, _i32]),
     ("resbm_workspace_bytes", _sz, [_i64, _i32, _i32]),
     ("resbm_io_dtype", _i32, []),
     ("resbm_strerror", ctypes.c_char_p, [_i32]),
@@ -105,6 +113,15 @@ class Library:
 
     def workspace(self, T: int, n: int, r: int, device) -> torch.Tensor:
         nbytes = self.workspace_bytes(T, n, r)
+        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        off = (-buf.data_ptr()) % 256
+        return buf[off:off + nbytes]
+
+    def matrix_workspace_bytes(self, p: int, q: int) -> int:
+        return int(self.cdll.resbm_matrix_workspace_bytes(p, q))
+
+    def matrix_workspace(self, p: int, q: int, device) -> torch.Tensor:
+        nbytes = self.matrix_workspace_bytes(p, q)
         buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
         off = (-buf.data_ptr()) % 256
         return buf[off:off + nbytes]
@@ -192,6 +209,52 @@ class Library:
                                         ld_gz, _ptr(g_x), ld_gx, _ptr(dW_e), int(bool(accumulate)), _ptr(ws),
                                         ws.numel(), _stream(stream, z))
         self._check("resbm_encode_bwd", st)
+
+
+    # ------------------------------------------------------------ optimizer-side ops
+    def newton_schulz(self, G, O, steps=5, coeffs=NS_QUINTIC, ws=None, stream=None):
+        p, q = G.shape
+        _dtype(G, torch.float32, "G")
+        _dtype(O, torch.float32, "O")
+        _packed(G, p, q, "G")
+        _packed(O, p, q, "O")
+        if ws is None:
+            ws = self.matrix_workspace(p, q, G.device)
+        a, b, c = coeffs
+        st = self.cdll.resbm_newton_schulz(p, q, _ptr(G), _ptr(O), steps, a, b, c, _ptr(ws), ws.numel(),
+                                           _stream(stream, G))
+        self._check("resbm_newton_schulz", st)
+
+    def muon_update(self, W, G, M, lr, momentum=0.95, weight_decay=0.0, scale=None, nesterov=False, steps=5,
+                    coeffs=NS_QUINTIC, ws=None, stream=None):
+        p, q = W.shape
+        for t, nm in ((W, "W"), (G, "G"), (M, "M")):
+            _dtype(t, torch.float32, nm)
+            if t is not None:
+                _packed(t, p, q, nm)
+        if scale is None:
+            scale = 0.2 * max(p, q) ** 0.5
+        if ws is None:
+            ws = self.matrix_workspace(p, q, W.device)
+        a, b, c = coeffs
+        st = self.cdll.resbm_muon_update(p, q, _ptr(W), _ptr(G), _ptr(M), lr, momentum, weight_decay, scale,
+                                         int(bool(nesterov)), steps, a, b, c, _ptr(ws), ws.numel(),
+                                         _stream(stream, W))
+        self._check("resbm_muon_update", st)
+
+    def spectrum(self, W, sigma, r_eff, ws=None, stream=None):
+        p, q = W.shape
+        _dtype(W, torch.float32, "W")
+        _packed(W, p, q, "W")
+        _dtype(sigma, torch.float64, "sigma")
+        _dtype(r_eff, torch.float64, "r_eff")
+        if sigma.numel() < min(p, q) or r_eff.numel() < 1 or not sigma.is_contiguous():
+            raise ValueError("sigma needs min(p, q) contiguous float64 elements, r_eff one")
+        if ws is None:
+            ws = self.matrix_workspace(p, q, W.device)
+        st = self.cdll.resbm_spectrum(p, q, _ptr(W), _ptr(sigma), _ptr(r_eff), _ptr(ws), ws.numel(),
+                                      _stream(stream, W))
+        self._check("resbm_spectrum", st)
 
 
 _LOADED: dict[str, Library] = {}

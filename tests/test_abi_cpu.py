@@ -32,9 +32,10 @@ def declared_functions():
     return sorted(set(re.findall(r"\b(resbm_\w+)\s*\(", text)))
 
 
-def test_header_declares_the_four_ops_and_helpers():
+def test_header_declares_the_ops_and_helpers():
     names = declared_functions()
     for op in ("resbm_encode_fwd", "resbm_decode_fwd", "resbm_decode_bwd", "resbm_encode_bwd",
+               "resbm_newton_schulz", "resbm_muon_update", "resbm_spectrum", "resbm_matrix_workspace_bytes",
                "resbm_workspace_bytes", "resbm_io_dtype", "resbm_strerror"):
         assert op in names
     assert sorted(n for n, _, _ in R.SIGNATURES) == names
@@ -200,3 +201,84 @@ def test_encode_bwd_validation(lib):
     assert call(ldgx=N - 8) == R.E_SHAPE
     assert call(wsb=256) == R.E_WORKSPACE
     assert call(gb=4 * A + 4) == R.E_ALIGN
+
+
+# ---------------------------------------------------------------- optimizer-side ops
+def test_matrix_workspace_bytes(lib):
+    assert lib.matrix_workspace_bytes(0, 32) == 0
+    assert lib.matrix_workspace_bytes(4096, 257) == 0        # short side > 256
+    assert lib.matrix_workspace_bytes(257, 4096) == 0
+    assert lib.matrix_workspace_bytes((1 << 20) + 1, 8) == 0  # long side > 2^20
+    for p, q in ((4096, 32), (32, 4096), (8192, 64), (4096, 256), (1, 1), (7, 3)):
+        w = lib.matrix_workspace_bytes(p, q)
+        assert w % 256 == 0 and w >= max(p, q) * ((min(p, q) + 3) // 4 * 4) * 8
+    assert lib.matrix_workspace_bytes(4096, 32) == lib.matrix_workspace_bytes(32, 4096)
+
+
+@needs_no_gpu
+def test_newton_schulz_validation(lib):
+    c = lib.cdll
+    p, q = 512, 32
+    ws = lib.matrix_workspace_bytes(p, q)
+    ok = [p, q, A, 2 * A, 5, 3.4445, -4.775, 2.0315, 3 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm_newton_schulz(*a)
+
+    assert call(0, 0) == R.E_SHAPE
+    assert call(1, 300) == R.E_SHAPE
+    assert call(4, -1) == R.E_SHAPE
+    assert call(4, 101) == R.E_SHAPE
+    assert call(2, None) == R.E_NULL
+    assert call(3, None) == R.E_NULL
+    assert call(8, None) == R.E_NULL
+    assert call(9, ws - 256) == R.E_WORKSPACE
+    assert call(8, 3 * A + 64) == R.E_ALIGN
+    assert call(2, A + 2) == R.E_ALIGN
+    assert call(3, A + 4096) == R.E_ALIAS      # O over G
+    assert call(8, 2 * A) == R.E_ALIAS         # ws over O
+
+
+@needs_no_gpu
+def test_muon_update_validation(lib):
+    c = lib.cdll
+    p, q = 32, 4096
+    ws = lib.matrix_workspace_bytes(p, q)
+    ok = [p, q, A, 2 * A, 3 * A, 0.02, 0.95, 0.0, 1.0, 0, 5, 3.4445, -4.775, 2.0315, 4 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm_muon_update(*a)
+
+    assert call(1, 0) == R.E_SHAPE
+    assert call(2, None) == R.E_NULL           # W
+    assert call(3, None) == R.E_NULL           # G
+    assert call(15, 0) == R.E_WORKSPACE
+    assert call(4, 3 * A + 1) == R.E_ALIGN     # M
+    assert call(4, 2 * A + 512) == R.E_ALIAS   # M over G
+    assert call(3, A) == R.E_ALIAS             # G over W
+    assert call(14, 3 * A) == R.E_ALIAS        # ws over M
+
+
+@needs_no_gpu
+def test_spectrum_validation(lib):
+    c = lib.cdll
+    p, q = 64, 4096
+    ws = lib.matrix_workspace_bytes(p, q)
+    ok = [p, q, A, 2 * A, 3 * A, 4 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm_spectrum(*a)
+
+    assert call(0, 129) == R.E_SHAPE           # short side > 128
+    assert call(2, None) == R.E_NULL
+    assert call(3, None) == R.E_NULL
+    assert call(4, None) == R.E_NULL
+    assert call(3, 2 * A + 4) == R.E_ALIGN
+    assert call(4, 2 * A + 8) == R.E_ALIAS     # r_eff inside sigma
+    assert call(6, 1024) == R.E_WORKSPACE
