@@ -21,6 +21,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -55,6 +57,8 @@ def parse():
                    help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
     p.add_argument("--cpu-tokens", type=int, default=None, help="tokens in the CPU oracle sample")
     p.add_argument("--no-graph", action="store_true", help="report the eager launches instead of graph replays")
+    p.add_argument("--no-optimizer", action="store_true",
+                   help="skip timing the optimizer-side ops (Muon update, spectrum) on the bottleneck weights")
     p.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="write profiles/ summaries from rocprofv3 output of this script (no GPU work)")
     p.add_argument("--commands", nargs=3, default=None, help="the three rocprofv3 commands, recorded in the summaries")
@@ -213,6 +217,65 @@ def cpu_baseline(d: dict, r: int, act: int, tokens: int, min_seconds: float = 10
             "sample": f"first {tokens} tokens of the workload (all of it when equal to T), all four ops in "
                       f"float64 with bf16 wire rounding, {reps} repetition(s) in {dt:.1f} s; "
                       f"{len(os.sched_getaffinity(0))} host cores visible"}
+
+
+def optimizer_timing(lib, d: dict, r: int, dev, iters: int, cpu: bool) -> dict:
+    """Graph-replayed time of one Muon update of each bottleneck weight (Sec. 3.4)
+    and of the spectrum / r_eff of W_d (App. B.1), with the float64 oracle timed
+    on the same update when `cpu` is set."""
+    import torch
+
+    from paper_2604_11947_amd import inputs as I
+    from paper_2604_11947_amd import resbm as R
+
+    def graph_us(fn):
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        for _ in range(20):
+            g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / iters
+
+    steps = 5
+    out = {"ns_steps": steps, "coefficients": list(R.NS_QUINTIC), "launches_per_update": 1 + 3 * steps,
+           "timing": "hip graph replay of one call", "iterations": iters}
+    keep = {}
+    for nm in ("W_e", "W_d"):
+        W0 = d[nm]
+        p, q = W0.shape
+        W, M = W0.to(dev).clone(), torch.zeros(p, q, device=dev)
+        G = I.make_matrix(p, q, "gaussian", seed=11, scale=1e-2).to(dev)
+        ws = lib.matrix_workspace(p, q, dev)
+        out[f"muon_update_us_{nm}"] = graph_us(
+            lambda W=W, G=G, M=M, ws=ws: lib.muon_update(W, G, M, 1e-4, momentum=0.95, ws=ws, steps=steps))
+        keep[nm] = (W0, G, ws)
+    if r <= 128:
+        W0, _, ws = keep["W_d"]
+        Wd = W0.to(dev)
+        sig = torch.empty(min(W0.shape), dtype=torch.float64, device=dev)
+        reff = torch.empty(1, dtype=torch.float64, device=dev)
+        out["spectrum_us_W_d"] = graph_us(lambda: lib.spectrum(Wd, sig, reff, ws=ws))
+        out["r_eff_W_d"] = float(reff.item())
+    if cpu:
+        from oracle import muon_oracle as MU
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 2.0:
+            for nm in ("W_e", "W_d"):
+                W0, G, _ = keep[nm]
+                MU.muon_update(W0.double().numpy(), G.cpu().double().numpy(), np.zeros(tuple(W0.shape)), 1e-4, 0.95)
+            reps += 1
+        out["oracle_us_per_update_pair"] = (time.perf_counter() - t0) * 1e6 / reps
+    return out
 
 
 COPY_PROBE_MIB = 256
@@ -378,6 +441,8 @@ def main():
         "wall_s_timed": wall,
         "input_gen_s": t_gen,
     }
+    if not args.no_optimizer:
+        out["optimizer"] = optimizer_timing(lib, d, r, dev, 200, cpu=not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         tokens = args.cpu_tokens or T
         out["cpu_baseline"] = cpu_baseline(d, r, act, min(tokens, T))

@@ -21,8 +21,9 @@
 // Launches per call: k_mx_rows in load mode (float32 input, momentum, X and
 // the per-chunk partial Grams), then per step k_mx_reduce (partials -> A in
 // chunk order), k_mx_poly (B, and on the first step the Frobenius scale
-// kappa = 1 / (||U||_F + eps)), and k_mx_rows (X <- kappa (a X + X B) and the
-// partial Grams of the result; on the last step the float32 outputs instead).
+// kappa = 1 / (||U||_F + eps); for s4 <= 64 the row kernel forms B itself),
+// and k_mx_rows (X <- kappa (a X + X B) and the partial Grams of the result;
+// on the last step the float32 outputs instead).
 // No atomics and no waits between blocks: every sum has a fixed order, so
 // results are reproducible run to run.
 #include <hip/hip_runtime.h>
@@ -50,9 +51,10 @@ struct Dims {
   int tall;      // 1: X is the matrix; 0: X is its transpose
   int q;         // columns (row stride) of the matrix as stored
   int sub;       // rows per LDS sub-chunk of the row kernel
-  int ch;        // rows per block (a multiple of sub)
+  int ch;        // rows per block
   int nch;       // blocks of the row kernel = partial Grams per step
   int b_lds;     // B fits LDS beside a sub-chunk
+  int fuse_b;    // the row kernel forms B (and kappa) itself from A (s4 <= 64)
 };
 
 // Index of logical element (row l, column k) in the stored p x q matrix.
@@ -82,8 +84,10 @@ struct RowArgs {
   double* X;
   double* part;
   const double* B;
-  const double* scal;  // scal[0] = kappa
-  double a;
+  const double* scal;  // scal[0] = kappa (when B comes from k_mx_poly)
+  const double* A;     // the reduced Gram (when the row kernel forms B)
+  int first;           // first step: kappa = 1 / (sqrt(trace A) + eps)
+  double a, cb, cc;    // Newton-Schulz coefficients
   const float* src;    // kLoad: gradient G
   float* mom;          // kLoad: momentum buffer M or NULL
   double mu;
@@ -97,6 +101,7 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
   __shared__ double s_mem[kLdsDoubles];
   const int t = threadIdx.x;
   const int s = d.s, s4 = d.s4;
+  const int ts = s4 + 1;  // LDS row stride: an odd number of doubles puts consecutive rows on other banks
   const int64_t r0 = (int64_t)blockIdx.x * d.ch;
   const int64_t r1 = r0 + d.ch < d.L ? r0 + d.ch : d.L;
   if (r0 >= r1) return;  // uniform per block
@@ -117,32 +122,77 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
       g.X[(r0 + e / (s4 - s)) * s4 + s + e % (s4 - s)] = 0.0;
   } else {
     // X <- kappa (a X + X B), one sub-chunk of rows at a time through LDS
+    __shared__ double s_kappa;
     double* s_b = s_mem;
     double* tile = s_mem + (d.b_lds ? s4 * s4 : 0);
     const double* Bm = d.b_lds ? s_b : g.B;
-    if (d.b_lds) {
-      for (int e = t; e < s4 * s4; e += kThreads) s_b[e] = g.B[e];
+    if (d.fuse_b) {
+      // B = b kappa^2 A + c kappa^4 A^2 from the reduced Gram, in LDS (A sits in
+      // the tile area until B is formed; A is exactly symmetric, so (A^2)[i][j]
+      // is the dot product of rows i and j)
+      double* s_a = tile;
+      for (int e = t; e < s4 * s4; e += kThreads) s_a[(e / s4) * ts + e % s4] = g.A[e];
+      __syncthreads();
+      if (t == 0) {
+        double k = 1.0;
+        if (g.first) {
+          double tr = 0.0;
+          for (int i = 0; i < s4; ++i) tr += s_a[i * ts + i];
+          k = 1.0 / (sqrt(tr) + kNsEps);
+        }
+        s_kappa = k;
+      }
+      __syncthreads();
+      const double k2 = s_kappa * s_kappa;
+      for (int e = t; e < s4 * s4; e += kThreads) {
+        const double* ri = s_a + (e / s4) * ts;
+        const double* rj = s_a + (e % s4) * ts;
+        double sq = 0.0;
+        for (int m = 0; m < s4; ++m) sq = fma(ri[m], rj[m], sq);
+        s_b[e] = g.cb * k2 * ri[e % s4] + g.cc * (k2 * k2) * sq;
+      }
+    } else {
+      if (d.b_lds) {
+        for (int e = t; e < s4 * s4; e += kThreads) s_b[e] = g.B[e];
+      }
+      if (t == 0) s_kappa = g.scal[0];
     }
-    const double kappa = g.scal[0];
+    __syncthreads();
+    const double kappa = s_kappa;
     const int ncg = s4 / 4;
     const int nrg = kThreads / ncg > 0 ? kThreads / ncg : 1;
     const int cg = t % ncg, rg = t / ncg;
     for (int64_t t0 = r0; t0 < r1; t0 += d.sub) {
       const int rows = (int)(r1 - t0 < d.sub ? r1 - t0 : d.sub);
-      for (int e = t; e < rows * s4; e += kThreads) tile[e] = g.X[t0 * s4 + e];
+      for (int e = t; e < rows * s4; e += kThreads) tile[(e / s4) * ts + e % s4] = g.X[t0 * s4 + e];
       __syncthreads();
       if (rg < nrg) {
-        for (int i = rg; i < rows; i += nrg) {
-          double acc[4] = {0.0, 0.0, 0.0, 0.0};
-          const double* xr = tile + i * s4;
+        // two rows per pass share the B loads
+        for (int i = rg; i < rows; i += 2 * nrg) {
+          const int i2 = i + nrg < rows ? i + nrg : i;
+          double acc0[4] = {0.0, 0.0, 0.0, 0.0}, acc1[4] = {0.0, 0.0, 0.0, 0.0};
+          const double* x0 = tile + i * ts;
+          const double* x1 = tile + i2 * ts;
+#pragma unroll 4
           for (int m = 0; m < s4; ++m) {
-            const double x = xr[m];
             const double* br = Bm + m * s4 + 4 * cg;
+            double bv[4];
 #pragma unroll
-            for (int v = 0; v < 4; ++v) acc[v] = fma(x, br[v], acc[v]);
+            for (int v = 0; v < 4; ++v) bv[v] = br[v];
+            const double a0 = x0[m], a1 = x1[m];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              acc0[v] = fma(a0, bv[v], acc0[v]);
+              acc1[v] = fma(a1, bv[v], acc1[v]);
+            }
           }
 #pragma unroll
-          for (int v = 0; v < 4; ++v) g.X[(t0 + i) * s4 + 4 * cg + v] = kappa * fma(g.a, xr[4 * cg + v], acc[v]);
+          for (int v = 0; v < 4; ++v) g.X[(t0 + i) * s4 + 4 * cg + v] = kappa * fma(g.a, x0[4 * cg + v], acc0[v]);
+          if (i2 != i) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              g.X[(t0 + i2) * s4 + 4 * cg + v] = kappa * fma(g.a, x1[4 * cg + v], acc1[v]);
+          }
         }
       }
       __syncthreads();  // the tile is reloaded next
@@ -170,7 +220,7 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
     // 4 x 4 entry blocks per thread; row groups (small s4) are added in order
     __syncthreads();  // this block's rows of X are complete
     double* tile = s_mem;
-    double* red = s_mem + d.sub * s4;
+    double* red = s_mem + d.sub * ts;
     const int nb4 = s4 / 4, nblk = nb4 * nb4;
     const int R = nblk < kThreads ? kThreads / nblk : 1;
     const int groups = nblk <= kThreads ? 1 : (nblk + 4 * kThreads - 1) / (4 * kThreads);
@@ -187,7 +237,7 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
       const int rgp = R > 1 ? t / nblk : 0;
       for (int64_t t0 = r0; t0 < r1; t0 += d.sub) {
         const int rows = (int)(r1 - t0 < d.sub ? r1 - t0 : d.sub);
-        for (int e = t; e < rows * s4; e += kThreads) tile[e] = g.X[t0 * s4 + e];
+        for (int e = t; e < rows * s4; e += kThreads) tile[(e / s4) * ts + e % s4] = g.X[t0 * s4 + e];
         __syncthreads();
         if (rgp < R) {
 #pragma unroll
@@ -196,7 +246,7 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
             if ((R > 1 && u > 0) || blk >= nblk) continue;
             const int bi = blk / nb4, bj = blk % nb4;
             for (int i = rgp; i < rows; i += R) {
-              const double* xr = tile + i * s4;
+              const double* xr = tile + i * ts;
               double xa[4], xb[4];
 #pragma unroll
               for (int v = 0; v < 4; ++v) { xa[v] = xr[4 * bi + v]; xb[v] = xr[4 * bj + v]; }
@@ -254,12 +304,12 @@ __global__ __launch_bounds__(kThreads) void k_mx_reduce(int ne, int nch, const d
   if (e >= ne) return;
   double v = 0.0;
   int c = 0;
-  for (; c + 8 <= nch; c += 8) {
-    double p[8];
+  for (; c + 32 <= nch; c += 32) {
+    double p[32];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) p[k] = part[(int64_t)(c + k) * ne + e];
+    for (int k = 0; k < 32; ++k) p[k] = part[(int64_t)(c + k) * ne + e];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v += p[k];
+    for (int k = 0; k < 32; ++k) v += p[k];
   }
   for (; c < nch; ++c) v += part[(int64_t)c * ne + e];
   A[e] = v;
@@ -267,120 +317,199 @@ __global__ __launch_bounds__(kThreads) void k_mx_reduce(int ne, int nch, const d
 
 // ---------------------------------------------------------------- poly
 // B = b Ah + c Ah^2 with Ah = kappa^2 A; kappa = 1 / (sqrt(trace A) + eps) on
-// the first step (X_0 = U / (||U||_F + eps)), else 1.  Block bx owns rows
-// [16 bx, 16 bx + 16) of B; block 0 publishes kappa for the row kernel.
+// the first step (X_0 = U / (||U||_F + eps)), else 1.  A is exactly symmetric
+// (its (i, j) and (j, i) partial sums take the same products in the same
+// order), so (A^2)[i][j] is the dot product of rows i and j.  Block bx owns
+// rows [16 bx, 16 bx + 16) of B and walks the rows j in chunks of 16, both
+// operands in LDS; block 0 publishes kappa for the row kernel.
 __global__ __launch_bounds__(kThreads) void k_mx_poly(int s4, const double* A, double* B, double* scal, int first,
                                                       double cb, double cc) {
-  __shared__ double s_rows[16 * kMaxShort];
+  __shared__ double s_i[16 * (kMaxShort + 1)];
+  __shared__ double s_j[16 * (kMaxShort + 1)];
   __shared__ double s_kappa;
   const int t = threadIdx.x;
+  const int ts = s4 + 1;  // padded LDS row stride
   const int i0 = blockIdx.x * 16;
-  const int nr = s4 - i0 < 16 ? s4 - i0 : 16;
+  const int ni = s4 - i0 < 16 ? s4 - i0 : 16;
+  for (int e = t; e < ni * s4; e += kThreads) s_i[(e / s4) * ts + e % s4] = A[(int64_t)i0 * s4 + e];
+  for (int i = t; i < s4; i += kThreads) s_j[i] = A[(int64_t)i * s4 + i];  // the diagonal, for the trace
+  __syncthreads();
   if (t == 0) {
     double k = 1.0;
     if (first) {
       double tr = 0.0;
-      for (int i = 0; i < s4; ++i) tr += A[i * s4 + i];
+      for (int i = 0; i < s4; ++i) tr += s_j[i];
       k = 1.0 / (sqrt(tr) + kNsEps);
     }
     s_kappa = k;
     if (blockIdx.x == 0) scal[0] = k;
   }
-  for (int e = t; e < nr * s4; e += kThreads) s_rows[e] = A[(int64_t)i0 * s4 + e];
-  __syncthreads();
-  const double k2 = s_kappa * s_kappa, k4 = k2 * k2;
-  for (int e = t; e < nr * s4; e += kThreads) {
-    const int i = e / s4, j = e % s4;
-    double sq = 0.0;
-    for (int m = 0; m < s4; ++m) sq = fma(s_rows[i * s4 + m], A[m * s4 + j], sq);
-    B[(int64_t)(i0 + i) * s4 + j] = cb * k2 * s_rows[e] + cc * k4 * sq;
+  const int ii = t / 16, jj = t % 16;
+  for (int j0 = 0; j0 < s4; j0 += 16) {
+    const int nj = s4 - j0 < 16 ? s4 - j0 : 16;
+    __syncthreads();  // kappa and s_i are ready; the previous chunk's readers are done
+    for (int e = t; e < nj * s4; e += kThreads) s_j[(e / s4) * ts + e % s4] = A[(int64_t)j0 * s4 + e];
+    __syncthreads();
+    if (ii < ni && jj < nj) {
+      const double* ri = s_i + ii * ts;
+      const double* rj = s_j + jj * ts;
+      double sq = 0.0;
+      for (int m = 0; m < s4; ++m) sq = fma(ri[m], rj[m], sq);
+      const double k2 = s_kappa * s_kappa;
+      B[(int64_t)(i0 + ii) * s4 + j0 + jj] = cb * k2 * ri[j0 + jj] + cc * (k2 * k2) * sq;
+    }
   }
 }
 
 // ---------------------------------------------------------------- spectrum
 // Eigenvalues of the s x s Gram A (row stride s4) by cyclic Jacobi rotations in
 // round-robin order (s/2 disjoint pairs per round, all rotated at once), in
-// LDS, until the off-diagonal mass is below 1e-30 of the diagonal mass.
+// LDS.  A pair is rotated unless its off-diagonal element is negligible next
+// to both its diagonal elements (1e-16 of their geometric mean) or to the whole
+// matrix (1e-18 of the trace: it cannot move any eigenvalue by more); a
+// rotated pair's off-diagonal elements are stored as exact zeros.  Sweeps stop
+// after one without a rotation (at most kMaxSweeps).
 // sigma[k] = sqrt(max(lambda, 0)) in descending order; r_eff = sum lambda^+ /
 // max lambda (0 for the zero matrix).
 __global__ __launch_bounds__(kThreads) void k_mx_eig(int s, int s4, const double* A, double* sigma,
                                                      double* r_eff) {
-  __shared__ double M[kMaxShortSpectrum * kMaxShortSpectrum];
+  const int nt = blockDim.x;  // 64 (one wave: its barriers cost almost nothing) or 256
+  __shared__ double M[kMaxShortSpectrum * (kMaxShortSpectrum + 1)];
   __shared__ double s_c[kMaxShortSpectrum / 2 + 1], s_s[kMaxShortSpectrum / 2 + 1];
   __shared__ int s_p[kMaxShortSpectrum / 2 + 1], s_q[kMaxShortSpectrum / 2 + 1];
-  __shared__ double s_red[2][kThreads];
-  __shared__ int s_done;
+  __shared__ double s_floor;
+  __shared__ int s_rotated;
   const int t = threadIdx.x;
-  for (int e = t; e < s * s; e += kThreads) M[e] = A[(e / s) * s4 + e % s];
+  const int ms = s + 1;  // padded LDS row stride (columns of M are read across lanes)
+  for (int e = t; e < s * s; e += nt) M[(e / s) * ms + e % s] = A[(e / s) * s4 + e % s];
   __syncthreads();
+  if (t == 0) {
+    double tr = 0.0;
+    for (int i = 0; i < s; ++i) tr += M[i * ms + i];
+    s_floor = 1e-18 * tr;
+  }
   const int m = s + (s & 1);  // players; index s is the bye when s is odd
   const int np = m / 2;
   for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
-    double off = 0.0, dg = 0.0;
-    for (int e = t; e < s * s; e += kThreads) {
-      const double v = M[e] * M[e];
-      if (e / s == e % s) dg += v; else off += v;
-    }
-    s_red[0][t] = off;
-    s_red[1][t] = dg;
-    __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
-      if (t < w) {
-        s_red[0][t] += s_red[0][t + w];
-        s_red[1][t] += s_red[1][t + w];
-      }
-      __syncthreads();
-    }
-    if (t == 0) s_done = s_red[0][0] <= 1e-30 * s_red[1][0];
-    __syncthreads();
-    if (s_done) break;
+    __syncthreads();  // s_floor is set; the previous sweep's s_rotated has been read
+    if (t == 0) s_rotated = 0;
     for (int round = 0; round < m - 1; ++round) {
+      __syncthreads();  // the previous round's updates are complete
       if (t < np) {
         // circle method: player 0 fixed, players 1 .. m-1 rotate by one per round
         const int a = t == 0 ? 0 : 1 + (t - 1 + round) % (m - 1);
         const int b = 1 + (m - 2 - t + round) % (m - 1);
         const int p = a < b ? a : b, q = a < b ? b : a;
         double c = 1.0, sn = 0.0;
-        if (q < s && M[p * s + q] != 0.0) {
-          const double tau = (M[q * s + q] - M[p * s + p]) / (2.0 * M[p * s + q]);
-          const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + hypot(1.0, tau));
-          c = 1.0 / sqrt(1.0 + tt * tt);
-          sn = tt * c;
+        bool rot = false;
+        if (q < s) {
+          const double apq = M[p * ms + q], app = M[p * ms + p], aqq = M[q * ms + q];
+          rot = fabs(apq) > s_floor && fabs(apq) > 1e-16 * sqrt(fabs(app * aqq));
+          if (rot) {
+            const double tau = (aqq - app) / (2.0 * apq);
+            const double at = fabs(tau);
+            // tan of the smaller rotation angle; 1 / (2 tau) where tau^2 would overflow
+            const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (at > 1e150 ? 2.0 * at : at + sqrt(1.0 + tau * tau));
+            c = 1.0 / sqrt(1.0 + tt * tt);
+            sn = tt * c;
+            s_rotated = 1;
+          }
         }
         s_c[t] = c;
         s_s[t] = sn;
         s_p[t] = p;
-        s_q[t] = q < s ? q : -1;
+        s_q[t] = rot ? q : -1;
       }
       __syncthreads();
-      for (int e = t; e < s * np; e += kThreads) {  // columns p, q of every row
-        const int i = e / np, k = e % np, q = s_q[k];
-        if (q < 0) continue;
-        const int p = s_p[k];
-        const double c = s_c[k], sn = s_s[k];
-        const double xp = M[i * s + p], xq = M[i * s + q];
-        M[i * s + p] = c * xp - sn * xq;
-        M[i * s + q] = sn * xp + c * xq;
+      // work item e = (row or column index) * np + pair; when nt is a multiple
+      // of np every thread keeps one pair, so its rotation is loaded once and
+      // the loop's iterations are independent
+      const int k0 = t % np, step = nt / np;
+      const bool fixed = nt % np == 0;
+      if (fixed) {
+        const int q = s_q[k0];
+        if (q >= 0) {
+          const int p = s_p[k0];
+          const double c = s_c[k0], sn = s_s[k0];
+          // columns p, q of every row, eight rows' loads ahead of their stores
+          for (int i0 = t / np; i0 < s; i0 += 8 * step) {
+            double xp[8], xq[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int i = i0 + u * step < s ? i0 + u * step : i0;
+              xp[u] = M[i * ms + p];
+              xq[u] = M[i * ms + q];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int i = i0 + u * step;
+              if (i < s) {
+                M[i * ms + p] = c * xp[u] - sn * xq[u];
+                M[i * ms + q] = sn * xp[u] + c * xq[u];
+              }
+            }
+          }
+        }
+      } else {
+        for (int e = t; e < s * np; e += nt) {
+          const int i = e / np, k = e % np, q = s_q[k];
+          if (q < 0) continue;
+          const int p = s_p[k];
+          const double c = s_c[k], sn = s_s[k];
+          const double xp = M[i * ms + p], xq = M[i * ms + q];
+          M[i * ms + p] = c * xp - sn * xq;
+          M[i * ms + q] = sn * xp + c * xq;
+        }
       }
       __syncthreads();
-      for (int e = t; e < s * np; e += kThreads) {  // rows p, q of every column
-        const int k = e / s, j = e % s, q = s_q[k];
-        if (q < 0) continue;
-        const int p = s_p[k];
-        const double c = s_c[k], sn = s_s[k];
-        const double xp = M[p * s + j], xq = M[q * s + j];
-        M[p * s + j] = c * xp - sn * xq;
-        M[q * s + j] = sn * xp + c * xq;
+      // rows p, q of every column; the rotation annihilates (p, q) and (q, p):
+      // store the exact zero, not the rounding residue, which would otherwise
+      // be rotated again
+      if (fixed) {
+        const int q = s_q[k0];
+        if (q >= 0) {
+          const int p = s_p[k0];
+          const double c = s_c[k0], sn = s_s[k0];
+          for (int j0 = t / np; j0 < s; j0 += 8 * step) {
+            double xp[8], xq[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int j = j0 + u * step < s ? j0 + u * step : j0;
+              xp[u] = M[p * ms + j];
+              xq[u] = M[q * ms + j];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int j = j0 + u * step;
+              if (j < s) {
+                M[p * ms + j] = j == q ? 0.0 : c * xp[u] - sn * xq[u];
+                M[q * ms + j] = j == p ? 0.0 : sn * xp[u] + c * xq[u];
+              }
+            }
+          }
+        }
+      } else {
+        for (int e = t; e < s * np; e += nt) {
+          const int j = e / np, k = e % np, q = s_q[k];
+          if (q < 0) continue;
+          const int p = s_p[k];
+          const double c = s_c[k], sn = s_s[k];
+          const double xp = M[p * ms + j], xq = M[q * ms + j];
+          M[p * ms + j] = j == q ? 0.0 : c * xp - sn * xq;
+          M[q * ms + j] = j == p ? 0.0 : sn * xp + c * xq;
+        }
       }
-      __syncthreads();
     }
+    __syncthreads();
+    if (!s_rotated) break;  // uniform: every thread reads the same flag
   }
+  __syncthreads();
   // descending order by rank (ties by index)
-  for (int i = t; i < s; i += kThreads) {
-    const double li = M[i * s + i];
+  for (int i = t; i < s; i += nt) {
+    const double li = M[i * ms + i];
     int rank = 0;
     for (int j = 0; j < s; ++j) {
-      const double lj = M[j * s + j];
+      const double lj = M[j * ms + j];
       rank += (lj > li) || (lj == li && j < i);
     }
     sigma[rank] = sqrt(li > 0.0 ? li : 0.0);
@@ -388,7 +517,7 @@ __global__ __launch_bounds__(kThreads) void k_mx_eig(int s, int s4, const double
   if (t == 0) {
     double tot = 0.0, top = 0.0;
     for (int i = 0; i < s; ++i) {
-      const double l = M[i * s + i] > 0.0 ? M[i * s + i] : 0.0;
+      const double l = M[i * ms + i] > 0.0 ? M[i * ms + i] : 0.0;
       tot += l;
       top = l > top ? l : top;
     }
@@ -418,20 +547,23 @@ Plan make_plan(int p, int q) {
   d.s4 = (d.s + 3) & ~3;
   d.q = q;
   d.b_lds = d.s4 * d.s4 <= 8192;
+  d.fuse_b = d.s4 <= 64;
   const int room = kLdsDoubles - (d.b_lds ? d.s4 * d.s4 : 0);
   // the Gram pass also keeps up to 4096 doubles of row-group sums beside the tile
-  int sub = (room - 4096) / d.s4;
+  int sub = (room - 4096) / (d.s4 + 1);
   sub = sub > 512 ? 512 : sub;
   sub = sub >= 16 ? sub & ~15 : (sub >= 1 ? sub : 1);
   d.sub = sub;
-  // about 64 blocks, each row chunk a whole number of sub-chunks, partial
-  // Grams capped at 64 MiB
+  // Chunks: at least one per 64 rows and one per 2^18 multiply-adds of the
+  // row update (L s4^2 in all), at most 256, partial Grams capped at 64 MiB.
+  // Fewer chunks make the ordered reduction short; more make each block short.
   const int64_t cap = (int64_t)(64u << 20) / ((int64_t)d.s4 * d.s4 * 8);
-  int64_t nch = (d.L + 63) / 64;
-  nch = nch > 64 ? 64 : nch;
+  const int64_t by_rows = (d.L + 63) / 64;
+  const int64_t by_work = ((int64_t)d.L * d.s4 * d.s4 + (1 << 18) - 1) >> 18;
+  int64_t nch = by_rows > by_work ? by_rows : by_work;
+  nch = nch > 256 ? 256 : nch;
   if (nch > cap) nch = cap > 0 ? cap : 1;
-  int64_t ch = (d.L + nch - 1) / nch;
-  ch = (ch + sub - 1) / sub * sub;
+  const int64_t ch = (d.L + nch - 1) / nch;
   d.ch = (int)ch;
   d.nch = (int)((d.L + ch - 1) / ch);
   size_t off = 0;
@@ -487,10 +619,15 @@ void run_ns(const Plan& P, char* ws, RowArgs g, int steps, double a, double b, d
   for (int i = 0; i < n; ++i) {
     hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), blk, 0, st, ne, d.nch,
                        (const double*)g.part, A);
-    hipLaunchKernelGGL(k_mx_poly, dim3((d.s4 + 15) / 16), blk, 0, st, d.s4, (const double*)A, B, scal, (int)(i == 0),
-                       b, c);
+    if (!d.fuse_b)
+      hipLaunchKernelGGL(k_mx_poly, dim3((d.s4 + 15) / 16), blk, 0, st, d.s4, (const double*)A, B, scal,
+                         (int)(i == 0), b, c);
     RowArgs gi = g;
+    gi.A = A;
+    gi.first = i == 0;
     gi.a = a;
+    gi.cb = b;
+    gi.cc = c;
     if (i + 1 < n)
       hipLaunchKernelGGL(k_mx_rows<kStep>, grid, blk, 0, st, d, gi);
     else
@@ -576,7 +713,8 @@ int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, doub
   double* A = (double*)(wsc + P.off_a);
   hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), dim3(kThreads), 0, st, ne, d.nch,
                      (const double*)g.part, A);
-  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(kThreads), 0, st, d.s, d.s4, (const double*)A, sigma, r_eff);
+  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(d.s <= 64 ? 64 : kThreads), 0, st, d.s, d.s4, (const double*)A, sigma,
+                     r_eff);
   return launch_status();
 }
 
