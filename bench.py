@@ -246,7 +246,9 @@ def optimizer_timing(lib, d: dict, r: int, dev, iters: int, cpu: bool) -> dict:
         return e0.elapsed_time(e1) * 1e3 / iters
 
     steps = 5
-    out = {"ns_steps": steps, "coefficients": list(R.NS_QUINTIC), "launches_per_update": 1 + 3 * steps,
+    # load, then per step: reduce (+ poly when the short side exceeds 64) + row update
+    out = {"ns_steps": steps, "coefficients": list(R.NS_QUINTIC),
+           "launches_per_update": 1 + (2 if r <= 64 else 3) * steps,
            "timing": "hip graph replay of one call", "iterations": iters}
     keep = {}
     for nm in ("W_e", "W_d"):
