@@ -109,18 +109,21 @@ def summarize_profiles(trace_dir: str, fetch_dir: str, write_dir: str, name: str
         for k, cn, v in db(d).execute("select kernel_name, counter_name, value from counters_collection"):
             if cn == cname:
                 out.setdefault(short(k), []).append(v)
-        return {k: sum(v) / len(v) for k, v in out.items()}
+        return out
 
-    fetch, write = counter(fetch_dir, "FETCH_SIZE"), counter(write_dir, "WRITE_SIZE")
+    fetch_all, write_all = counter(fetch_dir, "FETCH_SIZE"), counter(write_dir, "WRITE_SIZE")
     copy_bytes = None
-    for k in fetch:
+    for k in fetch_all:
         if "copyBuffer" in k or "copy" in k.lower():
+            # the probe is the largest copy of the run (inputs are also copied, in smaller pieces)
             copy_bytes = COPY_PROBE_MIB * 2**20
-            f_fetch = copy_bytes / (fetch[k] * 1024)
-            f_write = copy_bytes / (write[k] * 1024)
+            f_fetch = copy_bytes / (max(fetch_all[k]) * 1024)
+            f_write = copy_bytes / (max(write_all[k]) * 1024)
             break
     if copy_bytes is None:
         raise SystemExit("the runs hold no plain copy kernel to calibrate the counters")
+    fetch = {k: sum(v) / len(v) for k, v in fetch_all.items()}
+    write = {k: sum(v) / len(v) for k, v in write_all.items()}
     ops = {}
     for k in fetch:
         op = kernel_op(k)
