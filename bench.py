@@ -263,6 +263,15 @@ def optimizer_timing(lib, d: dict, r: int, dev, iters: int, cpu: bool) -> dict:
         out[f"muon_update_us_{nm}"] = graph_us(
             lambda W=W, G=G, M=M, ws=ws: lib.muon_update(W, G, M, 1e-4, momentum=0.95, ws=ws, steps=steps))
         keep[nm] = (W0, G, ws)
+    # algorithmic flops of one update: per step the Gram (2 L s^2), B (2 s^3) and
+    # X B (2 L s^2), plus the Gram of the loaded matrix; float64 vector peak
+    W0 = d["W_e"]
+    L_, s_ = max(W0.shape), min(W0.shape)
+    flops = 2 * L_ * s_ * s_ + steps * (4 * L_ * s_ * s_ + 2 * s_ ** 3)
+    tf = flops / (out["muon_update_us_W_e"] * 1e-6) / 1e12
+    out["roofline"] = {"bound": "latency", "kernel": "muon_update", "achieved": tf, "peak": 78.6,
+                       "unit": "TFLOP/s", "frac": tf / 78.6, "flops_per_update": flops,
+                       "note": "11 launches on 64 blocks; launch and memory latency bound the chain"}
     if r <= 128:
         W0, _, ws = keep["W_d"]
         Wd = W0.to(dev)
