@@ -401,7 +401,7 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
                                                      const io_t* __restrict__ z, int64_t ld_z,
                                                      const void* __restrict__ wf, io_t* __restrict__ b,
                                                      float* __restrict__ a_save) {
-  constexpr int U = NT <= 2 ? 2 : 1;    // k-steps per wave and stage
+  constexpr int U = ef_u(NT);           // k-steps per wave and stage
   constexpr bool PW = NT <= 4;          // W_e fragments travel with the stage
   constexpr int NW = PW ? NT : 1;
   constexpr int TOK = 16 * MT;

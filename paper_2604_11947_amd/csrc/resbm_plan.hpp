@@ -38,7 +38,11 @@ constexpr int kNumCU = 256;          // MI355X compute units (8 XCDs x 32)
 constexpr size_t kWsAlign = 256;
 
 // ---- encode_fwd: a block owns 16*MT tokens; its KW waves split the n-contraction.
-constexpr int ef_mt(int NT) { return NT <= 2 ? RESBM_EF_MT_SMALL_R : (NT <= 4 ? 2 : 1); }
+// 64 tokens per block up to r = 64 (at r = 64: 55 -> 46 us at n = 4096, T = 16384).
+constexpr int ef_mt(int NT) { return NT <= 2 ? RESBM_EF_MT_SMALL_R : (NT <= 4 ? 4 : 1); }
+// k-steps of 32 columns per wave and stage: two up to r = 64, so that a stage
+// row is 512 bytes (at r = 64: 51 -> 41 us with the 64-token blocks)
+constexpr int ef_u(int NT) { return NT <= 4 ? 2 : 1; }
 #ifndef RESBM_EF_KW
 #define RESBM_EF_KW 4
 #endif
@@ -58,7 +62,13 @@ constexpr int db_jt(int NT) { return NT < 4 ? NT : 4; }
 // ---- encode_bwd: blocks of CW x TW waves; a wave owns 16*CT columns, a block
 // step covers 32*TW tokens (g_z is written by the decode_fwd expand kernel).
 // Workspace: the dW_e partials of the token groups, then g_h (split) for g_z.
+// a 256-column block up to r = 64 (at r = 64: 127 -> 112 us for the op); the
+// float32 build's tiles are twice as large and keep 128 columns at r > 32
+#if RESBM_IO_F32_BUILD
 constexpr int eb_ct(int KS) { return KS <= 1 ? 4 : (KS <= 2 ? 2 : 1); }
+#else
+constexpr int eb_ct(int KS) { return KS <= 2 ? 4 : 1; }
+#endif
 #ifndef RESBM_EB_CW
 #define RESBM_EB_CW 4
 #endif
