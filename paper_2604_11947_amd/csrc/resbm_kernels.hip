@@ -172,20 +172,29 @@ __device__ __forceinline__ void bst_frag(rsrc_t r, uint32_t off, const XFrag& f)
 // 8 consecutive elements m[row][kb .. kb + 8) of a packed matrix with r columns
 // (payload, wire gradient), zeros at columns >= r; r % 4 == 0, so a lane gets 8,
 // 4 or 0 of them.  `row_off` is the row's byte offset in the descriptor (or kOOB).
+// R8: the caller knows r % 8 == 0 (at compile time), so the 8 elements are in
+// range together and one aligned 16-byte load fetches them.  A run-time test
+// here would put a branch around the loads of the callers' loops.
+template <bool R8 = false>
 __device__ __forceinline__ XFrag bld_r8(rsrc_t m, uint32_t row_off, int r, int kb) {
   const bool lo = kb < r, hi = kb + 4 < r;
   const uint32_t olo = (row_off == kOOB || !lo) ? kOOB : row_off + kb * kEs;
-  const uint32_t ohi = (row_off == kOOB || !hi) ? kOOB : row_off + (kb + 4) * kEs;
   XFrag f;
 #if RESBM_IO_F32_BUILD
+  const uint32_t ohi = (row_off == kOOB || !hi) ? kOOB : row_off + (kb + 4) * kEs;
   const uint4 a = bld16(m, olo), b = bld16(m, ohi);
   f.v[0] = __builtin_bit_cast(float, a.x); f.v[1] = __builtin_bit_cast(float, a.y);
   f.v[2] = __builtin_bit_cast(float, a.z); f.v[3] = __builtin_bit_cast(float, a.w);
   f.v[4] = __builtin_bit_cast(float, b.x); f.v[5] = __builtin_bit_cast(float, b.y);
   f.v[6] = __builtin_bit_cast(float, b.z); f.v[7] = __builtin_bit_cast(float, b.w);
 #else
-  const uint2 a = bld8(m, olo), b = bld8(m, ohi);
-  f.v = __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+  if constexpr (R8) {
+    f.v = __builtin_bit_cast(bf16x8, bld16(m, olo));
+  } else {
+    const uint32_t ohi = (row_off == kOOB || !hi) ? kOOB : row_off + (kb + 4) * kEs;
+    const uint2 a = bld8(m, olo), b = bld8(m, ohi);
+    f.v = __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+  }
 #endif
   return f;
 }
@@ -1246,7 +1255,7 @@ struct FinArgs {
   int64_t ld_gx;
 };
 
-template <int KS, int CT, bool ADD, bool GZ>
+template <int KS, int CT, bool ADD, bool GZ, bool R8>
 __global__ __launch_bounds__(256) void k_expand(int64_t T, int n, int r,
                                                 const io_t* __restrict__ in, const io_t* __restrict__ in_lo,
                                                 const io_t* __restrict__ idsrc, const float* __restrict__ W,
@@ -1321,8 +1330,8 @@ __global__ __launch_bounds__(256) void k_expand(int64_t T, int n, int r,
     const uint32_t ro = (uint32_t)(t * r * kEs);  // rows >= `rows` are out of range
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      x.p[ks] = bld_r8(br, ro, r, ks * 32 + grp * 8);
-      if constexpr (LO) x.q[ks] = bld_r8(lr, ro, r, ks * 32 + grp * 8);
+      x.p[ks] = bld_r8<R8>(br, ro, r, ks * 32 + grp * 8);
+      if constexpr (LO) x.q[ks] = bld_r8<R8>(lr, ro, r, ks * 32 + grp * 8);
     }
     if constexpr (ADD) {
 #pragma unroll
@@ -1469,6 +1478,11 @@ void launch_enc_fwd(const Plan& p, int act, const io_t* x, int64_t ld_x, const i
                      z, ld_z, wf, b, a_save);
 }
 
+// The expand kernel's input rows are fetched 8 elements per 16-byte load when
+// r % 8 == 0 (else as two 8-byte halves, one of them past r at r % 8 == 4);
+// at r = 64 that took decode_fwd from 40 to 28 us and encode_bwd from 112 to 86.
+bool expand_r8(int r) { return r % 8 == 0; }
+
 template <int KS>
 void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, io_t* zt, int64_t ld,
                     hipStream_t st) {
@@ -1479,12 +1493,16 @@ void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, 
   dim3 grid(p.df_nwg, p.df_ngrp);
 #endif
   const FinArgs none{};
-  if (add_id)
-    hipLaunchKernelGGL((k_expand<KS, CT, true, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt,
-                       ld, p.df_tpg, (int)grid.y, none);
-  else
-    hipLaunchKernelGGL((k_expand<KS, CT, false, false>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt,
-                       ld, p.df_tpg, (int)grid.y, none);
+  const bool r8 = expand_r8(p.r);
+#define CALL_DF(ADD, R8)                                                                                      \
+  hipLaunchKernelGGL((k_expand<KS, CT, ADD, false, R8>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt, \
+                     ld, p.df_tpg, (int)grid.y, none)
+  if (add_id) {
+    if (r8) CALL_DF(true, true); else CALL_DF(true, false);
+  } else {
+    if (r8) CALL_DF(false, true); else CALL_DF(false, false);
+  }
+#undef CALL_DF
 }
 
 template <int JT>
@@ -1523,12 +1541,16 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
   // the finishing blocks follow in extra grid rows (dispatched after the g_z blocks, run beside them)
   const int main_y = (int)ggrid.y;
   ggrid.y += (unsigned)ceil_div(fin.nb_all, (int64_t)ggrid.x);
-  if (fused)
-    hipLaunchKernelGGL((k_expand<KS, GCT, true, true>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b,
-                       W_e, g_z, ld_gz, p.df_tpg, main_y, fin);
-  else
-    hipLaunchKernelGGL((k_expand<KS, GCT, false, true>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b,
-                       W_e, g_z, ld_gz, p.df_tpg, main_y, fin);
+  const bool r8 = expand_r8(p.r);
+#define CALL_GZ(ADD, R8)                                                                                          \
+  hipLaunchKernelGGL((k_expand<KS, GCT, ADD, true, R8>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b, \
+                     W_e, g_z, ld_gz, p.df_tpg, main_y, fin)
+  if (fused) {
+    if (r8) CALL_GZ(true, true); else CALL_GZ(true, false);
+  } else {
+    if (r8) CALL_GZ(false, true); else CALL_GZ(false, false);
+  }
+#undef CALL_GZ
 }
 
 #define RESBM_DISPATCH_NT(NTV, CALL) \
