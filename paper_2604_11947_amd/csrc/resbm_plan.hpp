@@ -38,8 +38,11 @@ constexpr int kNumCU = 256;          // MI355X compute units (8 XCDs x 32)
 constexpr size_t kWsAlign = 256;
 
 // ---- encode_fwd: a block owns 16*MT tokens; its KW waves split the n-contraction.
-// 64 tokens per block up to r = 64 (at r = 64: 55 -> 46 us at n = 4096, T = 16384).
-constexpr int ef_mt(int NT) { return NT <= 2 ? RESBM_EF_MT_SMALL_R : (NT <= 4 ? 4 : 1); }
+// 64 tokens per block up to r = 64 (at r = 64: 55 -> 46 us at n = 4096, T = 16384),
+// 32 up to r = 128 (at r = 128: 116 -> 90 us; every block reads all of W_e's
+// fragments, so more tokens per block mean less L2 traffic), 16 beyond (32 was
+// slower at r = 256).
+constexpr int ef_mt(int NT) { return NT <= 2 ? RESBM_EF_MT_SMALL_R : (NT <= 4 ? 4 : (NT <= 8 ? 2 : 1)); }
 // k-steps of 32 columns per wave and stage: two up to r = 64, so that a stage
 // row is 512 bytes (at r = 64: 51 -> 41 us with the 64-token blocks)
 constexpr int ef_u(int NT) { return NT <= 4 ? 2 : 1; }
@@ -49,7 +52,9 @@ constexpr int ef_u(int NT) { return NT <= 4 ? 2 : 1; }
 constexpr int ef_kw(int NT) { return 8 * 16 * ef_mt(NT) * (16 * NT + 4) * 4 <= 73728 ? RESBM_EF_KW : 4; }
 
 // ---- decode_fwd: a wave owns 16*CT columns and walks a token range.
-constexpr int df_ct(int KS) { return KS <= 2 ? 4 : (KS <= 4 ? 2 : 1); }
+// Four column tiles up to r = 128 (at r = 128: 69 -> 45 us), two beyond (at
+// r = 256: 236 -> 128 us); the g_z pass of encode_bwd follows the same shape.
+constexpr int df_ct(int KS) { return KS <= 4 ? 4 : 2; }
 
 // ---- decode_bwd: 8 waves x 64 columns per block, JT j-tiles (16 of r each) per pass.
 #ifndef RESBM_DB_WAVES
@@ -63,11 +68,13 @@ constexpr int db_jt(int NT) { return NT < 4 ? NT : 4; }
 // step covers 32*TW tokens (g_z is written by the decode_fwd expand kernel).
 // Workspace: the dW_e partials of the token groups, then g_h (split) for g_z.
 // a 256-column block up to r = 64 (at r = 64: 127 -> 112 us for the op); the
-// float32 build's tiles are twice as large and keep 128 columns at r > 32
+// float32 build's tiles are twice as large and keep 128 columns up to r = 128
 #if RESBM_IO_F32_BUILD
-constexpr int eb_ct(int KS) { return KS <= 1 ? 4 : (KS <= 2 ? 2 : 1); }
+constexpr int eb_ct(int KS) { return KS <= 1 ? 4 : (KS <= 4 ? 2 : 1); }
 #else
-constexpr int eb_ct(int KS) { return KS <= 2 ? 4 : 1; }
+// 128 columns beyond r = 64 (at r = 128, with two token waves: 351 -> 219 us
+// for the op; at r = 256: 867 -> 696 us)
+constexpr int eb_ct(int KS) { return KS <= 2 ? 4 : 2; }
 #endif
 #ifndef RESBM_EB_CW
 #define RESBM_EB_CW 4
@@ -76,7 +83,8 @@ constexpr int eb_cw(int) { return RESBM_EB_CW; }
 #ifndef RESBM_EB_TW
 #define RESBM_EB_TW 2
 #endif
-constexpr int eb_tw(int KS) { return KS <= 2 ? RESBM_EB_TW : 1; }
+// two token waves up to r = 128; at r = 256 the g_h tiles of two would not fit LDS
+constexpr int eb_tw(int KS) { return KS <= 4 ? RESBM_EB_TW : 1; }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
