@@ -70,12 +70,16 @@ KERNEL_OP = (("k_enc_fwd", "encode_fwd"), ("k_dec_bwd", "decode_bwd"), ("k_enc_b
 
 def kernel_op(name: str):
     """The boundary op a kernel name belongs to (prologue and finishing kernels included).
-    The expand kernel serves decode_fwd (last template flag false) and the g_z pass of
-    encode_bwd (true)."""
+    The expand kernel <KS, CT, ADD, GZ, R8> serves decode_fwd (GZ false) and the g_z pass
+    of encode_bwd (GZ true)."""
     import re
     base = re.sub(r"\(.*", "", name)
     if "k_expand" in base:
-        gz = base.rstrip().endswith("true>") or re.search(r"k_expandI(?:Li\d+E){2}Lb[01]ELb1E", base) is not None
+        m = re.search(r"k_expand<([^>]*)>", base)
+        if m:
+            gz = m.group(1).split(",")[3].strip() == "true"
+        else:  # mangled: two int arguments, then the ADD and GZ flags
+            gz = re.search(r"k_expandI(?:Li\d+E){2}Lb[01]ELb1E", base) is not None
         return "encode_bwd" if gz else "decode_fwd"
     for key, op in KERNEL_OP:
         if key in base or key.replace("_", "") in base.replace("_", ""):
