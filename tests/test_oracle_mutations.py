@@ -134,3 +134,53 @@ def test_muon_pin_rejects_planted_mistake(monkeypatch, name, bad, pin):
     monkeypatch.setattr(MU, name, bad)
     with pytest.raises(AssertionError):
         pin()
+
+
+# ---------------------------------------------------------------- two-linears-per-side oracle
+import test_two_linear_oracle_pins as TP  # noqa: E402
+from oracle import two_linear_oracle as TL  # noqa: E402
+
+
+def _dec2_bwd_no_dphi(b, v, g_zt, g_id, W3, W4, act):
+    p = R.phi(v, act)
+    g_v = g_zt @ W4.T
+    g_b = g_v @ W3.T + (g_id[:, :W3.shape[0]] if g_id is not None else 0)
+    return g_b, b.T @ g_v, p.T @ g_zt
+
+
+def _dec2_bwd_no_identity(b, v, g_zt, g_id, W3, W4, act):
+    p = R.phi(v, act)
+    g_v = (g_zt @ W4.T) * R.dphi(v, act)
+    return g_v @ W3.T, b.T @ g_v, p.T @ g_zt
+
+
+def _enc2_bwd_dw2_before_phi(z, u, g_b, W1, W2, act):
+    g_u = (g_b @ W2.T) * R.dphi(u, act)
+    return g_u @ W1.T, z.T @ g_u, u.T @ g_b
+
+
+def _enc2_fwd_phi_after_second_layer(x_attn, z, W1, W2, act):
+    u = z @ W1
+    return x_attn[:, :W2.shape[1]] + R.phi(u @ W2, act), u
+
+
+def _dec2_fwd_phi_on_input(b, W3, W4, act):
+    v = b @ W3
+    return R.phi(b, act) @ W3 @ W4, v
+
+
+TWO_LINEAR_MUTATIONS = [
+    ("decode2_bwd", _dec2_bwd_no_dphi, lambda: TP.test_gradients_finite_differences(R.ACT_SILU)),
+    ("decode2_bwd", _dec2_bwd_no_identity, lambda: TP.test_gradients_torch_autograd(R.ACT_IDENTITY)),
+    ("encode2_bwd", _enc2_bwd_dw2_before_phi, TP.test_unit_second_layer_is_one_linear_encoder),
+    ("encode2_fwd", _enc2_fwd_phi_after_second_layer, lambda: TP.test_gradients_torch_autograd(R.ACT_SILU)),
+    ("decode2_fwd", _dec2_fwd_phi_on_input, lambda: TP.test_gradients_torch_autograd(R.ACT_SILU)),
+]
+
+
+@pytest.mark.parametrize("name,bad,pin", TWO_LINEAR_MUTATIONS,
+                         ids=[f"{m[0]}:{m[1].__name__.lstrip('_')}" for m in TWO_LINEAR_MUTATIONS])
+def test_two_linear_pin_rejects_planted_mistake(monkeypatch, name, bad, pin):
+    monkeypatch.setattr(TL, name, bad)
+    with pytest.raises(AssertionError):
+        pin()
