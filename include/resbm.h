@@ -211,6 +211,81 @@ size_t resbm_matrix_workspace_bytes(int32_t p, int32_t q);
  * the four ops, a multiple of 256.  Returns 0 when (n, r) break the shape rules. */
 size_t resbm_workspace_bytes(int64_t T, int32_t n, int32_t r);
 
+/*
+ * Two-linears-per-side variant.  Sec. 3.2 describes the encoder and the
+ * decoder each as two linear layers with a non-linearity between them; with
+ * the intermediate width m (paper: not stated):
+ *     encoder  u = z W1               (T x m)
+ *              b = x_attn I_{n x r} + phi(u) W2
+ *     decoder  v = b W3               (T x m)
+ *              z_tilde = phi(v) W4    (decoder identity: the caller adds
+ *                                      b I_{r x n}, as with add_identity == 0)
+ * The n x m and m x n products (2 T n m flops each) make these ops
+ * matrix-core bound, so the weights are bfloat16 (the caller's working copy
+ * of its float32 masters) and enter the matrix cores once.  Conventions as
+ * above, except:
+ *  - every activation, payload, saved pre-activation and weight is bfloat16
+ *    in both libraries; weight gradients are float32, overwritten;
+ *  - shape rules: n, m, r multiples of 8; 8 <= r <= n <= 65536;
+ *    8 <= m <= 65536; T * max(n, m) * 2 bytes below 4 GiB; leading
+ *    dimensions ld >= n with ld % 8 == 0; all pointers 16-byte aligned;
+ *  - weights row-major and contiguous: W1 n x m, W2 m x r, W3 r x m, W4 m x n;
+ *  - u and v (T x m, packed) are written by the forward ops for the
+ *    backward ops;
+ *  - products inside an op consume bf16 operands: phi(u), phi(v), and the
+ *    gradients g_u, g_v held in the workspace between two products, are
+ *    rounded to bf16 first (accumulation is float32);
+ *  - the backward ops take ws of resbm2_workspace_bytes(T, n, m, r) bytes
+ *    (the T x m gradient and split-K partial sums); the forward ops take
+ *    none (ws may be NULL).
+ */
+size_t resbm2_workspace_bytes(int64_t T, int32_t n, int32_t m, int32_t r);
+
+/*  x_attn  T x n, row stride ld_x; only columns [0, r) are read.
+ *  z       T x n, row stride ld_z (the feed-forward output).
+ *  b       out, T x r packed (the payload).
+ *  u       out, T x m packed (saved for resbm2_encode_bwd). */
+int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act,
+                          const void* x_attn, int64_t ld_x, const void* z, int64_t ld_z,
+                          const void* W1, const void* W2, void* b, void* u,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/*  b        T x r packed.
+ *  z_tilde  out, T x n, row stride ld_zt.
+ *  v        out, T x m packed (saved for resbm2_decode_bwd). */
+int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act,
+                          const void* b, const void* W3, const void* W4,
+                          void* z_tilde, int64_t ld_zt, void* v,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/* Adjoint of resbm2_decode_fwd:
+ *     g_v  = (g_zt W4^T) * phi'(v)         (workspace, bf16)
+ *     dW4  = phi(v)^T g_zt,  dW3 = b^T g_v (token sums in a fixed order)
+ *     g_b  = g_v W3^T + g_id I_{n x r}     (g_id NULL: no identity gradient)
+ *  b, v as the forward received and wrote them; g_zt, g_id T x n with row
+ *  strides ld_gzt, ld_gid (only columns [0, r) of g_id are read). */
+int32_t resbm2_decode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act,
+                          const void* b, const void* v,
+                          const void* g_zt, int64_t ld_gzt, const void* g_id, int64_t ld_gid,
+                          const void* W3, const void* W4,
+                          void* g_b, float* dW3, float* dW4,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/* Adjoint of resbm2_encode_fwd:
+ *     g_u  = (g_b W2^T) * phi'(u)          (workspace, bf16)
+ *     dW2  = phi(u)^T g_b,  dW1 = z^T g_u  (token sums in a fixed order)
+ *     g_z  = g_u W1^T
+ *     g_x[:, 0:r] += g_b                   (when g_x != NULL; g_x may equal g_z
+ *                                           with ld_gx == ld_gz: then
+ *                                           g_z = g_u W1^T + g_b I_{r x n},
+ *                                           rounded once) */
+int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act,
+                          const void* z, int64_t ld_z, const void* u, const void* g_b,
+                          const void* W1, const void* W2,
+                          void* g_z, int64_t ld_gz, void* g_x, int64_t ld_gx,
+                          float* dW1, float* dW2,
+                          void* ws, size_t ws_bytes, void* stream);
+
 /* RESBM_IO_BF16 for libresbm.so, RESBM_IO_F32 for the validation build. */
 int32_t resbm_io_dtype(void);
 

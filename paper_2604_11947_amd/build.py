@@ -14,7 +14,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "resbm_kernels.hip")
 SRC_MATRIX = os.path.join(PKG, "csrc", "resbm_matrix.hip")
-DEPS = [SRC, SRC_MATRIX, os.path.join(PKG, "csrc", "resbm_mfma.hpp"), os.path.join(PKG, "csrc", "resbm_plan.hpp"),
+SRC_TWO = os.path.join(PKG, "csrc", "resbm_two.hip")
+DEPS = [SRC, SRC_MATRIX, SRC_TWO, os.path.join(PKG, "csrc", "resbm_buffer.hpp"), os.path.join(PKG, "csrc", "resbm_mfma.hpp"), os.path.join(PKG, "csrc", "resbm_plan.hpp"),
         os.path.join(ROOT, "include", "resbm.h")]
 
 LIBS = {"bf16": "libresbm.so", "f32": "libresbm_f32.so"}
@@ -31,7 +32,7 @@ def command(variant: str, out: str) -> list[str]:
     cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
            # packed fp32 VALU ops stay disabled in every HIP build of this library
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-I", os.path.join(ROOT, "include"), "-o", out, SRC, SRC_MATRIX]
+           "-I", os.path.join(ROOT, "include"), "-o", out, SRC, SRC_MATRIX, SRC_TWO]
     if variant == "f32":
         cmd.insert(1, "-DRESBM_IO_F32_BUILD=1")
     return cmd

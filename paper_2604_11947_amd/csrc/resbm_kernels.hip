@@ -32,25 +32,15 @@
 #include <string.h>
 
 #include "resbm.h"
+#include "resbm_buffer.hpp"
 #include "resbm_mfma.hpp"
 #include "resbm_plan.hpp"
 
 namespace resbm {
 
 // ---------------------------------------------------------------- buffer access
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-typedef int v2i __attribute__((ext_vector_type(2)));
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-constexpr uint32_t kOOB = 0xFFFFFFF0u;        // a byte offset outside every descriptor
-constexpr int64_t kMaxRange = 0xFFFFF000ll;   // descriptor ranges are clamped below kOOB
 constexpr int kEs = (int)sizeof(io_t);
 
-// Raw buffer descriptor over [base, base + bytes): gfx9-family dword 3, no stride.
-__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
-  const uint32_t nb = bytes <= 0 ? 0u : (bytes > kMaxRange ? (uint32_t)kMaxRange : (uint32_t)bytes);
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nb, 0x00020000);
-}
 // Cache policy of the T x n streams, read or written once per op: non-temporal
 // loads, and non-temporal device-scope stores (streamed out instead of left
 // dirty in the caches for the next kernel to write back).  Everything reused
@@ -67,23 +57,6 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
 #endif
 constexpr int kLdStream = RESBM_LD_STREAM;
 constexpr int kStStream = RESBM_ST_STREAM;
-
-template <int POL = 0>
-__device__ __forceinline__ uint4 bld16(rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, POL));
-}
-template <int POL = 0>
-__device__ __forceinline__ uint2 bld8(rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, POL));
-}
-template <int POL = 0>
-__device__ __forceinline__ void bst16(rsrc_t r, uint32_t off, uint4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, v), r, off, 0, POL);
-}
-template <int POL = 0>
-__device__ __forceinline__ void bst8(rsrc_t r, uint32_t off, uint2 v) {
-  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, v), r, off, 0, POL);
-}
 
 // Byte extent of rows [0, rows) of a row-major matrix with n used columns.
 __device__ __forceinline__ int64_t rows_bytes(int64_t rows, int n, int64_t ld, int es) {
@@ -252,25 +225,6 @@ __device__ __forceinline__ int opaque(int v) {
   return v;
 }
 
-// Column permutation of a row-major tile with WC elements per row staged in
-// LDS.  The 8-element chunks of a row are permuted by an XOR with the row's
-// index among the rows that share a 256-byte bank window (16 / (WC / 8) rows in
-// the bf16 build), so that a wave touches distinct banks both when it copies
-// whole rows (8 lanes per 128 bytes, the layout of coalesced global accesses)
-// and when it reads one chunk from each of 16 rows (matrix-core fragments).
-// Chunks stay contiguous and never leave their row; WC whose chunk count is not
-// a power of two up to 8 is left as is.
-template <int WC>
-__device__ __forceinline__ int tile_col(int row, int col) {
-  constexpr int CPR = WC / 8;
-  if constexpr (CPR == 8 || CPR == 4 || CPR == 2) {
-    constexpr int RPW = 16 / CPR;
-    return ((((col >> 3) ^ (row / RPW)) & (CPR - 1)) << 3) | (col & 7);
-  } else {
-    return col;
-  }
-}
-
 // Loads 8 consecutive elements at (row, col) of a WC-wide tile (col % 8 == 0).
 template <int WC>
 __device__ __forceinline__ XFrag tile_get8(const io_t* tile, int row, int col) {
@@ -326,15 +280,6 @@ __device__ __forceinline__ XFrag tr_frag(const io_t* tile, int c0, int row16, in
                                                                                h[1][0], h[1][1], h[1][2], h[1][3]});
 #endif
   return f;
-}
-
-// Column permutation of a block-wide row-major tile (WIDE elements per row, a
-// multiple of 128): the 8-element chunk index is XORed with the row's low four
-// bits, which keeps rows written whole (64 lanes x 16 bytes, the layout of
-// 1 KiB-contiguous global loads) conflict-free and spreads one chunk read from
-// 16 rows (matrix-core fragments) over all banks.
-__device__ __forceinline__ int wide_col(int row, int col) {
-  return ((((col >> 3) ^ row) & 15) | ((col >> 3) & ~15)) << 3 | (col & 7);
 }
 
 // Transposed fragment from a block-wide tile (see wide_col): lane (row16, grp)

@@ -196,6 +196,35 @@ __device__ __forceinline__ void store_x4(io_t* p, const float (&v)[4]) {
 #endif
 }
 
+// ---------------------------------------------------------------- LDS tile layouts
+// Column permutation of a row-major tile with WC elements per row staged in
+// LDS.  The 8-element chunks of a row are permuted by an XOR with the row's
+// index among the rows that share a 256-byte bank window (16 / (WC / 8) rows in
+// the bf16 build), so that a wave touches distinct banks both when it copies
+// whole rows (8 lanes per 128 bytes, the layout of coalesced global accesses)
+// and when it reads one chunk from each of 16 rows (matrix-core fragments).
+// Chunks stay contiguous and never leave their row; WC whose chunk count is not
+// a power of two up to 8 is left as is.
+template <int WC>
+__device__ __forceinline__ int tile_col(int row, int col) {
+  constexpr int CPR = WC / 8;
+  if constexpr (CPR == 8 || CPR == 4 || CPR == 2) {
+    constexpr int RPW = 16 / CPR;
+    return ((((col >> 3) ^ (row / RPW)) & (CPR - 1)) << 3) | (col & 7);
+  } else {
+    return col;
+  }
+}
+
+// Column permutation of a block-wide row-major tile (WIDE elements per row, a
+// multiple of 128): the 8-element chunk index is XORed with the row's low four
+// bits, which keeps rows written whole (64 lanes x 16 bytes, the layout of
+// 1 KiB-contiguous global loads) conflict-free and spreads one chunk read from
+// 16 rows (matrix-core fragments) over all banks.
+__device__ __forceinline__ int wide_col(int row, int col) {
+  return ((((col >> 3) ^ row) & 15) | ((col >> 3) & ~15)) << 3 | (col & 7);
+}
+
 // Activation function and its derivative (float32).
 __device__ __forceinline__ float act_phi(float a, int act) {
   return act == 1 ? a / (1.0f + expf(-a)) : a;

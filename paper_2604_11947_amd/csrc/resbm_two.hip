@@ -1,0 +1,628 @@
+// HIP kernels of the two-linears-per-side bottleneck for gfx950 and its C ABI.
+//
+// Paper: ResBM, Sec. 3.2 (encoder and decoder each two linear layers with a
+// non-linearity between them; encoder at the end of stage l, decoder at the
+// start of stage l+1, only b crosses the boundary), Eq. 2 and Eq. 5 (the
+// encoder's skip keeps columns [0, r) of the attention output).  With the
+// intermediate width m:
+//     encoder  u = z W1,  b = x_attn P^id + phi(u) W2
+//     decoder  v = b W3,  z~ = phi(v) W4
+// and the backward steps are the adjoints of these maps.
+//
+// Every step is one launch of a single matrix-core GEMM kernel, C = A B over
+// bf16 operands with float32 accumulation, whose two template switches say
+// which of A and B is stored K-contiguous.  The steps differ only in a prologue
+// (phi applied to the A operand while it is staged into LDS) and an epilogue
+// (bf16 or float32 store, multiplication by phi'(X) of a saved pre-activation,
+// addition of identity-path columns, or a split-K partial sum).  The n x m
+// products (2 T n m flops each) are matrix-core bound; the r-wide ones stream a
+// T x m tensor and are memory bound.
+//
+// A block computes a BM x BN tile of C in 64-deep stages: the stage's A and B
+// tiles go global -> registers -> LDS (double buffered, one barrier per stage,
+// the next stage's loads in flight during the current stage's products), then
+// every wave multiplies its (16 FM) x (16 FN) sub-tile with
+// v_mfma_f32_16x16x32_bf16.  The B operand takes the instruction's first slot,
+// so a lane's accumulator holds four consecutive columns of one output row and
+// stores them with one 8-byte (bf16) or 16-byte (float32) store.
+// K-contiguous operands are staged as [rows][64] and read as 16-byte chunks;
+// the others as [64][rows] and read transposed with ds_read_b64_tr_b16.
+// Split-K partial sums are added in split order by a second kernel, so every
+// result is reproducible bit for bit.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "resbm.h"
+#include "resbm_buffer.hpp"
+#include "resbm_mfma.hpp"
+
+namespace resbm2 {
+
+using resbm::bf16x4;
+using resbm::bf16x8;
+using resbm::bld16;
+using resbm::bld8;
+using resbm::bst16;
+using resbm::bst8;
+using resbm::f32x4;
+using resbm::kMaxRange;
+using resbm::kOOB;
+using resbm::make_rsrc;
+using resbm::rsrc_t;
+
+constexpr int KT = 64;  // K depth of one stage
+
+enum Epi : int {
+  kEpiBf16 = 0,   // C = rne(acc)
+  kEpiF32 = 1,    // C = acc (float32)
+  kEpiDphi = 2,   // C = rne(acc * phi'(X))   (X: saved pre-activation, same shape as C)
+  kEpiAdd = 3,    // C = rne(acc + X) on columns < x_cols, rne(acc) elsewhere
+  kEpiPart = 4,   // partial[split] = acc (float32, M x N contiguous per split)
+};
+
+struct GemmArgs {
+  int M, N, K;
+  const void* A; int64_t lda; int64_t a_bytes;
+  const void* B; int64_t ldb; int64_t b_bytes;
+  void* C; int64_t ldc; int64_t c_bytes;
+  const void* X; int64_t ldx; int64_t x_bytes; int x_cols;
+  int kc;  // K per split (a multiple of KT); gridDim.z splits
+};
+
+// SiLU on 8 bf16 values, each result rounded to bf16 (the operand the next
+// product consumes).
+__device__ __forceinline__ uint4 silu8(uint4 v) {
+  bf16x8 h = __builtin_bit_cast(bf16x8, v);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float a = (float)h[e];
+    h[e] = (__bf16)(a * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-a * 1.44269504088896341f)));
+  }
+  return __builtin_bit_cast(uint4, h);
+}
+
+// Position of element (row, col) in a staged tile.  K-contiguous operands are
+// staged [I][64] (row = index along M or N, col = k); the others [64][I]
+// (row = k, col = index), I = 32, 64 or a multiple of 128.
+template <bool KC, int I>
+__device__ __forceinline__ int tile_pos(int row, int col) {
+  if constexpr (KC) {
+    return row * KT + resbm::tile_col<KT>(row, col);
+  } else if constexpr (I % 128 == 0) {
+    return row * I + resbm::wide_col(row, col);
+  } else {
+    return row * I + resbm::tile_col<I>(row, col);
+  }
+}
+
+// Operand fragment for 16 indices starting at i0 and the 32-deep K step kk of
+// the staged tile: lane (row16, grp) receives Op[i0 + row16][32 kk + 8 grp + e].
+template <bool KC, int I>
+__device__ __forceinline__ bf16x8 frag(const __bf16* tile, int i0, int kk, int row16, int grp) {
+  if constexpr (KC) {
+    return __builtin_bit_cast(bf16x8,
+                              *reinterpret_cast<const uint4*>(tile + tile_pos<true, I>(i0 + row16, 32 * kk + 8 * grp)));
+  } else {
+    // Two ds_read_b64_tr_b16: within a 16-lane group, lane j addresses row
+    // 32 kk + 8 grp + 4 q + j / 4, columns i0 + 4 (j % 4) .. + 3, and lane i
+    // collects four consecutive rows of column i0 + i.
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    s16x4 h[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int row = 32 * kk + 8 * grp + 4 * q + (row16 >> 2);
+      const __bf16* p = tile + tile_pos<false, I>(row, i0 + 4 * (row16 & 3));
+      h[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+    }
+    return __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){h[0][0], h[0][1], h[0][2], h[0][3],
+                                                                                 h[1][0], h[1][1], h[1][2], h[1][3]});
+  }
+}
+
+// One operand of a GEMM stage: which 16-byte chunks a thread moves from global
+// memory into the staged tile.  NI = extent along M or N (for range checks).
+template <bool KC, int I, int NTH>
+struct Operand {
+  static constexpr int CHUNKS = I * KT / 8;
+  static constexpr int PER = CHUNKS / NTH;
+  static_assert(CHUNKS % NTH == 0, "tile chunks must divide over the block");
+  uint4 r[PER];
+
+  // Chunk c covers 8 elements: K-contiguous (row = c / 8 along I, k = 8 (c % 8));
+  // otherwise (row = c / (I / 8) along k, index = 8 (c % (I / 8))).
+  __device__ __forceinline__ void load(rsrc_t src, int64_t ld, int i0, int NI, int k0, int kend, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = tid + NTH * p;
+      int idx, k;
+      if constexpr (KC) {
+        idx = i0 + c / 8;
+        k = k0 + 8 * (c % 8);
+      } else {
+        k = k0 + c / (I / 8);
+        idx = i0 + 8 * (c % (I / 8));
+      }
+      const bool ok = idx < NI && k < kend;
+      const int64_t off = KC ? ((int64_t)idx * ld + k) * 2 : ((int64_t)k * ld + idx) * 2;
+      r[p] = bld16(src, ok ? (uint32_t)off : kOOB);
+    }
+  }
+  template <bool PHI>
+  __device__ __forceinline__ void put(__bf16* tile, int tid) const {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = tid + NTH * p;
+      const int row = KC ? c / 8 : c / (I / 8);
+      const int col = KC ? 8 * (c % 8) : 8 * (c % (I / 8));
+      *reinterpret_cast<uint4*>(tile + tile_pos<KC, I>(row, col)) = PHI ? silu8(r[p]) : r[p];
+    }
+  }
+};
+
+// Block index -> tile index.  Consecutive blocks are dispatched to the eight
+// XCDs in turn; each XCD is given a contiguous range of tiles, and tile indices
+// run along N first, so the tiles resident on one XCD share the rows of A (the
+// token stream in the T-row products) through its L2.
+__device__ __forceinline__ int xcd_tile(int id, int nb) {
+  const int x = id & 7, li = id >> 3;
+  return x * (nb >> 3) + min(x, nb & 7) + li;
+}
+
+template <bool AK, bool BKC, int BM, int BN, int WM, int WN, int EPI, bool PHI_A>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
+  constexpr int NTH = 64 * WM * WN;
+  constexpr int FM = BM / (16 * WM), FN = BN / (16 * WN);
+  static_assert(FM * 16 * WM == BM && FN * 16 * WN == BN, "wave tiling must cover the block tile");
+  __shared__ __attribute__((aligned(16))) __bf16 s_a[2][BM * KT];
+  __shared__ __attribute__((aligned(16))) __bf16 s_b[2][BN * KT];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int row16 = lane & 15, grp = lane >> 4;
+  const int wm = wave % WM, wn = wave / WM;
+  const int tiles_n = (g.N + BN - 1) / BN;
+  const int t = xcd_tile(blockIdx.x, gridDim.x);
+  const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
+  const int kbeg = blockIdx.z * g.kc, kend = min(g.K, kbeg + g.kc);
+  const int nst = (kend - kbeg + KT - 1) / KT;
+
+  const rsrc_t ra = make_rsrc(g.A, g.a_bytes), rb = make_rsrc(g.B, g.b_bytes);
+  Operand<AK, BM, NTH> opa;
+  Operand<BKC, BN, NTH> opb;
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (nst > 0) {
+    opa.load(ra, g.lda, m0, g.M, kbeg, kend, tid);
+    opb.load(rb, g.ldb, n0, g.N, kbeg, kend, tid);
+    opa.template put<PHI_A>(s_a[0], tid);
+    opb.template put<false>(s_b[0], tid);
+  }
+  __syncthreads();
+  for (int s = 0; s < nst; ++s) {
+    const bool more = s + 1 < nst;
+    if (more) {
+      opa.load(ra, g.lda, m0, g.M, kbeg + (s + 1) * KT, kend, tid);
+      opb.load(rb, g.ldb, n0, g.N, kbeg + (s + 1) * KT, kend, tid);
+    }
+    const __bf16* ta = s_a[s & 1];
+    const __bf16* tb = s_b[s & 1];
+#pragma unroll
+    for (int kk = 0; kk < KT / 32; ++kk) {
+      bf16x8 fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) fa[i] = frag<AK, BM>(ta, (wm * FM + i) * 16, kk, row16, grp);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) fb[j] = frag<BKC, BN>(tb, (wn * FN + j) * 16, kk, row16, grp);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+    }
+    if (more) {
+      opa.template put<PHI_A>(s_a[(s + 1) & 1], tid);
+      opb.template put<false>(s_b[(s + 1) & 1], tid);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue: lane (row16, grp) of tile (i, j) holds C[m][n .. n + 3].
+  const rsrc_t rc = make_rsrc(g.C, g.c_bytes);
+  const rsrc_t rx = make_rsrc(g.X, g.x_bytes);
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int m = m0 + (wm * FM + i) * 16 + row16;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + (wn * FN + j) * 16 + 4 * grp;
+      const bool ok = m < g.M && n < g.N;
+      f32x4 v = acc[i][j];
+      if constexpr (EPI == kEpiF32 || EPI == kEpiPart) {
+        const int64_t off = EPI == kEpiPart ? (((int64_t)blockIdx.z * g.M + m) * g.N + n) * 4
+                                            : ((int64_t)m * g.ldc + n) * 4;
+        bst16(rc, ok ? (uint32_t)off : kOOB, __builtin_bit_cast(uint4, v));
+      } else {
+        if constexpr (EPI == kEpiDphi || EPI == kEpiAdd) {
+          const bool xok = ok && (EPI == kEpiDphi || n < g.x_cols);
+          const uint2 xr = bld8(rx, xok ? (uint32_t)(((int64_t)m * g.ldx + n) * 2) : kOOB);
+          const bf16x4 x = __builtin_bit_cast(bf16x4, xr);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if constexpr (EPI == kEpiDphi) v[e] *= resbm::silu_grad((float)x[e]);
+            else v[e] += (float)x[e];
+          }
+        }
+        bf16x4 h;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) h[e] = (__bf16)v[e];
+        bst8(rc, ok ? (uint32_t)(((int64_t)m * g.ldc + n) * 2) : kOOB, __builtin_bit_cast(uint2, h));
+      }
+    }
+  }
+}
+
+// out[i] = sum over s in order of part[s][i], i < count (count % 4 == 0).
+__global__ __launch_bounds__(256) void k_splitk_sum(const float* __restrict__ part, int S, int64_t count,
+                                                    float* __restrict__ out) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q * 4 >= count) return;
+  const float4* p = reinterpret_cast<const float4*>(part) + q;
+  float4 a = p[0];
+  for (int s = 1; s < S; ++s) {
+    const float4 b = p[(int64_t)s * (count / 4)];
+    a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+  }
+  reinterpret_cast<float4*>(out)[q] = a;
+}
+
+// g_x[t][0 .. r) <- rne(g_x + g_b), 4 columns per thread (r % 8 == 0).
+__global__ __launch_bounds__(256) void k_skip_grad(int64_t T, int r, const __bf16* __restrict__ g_b,
+                                                   __bf16* __restrict__ g_x, int64_t ld_gx) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int per = r / 4;
+  if (q >= T * per) return;
+  const int64_t t = q / per;
+  const int c = (int)(q % per) * 4;
+  const bf16x4 b = __builtin_bit_cast(bf16x4, *reinterpret_cast<const uint2*>(g_b + t * r + c));
+  uint2* px = reinterpret_cast<uint2*>(g_x + t * ld_gx + c);
+  bf16x4 x = __builtin_bit_cast(bf16x4, *px);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] = (__bf16)((float)x[e] + (float)b[e]);
+  *px = __builtin_bit_cast(uint2, x);
+}
+
+}  // namespace resbm2
+
+// ============================================================ host side
+using namespace resbm2;
+
+namespace {
+
+constexpr size_t kWsAlign2 = 256;
+constexpr int kTargetBlocks = 256;   // split-K aims at one block per compute unit
+
+bool aligned2(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+size_t extent2(int64_t rows, int64_t cols, int64_t ld, size_t es) {
+  return rows > 0 ? (size_t)(((rows - 1) * ld + cols) * (int64_t)es) : 0;
+}
+bool overlap2(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+  return pa < pb + nb && pb < pa + na;
+}
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+bool shape_ok2(int64_t T, int n, int m, int r) {
+  return T >= 0 && T <= (1ll << 31) && n >= 8 && n <= 65536 && n % 8 == 0 && m >= 8 && m <= 65536 && m % 8 == 0 &&
+         r >= 8 && r <= n && r % 8 == 0;
+}
+bool ld_ok2(int64_t ld, int n) { return ld >= n && ld % 8 == 0; }
+bool fits(size_t bytes) { return bytes <= (size_t)kMaxRange; }
+
+// Block tile shapes: the wide one for products with an n- or m-wide output,
+// a narrow one for an r-wide output (N = r).  Products with M = r use the wide
+// one; the rows beyond r read nothing.
+enum Shape { kWide = 0, kNarrow32 = 1, kNarrow64 = 2, kNarrow128 = 3 };
+
+Shape narrow_for(int N) { return N <= 32 ? kNarrow32 : (N <= 64 ? kNarrow64 : kNarrow128); }
+int shape_bm(Shape s) { return s == kWide ? 128 : 64; }
+int shape_bn(Shape s) { return s == kWide ? 128 : (s == kNarrow32 ? 32 : (s == kNarrow64 ? 64 : 128)); }
+
+struct Split {
+  int S;
+  int kc;
+};
+// Splits of a token-deep (K = T) product: enough blocks to fill the chip, each
+// split at least 4 stages deep.
+Split split_for(int M, int N, int K, Shape s) {
+  const int64_t tiles = (int64_t)((M + shape_bm(s) - 1) / shape_bm(s)) * ((N + shape_bn(s) - 1) / shape_bn(s));
+  int64_t S = (kTargetBlocks + tiles - 1) / tiles;
+  const int64_t maxS = std::max<int64_t>(1, K / (4 * KT));
+  S = std::min(S, maxS);
+  const int64_t per = (K + S - 1) / S;
+  const int kc = (int)round_up((size_t)per, KT);
+  return {(int)((K + kc - 1) / kc), kc};
+}
+size_t part_bytes(int M, int N, const Split& sp) {
+  return sp.S > 1 ? round_up((size_t)sp.S * M * N * 4, kWsAlign2) : 0;
+}
+
+struct Plan2 {
+  Split dW4, dW3, dW2, dW1;
+  size_t inter;      // T x m bf16 intermediate (g_v or g_u)
+  size_t dec_bwd, enc_bwd;
+};
+Plan2 make_plan2(int64_t T, int n, int m, int r) {
+  Plan2 p;
+  p.dW4 = split_for(m, n, (int)T, kWide);
+  p.dW3 = split_for(r, m, (int)T, kWide);
+  p.dW2 = split_for(m, r, (int)T, narrow_for(r));
+  p.dW1 = split_for(n, m, (int)T, kWide);
+  p.inter = round_up((size_t)T * m * 2, kWsAlign2);
+  p.dec_bwd = p.inter + std::max(part_bytes(m, n, p.dW4), part_bytes(r, m, p.dW3));
+  p.enc_bwd = p.inter + std::max(part_bytes(m, r, p.dW2), part_bytes(n, m, p.dW1));
+  return p;
+}
+
+template <bool AK, bool BKC, int BM, int BN, int WM, int WN, int EPI, bool PHI>
+void launch(const GemmArgs& g, int S, hipStream_t st) {
+  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  hipLaunchKernelGGL((k_gemm<AK, BKC, BM, BN, WM, WN, EPI, PHI>), dim3(tiles, 1, S), dim3(64 * WM * WN), 0, st, g);
+}
+
+// Runs C = op(A) op(B) with the epilogue EPI and tile shape s.
+template <bool AK, bool BKC, int EPI, bool PHI>
+void gemm(Shape s, const GemmArgs& g, int S, hipStream_t st) {
+  switch (s) {
+    case kWide: launch<AK, BKC, 128, 128, 2, 2, EPI, PHI>(g, S, st); break;
+    case kNarrow32: launch<AK, BKC, 64, 32, 4, 1, EPI, PHI>(g, S, st); break;
+    case kNarrow64: launch<AK, BKC, 64, 64, 4, 1, EPI, PHI>(g, S, st); break;
+    case kNarrow128: launch<AK, BKC, 64, 128, 4, 1, EPI, PHI>(g, S, st); break;
+  }
+}
+
+GemmArgs args(int M, int N, int K, const void* A, int64_t lda, size_t ab, const void* B, int64_t ldb, size_t bb,
+              void* C, int64_t ldc, size_t cb) {
+  GemmArgs g{};
+  g.M = M; g.N = N; g.K = K;
+  g.A = A; g.lda = lda; g.a_bytes = (int64_t)ab;
+  g.B = B; g.ldb = ldb; g.b_bytes = (int64_t)bb;
+  g.C = C; g.ldc = ldc; g.c_bytes = (int64_t)cb;
+  g.kc = (int)round_up((size_t)K, KT);
+  return g;
+}
+
+// A token-deep weight-gradient product (K = T): float32 result W (M x N,
+// contiguous), split over tokens with the partial sums in `part` when that
+// fills the chip better.
+template <bool PHI>
+void weight_grad(Shape s, GemmArgs g, const Split& sp, float* W, void* part, hipStream_t st) {
+  if (sp.S == 1) {
+    g.C = W; g.ldc = g.N; g.c_bytes = (int64_t)g.M * g.N * 4;
+    gemm<false, false, kEpiF32, PHI>(s, g, 1, st);
+    return;
+  }
+  g.C = part; g.c_bytes = (int64_t)sp.S * g.M * g.N * 4; g.kc = sp.kc;
+  gemm<false, false, kEpiPart, PHI>(s, g, sp.S, st);
+  const int64_t count = (int64_t)g.M * g.N;
+  hipLaunchKernelGGL(k_splitk_sum, dim3((unsigned)((count / 4 + 255) / 256)), dim3(256), 0, st, (const float*)part,
+                     sp.S, count, W);
+}
+
+int32_t status2() { return hipGetLastError() == hipSuccess ? RESBM_OK : RESBM_E_HIP; }
+
+int32_t check_ws(size_t need, const void* ws, size_t ws_bytes) {
+  if (need == 0) return RESBM_OK;
+  if (!ws) return RESBM_E_NULL;
+  if (!aligned2(ws, kWsAlign2)) return RESBM_E_ALIGN;
+  return ws_bytes < need ? RESBM_E_WORKSPACE : RESBM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t resbm2_workspace_bytes(int64_t T, int32_t n, int32_t m, int32_t r) {
+  if (!shape_ok2(T, n, m, r) || T == 0) return 0;
+  const Plan2 p = make_plan2(T, n, m, r);
+  return std::max(p.dec_bwd, p.enc_bwd);
+}
+
+int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* x_attn, int64_t ld_x,
+                          const void* z, int64_t ld_z, const void* W1, const void* W2, void* b, void* u, void* ws,
+                          size_t ws_bytes, void* stream) {
+  (void)ws; (void)ws_bytes;
+  if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
+  if (!shape_ok2(T, n, m, r)) return RESBM_E_SHAPE;
+  if (T == 0) return RESBM_OK;
+  if (!x_attn || !z || !W1 || !W2 || !b || !u) return RESBM_E_NULL;
+  if (!ld_ok2(ld_x, n) || !ld_ok2(ld_z, n)) return RESBM_E_SHAPE;
+  if (!aligned2(x_attn, 16) || !aligned2(z, 16) || !aligned2(W1, 16) || !aligned2(W2, 16) || !aligned2(b, 16) ||
+      !aligned2(u, 16))
+    return RESBM_E_ALIGN;
+  const size_t bx = extent2(T, n, ld_x, 2), bz = extent2(T, n, ld_z, 2), bw1 = (size_t)n * m * 2,
+               bw2 = (size_t)m * r * 2, bb = (size_t)T * r * 2, bu = (size_t)T * m * 2;
+  if (!fits(bx) || !fits(bz) || !fits(bu) || !fits(bw1)) return RESBM_E_SHAPE;
+  if (overlap2(b, bb, x_attn, bx) || overlap2(b, bb, z, bz) || overlap2(b, bb, W1, bw1) || overlap2(b, bb, W2, bw2) ||
+      overlap2(u, bu, x_attn, bx) || overlap2(u, bu, z, bz) || overlap2(u, bu, W1, bw1) || overlap2(u, bu, W2, bw2) ||
+      overlap2(u, bu, b, bb))
+    return RESBM_E_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  const int Ti = (int)T;
+  // u = z W1  (A = z, K-contiguous; B = W1 [n][m], m-contiguous)
+  GemmArgs g = args(Ti, m, n, z, ld_z, bz, W1, m, bw1, u, m, bu);
+  gemm<true, false, kEpiBf16, false>(kWide, g, 1, st);
+  // b = x_attn[:, :r] + phi(u) W2
+  g = args(Ti, r, m, u, m, bu, W2, r, bw2, b, r, bb);
+  g.X = x_attn; g.ldx = ld_x; g.x_bytes = (int64_t)bx; g.x_cols = r;
+  if (act == RESBM_ACT_SILU) gemm<true, false, kEpiAdd, true>(narrow_for(r), g, 1, st);
+  else gemm<true, false, kEpiAdd, false>(narrow_for(r), g, 1, st);
+  return status2();
+}
+
+int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* b, const void* W3,
+                          const void* W4, void* z_tilde, int64_t ld_zt, void* v, void* ws, size_t ws_bytes,
+                          void* stream) {
+  (void)ws; (void)ws_bytes;
+  if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
+  if (!shape_ok2(T, n, m, r)) return RESBM_E_SHAPE;
+  if (T == 0) return RESBM_OK;
+  if (!b || !W3 || !W4 || !z_tilde || !v) return RESBM_E_NULL;
+  if (!ld_ok2(ld_zt, n)) return RESBM_E_SHAPE;
+  if (!aligned2(b, 16) || !aligned2(W3, 16) || !aligned2(W4, 16) || !aligned2(z_tilde, 16) || !aligned2(v, 16))
+    return RESBM_E_ALIGN;
+  const size_t bb = (size_t)T * r * 2, bw3 = (size_t)r * m * 2, bw4 = (size_t)m * n * 2,
+               bzt = extent2(T, n, ld_zt, 2), bv = (size_t)T * m * 2;
+  if (!fits(bzt) || !fits(bv) || !fits(bw4)) return RESBM_E_SHAPE;
+  if (overlap2(z_tilde, bzt, b, bb) || overlap2(z_tilde, bzt, W3, bw3) || overlap2(z_tilde, bzt, W4, bw4) ||
+      overlap2(v, bv, b, bb) || overlap2(v, bv, W3, bw3) || overlap2(v, bv, W4, bw4) || overlap2(v, bv, z_tilde, bzt))
+    return RESBM_E_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  const int Ti = (int)T;
+  // v = b W3
+  GemmArgs g = args(Ti, m, r, b, r, bb, W3, m, bw3, v, m, bv);
+  gemm<true, false, kEpiBf16, false>(kWide, g, 1, st);
+  // z~ = phi(v) W4
+  g = args(Ti, n, m, v, m, bv, W4, n, bw4, z_tilde, ld_zt, bzt);
+  if (act == RESBM_ACT_SILU) gemm<true, false, kEpiBf16, true>(kWide, g, 1, st);
+  else gemm<true, false, kEpiBf16, false>(kWide, g, 1, st);
+  return status2();
+}
+
+int32_t resbm2_decode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* b, const void* v,
+                          const void* g_zt, int64_t ld_gzt, const void* g_id, int64_t ld_gid, const void* W3,
+                          const void* W4, void* g_b, float* dW3, float* dW4, void* ws, size_t ws_bytes,
+                          void* stream) {
+  if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
+  if (!shape_ok2(T, n, m, r)) return RESBM_E_SHAPE;
+  if (T == 0) return RESBM_OK;
+  const Plan2 p = make_plan2(T, n, m, r);
+  int32_t e = check_ws(p.dec_bwd, ws, ws_bytes);
+  if (e) return e;
+  if (!b || !v || !g_zt || !W3 || !W4 || !g_b || !dW3 || !dW4) return RESBM_E_NULL;
+  if (!ld_ok2(ld_gzt, n) || (g_id && !ld_ok2(ld_gid, n))) return RESBM_E_SHAPE;
+  if (!aligned2(b, 16) || !aligned2(v, 16) || !aligned2(g_zt, 16) || (g_id && !aligned2(g_id, 16)) ||
+      !aligned2(W3, 16) || !aligned2(W4, 16) || !aligned2(g_b, 16) || !aligned2(dW3, 16) || !aligned2(dW4, 16))
+    return RESBM_E_ALIGN;
+  const size_t bb = (size_t)T * r * 2, bv = (size_t)T * m * 2, bg = extent2(T, n, ld_gzt, 2),
+               bid = g_id ? extent2(T, n, ld_gid, 2) : 0, bw3 = (size_t)r * m * 2, bw4 = (size_t)m * n * 2,
+               bd3 = (size_t)r * m * 4, bd4 = (size_t)m * n * 4;
+  if (!fits(bg) || !fits(bid) || !fits(bv) || !fits(bw4) || !fits(p.dec_bwd)) return RESBM_E_SHAPE;
+  const void* ins[] = {b, v, g_zt, g_id, W3, W4};
+  const size_t inb[] = {bb, bv, bg, bid, bw3, bw4};
+  void* outs[] = {g_b, dW3, dW4, ws};
+  const size_t outb[] = {bb, bd3, bd4, p.dec_bwd};
+  for (int o = 0; o < 4; ++o) {
+    for (int i = 0; i < 6; ++i)
+      if (overlap2(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
+    for (int o2 = o + 1; o2 < 4; ++o2)
+      if (overlap2(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  const int Ti = (int)T;
+  char* w = (char*)ws;
+  void* g_v = w;
+  void* part = w + p.inter;
+  const bool silu = act == RESBM_ACT_SILU;
+  // g_v = (g_zt W4^T) * phi'(v)   (B(k, j) = W4[j][k]: K-contiguous)
+  GemmArgs g = args(Ti, m, n, g_zt, ld_gzt, bg, W4, n, bw4, g_v, m, bv);
+  if (silu) {
+    g.X = v; g.ldx = m; g.x_bytes = (int64_t)bv;
+    gemm<true, true, kEpiDphi, false>(kWide, g, 1, st);
+  } else {
+    gemm<true, true, kEpiBf16, false>(kWide, g, 1, st);
+  }
+  // dW4 = phi(v)^T g_zt   (A(i, k) = v[k][i], B(k, j) = g_zt[k][j])
+  g = args(m, n, Ti, v, m, bv, g_zt, ld_gzt, bg, nullptr, 0, 0);
+  if (silu) weight_grad<true>(kWide, g, p.dW4, dW4, part, st);
+  else weight_grad<false>(kWide, g, p.dW4, dW4, part, st);
+  // dW3 = b^T g_v
+  g = args(r, m, Ti, b, r, bb, g_v, m, bv, nullptr, 0, 0);
+  weight_grad<false>(kWide, g, p.dW3, dW3, part, st);
+  // g_b = g_v W3^T + g_id[:, :r]
+  g = args(Ti, r, m, g_v, m, bv, W3, m, bw3, g_b, r, bb);
+  if (g_id) {
+    g.X = g_id; g.ldx = ld_gid; g.x_bytes = (int64_t)bid; g.x_cols = r;
+    gemm<true, true, kEpiAdd, false>(narrow_for(r), g, 1, st);
+  } else {
+    gemm<true, true, kEpiBf16, false>(narrow_for(r), g, 1, st);
+  }
+  return status2();
+}
+
+int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* z, int64_t ld_z,
+                          const void* u, const void* g_b, const void* W1, const void* W2, void* g_z, int64_t ld_gz,
+                          void* g_x, int64_t ld_gx, float* dW1, float* dW2, void* ws, size_t ws_bytes,
+                          void* stream) {
+  if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
+  if (!shape_ok2(T, n, m, r)) return RESBM_E_SHAPE;
+  if (T == 0) return RESBM_OK;
+  const Plan2 p = make_plan2(T, n, m, r);
+  int32_t e = check_ws(p.enc_bwd, ws, ws_bytes);
+  if (e) return e;
+  if (!z || !u || !g_b || !W1 || !W2 || !g_z || !dW1 || !dW2) return RESBM_E_NULL;
+  if (!ld_ok2(ld_z, n) || !ld_ok2(ld_gz, n) || (g_x && !ld_ok2(ld_gx, n))) return RESBM_E_SHAPE;
+  if (!aligned2(z, 16) || !aligned2(u, 16) || !aligned2(g_b, 16) || !aligned2(W1, 16) || !aligned2(W2, 16) ||
+      !aligned2(g_z, 16) || (g_x && !aligned2(g_x, 16)) || !aligned2(dW1, 16) || !aligned2(dW2, 16))
+    return RESBM_E_ALIGN;
+  const bool fused = g_x == g_z;
+  if (fused && ld_gx != ld_gz) return RESBM_E_ALIAS;
+  const size_t bz = extent2(T, n, ld_z, 2), bu = (size_t)T * m * 2, bgb = (size_t)T * r * 2,
+               bw1 = (size_t)n * m * 2, bw2 = (size_t)m * r * 2, bgz = extent2(T, n, ld_gz, 2),
+               bgx = (g_x && !fused) ? extent2(T, n, ld_gx, 2) : 0, bd1 = (size_t)n * m * 4,
+               bd2 = (size_t)m * r * 4;
+  if (!fits(bz) || !fits(bu) || !fits(bgz) || !fits(bgx) || !fits(bw1) || !fits(p.enc_bwd)) return RESBM_E_SHAPE;
+  const void* ins[] = {z, u, g_b, W1, W2};
+  const size_t inb[] = {bz, bu, bgb, bw1, bw2};
+  void* outs[] = {g_z, fused ? nullptr : g_x, dW1, dW2, ws};
+  const size_t outb[] = {bgz, bgx, bd1, bd2, p.enc_bwd};
+  for (int o = 0; o < 5; ++o) {
+    for (int i = 0; i < 5; ++i)
+      if (overlap2(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
+    for (int o2 = o + 1; o2 < 5; ++o2)
+      if (overlap2(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  const int Ti = (int)T;
+  char* w = (char*)ws;
+  void* g_u = w;
+  void* part = w + p.inter;
+  const bool silu = act == RESBM_ACT_SILU;
+  // g_u = (g_b W2^T) * phi'(u)   (B(k, j) = W2[j][k]: K-contiguous)
+  GemmArgs g = args(Ti, m, r, g_b, r, bgb, W2, r, bw2, g_u, m, bu);
+  if (silu) {
+    g.X = u; g.ldx = m; g.x_bytes = (int64_t)bu;
+    gemm<true, true, kEpiDphi, false>(kWide, g, 1, st);
+  } else {
+    gemm<true, true, kEpiBf16, false>(kWide, g, 1, st);
+  }
+  // dW2 = phi(u)^T g_b
+  g = args(m, r, Ti, u, m, bu, g_b, r, bgb, nullptr, 0, 0);
+  if (silu) weight_grad<true>(narrow_for(r), g, p.dW2, dW2, part, st);
+  else weight_grad<false>(narrow_for(r), g, p.dW2, dW2, part, st);
+  // dW1 = z^T g_u
+  g = args(n, m, Ti, z, ld_z, bz, g_u, m, bu, nullptr, 0, 0);
+  weight_grad<false>(kWide, g, p.dW1, dW1, part, st);
+  // g_z = g_u W1^T (+ g_b on columns [0, r) when g_x is g_z)   (B(k, j) = W1[j][k])
+  g = args(Ti, n, m, g_u, m, bu, W1, m, bw1, g_z, ld_gz, bgz);
+  if (fused) {
+    g.X = g_b; g.ldx = r; g.x_bytes = (int64_t)bgb; g.x_cols = r;
+    gemm<true, true, kEpiAdd, false>(kWide, g, 1, st);
+  } else {
+    gemm<true, true, kEpiBf16, false>(kWide, g, 1, st);
+    if (g_x) {
+      const int64_t cnt = T * (r / 4);
+      hipLaunchKernelGGL(k_skip_grad, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, T, r,
+                         (const __bf16*)g_b, (__bf16*)g_x, ld_gx);
+    }
+  }
+  return status2();
+}
+
+}  // extern "C"

@@ -234,3 +234,28 @@ def make_matrix(p: int, q: int, kind: str = "gaussian", seed: int = 0, scale: fl
     else:
         raise ValueError(f"unknown matrix kind {kind!r}")
     return torch.from_numpy(np.ascontiguousarray(m).astype(np.float32))
+
+
+# ---------------------------------------------------------------- two-linears-per-side variant
+def make_two_weights(n: int, m: int, r: int, seed: int = 0) -> dict[str, torch.Tensor]:
+    """bf16 weights of the two-linears-per-side bottleneck: W1 [n][m] ~ N(0, 1/n),
+    W2 [m][r] ~ N(0, 1/m), W3 [r][m] ~ N(0, 1/r), W4 [m][n] ~ N(0, 1/m)."""
+    ss = np.random.SeedSequence([seed, n, m, r, 2]).spawn(4)
+    g = [np.random.Generator(np.random.PCG64(s)) for s in ss]
+    return {
+        "W1": _to_bf16(g[0].standard_normal((n, m)) / np.sqrt(n)),
+        "W2": _to_bf16(g[1].standard_normal((m, r)) / np.sqrt(m)),
+        "W3": _to_bf16(g[2].standard_normal((r, m)) / np.sqrt(r)),
+        "W4": _to_bf16(g[3].standard_normal((m, n)) / np.sqrt(m)),
+    }
+
+
+def make_bf16(rows: int, cols: int, seed: int, std: float = 1.0) -> torch.Tensor:
+    """rows x cols bf16 N(0, std^2) from its own seed (payloads, saved
+    pre-activations, wire gradients of the two-linears-per-side ops)."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, rows, cols, 3])))
+    out = torch.empty((rows, cols), dtype=torch.bfloat16)
+    for r0 in range(0, rows, _CHUNK_ROWS):
+        r1 = min(rows, r0 + _CHUNK_ROWS)
+        out[r0:r1].copy_(_to_bf16(std * rng.standard_normal((r1 - r0, cols))))
+    return out

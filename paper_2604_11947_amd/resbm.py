@@ -45,6 +45,13 @@ SIGNATURES = [
     ("resbm_spectrum", _i32, [_i32, _i32, _p, _p, _p, _p, _sz, _p]),
     ("resbm_matrix_workspace_bytes", _sz, [_i32, _i32]),
     ("resbm_workspace_bytes", _sz, [_i64, _i32, _i32]),
+    ("resbm2_encode_fwd", _i32, [_i64, _i32, _i32, _i32, _i32, _p, _i64, _p, _i64, _p, _p, _p, _p, _p, _sz, _p]),
+    ("resbm2_decode_fwd", _i32, [_i64, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _i64, _p, _p, _sz, _p]),
+    ("resbm2_decode_bwd", _i32, [_i64, _i32, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _i64, _p, _p, _p, _p, _p,
+                                 _p, _sz, _p]),
+    ("resbm2_encode_bwd", _i32, [_i64, _i32, _i32, _i32, _i32, _p, _i64, _p, _p, _p, _p, _p, _i64, _p, _i64,
+                                 _p, _p, _p, _sz, _p]),
+    ("resbm2_workspace_bytes", _sz, [_i64, _i32, _i32, _i32]),
     ("resbm_io_dtype", _i32, []),
     ("resbm_strerror", ctypes.c_char_p, [_i32]),
 ]
@@ -210,6 +217,101 @@ class Library:
                                         ws.numel(), _stream(stream, z))
         self._check("resbm_encode_bwd", st)
 
+
+    # ------------------------------------------------------------ two-linears-per-side ops
+    # Weights W1 (n x m), W2 (m x r), W3 (r x m), W4 (m x n) and every activation
+    # are bf16; the weight gradients float32.
+    def two_workspace_bytes(self, T: int, n: int, m: int, r: int) -> int:
+        return int(self.cdll.resbm2_workspace_bytes(T, n, m, r))
+
+    def two_workspace(self, T: int, n: int, m: int, r: int, device) -> torch.Tensor:
+        nbytes = self.two_workspace_bytes(T, n, m, r)
+        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        off = (-buf.data_ptr()) % 256
+        return buf[off:off + nbytes]
+
+    @staticmethod
+    def _two_weights(W1, W2, W3=None, W4=None):
+        n, m = W1.shape
+        r = W2.shape[1]
+        for t, nm, shape in ((W1, "W1", (n, m)), (W2, "W2", (m, r)), (W3, "W3", (r, m)), (W4, "W4", (m, n))):
+            if t is not None:
+                _dtype(t, torch.bfloat16, nm)
+                _packed(t, *shape, nm)
+        return n, m, r
+
+    def encode2_fwd(self, x_attn, z, W1, W2, b, u, act=ACT_SILU, stream=None):
+        T = z.shape[0]
+        n, m, r = self._two_weights(W1, W2)
+        for t, nm in ((x_attn, "x_attn"), (z, "z"), (b, "b"), (u, "u")):
+            _dtype(t, torch.bfloat16, nm)
+        ld_x, ld_z = _ld(x_attn, T, n, "x_attn"), _ld(z, T, n, "z")
+        _packed(b, T, r, "b")
+        _packed(u, T, m, "u")
+        st = self.cdll.resbm2_encode_fwd(T, n, m, r, act, _ptr(x_attn), ld_x, _ptr(z), ld_z, _ptr(W1), _ptr(W2),
+                                         _ptr(b), _ptr(u), None, 0, _stream(stream, z))
+        self._check("resbm2_encode_fwd", st)
+
+    def decode2_fwd(self, b, W3, W4, z_tilde, v, act=ACT_SILU, stream=None):
+        T = b.shape[0]
+        m, n = W4.shape
+        r = W3.shape[0]
+        for t, nm, shape in ((W3, "W3", (r, m)), (W4, "W4", (m, n))):
+            _dtype(t, torch.bfloat16, nm)
+            _packed(t, *shape, nm)
+        for t, nm in ((b, "b"), (z_tilde, "z_tilde"), (v, "v")):
+            _dtype(t, torch.bfloat16, nm)
+        _packed(b, T, r, "b")
+        _packed(v, T, m, "v")
+        ld_zt = _ld(z_tilde, T, n, "z_tilde")
+        st = self.cdll.resbm2_decode_fwd(T, n, m, r, act, _ptr(b), _ptr(W3), _ptr(W4), _ptr(z_tilde), ld_zt, _ptr(v),
+                                         None, 0, _stream(stream, b))
+        self._check("resbm2_decode_fwd", st)
+
+    def decode2_bwd(self, b, v, g_zt, g_id, W3, W4, g_b, dW3, dW4, act=ACT_SILU, ws=None, stream=None):
+        T = b.shape[0]
+        m, n = W4.shape
+        r = W3.shape[0]
+        for t, nm, shape in ((W3, "W3", (r, m)), (W4, "W4", (m, n))):
+            _dtype(t, torch.bfloat16, nm)
+            _packed(t, *shape, nm)
+        for t, nm in ((b, "b"), (v, "v"), (g_zt, "g_zt"), (g_id, "g_id"), (g_b, "g_b")):
+            _dtype(t, torch.bfloat16, nm)
+        _dtype(dW3, torch.float32, "dW3")
+        _dtype(dW4, torch.float32, "dW4")
+        _packed(b, T, r, "b")
+        _packed(v, T, m, "v")
+        _packed(g_b, T, r, "g_b")
+        _packed(dW3, r, m, "dW3")
+        _packed(dW4, m, n, "dW4")
+        ld_gzt = _ld(g_zt, T, n, "g_zt")
+        ld_gid = _ld(g_id, T, n, "g_id") if g_id is not None else 0
+        if ws is None:
+            ws = self.two_workspace(T, n, m, r, b.device)
+        st = self.cdll.resbm2_decode_bwd(T, n, m, r, act, _ptr(b), _ptr(v), _ptr(g_zt), ld_gzt, _ptr(g_id), ld_gid,
+                                         _ptr(W3), _ptr(W4), _ptr(g_b), _ptr(dW3), _ptr(dW4), _ptr(ws), ws.numel(),
+                                         _stream(stream, b))
+        self._check("resbm2_decode_bwd", st)
+
+    def encode2_bwd(self, z, u, g_b, W1, W2, g_z, dW1, dW2, g_x=None, act=ACT_SILU, ws=None, stream=None):
+        T = z.shape[0]
+        n, m, r = self._two_weights(W1, W2)
+        for t, nm in ((z, "z"), (u, "u"), (g_b, "g_b"), (g_z, "g_z"), (g_x, "g_x")):
+            _dtype(t, torch.bfloat16, nm)
+        _dtype(dW1, torch.float32, "dW1")
+        _dtype(dW2, torch.float32, "dW2")
+        _packed(u, T, m, "u")
+        _packed(g_b, T, r, "g_b")
+        _packed(dW1, n, m, "dW1")
+        _packed(dW2, m, r, "dW2")
+        ld_z, ld_gz = _ld(z, T, n, "z"), _ld(g_z, T, n, "g_z")
+        ld_gx = _ld(g_x, T, n, "g_x") if g_x is not None else 0
+        if ws is None:
+            ws = self.two_workspace(T, n, m, r, z.device)
+        st = self.cdll.resbm2_encode_bwd(T, n, m, r, act, _ptr(z), ld_z, _ptr(u), _ptr(g_b), _ptr(W1), _ptr(W2),
+                                         _ptr(g_z), ld_gz, _ptr(g_x), ld_gx, _ptr(dW1), _ptr(dW2), _ptr(ws),
+                                         ws.numel(), _stream(stream, z))
+        self._check("resbm2_encode_bwd", st)
 
     # ------------------------------------------------------------ optimizer-side ops
     def newton_schulz(self, G, O, steps=5, coeffs=NS_QUINTIC, ws=None, stream=None):

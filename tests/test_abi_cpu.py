@@ -29,21 +29,22 @@ def lib(request):
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(resbm_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(resbm2?_\w+)\s*\(", text)))
 
 
 def test_header_declares_the_ops_and_helpers():
     names = declared_functions()
     for op in ("resbm_encode_fwd", "resbm_decode_fwd", "resbm_decode_bwd", "resbm_encode_bwd",
                "resbm_newton_schulz", "resbm_muon_update", "resbm_spectrum", "resbm_matrix_workspace_bytes",
-               "resbm_workspace_bytes", "resbm_io_dtype", "resbm_strerror"):
+               "resbm_workspace_bytes", "resbm_io_dtype", "resbm_strerror", "resbm2_encode_fwd", "resbm2_decode_fwd",
+               "resbm2_decode_bwd", "resbm2_encode_bwd", "resbm2_workspace_bytes"):
         assert op in names
     assert sorted(n for n, _, _ in R.SIGNATURES) == names
 
 
 def test_every_declared_symbol_is_exported(lib):
     out = subprocess.run(["nm", "-D", "--defined-only", lib.path], capture_output=True, text=True, check=True).stdout
-    exported = set(re.findall(r"\bT (resbm_\w+)$", out, flags=re.M))
+    exported = set(re.findall(r"\bT (resbm2?_\w+)$", out, flags=re.M))
     for name in declared_functions():
         assert name in exported, name
         assert getattr(lib.cdll, name)
@@ -282,3 +283,81 @@ def test_spectrum_validation(lib):
     assert call(3, 2 * A + 4) == R.E_ALIGN
     assert call(4, 2 * A + 8) == R.E_ALIAS     # r_eff inside sigma
     assert call(6, 1024) == R.E_WORKSPACE
+
+
+# ---------------------------------------------------------------- two-linears-per-side ops
+M2 = 128
+
+
+def test_two_workspace_bytes(lib):
+    c = lib.cdll
+    assert c.resbm2_workspace_bytes(0, N, M2, RR) == 0
+    assert c.resbm2_workspace_bytes(T, N, M2, 12) == 0          # r % 8
+    assert c.resbm2_workspace_bytes(T, N, 100, RR) == 0         # m % 8
+    assert c.resbm2_workspace_bytes(T, 64, M2, 72) == 0         # r > n
+    w = c.resbm2_workspace_bytes(T, N, M2, RR)
+    assert w >= T * M2 * 2 and w % 256 == 0
+
+
+@needs_no_gpu
+def test_two_encode_fwd_validation(lib):
+    c = lib.cdll
+    ok = [T, N, M2, RR, 1, A, N, 2 * A, N, 3 * A, 4 * A, 5 * A, 6 * A, None, 0, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm2_encode_fwd(*a)
+
+    assert call(4, 7) == R.E_ACT
+    assert call(3, 12) == R.E_SHAPE
+    assert call(2, 4) == R.E_SHAPE
+    assert call(6, N - 8) == R.E_SHAPE
+    assert call(0, 0) == R.OK                 # T = 0: nothing read
+    for i in (5, 7, 9, 10, 11, 12):
+        assert call(i, None) == R.E_NULL, i
+    assert call(11, 5 * A + 8) == R.E_ALIGN
+    assert call(11, 2 * A) == R.E_ALIAS       # b over z
+    assert call(12, 3 * A) == R.E_ALIAS       # u over W1
+
+
+@needs_no_gpu
+def test_two_decode_bwd_validation(lib):
+    c = lib.cdll
+    ws = c.resbm2_workspace_bytes(T, N, M2, RR)
+    ok = [T, N, M2, RR, 1, A, 2 * A, 3 * A, N, 4 * A, N, 5 * A, 6 * A, 7 * A, 8 * A, 9 * A, 10 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm2_decode_bwd(*a)
+
+    assert call(16, None) == R.E_NULL
+    assert call(17, ws - 256) == R.E_WORKSPACE
+    assert call(16, 10 * A + 64) == R.E_ALIGN
+    assert call(10, N - 8) == R.E_SHAPE
+    assert call(13, 3 * A) == R.E_ALIAS       # g_b over g_zt
+    assert call(15, 8 * A) == R.E_ALIAS       # dW4 over dW3... distinct outputs may not overlap
+    assert call(16, 2 * A) == R.E_ALIAS       # workspace over v
+
+
+@needs_no_gpu
+def test_two_encode_bwd_validation(lib):
+    c = lib.cdll
+    ws = c.resbm2_workspace_bytes(T, N, M2, RR)
+    ok = [T, N, M2, RR, 1, A, N, 2 * A, 3 * A, 4 * A, 5 * A, 6 * A, N, 7 * A, N, 8 * A, 9 * A, 10 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm2_encode_bwd(*a)
+
+    assert call(4, 2) == R.E_ACT
+    assert call(17, None) == R.E_NULL
+    assert call(18, 0) == R.E_WORKSPACE
+    assert call(12, N + 4) == R.E_SHAPE
+    fused = list(ok)
+    fused[13], fused[14] = 6 * A, N + 8
+    assert c.resbm2_encode_bwd(*fused) == R.E_ALIAS   # g_x == g_z needs equal leading dimensions
+    assert call(11, A) == R.E_ALIAS           # g_z over z
+    assert call(15, 9 * A) == R.E_ALIAS       # dW1 over dW2

@@ -1,0 +1,238 @@
+"""Two-linears-per-side ops (resbm2_*) against the float64 oracle.
+
+Inputs are seeded bf16 tensors; the oracle computes in float64 on the same
+values.  Bound (as for the one-linear ops): max error <= 2e-2 RMS(ref), after
+a half-ulp discount for bf16 outputs.  Error budget: the GPU rounds phi(u),
+phi(v), g_u and g_v to bf16 before the next product (relative 2^-9 per element,
+averaging out over the contraction) and accumulates in float32.
+Small shapes are checked everywhere; the full 16384-token shape on sampled rows
+(row-local outputs) and sampled columns (token sums).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import resbm_oracle as R
+from oracle import two_linear_oracle as TL
+from gpu_helpers import check, f64, guarded, lib, say, strided
+from paper_2604_11947_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(333, 520, 136, 40), (1000, 256, 1024, 32), (64, 64, 8, 8), (1, 128, 64, 16), (513, 384, 520, 128)]
+IDS = [f"T{T}_n{n}_m{m}_r{r}" for T, n, m, r in SHAPES]
+ACTS = [R.ACT_IDENTITY, R.ACT_SILU]
+
+
+def data(T, n, m, r, seed=0):
+    d = I.make_activations(T, n, "normal", seed)
+    d.update(I.make_two_weights(n, m, r, seed))
+    d["b"] = I.make_bf16(T, r, seed + 11)
+    d["u"] = I.make_bf16(T, m, seed + 12)
+    d["v"] = I.make_bf16(T, m, seed + 13)
+    d["g_b"] = I.make_bf16(T, r, seed + 14, std=0.1)
+    return d
+
+
+def np64(d, k):
+    return d[k].to(torch.float64).numpy()
+
+
+# The token-sum products consume a bf16 operand the op forms itself (phi(u),
+# phi(v), g_u, g_v: relative rounding <= 2^-9 per element), so an element of a
+# weight gradient sum_t A[t, i] B[t, j] may be off by 2^-9 sum_t |A[t, i]| |B[t, j]|
+# before any averaging; the allowance is twice that.  It matters where few
+# tokens are summed (T = 1: a single outer product).
+def allow(A, B):
+    return 2.0 ** -8 * (np.abs(A).T @ np.abs(B))
+
+
+@pytest.mark.parametrize("act", ACTS)
+@pytest.mark.parametrize("T,n,m,r", SHAPES, ids=IDS)
+def test_encode2_fwd(T, n, m, r, act):
+    L = lib()
+    say(f"encode2_fwd T={T} n={n} m={m} r={r} act={act}")
+    d = data(T, n, m, r)
+    x, z = strided(d["x_attn"].cuda(), 8), strided(d["z"].cuda(), 24)
+    b, _, chk_b = guarded((T, r), torch.bfloat16, "cuda")
+    u, _, chk_u = guarded((T, m), torch.bfloat16, "cuda")
+    L.encode2_fwd(x, z, d["W1"].cuda(), d["W2"].cuda(), b, u, act=act)
+    torch.cuda.synchronize()
+    chk_b()
+    chk_u()
+    rb, ru = TL.encode2_fwd(np64(d, "x_attn"), np64(d, "z"), np64(d, "W1"), np64(d, "W2"), act)
+    check("u", u, ru, True)
+    check("b", b, rb, True)
+
+
+@pytest.mark.parametrize("act", ACTS)
+@pytest.mark.parametrize("T,n,m,r", SHAPES, ids=IDS)
+def test_decode2_fwd(T, n, m, r, act):
+    L = lib()
+    say(f"decode2_fwd T={T} n={n} m={m} r={r} act={act}")
+    d = data(T, n, m, r)
+    zt_buf = torch.full((T, n + 16), float("nan"), dtype=torch.bfloat16, device="cuda")
+    zt = zt_buf[:, :n]
+    v, _, chk_v = guarded((T, m), torch.bfloat16, "cuda")
+    L.decode2_fwd(d["b"].cuda(), d["W3"].cuda(), d["W4"].cuda(), zt, v, act=act)
+    torch.cuda.synchronize()
+    chk_v()
+    assert bool(torch.isnan(zt_buf[:, n:].float()).all()), "row padding of z~ overwritten"
+    rzt, rv = TL.decode2_fwd(np64(d, "b"), np64(d, "W3"), np64(d, "W4"), act)
+    check("v", v, rv, True)
+    check("z~", zt, rzt, True)
+
+
+@pytest.mark.parametrize("with_gid", [True, False])
+@pytest.mark.parametrize("act", ACTS)
+@pytest.mark.parametrize("T,n,m,r", SHAPES, ids=IDS)
+def test_decode2_bwd(T, n, m, r, act, with_gid):
+    L = lib()
+    say(f"decode2_bwd T={T} n={n} m={m} r={r} act={act} g_id={with_gid}")
+    d = data(T, n, m, r)
+    g_zt = strided(d["g_zt"].cuda(), 8)
+    g_id = strided(d["g_id"].cuda(), 40) if with_gid else None
+    g_b, _, chk = guarded((T, r), torch.bfloat16, "cuda")
+    dW3 = torch.full((r, m), float("nan"), device="cuda")
+    dW4 = torch.full((m, n), float("nan"), device="cuda")
+    L.decode2_bwd(d["b"].cuda(), d["v"].cuda(), g_zt, g_id, d["W3"].cuda(), d["W4"].cuda(), g_b, dW3, dW4, act=act)
+    torch.cuda.synchronize()
+    chk()
+    rg_b, rdW3, rdW4 = TL.decode2_bwd(np64(d, "b"), np64(d, "v"), np64(d, "g_zt"),
+                                      np64(d, "g_id") if with_gid else None, np64(d, "W3"), np64(d, "W4"), act)
+    check("g_b", g_b, rg_b, True)
+    b, v, g_zt = np64(d, "b"), np64(d, "v"), np64(d, "g_zt")
+    g_v = (g_zt @ np64(d, "W4").T) * R.dphi(v, act)
+    check("dW3", dW3, rdW3, False, allow=allow(b, g_v))
+    check("dW4", dW4, rdW4, False, allow=allow(R.phi(v, act), g_zt))
+
+
+@pytest.mark.parametrize("gx_mode", ["separate", "fused", "none"])
+@pytest.mark.parametrize("act", ACTS)
+@pytest.mark.parametrize("T,n,m,r", SHAPES, ids=IDS)
+def test_encode2_bwd(T, n, m, r, act, gx_mode):
+    L = lib()
+    say(f"encode2_bwd T={T} n={n} m={m} r={r} act={act} g_x={gx_mode}")
+    d = data(T, n, m, r)
+    z = strided(d["z"].cuda(), 16)
+    gz_buf = torch.full((T, n + 8), float("nan"), dtype=torch.bfloat16, device="cuda")
+    g_z = gz_buf[:, :n]
+    g_x = None
+    gx0 = I.make_bf16(T, n, 21, std=0.1)
+    if gx_mode == "separate":
+        g_x = strided(gx0.cuda(), 8)
+    elif gx_mode == "fused":
+        g_x = g_z
+    dW1 = torch.full((n, m), float("nan"), device="cuda")
+    dW2 = torch.full((m, r), float("nan"), device="cuda")
+    L.encode2_bwd(z, d["u"].cuda(), d["g_b"].cuda(), d["W1"].cuda(), d["W2"].cuda(), g_z, dW1, dW2, g_x=g_x,
+                  act=act)
+    torch.cuda.synchronize()
+    assert bool(torch.isnan(gz_buf[:, n:].float()).all()), "row padding of g_z overwritten"
+    rg_z, rdW1, rdW2 = TL.encode2_bwd(np64(d, "z"), np64(d, "u"), np64(d, "g_b"), np64(d, "W1"), np64(d, "W2"), act)
+    if gx_mode == "fused":
+        rg_z = R.skip_grad(rg_z, np64(d, "g_b"))
+    check("g_z", g_z, rg_z, True)
+    u, gb = np64(d, "u"), np64(d, "g_b")
+    g_u = (gb @ np64(d, "W2").T) * R.dphi(u, act)
+    check("dW1", dW1, rdW1, False, allow=allow(np64(d, "z"), g_u))
+    check("dW2", dW2, rdW2, False, allow=allow(R.phi(u, act), gb))
+    if gx_mode == "separate":
+        gx_ref = R.skip_grad(gx0.to(torch.float64).numpy(), np64(d, "g_b"))
+        got = f64(g_x)
+        assert np.array_equal(got[:, r:], gx_ref[:, r:]), "g_x columns >= r changed"
+        check("g_x", g_x, gx_ref, True)
+
+
+def test_two_empty_batch_is_noop():
+    L = lib()
+    n, m, r = 64, 32, 8
+    w = {k: v.cuda() for k, v in I.make_two_weights(n, m, r).items()}
+    e = torch.empty((0, n), dtype=torch.bfloat16, device="cuda")
+    L.encode2_fwd(e, e, w["W1"], w["W2"], torch.empty((0, r), dtype=torch.bfloat16, device="cuda"),
+                  torch.empty((0, m), dtype=torch.bfloat16, device="cuda"))
+    torch.cuda.synchronize()
+
+
+def test_two_deterministic():
+    L = lib()
+    T, n, m, r = 4096, 512, 256, 32
+    d = data(T, n, m, r, seed=3)
+    outs = []
+    for _ in range(2):
+        g_z = torch.empty((T, n), dtype=torch.bfloat16, device="cuda")
+        dW1, dW2 = torch.empty((n, m), device="cuda"), torch.empty((m, r), device="cuda")
+        L.encode2_bwd(d["z"].cuda(), d["u"].cuda(), d["g_b"].cuda(), d["W1"].cuda(), d["W2"].cuda(), g_z, dW1, dW2)
+        torch.cuda.synchronize()
+        outs.append((g_z.view(torch.int16).clone(), dW1.view(torch.int32).clone(), dW2.view(torch.int32).clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------- full size, sampled
+FULL = (16384, 4096, 1024, 32)
+
+
+@pytest.fixture(scope="module")
+def full():
+    T, n, m, r = FULL
+    say(f"drawing full-size inputs T={T} n={n} m={m} r={r}")
+    d = data(T, n, m, r, seed=5)
+    dev = {k: v.cuda() for k, v in d.items() if isinstance(v, torch.Tensor)}
+    rng = np.random.default_rng(17)
+    rows = np.unique(np.concatenate([[0, T - 1], rng.choice(T, 61, replace=False)]))
+    cols_m = np.unique(np.concatenate([[0, m - 1], rng.choice(m, 14, replace=False)]))
+    cols_n = np.unique(np.concatenate([[0, n - 1], rng.choice(n, 14, replace=False)]))
+    return d, dev, rows, cols_m, cols_n
+
+
+def test_full_forward_sampled(full):
+    L = lib()
+    d, dv, rows, _, _ = full
+    T, n, m, r = FULL
+    act = R.ACT_SILU
+    b = torch.empty((T, r), dtype=torch.bfloat16, device="cuda")
+    u = torch.empty((T, m), dtype=torch.bfloat16, device="cuda")
+    L.encode2_fwd(dv["x_attn"], dv["z"], dv["W1"], dv["W2"], b, u, act=act)
+    zt = torch.empty((T, n), dtype=torch.bfloat16, device="cuda")
+    v = torch.empty((T, m), dtype=torch.bfloat16, device="cuda")
+    L.decode2_fwd(dv["b"], dv["W3"], dv["W4"], zt, v, act=act)
+    torch.cuda.synchronize()
+    sel = lambda k: d[k][rows].to(torch.float64).numpy()  # noqa: E731
+    rb, ru = TL.encode2_fwd(sel("x_attn"), sel("z"), np64(d, "W1"), np64(d, "W2"), act)
+    check("u", u[rows].cpu(), ru, True)
+    check("b", b[rows].cpu(), rb, True)
+    rzt, rv = TL.decode2_fwd(sel("b"), np64(d, "W3"), np64(d, "W4"), act)
+    check("v", v[rows].cpu(), rv, True)
+    check("z~", zt[rows].cpu(), rzt, True)
+
+
+def test_full_backward_sampled(full):
+    L = lib()
+    d, dv, rows, cols_m, cols_n = full
+    T, n, m, r = FULL
+    act = R.ACT_SILU
+    g_b = torch.empty((T, r), dtype=torch.bfloat16, device="cuda")
+    dW3, dW4 = torch.empty((r, m), device="cuda"), torch.empty((m, n), device="cuda")
+    L.decode2_bwd(dv["b"], dv["v"], dv["g_zt"], dv["g_id"], dv["W3"], dv["W4"], g_b, dW3, dW4, act=act)
+    g_z = torch.empty((T, n), dtype=torch.bfloat16, device="cuda")
+    dW1, dW2 = torch.empty((n, m), device="cuda"), torch.empty((m, r), device="cuda")
+    L.encode2_bwd(dv["z"], dv["u"], dv["g_b"], dv["W1"], dv["W2"], g_z, dW1, dW2, g_x=g_z, act=act)
+    torch.cuda.synchronize()
+    W1, W2, W3, W4 = (np64(d, k) for k in ("W1", "W2", "W3", "W4"))
+    b, v, u, gb_in = np64(d, "b"), np64(d, "v"), np64(d, "u"), np64(d, "g_b")
+    g_zt, g_id, z = np64(d, "g_zt"), np64(d, "g_id"), np64(d, "z")
+    # row-local outputs on sampled rows
+    rg_b, _, _ = TL.decode2_bwd(b[rows], v[rows], g_zt[rows], g_id[rows], W3, W4, act)
+    check("g_b", g_b[rows].cpu(), rg_b, True)
+    rg_z, _, _ = TL.encode2_bwd(z[rows], u[rows], gb_in[rows], W1, W2, act)
+    check("g_z", g_z[rows].cpu(), R.skip_grad(rg_z, gb_in[rows]), True)
+    # token sums on sampled columns: dW4[:, j] = phi(v)^T g_zt[:, j]; dW3[:, j] = b^T g_v[:, j];
+    # dW1[:, j] = z^T g_u[:, j]; dW2 whole
+    p = R.phi(v, act)
+    check("dW4[:, s]", dW4[:, cols_n].cpu(), p.T @ g_zt[:, cols_n], False)
+    g_v = (g_zt @ W4[cols_m].T) * R.dphi(v[:, cols_m], act)
+    check("dW3[:, s]", dW3[:, cols_m].cpu(), b.T @ g_v, False)
+    g_u = (gb_in @ W2[cols_m].T) * R.dphi(u[:, cols_m], act)
+    check("dW1[:, s]", dW1[:, cols_m].cpu(), z.T @ g_u, False)
+    check("dW2", dW2, R.phi(u, act).T @ gb_in, False)
