@@ -59,6 +59,8 @@ def parse():
     p.add_argument("--no-graph", action="store_true", help="report the eager launches instead of graph replays")
     p.add_argument("--no-optimizer", action="store_true",
                    help="skip timing the optimizer-side ops (Muon update, spectrum) on the bottleneck weights")
+    p.add_argument("--two-m", type=int, default=1024,
+                   help="intermediate width m of the two-linears-per-side variant (0: skip timing it)")
     p.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="write profiles/ summaries from rocprofv3 output of this script (no GPU work)")
     p.add_argument("--commands", nargs=3, default=None, help="the three rocprofv3 commands, recorded in the summaries")
@@ -296,6 +298,95 @@ def optimizer_timing(lib, d: dict, r: int, dev, iters: int, cpu: bool) -> dict:
     return out
 
 
+def two_linear_timing(lib, d: dict, r: int, m: int, dev, iters: int, cpu: bool, act: int) -> dict:
+    """One training step of the two-linears-per-side bottleneck (Sec. 3.2) on the
+    workload's activations: encode2_fwd, decode2_fwd, decode2_bwd, encode2_bwd
+    (g_x fused into g_z).  Per-op times from HIP events on the launch stream
+    around eager calls; the whole step from graph replays."""
+    import torch
+
+    from paper_2604_11947_amd import inputs as I
+
+    T, n = d["z"].shape
+    bf = torch.bfloat16
+    w = {k: v.to(dev) for k, v in I.make_two_weights(n, m, r, seed=1).items()}
+    x, z, g_zt, g_id = (d[k].to(dev) for k in ("x_attn", "z", "g_zt", "g_id"))
+    b, u = torch.empty(T, r, dtype=bf, device=dev), torch.empty(T, m, dtype=bf, device=dev)
+    zt, v = torch.empty(T, n, dtype=bf, device=dev), torch.empty(T, m, dtype=bf, device=dev)
+    g_b, g_z = torch.empty(T, r, dtype=bf, device=dev), torch.empty(T, n, dtype=bf, device=dev)
+    dW1, dW2 = torch.empty(n, m, device=dev), torch.empty(m, r, device=dev)
+    dW3, dW4 = torch.empty(r, m, device=dev), torch.empty(m, n, device=dev)
+    ws = lib.two_workspace(T, n, m, r, dev)
+    ops = {
+        "encode2_fwd": lambda: lib.encode2_fwd(x, z, w["W1"], w["W2"], b, u, act=act),
+        "decode2_fwd": lambda: lib.decode2_fwd(b, w["W3"], w["W4"], zt, v, act=act, ws=ws),
+        "decode2_bwd": lambda: lib.decode2_bwd(b, v, g_zt, g_id, w["W3"], w["W4"], g_b, dW3, dW4, act=act, ws=ws),
+        "encode2_bwd": lambda: lib.encode2_bwd(z, u, g_b, w["W1"], w["W2"], g_z, dW1, dW2, g_x=g_z, act=act, ws=ws),
+    }
+
+    def step():
+        for f in ops.values():
+            f()
+
+    for _ in range(5):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(iters)]
+    for i in range(iters):
+        ev[i][0].record(stream)
+        for k, f in enumerate(ops.values()):
+            f()
+            ev[i][k + 1].record(stream)
+    torch.cuda.synchronize()
+    op_us = {nm: sum(e[k].elapsed_time(e[k + 1]) for e in ev) * 1e3 / iters for k, nm in enumerate(ops)}
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(5):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / iters
+    big, small = 2.0 * T * n * m, 2.0 * T * m * r
+    # algorithmic flops per op: the n x m products and the r-wide ones
+    flops = {"encode2_fwd": big + small, "decode2_fwd": big + small,
+             "decode2_bwd": 2 * big + 2 * small, "encode2_bwd": 2 * big + 2 * small}
+    dom = max(op_us, key=op_us.get)
+    tf = flops[dom] / (op_us[dom] * 1e-6) / 1e12
+    out = {"m": m, "tokens": T, "us_per_step": us, "tokens_per_s": T / (us * 1e-6),
+           "tflops_step": sum(flops.values()) / (us * 1e-6) / 1e12,
+           "ops_us": op_us, "iterations": iters, "timing": "ops: events around eager calls; step: graph replay",
+           "roofline": {"bound": "mfma", "op": dom, "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": tf / MFMA_BF16_PEAK_TFLOPS, "flops": flops[dom]}}
+    if cpu:
+        from oracle import resbm_oracle as RO
+        from oracle import two_linear_oracle as TL
+        f64 = lambda t: t.to(torch.float64).cpu().numpy()  # noqa: E731
+        W = {k: f64(v) for k, v in w.items()}
+        Ts = 256
+        xs, zs, gzs, gis = (f64(t[:Ts]) for t in (x, z, g_zt, g_id))
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 10.0:
+            bb, uu = TL.encode2_fwd(xs, zs, W["W1"], W["W2"], act)
+            _, vv = TL.decode2_fwd(bb, W["W3"], W["W4"], act)
+            gb, _, _ = TL.decode2_bwd(bb, vv, gzs, gis, W["W3"], W["W4"], act)
+            gz, _, _ = TL.encode2_bwd(zs, uu, gb, W["W1"], W["W2"], act)
+            RO.skip_grad(gz, gb)
+            reps += 1
+        sec = (time.perf_counter() - t0) / reps
+        out["cpu_baseline"] = {"value": Ts / sec, "unit": "tokens/s", "cores": torch.get_num_threads(),
+                               "kind": "oracle", "sample": f"{Ts} tokens of the same step, {reps} repetitions"}
+    return out
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 COPY_PROBE_MIB = 256
 
 
@@ -461,6 +552,8 @@ def main():
     }
     if not args.no_optimizer:
         out["optimizer"] = optimizer_timing(lib, d, r, dev, 200, cpu=not args.no_cpu_baseline)
+    if args.two_m > 0:
+        out["two_linear"] = two_linear_timing(lib, d, r, args.two_m, dev, 50, not args.no_cpu_baseline, act)
     if not args.no_cpu_baseline:
         tokens = args.cpu_tokens or T
         out["cpu_baseline"] = cpu_baseline(d, r, act, min(tokens, T))

@@ -235,9 +235,9 @@ size_t resbm_workspace_bytes(int64_t T, int32_t n, int32_t r);
  *  - products inside an op consume bf16 operands: phi(u), phi(v), and the
  *    gradients g_u, g_v held in the workspace between two products, are
  *    rounded to bf16 first (accumulation is float32);
- *  - the backward ops take ws of resbm2_workspace_bytes(T, n, m, r) bytes
- *    (the T x m gradient and split-K partial sums); the forward ops take
- *    none (ws may be NULL).
+ *  - ws holds resbm2_workspace_bytes(T, n, m, r) bytes (T x m
+ *    intermediates and split-K partial sums); resbm2_encode_fwd needs none,
+ *    and resbm2_decode_fwd none with act = identity (ws may then be NULL).
  */
 size_t resbm2_workspace_bytes(int64_t T, int32_t n, int32_t m, int32_t r);
 

@@ -61,6 +61,7 @@ enum Epi : int {
   kEpiDphi = 2,   // C = rne(acc * phi'(X))   (X: saved pre-activation, same shape as C)
   kEpiAdd = 3,    // C = rne(acc + X) on columns < x_cols, rne(acc) elsewhere
   kEpiPart = 4,   // partial[split] = acc (float32, M x N contiguous per split)
+  kEpiBf16Phi = 5,  // C = rne(acc) and D = rne(phi(C)) (a pre-activation and its activation)
 };
 
 struct GemmArgs {
@@ -69,18 +70,22 @@ struct GemmArgs {
   const void* B; int64_t ldb; int64_t b_bytes;
   void* C; int64_t ldc; int64_t c_bytes;
   const void* X; int64_t ldx; int64_t x_bytes; int x_cols;
+  void* D; int64_t ldd; int64_t d_bytes;
   int kc;  // K per split (a multiple of KT); gridDim.z splits
 };
+
+// SiLU, a sigmoid(a) with sigmoid(a) = 1 / (1 + 2^(-a log2 e)) from the
+// hardware exp2 and reciprocal (about 1 ulp each).
+__device__ __forceinline__ float silu(float a) {
+  return a * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-a * 1.44269504088896341f));
+}
 
 // SiLU on 8 bf16 values, each result rounded to bf16 (the operand the next
 // product consumes).
 __device__ __forceinline__ uint4 silu8(uint4 v) {
   bf16x8 h = __builtin_bit_cast(bf16x8, v);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float a = (float)h[e];
-    h[e] = (__bf16)(a * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-a * 1.44269504088896341f)));
-  }
+  for (int e = 0; e < 8; ++e) h[e] = (__bf16)silu((float)h[e]);
   return __builtin_bit_cast(uint4, h);
 }
 
@@ -236,6 +241,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
   // Epilogue: lane (row16, grp) of tile (i, j) holds C[m][n .. n + 3].
   const rsrc_t rc = make_rsrc(g.C, g.c_bytes);
   const rsrc_t rx = make_rsrc(g.X, g.x_bytes);
+  const rsrc_t rd = make_rsrc(g.D, g.d_bytes);
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     const int m = m0 + (wm * FM + i) * 16 + row16;
@@ -263,6 +269,11 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) h[e] = (__bf16)v[e];
         bst8(rc, ok ? (uint32_t)(((int64_t)m * g.ldc + n) * 2) : kOOB, __builtin_bit_cast(uint2, h));
+        if constexpr (EPI == kEpiBf16Phi) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) h[e] = (__bf16)silu((float)h[e]);
+          bst8(rd, ok ? (uint32_t)(((int64_t)m * g.ldd + n) * 2) : kOOB, __builtin_bit_cast(uint2, h));
+        }
       }
     }
   }
@@ -280,6 +291,13 @@ __global__ __launch_bounds__(256) void k_splitk_sum(const float* __restrict__ pa
     a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
   }
   reinterpret_cast<float4*>(out)[q] = a;
+}
+
+// p[i] = rne(silu(v[i])), 8 elements per thread (count % 8 == 0).
+__global__ __launch_bounds__(256) void k_silu(const __bf16* __restrict__ v, int64_t count, __bf16* __restrict__ p) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q * 8 >= count) return;
+  reinterpret_cast<uint4*>(p)[q] = silu8(reinterpret_cast<const uint4*>(v)[q]);
 }
 
 // g_x[t][0 .. r) <- rne(g_x + g_b), 4 columns per thread (r % 8 == 0).
@@ -325,14 +343,18 @@ bool shape_ok2(int64_t T, int n, int m, int r) {
 bool ld_ok2(int64_t ld, int n) { return ld >= n && ld % 8 == 0; }
 bool fits(size_t bytes) { return bytes <= (size_t)kMaxRange; }
 
-// Block tile shapes: the wide one for products with an n- or m-wide output,
-// a narrow one for an r-wide output (N = r).  Products with M = r use the wide
-// one; the rows beyond r read nothing.
-enum Shape { kWide = 0, kNarrow32 = 1, kNarrow64 = 2, kNarrow128 = 3 };
+// Block tile shapes: 256 x 256 (8 waves of 128 x 64) for the n x m products,
+// 128 x 128 (4 waves of 64 x 64) where M or N is below 256, and a narrow one
+// for an r-wide output (N = r).  Products with M = r use 128 x 128; the rows
+// beyond r read nothing.
+enum Shape { kBig = 0, kWide = 1, kNarrow32 = 2, kNarrow64 = 3, kNarrow128 = 4 };
 
+Shape wide_for(int M, int N) { return M >= 256 && N >= 256 ? kBig : kWide; }
 Shape narrow_for(int N) { return N <= 32 ? kNarrow32 : (N <= 64 ? kNarrow64 : kNarrow128); }
-int shape_bm(Shape s) { return s == kWide ? 128 : 64; }
-int shape_bn(Shape s) { return s == kWide ? 128 : (s == kNarrow32 ? 32 : (s == kNarrow64 ? 64 : 128)); }
+int shape_bm(Shape s) { return s == kBig ? 256 : (s == kWide ? 128 : 64); }
+int shape_bn(Shape s) {
+  return s == kBig ? 256 : (s == kWide || s == kNarrow128 ? 128 : (s == kNarrow32 ? 32 : 64));
+}
 
 struct Split {
   int S;
@@ -355,17 +377,18 @@ size_t part_bytes(int M, int N, const Split& sp) {
 
 struct Plan2 {
   Split dW4, dW3, dW2, dW1;
-  size_t inter;      // T x m bf16 intermediate (g_v or g_u)
-  size_t dec_bwd, enc_bwd;
+  size_t inter;      // one T x m bf16 intermediate (phi(v), g_v or g_u)
+  size_t dec_fwd, dec_bwd, enc_bwd;
 };
 Plan2 make_plan2(int64_t T, int n, int m, int r) {
   Plan2 p;
-  p.dW4 = split_for(m, n, (int)T, kWide);
+  p.dW4 = split_for(m, n, (int)T, wide_for(m, n));
   p.dW3 = split_for(r, m, (int)T, kWide);
   p.dW2 = split_for(m, r, (int)T, narrow_for(r));
-  p.dW1 = split_for(n, m, (int)T, kWide);
+  p.dW1 = split_for(n, m, (int)T, wide_for(n, m));
   p.inter = round_up((size_t)T * m * 2, kWsAlign2);
-  p.dec_bwd = p.inter + std::max(part_bytes(m, n, p.dW4), part_bytes(r, m, p.dW3));
+  p.dec_fwd = p.inter;
+  p.dec_bwd = 2 * p.inter + std::max(part_bytes(m, n, p.dW4), part_bytes(r, m, p.dW3));
   p.enc_bwd = p.inter + std::max(part_bytes(m, r, p.dW2), part_bytes(n, m, p.dW1));
   return p;
 }
@@ -380,6 +403,7 @@ void launch(const GemmArgs& g, int S, hipStream_t st) {
 template <bool AK, bool BKC, int EPI, bool PHI>
 void gemm(Shape s, const GemmArgs& g, int S, hipStream_t st) {
   switch (s) {
+    case kBig: launch<AK, BKC, 256, 256, 2, 4, EPI, PHI>(g, S, st); break;
     case kWide: launch<AK, BKC, 128, 128, 2, 2, EPI, PHI>(g, S, st); break;
     case kNarrow32: launch<AK, BKC, 64, 32, 4, 1, EPI, PHI>(g, S, st); break;
     case kNarrow64: launch<AK, BKC, 64, 64, 4, 1, EPI, PHI>(g, S, st); break;
@@ -431,7 +455,7 @@ extern "C" {
 size_t resbm2_workspace_bytes(int64_t T, int32_t n, int32_t m, int32_t r) {
   if (!shape_ok2(T, n, m, r) || T == 0) return 0;
   const Plan2 p = make_plan2(T, n, m, r);
-  return std::max(p.dec_bwd, p.enc_bwd);
+  return std::max(p.dec_fwd, std::max(p.dec_bwd, p.enc_bwd));
 }
 
 int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* x_attn, int64_t ld_x,
@@ -457,7 +481,7 @@ int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   const int Ti = (int)T;
   // u = z W1  (A = z, K-contiguous; B = W1 [n][m], m-contiguous)
   GemmArgs g = args(Ti, m, n, z, ld_z, bz, W1, m, bw1, u, m, bu);
-  gemm<true, false, kEpiBf16, false>(kWide, g, 1, st);
+  gemm<true, false, kEpiBf16, false>(wide_for(Ti, m), g, 1, st);
   // b = x_attn[:, :r] + phi(u) W2
   g = args(Ti, r, m, u, m, bu, W2, r, bw2, b, r, bb);
   g.X = x_attn; g.ldx = ld_x; g.x_bytes = (int64_t)bx; g.x_cols = r;
@@ -469,10 +493,14 @@ int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
 int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* b, const void* W3,
                           const void* W4, void* z_tilde, int64_t ld_zt, void* v, void* ws, size_t ws_bytes,
                           void* stream) {
-  (void)ws; (void)ws_bytes;
   if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
   if (!shape_ok2(T, n, m, r)) return RESBM_E_SHAPE;
   if (T == 0) return RESBM_OK;
+  const bool silu = act == RESBM_ACT_SILU;
+  const Plan2 p = make_plan2(T, n, m, r);
+  const size_t need = silu ? p.dec_fwd : 0;
+  int32_t e = check_ws(need, ws, ws_bytes);
+  if (e) return e;
   if (!b || !W3 || !W4 || !z_tilde || !v) return RESBM_E_NULL;
   if (!ld_ok2(ld_zt, n)) return RESBM_E_SHAPE;
   if (!aligned2(b, 16) || !aligned2(W3, 16) || !aligned2(W4, 16) || !aligned2(z_tilde, 16) || !aligned2(v, 16))
@@ -481,17 +509,23 @@ int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
                bzt = extent2(T, n, ld_zt, 2), bv = (size_t)T * m * 2;
   if (!fits(bzt) || !fits(bv) || !fits(bw4)) return RESBM_E_SHAPE;
   if (overlap2(z_tilde, bzt, b, bb) || overlap2(z_tilde, bzt, W3, bw3) || overlap2(z_tilde, bzt, W4, bw4) ||
-      overlap2(v, bv, b, bb) || overlap2(v, bv, W3, bw3) || overlap2(v, bv, W4, bw4) || overlap2(v, bv, z_tilde, bzt))
+      overlap2(v, bv, b, bb) || overlap2(v, bv, W3, bw3) || overlap2(v, bv, W4, bw4) || overlap2(v, bv, z_tilde, bzt) ||
+      overlap2(ws, need, b, bb) || overlap2(ws, need, W3, bw3) || overlap2(ws, need, W4, bw4) ||
+      overlap2(ws, need, z_tilde, bzt) || overlap2(ws, need, v, bv))
     return RESBM_E_ALIAS;
   hipStream_t st = (hipStream_t)stream;
   const int Ti = (int)T;
-  // v = b W3
+  // v = b W3, and with SiLU also phi(v) (workspace), formed once from the rounded v
   GemmArgs g = args(Ti, m, r, b, r, bb, W3, m, bw3, v, m, bv);
-  gemm<true, false, kEpiBf16, false>(kWide, g, 1, st);
+  if (silu) {
+    g.D = ws; g.ldd = m; g.d_bytes = (int64_t)bv;
+    gemm<true, false, kEpiBf16Phi, false>(wide_for(Ti, m), g, 1, st);
+  } else {
+    gemm<true, false, kEpiBf16, false>(wide_for(Ti, m), g, 1, st);
+  }
   // z~ = phi(v) W4
-  g = args(Ti, n, m, v, m, bv, W4, n, bw4, z_tilde, ld_zt, bzt);
-  if (act == RESBM_ACT_SILU) gemm<true, false, kEpiBf16, true>(kWide, g, 1, st);
-  else gemm<true, false, kEpiBf16, false>(kWide, g, 1, st);
+  g = args(Ti, n, m, silu ? ws : v, m, bv, W4, n, bw4, z_tilde, ld_zt, bzt);
+  gemm<true, false, kEpiBf16, false>(wide_for(Ti, n), g, 1, st);
   return status2();
 }
 
@@ -528,20 +562,25 @@ int32_t resbm2_decode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   const int Ti = (int)T;
   char* w = (char*)ws;
   void* g_v = w;
-  void* part = w + p.inter;
+  void* pv = w + p.inter;
+  void* part = w + 2 * p.inter;
   const bool silu = act == RESBM_ACT_SILU;
   // g_v = (g_zt W4^T) * phi'(v)   (B(k, j) = W4[j][k]: K-contiguous)
   GemmArgs g = args(Ti, m, n, g_zt, ld_gzt, bg, W4, n, bw4, g_v, m, bv);
   if (silu) {
     g.X = v; g.ldx = m; g.x_bytes = (int64_t)bv;
-    gemm<true, true, kEpiDphi, false>(kWide, g, 1, st);
+    gemm<true, true, kEpiDphi, false>(wide_for(Ti, m), g, 1, st);
   } else {
-    gemm<true, true, kEpiBf16, false>(kWide, g, 1, st);
+    gemm<true, true, kEpiBf16, false>(wide_for(Ti, m), g, 1, st);
   }
-  // dW4 = phi(v)^T g_zt   (A(i, k) = v[k][i], B(k, j) = g_zt[k][j])
-  g = args(m, n, Ti, v, m, bv, g_zt, ld_gzt, bg, nullptr, 0, 0);
-  if (silu) weight_grad<true>(kWide, g, p.dW4, dW4, part, st);
-  else weight_grad<false>(kWide, g, p.dW4, dW4, part, st);
+  // dW4 = phi(v)^T g_zt   (A(i, k) = phi(v)[k][i], B(k, j) = g_zt[k][j]); phi(v) formed once
+  if (silu) {
+    const int64_t cnt = T * m;
+    hipLaunchKernelGGL(k_silu, dim3((unsigned)((cnt / 8 + 255) / 256)), dim3(256), 0, st, (const __bf16*)v, cnt,
+                       (__bf16*)pv);
+  }
+  g = args(m, n, Ti, silu ? pv : v, m, bv, g_zt, ld_gzt, bg, nullptr, 0, 0);
+  weight_grad<false>(wide_for(m, n), g, p.dW4, dW4, part, st);
   // dW3 = b^T g_v
   g = args(r, m, Ti, b, r, bb, g_v, m, bv, nullptr, 0, 0);
   weight_grad<false>(kWide, g, p.dW3, dW3, part, st);
@@ -598,9 +637,9 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   GemmArgs g = args(Ti, m, r, g_b, r, bgb, W2, r, bw2, g_u, m, bu);
   if (silu) {
     g.X = u; g.ldx = m; g.x_bytes = (int64_t)bu;
-    gemm<true, true, kEpiDphi, false>(kWide, g, 1, st);
+    gemm<true, true, kEpiDphi, false>(wide_for(Ti, m), g, 1, st);
   } else {
-    gemm<true, true, kEpiBf16, false>(kWide, g, 1, st);
+    gemm<true, true, kEpiBf16, false>(wide_for(Ti, m), g, 1, st);
   }
   // dW2 = phi(u)^T g_b
   g = args(m, r, Ti, u, m, bu, g_b, r, bgb, nullptr, 0, 0);
@@ -608,14 +647,14 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   else weight_grad<false>(narrow_for(r), g, p.dW2, dW2, part, st);
   // dW1 = z^T g_u
   g = args(n, m, Ti, z, ld_z, bz, g_u, m, bu, nullptr, 0, 0);
-  weight_grad<false>(kWide, g, p.dW1, dW1, part, st);
+  weight_grad<false>(wide_for(n, m), g, p.dW1, dW1, part, st);
   // g_z = g_u W1^T (+ g_b on columns [0, r) when g_x is g_z)   (B(k, j) = W1[j][k])
   g = args(Ti, n, m, g_u, m, bu, W1, m, bw1, g_z, ld_gz, bgz);
   if (fused) {
     g.X = g_b; g.ldx = r; g.x_bytes = (int64_t)bgb; g.x_cols = r;
-    gemm<true, true, kEpiAdd, false>(kWide, g, 1, st);
+    gemm<true, true, kEpiAdd, false>(wide_for(Ti, n), g, 1, st);
   } else {
-    gemm<true, true, kEpiBf16, false>(kWide, g, 1, st);
+    gemm<true, true, kEpiBf16, false>(wide_for(Ti, n), g, 1, st);
     if (g_x) {
       const int64_t cnt = T * (r / 4);
       hipLaunchKernelGGL(k_skip_grad, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, T, r,

@@ -252,7 +252,7 @@ class Library:
                                          _ptr(b), _ptr(u), None, 0, _stream(stream, z))
         self._check("resbm2_encode_fwd", st)
 
-    def decode2_fwd(self, b, W3, W4, z_tilde, v, act=ACT_SILU, stream=None):
+    def decode2_fwd(self, b, W3, W4, z_tilde, v, act=ACT_SILU, ws=None, stream=None):
         T = b.shape[0]
         m, n = W4.shape
         r = W3.shape[0]
@@ -264,8 +264,10 @@ class Library:
         _packed(b, T, r, "b")
         _packed(v, T, m, "v")
         ld_zt = _ld(z_tilde, T, n, "z_tilde")
+        if ws is None:
+            ws = self.two_workspace(T, n, m, r, b.device)
         st = self.cdll.resbm2_decode_fwd(T, n, m, r, act, _ptr(b), _ptr(W3), _ptr(W4), _ptr(z_tilde), ld_zt, _ptr(v),
-                                         None, 0, _stream(stream, b))
+                                         _ptr(ws), ws.numel(), _stream(stream, b))
         self._check("resbm2_decode_fwd", st)
 
     def decode2_bwd(self, b, v, g_zt, g_id, W3, W4, g_b, dW3, dW4, act=ACT_SILU, ws=None, stream=None):
