@@ -167,6 +167,38 @@ struct Operand {
   }
 };
 
+// Direct-to-LDS staging of one operand tile (buffer loads with the LDS
+// destination): wave w of NW moves the 1 KiB blocks p NW + w of the tile, lane l
+// filling bytes [16 l, 16 l + 16) of its block, so each lane fetches the chunk
+// whose swizzled position that is (both swizzles are XORs, their own inverse).
+// Out-of-range chunks are fetched at kOOB and land as zeros.
+template <bool KC, int I, int NW>
+__device__ __forceinline__ void dma_tile(rsrc_t src, int64_t ld, int i0, int NI, int k0, int kend, __bf16* tile,
+                                         int wave, int lane) {
+  static_assert(KC || I % 128 == 0, "direct staging of a k-major tile needs rows of a multiple of 128");
+  constexpr int BLOCKS = I * KT * 2 / 1024;
+  static_assert(BLOCKS % NW == 0, "tile blocks must divide over the waves");
+#pragma unroll
+  for (int p = 0; p < BLOCKS / NW; ++p) {
+    const int blk = p * NW + wave;
+    const int o = blk * 1024 + lane * 16;
+    int idx, k;
+    if constexpr (KC) {
+      const int row = o >> 7, pc = (o >> 4) & 7;
+      idx = i0 + row;
+      k = k0 + 8 * ((pc ^ (row >> 1)) & 7);
+    } else {
+      const int row = o / (I * 2), pc = (o >> 4) % (I / 8);
+      k = k0 + row;
+      idx = i0 + 8 * (((pc ^ row) & 15) | (pc & ~15));
+    }
+    const bool ok = idx < NI && k < kend;
+    const int64_t off = KC ? ((int64_t)idx * ld + k) * 2 : ((int64_t)k * ld + idx) * 2;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (__attribute__((address_space(3))) void*)(tile + blk * 512), 16,
+                                             ok ? (uint32_t)off : kOOB, 0, 0, 0);
+  }
+}
+
 // Block index -> tile index.  Consecutive blocks are dispatched to the eight
 // XCDs in turn; each XCD is given a contiguous range of tiles, and tile indices
 // run along N first, so the tiles resident on one XCD share the rows of A (the
@@ -181,8 +213,12 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
   constexpr int NTH = 64 * WM * WN;
   constexpr int FM = BM / (16 * WM), FN = BN / (16 * WN);
   static_assert(FM * 16 * WM == BM && FN * 16 * WN == BN, "wave tiling must cover the block tile");
-  __shared__ __attribute__((aligned(16))) __bf16 s_a[2][BM * KT];
-  __shared__ __attribute__((aligned(16))) __bf16 s_b[2][BN * KT];
+  // Direct-to-LDS staging for the 256 x 256 tiles without an A prologue; the
+  // others stage through registers.  Four separate LDS arrays keep the stage
+  // buffers distinct objects for the compiler's wait-count analysis.
+  constexpr bool kDma = BM == 256 && BN == 256 && !PHI_A;
+  __shared__ __attribute__((aligned(16))) __bf16 s_a0[BM * KT], s_a1[BM * KT];
+  __shared__ __attribute__((aligned(16))) __bf16 s_b0[BN * KT], s_b1[BN * KT];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -195,8 +231,6 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
   const int nst = (kend - kbeg + KT - 1) / KT;
 
   const rsrc_t ra = make_rsrc(g.A, g.a_bytes), rb = make_rsrc(g.B, g.b_bytes);
-  Operand<AK, BM, NTH> opa;
-  Operand<BKC, BN, NTH> opb;
 
   f32x4 acc[FM][FN];
 #pragma unroll
@@ -204,21 +238,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (nst > 0) {
-    opa.load(ra, g.lda, m0, g.M, kbeg, kend, tid);
-    opb.load(rb, g.ldb, n0, g.N, kbeg, kend, tid);
-    opa.template put<PHI_A>(s_a[0], tid);
-    opb.template put<false>(s_b[0], tid);
-  }
-  __syncthreads();
-  for (int s = 0; s < nst; ++s) {
-    const bool more = s + 1 < nst;
-    if (more) {
-      opa.load(ra, g.lda, m0, g.M, kbeg + (s + 1) * KT, kend, tid);
-      opb.load(rb, g.ldb, n0, g.N, kbeg + (s + 1) * KT, kend, tid);
-    }
-    const __bf16* ta = s_a[s & 1];
-    const __bf16* tb = s_b[s & 1];
+  auto products = [&](const __bf16* ta, const __bf16* tb) {
 #pragma unroll
     for (int kk = 0; kk < KT / 32; ++kk) {
       bf16x8 fa[FM], fb[FN];
@@ -231,11 +251,50 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
-    if (more) {
-      opa.template put<PHI_A>(s_a[(s + 1) & 1], tid);
-      opb.template put<false>(s_b[(s + 1) & 1], tid);
+  };
+
+  if constexpr (kDma) {
+    constexpr int NW = WM * WN;
+    auto stage = [&](int s, __bf16* a, __bf16* b) {
+      dma_tile<AK, BM, NW>(ra, g.lda, m0, g.M, kbeg + s * KT, kend, a, wave, lane);
+      dma_tile<BKC, BN, NW>(rb, g.ldb, n0, g.N, kbeg + s * KT, kend, b, wave, lane);
+    };
+    // Stage s + 1 streams into the other buffers while stage s is multiplied;
+    // a stage is complete once every wave has seen its own loads land.
+    auto step = [&](int s, const __bf16* a, const __bf16* b, __bf16* na, __bf16* nb) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (s + 1 < nst) stage(s + 1, na, nb);
+      products(a, b);
+    };
+    if (nst > 0) stage(0, s_a0, s_b0);
+    for (int s = 0; s < nst; s += 2) {
+      step(s, s_a0, s_b0, s_a1, s_b1);
+      if (s + 1 < nst) step(s + 1, s_a1, s_b1, s_a0, s_b0);
+    }
+  } else {
+    Operand<AK, BM, NTH> opa;
+    Operand<BKC, BN, NTH> opb;
+    if (nst > 0) {
+      opa.load(ra, g.lda, m0, g.M, kbeg, kend, tid);
+      opb.load(rb, g.ldb, n0, g.N, kbeg, kend, tid);
+      opa.template put<PHI_A>(s_a0, tid);
+      opb.template put<false>(s_b0, tid);
     }
     __syncthreads();
+    for (int s = 0; s < nst; ++s) {
+      const bool more = s + 1 < nst;
+      if (more) {
+        opa.load(ra, g.lda, m0, g.M, kbeg + (s + 1) * KT, kend, tid);
+        opb.load(rb, g.ldb, n0, g.N, kbeg + (s + 1) * KT, kend, tid);
+      }
+      products(s & 1 ? s_a1 : s_a0, s & 1 ? s_b1 : s_b0);
+      if (more) {
+        opa.template put<PHI_A>(s & 1 ? s_a0 : s_a1, tid);
+        opb.template put<false>(s & 1 ? s_b0 : s_b1, tid);
+      }
+      __syncthreads();
+    }
   }
 
   // Epilogue: lane (row16, grp) of tile (i, j) holds C[m][n .. n + 3].
