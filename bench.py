@@ -157,13 +157,22 @@ def summarize_profiles(trace_dir: str, fetch_dir: str, write_dir: str, name: str
     with open(os.path.join(ROOT, "profiles", f"kernels_{name}.txt"), "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+    two = {k: v for k, v in stats.items() if k.startswith("resbm2::")}
+    if two:
+        lines = [f"# rocprofv3 kernel trace of the two-linears-per-side step (bench.py two_linear, m = 1024),"
+                 f" workload {name}", "", "command:", f"    {commands[0] if commands else '?'}", "",
+                 f"{'kernel':60s} {'calls':>6s} {'avg us':>9s} {'min us':>9s} {'max us':>9s}"]
+        for k, v in sorted(two.items(), key=lambda kv: -sum(kv[1])):
+            lines.append(f"{k[:60]:60s} {len(v):6d} {sum(v) / len(v):9.2f} {min(v):9.2f} {max(v):9.2f}")
+        with open(os.path.join(ROOT, "profiles", f"kernels_two_linear_{name}.txt"), "w") as fh:
+            fh.write("\n".join(lines) + "\n")
 
 
 def source_digest() -> str:
     """sha256 over the kernel sources; HBM traffic measured on other sources is not reported."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("resbm_kernels.hip", "resbm_plan.hpp", "resbm_mfma.hpp"):
+    for f in ("resbm_kernels.hip", "resbm_plan.hpp", "resbm_mfma.hpp", "resbm_buffer.hpp"):
         with open(os.path.join(ROOT, "paper_2604_11947_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
