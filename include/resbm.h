@@ -286,6 +286,32 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
                           float* dW1, float* dW2,
                           void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * Encoder fused into the feed-forward output projection.  Sec. 3.2 places the
+ * encoder directly after the feed-forward layer, so its contraction can run in
+ * the epilogue of the FFN's down projection while the output tile is still on
+ * chip, instead of a second pass over z:
+ *     z = h W_down                       (T x n, rounded to bf16, written: the
+ *                                         backward needs it)
+ *     a = z W_e,  b = x_attn I_{n x r} + phi(a)   (as resbm_encode_fwd on z)
+ *  h       T x d_ff bf16, row stride ld_h (the FFN's hidden activation).
+ *  W_down  d_ff x n bf16, row-major, contiguous.
+ *  x_attn  T x n act, row stride ld_x; only columns [0, r) are read.
+ *  W_e     n x r float32 (hi + lo bf16 on the matrix cores, as in
+ *          resbm_encode_fwd).
+ *  z       out, T x n bf16, row stride ld_z.   b, a_save as resbm_encode_fwd.
+ * Activations are bf16 in both libraries.  Shape rules: d_ff, n, r multiples
+ * of 8, 8 <= r <= n <= 65536, d_ff <= 262144.  ws: at least
+ * resbm_ffn_encode_workspace_bytes(T, n, r) bytes (float32 partial sums of a,
+ * one T x r slab per 256 columns of z, added in a fixed order).
+ */
+size_t resbm_ffn_encode_workspace_bytes(int64_t T, int32_t n, int32_t r);
+int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int32_t act,
+                             const void* h, int64_t ld_h, const void* W_down,
+                             const void* x_attn, int64_t ld_x, const float* W_e,
+                             void* z, int64_t ld_z, void* b, float* a_save,
+                             void* ws, size_t ws_bytes, void* stream);
+
 /* RESBM_IO_BF16 for libresbm.so, RESBM_IO_F32 for the validation build. */
 int32_t resbm_io_dtype(void);
 

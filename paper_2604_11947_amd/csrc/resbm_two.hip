@@ -62,6 +62,7 @@ enum Epi : int {
   kEpiAdd = 3,    // C = rne(acc + X) on columns < x_cols, rne(acc) elsewhere
   kEpiPart = 4,   // partial[split] = acc (float32, M x N contiguous per split)
   kEpiBf16Phi = 5,  // C = rne(acc) and D = rne(phi(C)) (a pre-activation and its activation)
+  kEpiEncode = 6,   // C = rne(acc) (the FFN output z) and D[tile column][row] = C_tile W_e[tile rows]
 };
 
 struct GemmArgs {
@@ -208,6 +209,88 @@ __device__ __forceinline__ int xcd_tile(int id, int nb) {
   return x * (nb >> 3) + min(x, nb & 7) + li;
 }
 
+// Encoder contraction in the epilogue of the FFN output projection (z = h W_down,
+// Sec. 3.2 places the encoder right after the feed-forward layer): the block's
+// rounded 256 x 256 tile of z goes to LDS (its four stage buffers, 64 rows
+// each), and wave w multiplies rows 32 w .. 32 w + 31 of it by the tile's 256
+// rows of W_e (float32, hi + lo bf16 parts), writing the float32 partial sum
+// D[tile column][row][0 .. r).  The partials are added in tile order by
+// k_enc_finish.
+template <int BM, int BN, int WM, int WN, int FM, int FN>
+__device__ __forceinline__ void encode_epilogue(const GemmArgs& g, const f32x4 (&acc)[FM][FN], __bf16* q0,
+                                                __bf16* q1, __bf16* q2, __bf16* q3, int m0, int n0) {
+  static_assert(BM == 256 && BN == 256 && WM * WN == 8, "the encoder epilogue runs on 256 x 256 tiles of 8 waves");
+  const int lane = threadIdx.x & 63, row16 = lane & 15, grp = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave % WM, wn = wave / WM;
+  auto quarter = [&](int q) { return q == 0 ? q0 : (q == 1 ? q1 : (q == 2 ? q2 : q3)); };
+  __syncthreads();  // every wave has finished reading the last stage
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int ml = (wm * FM + i) * 16 + row16;
+    __bf16* q = quarter(ml >> 6);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int nl = (wn * FN + j) * 16 + 4 * grp;
+      bf16x4 h;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) h[e] = (__bf16)acc[i][j][e];
+      *reinterpret_cast<uint2*>(q + (ml & 63) * 256 + resbm::wide_col(ml & 63, nl)) = __builtin_bit_cast(uint2, h);
+    }
+  }
+  __syncthreads();
+  const float* We = static_cast<const float*>(g.X);
+  const int r = g.x_cols, nt = n0 / BN;
+  const __bf16* zq = quarter(wave >> 1);
+  const rsrc_t rd = make_rsrc(g.D, g.d_bytes);
+  for (int jg = 0; jg < r; jg += 64) {
+    f32x4 a2[2][4];
+#pragma unroll
+    for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) a2[ib][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+    for (int ks = 0; ks < 8; ++ks) {
+      bf16x8 zf[2];
+#pragma unroll
+      for (int ib = 0; ib < 2; ++ib) {
+        const int row = 32 * (wave & 1) + 16 * ib + row16, col = 32 * ks + 8 * grp;
+        zf[ib] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(zq + row * 256 + resbm::wide_col(row, col)));
+      }
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const int jj = jg + 16 * jb + row16, k = n0 + 32 * ks + 8 * grp;
+        bf16x8 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float w = (jj < r && k + e < g.N) ? We[(int64_t)(k + e) * r + jj] : 0.0f;
+          __bf16 wh, wl;
+          resbm::split_hi_lo(w, wh, wl);
+          hi[e] = wh;
+          lo[e] = wl;
+        }
+#pragma unroll
+        for (int ib = 0; ib < 2; ++ib) {
+          a2[ib][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, zf[ib], a2[ib][jb], 0, 0, 0);
+          a2[ib][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, zf[ib], a2[ib][jb], 0, 0, 0);
+        }
+      }
+    }
+    // lane (row16, grp) of (ib, jb) holds D[row][jg + 16 jb + 4 grp .. + 3] of tile row 32 w + 16 ib + row16
+#pragma unroll
+    for (int ib = 0; ib < 2; ++ib) {
+      const int t = m0 + 32 * wave + 16 * ib + row16;
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const int jj = jg + 16 * jb + 4 * grp;
+        const bool ok = t < g.M && jj < r;
+        const int64_t off = (((int64_t)nt * g.M + t) * r + jj) * 4;
+        bst16(rd, ok ? (uint32_t)off : kOOB, __builtin_bit_cast(uint4, a2[ib][jb]));
+      }
+    }
+  }
+}
+
 template <bool AK, bool BKC, int BM, int BN, int WM, int WN, int EPI, bool PHI_A>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
   constexpr int NTH = 64 * WM * WN;
@@ -336,6 +419,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
       }
     }
   }
+  if constexpr (EPI == kEpiEncode) encode_epilogue<BM, BN, WM, WN, FM, FN>(g, acc, s_a0, s_a1, s_b0, s_b1, m0, n0);
 }
 
 // out[i] = sum over s in order of part[s][i], i < count (count % 4 == 0).
@@ -357,6 +441,30 @@ __global__ __launch_bounds__(256) void k_silu(const __bf16* __restrict__ v, int6
   const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (q * 8 >= count) return;
   reinterpret_cast<uint4*>(p)[q] = silu8(reinterpret_cast<const uint4*>(v)[q]);
+}
+
+// a = sum over the NT column tiles, in order, of the encoder partials;
+// b = rne(x_attn[:, :r] + phi(a)); a_save = a.  4 columns per thread.
+__global__ __launch_bounds__(256) void k_enc_finish(int64_t T, int r, int NT, int act, const float* __restrict__ part,
+                                                    const __bf16* __restrict__ x, int64_t ld_x, __bf16* __restrict__ b,
+                                                    float* __restrict__ a_save) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int per = r / 4;
+  if (q >= T * per) return;
+  const int64_t t = q / per;
+  const int c = (int)(q % per) * 4;
+  float4 a = *reinterpret_cast<const float4*>(part + t * r + c);
+  for (int k = 1; k < NT; ++k) {
+    const float4 p = *reinterpret_cast<const float4*>(part + ((int64_t)k * T + t) * r + c);
+    a.x += p.x; a.y += p.y; a.z += p.z; a.w += p.w;
+  }
+  if (a_save) *reinterpret_cast<float4*>(a_save + t * r + c) = a;
+  const bf16x4 xv = __builtin_bit_cast(bf16x4, *reinterpret_cast<const uint2*>(x + t * ld_x + c));
+  const float av[4] = {a.x, a.y, a.z, a.w};
+  bf16x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = (__bf16)((float)xv[e] + resbm::act_phi(av[e], act));
+  *reinterpret_cast<uint2*>(b + t * r + c) = __builtin_bit_cast(uint2, o);
 }
 
 // g_x[t][0 .. r) <- rne(g_x + g_b), 4 columns per thread (r % 8 == 0).
@@ -720,6 +828,53 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
                          (const __bf16*)g_b, (__bf16*)g_x, ld_gx);
     }
   }
+  return status2();
+}
+
+size_t resbm_ffn_encode_workspace_bytes(int64_t T, int32_t n, int32_t r) {
+  if (T <= 0 || n < 8 || n > 65536 || n % 8 || r < 8 || r > n || r % 8) return 0;
+  return round_up((size_t)((n + 255) / 256) * (size_t)T * r * 4, kWsAlign2);
+}
+
+int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int32_t act, const void* h, int64_t ld_h,
+                             const void* W_down, const void* x_attn, int64_t ld_x, const float* W_e, void* z,
+                             int64_t ld_z, void* b, float* a_save, void* ws, size_t ws_bytes, void* stream) {
+  if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
+  if (T < 0 || T > (1ll << 31) || d_ff < 8 || d_ff > 262144 || d_ff % 8 || n < 8 || n > 65536 || n % 8 || r < 8 ||
+      r > n || r % 8)
+    return RESBM_E_SHAPE;
+  if (T == 0) return RESBM_OK;
+  const size_t need = resbm_ffn_encode_workspace_bytes(T, n, r);
+  int32_t e = check_ws(need, ws, ws_bytes);
+  if (e) return e;
+  if (!h || !W_down || !x_attn || !W_e || !z || !b) return RESBM_E_NULL;
+  if (!ld_ok2(ld_h, d_ff) || !ld_ok2(ld_x, n) || !ld_ok2(ld_z, n)) return RESBM_E_SHAPE;
+  if (!aligned2(h, 16) || !aligned2(W_down, 16) || !aligned2(x_attn, 16) || !aligned2(W_e, 16) || !aligned2(z, 16) ||
+      !aligned2(b, 16) || (a_save && !aligned2(a_save, 16)))
+    return RESBM_E_ALIGN;
+  const size_t bh = extent2(T, d_ff, ld_h, 2), bwd = (size_t)d_ff * n * 2, bx = extent2(T, n, ld_x, 2),
+               bwe = (size_t)n * r * 4, bz = extent2(T, n, ld_z, 2), bb = (size_t)T * r * 2,
+               ba = a_save ? (size_t)T * r * 4 : 0;
+  if (!fits(bh) || !fits(bwd) || !fits(bz) || !fits(need)) return RESBM_E_SHAPE;
+  const void* ins[] = {h, W_down, x_attn, W_e};
+  const size_t inb[] = {bh, bwd, bx, bwe};
+  void* outs[] = {z, b, a_save, ws};
+  const size_t outb[] = {bz, bb, ba, need};
+  for (int o = 0; o < 4; ++o) {
+    for (int i = 0; i < 4; ++i)
+      if (overlap2(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
+    for (int o2 = o + 1; o2 < 4; ++o2)
+      if (overlap2(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  // z = h W_down with the encoder partials in the epilogue
+  GemmArgs g = args((int)T, n, d_ff, h, ld_h, bh, W_down, n, bwd, z, ld_z, bz);
+  g.X = W_e; g.x_cols = r; g.x_bytes = (int64_t)bwe;
+  g.D = ws; g.d_bytes = (int64_t)need;
+  launch<true, false, 256, 256, 2, 4, kEpiEncode, false>(g, 1, st);
+  const int64_t cnt = T * (r / 4);
+  hipLaunchKernelGGL(k_enc_finish, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, T, r, (n + 255) / 256, act,
+                     (const float*)ws, (const __bf16*)x_attn, ld_x, (__bf16*)b, a_save);
   return status2();
 }
 

@@ -52,6 +52,9 @@ SIGNATURES = [
     ("resbm2_encode_bwd", _i32, [_i64, _i32, _i32, _i32, _i32, _p, _i64, _p, _p, _p, _p, _p, _i64, _p, _i64,
                                  _p, _p, _p, _sz, _p]),
     ("resbm2_workspace_bytes", _sz, [_i64, _i32, _i32, _i32]),
+    ("resbm_ffn_encode_fwd", _i32, [_i64, _i32, _i32, _i32, _i32, _p, _i64, _p, _p, _i64, _p, _p, _i64, _p, _p, _p,
+                                    _sz, _p]),
+    ("resbm_ffn_encode_workspace_bytes", _sz, [_i64, _i32, _i32]),
     ("resbm_io_dtype", _i32, []),
     ("resbm_strerror", ctypes.c_char_p, [_i32]),
 ]
@@ -314,6 +317,29 @@ class Library:
                                          _ptr(g_z), ld_gz, _ptr(g_x), ld_gx, _ptr(dW1), _ptr(dW2), _ptr(ws),
                                          ws.numel(), _stream(stream, z))
         self._check("resbm2_encode_bwd", st)
+
+    # ------------------------------------------------------------ encoder fused into the FFN output projection
+    def ffn_encode_fwd(self, h, W_down, x_attn, W_e, z, b, a_save=None, act=ACT_SILU, ws=None, stream=None):
+        T, d_ff = h.shape
+        n, r = W_e.shape
+        for t, nm in ((h, "h"), (W_down, "W_down"), (x_attn, "x_attn"), (z, "z"), (b, "b")):
+            _dtype(t, torch.bfloat16, nm)
+        _dtype(W_e, torch.float32, "W_e")
+        _dtype(a_save, torch.float32, "a_save")
+        _packed(W_down, d_ff, n, "W_down")
+        _packed(W_e, n, r, "W_e")
+        _packed(b, T, r, "b")
+        if a_save is not None:
+            _packed(a_save, T, r, "a_save")
+        ld_h, ld_x, ld_z = _ld(h, T, d_ff, "h"), _ld(x_attn, T, n, "x_attn"), _ld(z, T, n, "z")
+        if ws is None:
+            nbytes = int(self.cdll.resbm_ffn_encode_workspace_bytes(T, n, r))
+            buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=h.device)
+            ws = buf[(-buf.data_ptr()) % 256:][:nbytes]
+        st = self.cdll.resbm_ffn_encode_fwd(T, d_ff, n, r, act, _ptr(h), ld_h, _ptr(W_down), _ptr(x_attn), ld_x,
+                                            _ptr(W_e), _ptr(z), ld_z, _ptr(b), _ptr(a_save), _ptr(ws), ws.numel(),
+                                            _stream(stream, h))
+        self._check("resbm_ffn_encode_fwd", st)
 
     # ------------------------------------------------------------ optimizer-side ops
     def newton_schulz(self, G, O, steps=5, coeffs=NS_QUINTIC, ws=None, stream=None):

@@ -37,7 +37,8 @@ def test_header_declares_the_ops_and_helpers():
     for op in ("resbm_encode_fwd", "resbm_decode_fwd", "resbm_decode_bwd", "resbm_encode_bwd",
                "resbm_newton_schulz", "resbm_muon_update", "resbm_spectrum", "resbm_matrix_workspace_bytes",
                "resbm_workspace_bytes", "resbm_io_dtype", "resbm_strerror", "resbm2_encode_fwd", "resbm2_decode_fwd",
-               "resbm2_decode_bwd", "resbm2_encode_bwd", "resbm2_workspace_bytes"):
+               "resbm2_decode_bwd", "resbm2_encode_bwd", "resbm2_workspace_bytes", "resbm_ffn_encode_fwd",
+               "resbm_ffn_encode_workspace_bytes"):
         assert op in names
     assert sorted(n for n, _, _ in R.SIGNATURES) == names
 

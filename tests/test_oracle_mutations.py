@@ -184,3 +184,34 @@ def test_two_linear_pin_rejects_planted_mistake(monkeypatch, name, bad, pin):
     monkeypatch.setattr(TL, name, bad)
     with pytest.raises(AssertionError):
         pin()
+
+
+# ---------------------------------------------------------------- fused FFN projection + encoder
+import test_fusion_oracle_pins as FP  # noqa: E402
+from oracle import fusion_oracle as FO  # noqa: E402
+
+
+def _fused_skip_dropped(x_attn, z, W_e, act):
+    a = z @ W_e
+    return R.phi(a, act), a
+
+
+def _fused_weight_rows_reversed(h, W_down, x_attn, W_e, act):
+    z = h @ W_down
+    b, a = R.encode_fwd(x_attn, R.rne_bf16(z), W_e[::-1], act)
+    return z, b, a
+
+
+@pytest.mark.parametrize("bad,pin", [
+    (_fused_weight_rows_reversed, lambda: FP.test_integer_inputs_follow_associativity(R.ACT_SILU)),
+])
+def test_fusion_pin_rejects_planted_mistake(monkeypatch, bad, pin):
+    monkeypatch.setattr(FO, "ffn_encode_fwd", bad)
+    with pytest.raises(AssertionError):
+        pin()
+
+
+def test_fusion_pin_rejects_dropped_skip(monkeypatch):
+    monkeypatch.setattr(FO, "encode_fwd", _fused_skip_dropped)
+    with pytest.raises(AssertionError):
+        FP.test_integer_inputs_follow_associativity(R.ACT_IDENTITY)
