@@ -61,6 +61,8 @@ def parse():
                    help="skip timing the optimizer-side ops (Muon update, spectrum) on the bottleneck weights")
     p.add_argument("--two-m", type=int, default=1024,
                    help="intermediate width m of the two-linears-per-side variant (0: skip timing it)")
+    p.add_argument("--ffn-width", type=int, default=14336,
+                   help="FFN hidden width for timing the encoder fused into the FFN output projection (0: skip)")
     p.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="write profiles/ summaries from rocprofv3 output of this script (no GPU work)")
     p.add_argument("--commands", nargs=3, default=None, help="the three rocprofv3 commands, recorded in the summaries")
@@ -395,6 +397,50 @@ def two_linear_timing(lib, d: dict, r: int, m: int, dev, iters: int, cpu: bool, 
     return out
 
 
+def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int) -> dict:
+    """The encoder fused into the FFN output projection (resbm_ffn_encode_fwd: z = h W_down
+    with the encoder in the epilogue) against the unfused pair: the same projection by
+    the framework's library GEMM (torch.matmul, hipBLASLt) followed by resbm_encode_fwd.
+    HIP events on the launch stream around each call."""
+    import torch
+
+    from paper_2604_11947_amd import inputs as I
+
+    T, n = d["z"].shape
+    bf = torch.bfloat16
+    h = I.make_bf16(T, d_ff, 41).to(dev)
+    W_down = I.make_bf16(d_ff, n, 42, std=d_ff ** -0.5).to(dev)
+    x, W_e = d["x_attn"].to(dev), d["W_e"].to(dev)
+    z, b = torch.empty(T, n, dtype=bf, device=dev), torch.empty(T, r, dtype=bf, device=dev)
+    a = torch.empty(T, r, device=dev)
+    ws = lib.workspace(T, n, r, dev)
+    calls = {
+        "fused": lambda: lib.ffn_encode_fwd(h, W_down, x, W_e, z, b, a_save=a, act=act),
+        "library_gemm": lambda: torch.matmul(h, W_down, out=z),
+        "encode_fwd": lambda: lib.encode_fwd(x, z, W_e, b, a_save=a, act=act, ws=ws),
+    }
+    stream = torch.cuda.current_stream()
+    us = {}
+    for nm, f in calls.items():
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us[nm] = e0.elapsed_time(e1) * 1e3 / iters
+    flops = 2.0 * T * d_ff * n + 2.0 * T * n * r
+    tf = flops / (us["fused"] * 1e-6) / 1e12
+    return {"d_ff": d_ff, "tokens": T, "us": us, "unfused_us": us["library_gemm"] + us["encode_fwd"],
+            "fused_over_unfused": us["fused"] / (us["library_gemm"] + us["encode_fwd"]), "iterations": iters,
+            "roofline": {"bound": "mfma", "kernel": "k_gemm<256x256, encoder epilogue>", "achieved": tf,
+                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": tf / MFMA_BF16_PEAK_TFLOPS,
+                         "flops": flops}}
+
+
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 COPY_PROBE_MIB = 256
 
@@ -563,6 +609,8 @@ def main():
         out["optimizer"] = optimizer_timing(lib, d, r, dev, 200, cpu=not args.no_cpu_baseline)
     if args.two_m > 0:
         out["two_linear"] = two_linear_timing(lib, d, r, args.two_m, dev, 50, not args.no_cpu_baseline, act)
+    if args.ffn_width > 0:
+        out["ffn_encode"] = ffn_encode_timing(lib, d, r, args.ffn_width, dev, 20, act)
     if not args.no_cpu_baseline:
         tokens = args.cpu_tokens or T
         out["cpu_baseline"] = cpu_baseline(d, r, act, min(tokens, T))
