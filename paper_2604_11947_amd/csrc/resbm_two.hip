@@ -90,6 +90,19 @@ __device__ __forceinline__ uint4 silu8(uint4 v) {
   return __builtin_bit_cast(uint4, h);
 }
 
+// Column permutation of a [KT][I] tile (I a multiple of 128) that is read with
+// ds_read_b64_tr_b16: the low four bits of the 8-element chunk index are XORed
+// with 2 (row % 4 + 4 ((row / 8) % 2)).  One transposed read of 32 lanes touches
+// two adjacent chunks in each of 8 rows (r0 .. r0 + 3 and r0 + 8 .. r0 + 11);
+// the XOR values are 8 distinct even numbers, so the 16 chunks land on 16
+// distinct 16-byte bank slots.  Chunks stay in their row and 256-byte window,
+// so whole-row copies stay conflict-free too.  (An XOR with the row's low four
+// bits leaves two rows of each such read on the same banks.)
+__device__ __forceinline__ int tr_col(int row, int col) {
+  const int f = ((row & 3) | ((row >> 1) & 4)) << 1;
+  return ((((col >> 3) ^ f) & 15) | ((col >> 3) & ~15)) << 3 | (col & 7);
+}
+
 // Position of element (row, col) in a staged tile.  K-contiguous operands are
 // staged [I][64] (row = index along M or N, col = k); the others [64][I]
 // (row = k, col = index), I = 32, 64 or a multiple of 128.
@@ -98,7 +111,7 @@ __device__ __forceinline__ int tile_pos(int row, int col) {
   if constexpr (KC) {
     return row * KT + resbm::tile_col<KT>(row, col);
   } else if constexpr (I % 128 == 0) {
-    return row * I + resbm::wide_col(row, col);
+    return row * I + tr_col(row, col);
   } else {
     return row * I + resbm::tile_col<I>(row, col);
   }
@@ -190,8 +203,9 @@ __device__ __forceinline__ void dma_tile(rsrc_t src, int64_t ld, int i0, int NI,
       k = k0 + 8 * ((pc ^ (row >> 1)) & 7);
     } else {
       const int row = o / (I * 2), pc = (o >> 4) % (I / 8);
+      const int f = ((row & 3) | ((row >> 1) & 4)) << 1;  // tr_col's XOR
       k = k0 + row;
-      idx = i0 + 8 * (((pc ^ row) & 15) | (pc & ~15));
+      idx = i0 + 8 * (((pc ^ f) & 15) | (pc & ~15));
     }
     const bool ok = idx < NI && k < kend;
     const int64_t off = KC ? ((int64_t)idx * ld + k) * 2 : ((int64_t)k * ld + idx) * 2;
