@@ -236,3 +236,52 @@ def test_full_backward_sampled(full):
     g_u = (gb_in @ W2[cols_m].T) * R.dphi(u[:, cols_m], act)
     check("dW1[:, s]", dW1[:, cols_m].cpu(), z.T @ g_u, False)
     check("dW2", dW2, R.phi(u, act).T @ gb_in, False)
+
+
+def test_two_graph_replay_matches_eager():
+    """The four two-linear ops and the fused FFN-projection encoder captured in one
+    HIP graph replay bit for bit like eager calls, with the workspaces and outputs
+    scribbled over and unrelated eager work between the replays."""
+    L = lib()
+    T, n, m, r, d_ff = 700, 512, 264, 40, 328
+    say(f"graph replay T={T} n={n} m={m} r={r} d_ff={d_ff}")
+    d = {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in data(T, n, m, r, seed=7).items()}
+    h = I.make_bf16(T, d_ff, 51).cuda()
+    W_down = I.make_bf16(d_ff, n, 52, std=d_ff ** -0.5).cuda()
+    W_e = I.make_weights(n, r, 7)["W_e"].cuda()
+    bf = torch.bfloat16
+    outs = {"b": torch.empty(T, r, dtype=bf, device="cuda"), "u": torch.empty(T, m, dtype=bf, device="cuda"),
+            "zt": torch.empty(T, n, dtype=bf, device="cuda"), "v": torch.empty(T, m, dtype=bf, device="cuda"),
+            "g_b": torch.empty(T, r, dtype=bf, device="cuda"), "g_z": torch.empty(T, n, dtype=bf, device="cuda"),
+            "dW1": torch.empty(n, m, device="cuda"), "dW2": torch.empty(m, r, device="cuda"),
+            "dW3": torch.empty(r, m, device="cuda"), "dW4": torch.empty(m, n, device="cuda"),
+            "z": torch.empty(T, n, dtype=bf, device="cuda"), "b2": torch.empty(T, r, dtype=bf, device="cuda"),
+            "a": torch.empty(T, r, device="cuda")}
+    ws = L.two_workspace(T, n, m, r, "cuda")
+    nb = int(L.cdll.resbm_ffn_encode_workspace_bytes(T, n, r))
+    ws2 = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    o = outs
+
+    def step():
+        L.encode2_fwd(d["x_attn"], d["z"], d["W1"], d["W2"], o["b"], o["u"])
+        L.decode2_fwd(o["b"], d["W3"], d["W4"], o["zt"], o["v"], ws=ws)
+        L.decode2_bwd(o["b"], o["v"], d["g_zt"], d["g_id"], d["W3"], d["W4"], o["g_b"], o["dW3"], o["dW4"], ws=ws)
+        L.encode2_bwd(d["z"], o["u"], o["g_b"], d["W1"], d["W2"], o["g_z"], o["dW1"], o["dW2"], g_x=o["g_z"], ws=ws)
+        L.ffn_encode_fwd(h, W_down, d["x_attn"], W_e, o["z"], o["b2"], a_save=o["a"], ws=ws2)
+
+    step()
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in o.items()}
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        for v in o.values():
+            v.view(torch.uint8).fill_(0x5A)
+        ws.fill_(0xA5)
+        ws2.fill_(0x3C)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in o.items():
+            assert torch.equal(v.view(torch.uint8), ref[k].view(torch.uint8)), f"replay {rep}: {k} differs"
