@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "resbm_kernels.hip")
 SRC_MATRIX = os.path.join(PKG, "csrc", "resbm_matrix.hip")
 SRC_TWO = os.path.join(PKG, "csrc", "resbm_two.hip")
-DEPS = [SRC, SRC_MATRIX, SRC_TWO, os.path.join(PKG, "csrc", "resbm_buffer.hpp"), os.path.join(PKG, "csrc", "resbm_mfma.hpp"), os.path.join(PKG, "csrc", "resbm_plan.hpp"),
+DEPS = [SRC, SRC_MATRIX, SRC_TWO, os.path.join(PKG, "csrc", "resbm_buffer.hpp"), os.path.join(PKG, "csrc", "resbm_host.hpp"), os.path.join(PKG, "csrc", "resbm_mfma.hpp"), os.path.join(PKG, "csrc", "resbm_plan.hpp"),
         os.path.join(ROOT, "include", "resbm.h")]
 
 LIBS = {"bf16": "libresbm.so", "f32": "libresbm_f32.so"}

@@ -33,6 +33,7 @@
 
 #include "resbm.h"
 #include "resbm_buffer.hpp"
+#include "resbm_host.hpp"
 #include "resbm_mfma.hpp"
 #include "resbm_plan.hpp"
 
@@ -1384,22 +1385,11 @@ namespace {
 
 constexpr size_t kIoBytes = sizeof(io_t);
 
-bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
-
-// Byte extent of a T x n matrix with row stride ld.
-size_t extent(int64_t T, int64_t n, int64_t ld, size_t es) {
-  return T > 0 ? (size_t)(((T - 1) * ld + n) * (int64_t)es) : 0;
-}
-
-bool overlap(const void* a, size_t na, const void* b, size_t nb) {
-  if (!a || !b || na == 0 || nb == 0) return false;
-  uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
-  return pa < pb + nb && pb < pa + na;
-}
-
-int32_t launch_status() {
-  return hipGetLastError() == hipSuccess ? RESBM_OK : RESBM_E_HIP;
-}
+using resbm_host::aligned;
+using resbm_host::extent;
+using resbm_host::launch_status;
+using resbm_host::ld_ok;
+using resbm_host::overlap;
 
 int32_t check_common(int64_t T, int n, int r, int64_t ws_need, const void* ws, size_t ws_bytes) {
   if (T < 0 || !shape_ok(n, r)) return RESBM_E_SHAPE;
@@ -1411,8 +1401,6 @@ int32_t check_common(int64_t T, int n, int r, int64_t ws_need, const void* ws, s
   }
   return RESBM_OK;
 }
-
-bool ld_ok(int64_t ld, int n) { return ld >= n && ld % 8 == 0; }
 
 template <int NT>
 void launch_enc_fwd(const Plan& p, int act, const io_t* x, int64_t ld_x, const io_t* z, int64_t ld_z,

@@ -32,6 +32,7 @@
 #include <stdint.h>
 
 #include "resbm.h"
+#include "resbm_host.hpp"
 
 namespace resbm_mx {
 
@@ -581,15 +582,9 @@ Plan make_plan(int p, int q) {
   return P;
 }
 
-bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
-
-bool overlap(const void* a, size_t na, const void* b, size_t nb) {
-  if (!a || !b || na == 0 || nb == 0) return false;
-  const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
-  return pa < pb + nb && pb < pa + na;
-}
-
-int32_t launch_status() { return hipGetLastError() == hipSuccess ? RESBM_OK : RESBM_E_HIP; }
+using resbm_host::aligned;
+using resbm_host::launch_status;
+using resbm_host::overlap;
 
 int32_t check_ws(const Plan& P, const void* ws, size_t ws_bytes) {
   if (!ws) return RESBM_E_NULL;

@@ -37,6 +37,7 @@
 
 #include "resbm.h"
 #include "resbm_buffer.hpp"
+#include "resbm_host.hpp"
 #include "resbm_mfma.hpp"
 
 namespace resbm2 {
@@ -507,21 +508,15 @@ namespace {
 constexpr size_t kWsAlign2 = 256;
 constexpr int kTargetBlocks = 256;   // split-K aims at one block per compute unit
 
-bool aligned2(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
-size_t extent2(int64_t rows, int64_t cols, int64_t ld, size_t es) {
-  return rows > 0 ? (size_t)(((rows - 1) * ld + cols) * (int64_t)es) : 0;
-}
-bool overlap2(const void* a, size_t na, const void* b, size_t nb) {
-  if (!a || !b || na == 0 || nb == 0) return false;
-  const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
-  return pa < pb + nb && pb < pa + na;
-}
+using resbm_host::aligned;
+using resbm_host::extent;
+using resbm_host::ld_ok;
+using resbm_host::overlap;
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 bool shape_ok2(int64_t T, int n, int m, int r) {
   return T >= 0 && T <= (1ll << 31) && n >= 8 && n <= 65536 && n % 8 == 0 && m >= 8 && m <= 65536 && m % 8 == 0 &&
          r >= 8 && r <= n && r % 8 == 0;
 }
-bool ld_ok2(int64_t ld, int n) { return ld >= n && ld % 8 == 0; }
 bool fits(size_t bytes) { return bytes <= (size_t)kMaxRange; }
 
 // Block tile shapes: 256 x 256 (8 waves of 128 x 64) for the n x m products,
@@ -620,12 +615,11 @@ void weight_grad(Shape s, GemmArgs g, const Split& sp, float* W, void* part, hip
                      sp.S, count, W);
 }
 
-int32_t status2() { return hipGetLastError() == hipSuccess ? RESBM_OK : RESBM_E_HIP; }
 
 int32_t check_ws(size_t need, const void* ws, size_t ws_bytes) {
   if (need == 0) return RESBM_OK;
   if (!ws) return RESBM_E_NULL;
-  if (!aligned2(ws, kWsAlign2)) return RESBM_E_ALIGN;
+  if (!aligned(ws, kWsAlign2)) return RESBM_E_ALIGN;
   return ws_bytes < need ? RESBM_E_WORKSPACE : RESBM_OK;
 }
 
@@ -647,16 +641,16 @@ int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   if (!shape_ok2(T, n, m, r)) return RESBM_E_SHAPE;
   if (T == 0) return RESBM_OK;
   if (!x_attn || !z || !W1 || !W2 || !b || !u) return RESBM_E_NULL;
-  if (!ld_ok2(ld_x, n) || !ld_ok2(ld_z, n)) return RESBM_E_SHAPE;
-  if (!aligned2(x_attn, 16) || !aligned2(z, 16) || !aligned2(W1, 16) || !aligned2(W2, 16) || !aligned2(b, 16) ||
-      !aligned2(u, 16))
+  if (!ld_ok(ld_x, n) || !ld_ok(ld_z, n)) return RESBM_E_SHAPE;
+  if (!aligned(x_attn, 16) || !aligned(z, 16) || !aligned(W1, 16) || !aligned(W2, 16) || !aligned(b, 16) ||
+      !aligned(u, 16))
     return RESBM_E_ALIGN;
-  const size_t bx = extent2(T, n, ld_x, 2), bz = extent2(T, n, ld_z, 2), bw1 = (size_t)n * m * 2,
+  const size_t bx = extent(T, n, ld_x, 2), bz = extent(T, n, ld_z, 2), bw1 = (size_t)n * m * 2,
                bw2 = (size_t)m * r * 2, bb = (size_t)T * r * 2, bu = (size_t)T * m * 2;
   if (!fits(bx) || !fits(bz) || !fits(bu) || !fits(bw1)) return RESBM_E_SHAPE;
-  if (overlap2(b, bb, x_attn, bx) || overlap2(b, bb, z, bz) || overlap2(b, bb, W1, bw1) || overlap2(b, bb, W2, bw2) ||
-      overlap2(u, bu, x_attn, bx) || overlap2(u, bu, z, bz) || overlap2(u, bu, W1, bw1) || overlap2(u, bu, W2, bw2) ||
-      overlap2(u, bu, b, bb))
+  if (overlap(b, bb, x_attn, bx) || overlap(b, bb, z, bz) || overlap(b, bb, W1, bw1) || overlap(b, bb, W2, bw2) ||
+      overlap(u, bu, x_attn, bx) || overlap(u, bu, z, bz) || overlap(u, bu, W1, bw1) || overlap(u, bu, W2, bw2) ||
+      overlap(u, bu, b, bb))
     return RESBM_E_ALIAS;
   hipStream_t st = (hipStream_t)stream;
   const int Ti = (int)T;
@@ -668,7 +662,7 @@ int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   g.X = x_attn; g.ldx = ld_x; g.x_bytes = (int64_t)bx; g.x_cols = r;
   if (act == RESBM_ACT_SILU) gemm<true, false, kEpiAdd, true>(narrow_for(r), g, 1, st);
   else gemm<true, false, kEpiAdd, false>(narrow_for(r), g, 1, st);
-  return status2();
+  return resbm_host::launch_status();
 }
 
 int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* b, const void* W3,
@@ -683,16 +677,16 @@ int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   int32_t e = check_ws(need, ws, ws_bytes);
   if (e) return e;
   if (!b || !W3 || !W4 || !z_tilde || !v) return RESBM_E_NULL;
-  if (!ld_ok2(ld_zt, n)) return RESBM_E_SHAPE;
-  if (!aligned2(b, 16) || !aligned2(W3, 16) || !aligned2(W4, 16) || !aligned2(z_tilde, 16) || !aligned2(v, 16))
+  if (!ld_ok(ld_zt, n)) return RESBM_E_SHAPE;
+  if (!aligned(b, 16) || !aligned(W3, 16) || !aligned(W4, 16) || !aligned(z_tilde, 16) || !aligned(v, 16))
     return RESBM_E_ALIGN;
   const size_t bb = (size_t)T * r * 2, bw3 = (size_t)r * m * 2, bw4 = (size_t)m * n * 2,
-               bzt = extent2(T, n, ld_zt, 2), bv = (size_t)T * m * 2;
+               bzt = extent(T, n, ld_zt, 2), bv = (size_t)T * m * 2;
   if (!fits(bzt) || !fits(bv) || !fits(bw4)) return RESBM_E_SHAPE;
-  if (overlap2(z_tilde, bzt, b, bb) || overlap2(z_tilde, bzt, W3, bw3) || overlap2(z_tilde, bzt, W4, bw4) ||
-      overlap2(v, bv, b, bb) || overlap2(v, bv, W3, bw3) || overlap2(v, bv, W4, bw4) || overlap2(v, bv, z_tilde, bzt) ||
-      overlap2(ws, need, b, bb) || overlap2(ws, need, W3, bw3) || overlap2(ws, need, W4, bw4) ||
-      overlap2(ws, need, z_tilde, bzt) || overlap2(ws, need, v, bv))
+  if (overlap(z_tilde, bzt, b, bb) || overlap(z_tilde, bzt, W3, bw3) || overlap(z_tilde, bzt, W4, bw4) ||
+      overlap(v, bv, b, bb) || overlap(v, bv, W3, bw3) || overlap(v, bv, W4, bw4) || overlap(v, bv, z_tilde, bzt) ||
+      overlap(ws, need, b, bb) || overlap(ws, need, W3, bw3) || overlap(ws, need, W4, bw4) ||
+      overlap(ws, need, z_tilde, bzt) || overlap(ws, need, v, bv))
     return RESBM_E_ALIAS;
   hipStream_t st = (hipStream_t)stream;
   const int Ti = (int)T;
@@ -707,7 +701,7 @@ int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   // z~ = phi(v) W4
   g = args(Ti, n, m, silu ? ws : v, m, bv, W4, n, bw4, z_tilde, ld_zt, bzt);
   gemm<true, false, kEpiBf16, false>(wide_for(Ti, n), g, 1, st);
-  return status2();
+  return resbm_host::launch_status();
 }
 
 int32_t resbm2_decode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* b, const void* v,
@@ -721,12 +715,12 @@ int32_t resbm2_decode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   int32_t e = check_ws(p.dec_bwd, ws, ws_bytes);
   if (e) return e;
   if (!b || !v || !g_zt || !W3 || !W4 || !g_b || !dW3 || !dW4) return RESBM_E_NULL;
-  if (!ld_ok2(ld_gzt, n) || (g_id && !ld_ok2(ld_gid, n))) return RESBM_E_SHAPE;
-  if (!aligned2(b, 16) || !aligned2(v, 16) || !aligned2(g_zt, 16) || (g_id && !aligned2(g_id, 16)) ||
-      !aligned2(W3, 16) || !aligned2(W4, 16) || !aligned2(g_b, 16) || !aligned2(dW3, 16) || !aligned2(dW4, 16))
+  if (!ld_ok(ld_gzt, n) || (g_id && !ld_ok(ld_gid, n))) return RESBM_E_SHAPE;
+  if (!aligned(b, 16) || !aligned(v, 16) || !aligned(g_zt, 16) || (g_id && !aligned(g_id, 16)) ||
+      !aligned(W3, 16) || !aligned(W4, 16) || !aligned(g_b, 16) || !aligned(dW3, 16) || !aligned(dW4, 16))
     return RESBM_E_ALIGN;
-  const size_t bb = (size_t)T * r * 2, bv = (size_t)T * m * 2, bg = extent2(T, n, ld_gzt, 2),
-               bid = g_id ? extent2(T, n, ld_gid, 2) : 0, bw3 = (size_t)r * m * 2, bw4 = (size_t)m * n * 2,
+  const size_t bb = (size_t)T * r * 2, bv = (size_t)T * m * 2, bg = extent(T, n, ld_gzt, 2),
+               bid = g_id ? extent(T, n, ld_gid, 2) : 0, bw3 = (size_t)r * m * 2, bw4 = (size_t)m * n * 2,
                bd3 = (size_t)r * m * 4, bd4 = (size_t)m * n * 4;
   if (!fits(bg) || !fits(bid) || !fits(bv) || !fits(bw4) || !fits(p.dec_bwd)) return RESBM_E_SHAPE;
   const void* ins[] = {b, v, g_zt, g_id, W3, W4};
@@ -735,9 +729,9 @@ int32_t resbm2_decode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   const size_t outb[] = {bb, bd3, bd4, p.dec_bwd};
   for (int o = 0; o < 4; ++o) {
     for (int i = 0; i < 6; ++i)
-      if (overlap2(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
+      if (overlap(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
     for (int o2 = o + 1; o2 < 4; ++o2)
-      if (overlap2(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
+      if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
   }
   hipStream_t st = (hipStream_t)stream;
   const int Ti = (int)T;
@@ -773,7 +767,7 @@ int32_t resbm2_decode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   } else {
     gemm<true, true, kEpiBf16, false>(narrow_for(r), g, 1, st);
   }
-  return status2();
+  return resbm_host::launch_status();
 }
 
 int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* z, int64_t ld_z,
@@ -787,15 +781,15 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   int32_t e = check_ws(p.enc_bwd, ws, ws_bytes);
   if (e) return e;
   if (!z || !u || !g_b || !W1 || !W2 || !g_z || !dW1 || !dW2) return RESBM_E_NULL;
-  if (!ld_ok2(ld_z, n) || !ld_ok2(ld_gz, n) || (g_x && !ld_ok2(ld_gx, n))) return RESBM_E_SHAPE;
-  if (!aligned2(z, 16) || !aligned2(u, 16) || !aligned2(g_b, 16) || !aligned2(W1, 16) || !aligned2(W2, 16) ||
-      !aligned2(g_z, 16) || (g_x && !aligned2(g_x, 16)) || !aligned2(dW1, 16) || !aligned2(dW2, 16))
+  if (!ld_ok(ld_z, n) || !ld_ok(ld_gz, n) || (g_x && !ld_ok(ld_gx, n))) return RESBM_E_SHAPE;
+  if (!aligned(z, 16) || !aligned(u, 16) || !aligned(g_b, 16) || !aligned(W1, 16) || !aligned(W2, 16) ||
+      !aligned(g_z, 16) || (g_x && !aligned(g_x, 16)) || !aligned(dW1, 16) || !aligned(dW2, 16))
     return RESBM_E_ALIGN;
   const bool fused = g_x == g_z;
   if (fused && ld_gx != ld_gz) return RESBM_E_ALIAS;
-  const size_t bz = extent2(T, n, ld_z, 2), bu = (size_t)T * m * 2, bgb = (size_t)T * r * 2,
-               bw1 = (size_t)n * m * 2, bw2 = (size_t)m * r * 2, bgz = extent2(T, n, ld_gz, 2),
-               bgx = (g_x && !fused) ? extent2(T, n, ld_gx, 2) : 0, bd1 = (size_t)n * m * 4,
+  const size_t bz = extent(T, n, ld_z, 2), bu = (size_t)T * m * 2, bgb = (size_t)T * r * 2,
+               bw1 = (size_t)n * m * 2, bw2 = (size_t)m * r * 2, bgz = extent(T, n, ld_gz, 2),
+               bgx = (g_x && !fused) ? extent(T, n, ld_gx, 2) : 0, bd1 = (size_t)n * m * 4,
                bd2 = (size_t)m * r * 4;
   if (!fits(bz) || !fits(bu) || !fits(bgz) || !fits(bgx) || !fits(bw1) || !fits(p.enc_bwd)) return RESBM_E_SHAPE;
   const void* ins[] = {z, u, g_b, W1, W2};
@@ -804,9 +798,9 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   const size_t outb[] = {bgz, bgx, bd1, bd2, p.enc_bwd};
   for (int o = 0; o < 5; ++o) {
     for (int i = 0; i < 5; ++i)
-      if (overlap2(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
+      if (overlap(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
     for (int o2 = o + 1; o2 < 5; ++o2)
-      if (overlap2(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
+      if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
   }
   hipStream_t st = (hipStream_t)stream;
   const int Ti = (int)T;
@@ -842,7 +836,7 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
                          (const __bf16*)g_b, (__bf16*)g_x, ld_gx);
     }
   }
-  return status2();
+  return resbm_host::launch_status();
 }
 
 size_t resbm_ffn_encode_workspace_bytes(int64_t T, int32_t n, int32_t r) {
@@ -862,12 +856,12 @@ int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int3
   int32_t e = check_ws(need, ws, ws_bytes);
   if (e) return e;
   if (!h || !W_down || !x_attn || !W_e || !z || !b) return RESBM_E_NULL;
-  if (!ld_ok2(ld_h, d_ff) || !ld_ok2(ld_x, n) || !ld_ok2(ld_z, n)) return RESBM_E_SHAPE;
-  if (!aligned2(h, 16) || !aligned2(W_down, 16) || !aligned2(x_attn, 16) || !aligned2(W_e, 16) || !aligned2(z, 16) ||
-      !aligned2(b, 16) || (a_save && !aligned2(a_save, 16)))
+  if (!ld_ok(ld_h, d_ff) || !ld_ok(ld_x, n) || !ld_ok(ld_z, n)) return RESBM_E_SHAPE;
+  if (!aligned(h, 16) || !aligned(W_down, 16) || !aligned(x_attn, 16) || !aligned(W_e, 16) || !aligned(z, 16) ||
+      !aligned(b, 16) || (a_save && !aligned(a_save, 16)))
     return RESBM_E_ALIGN;
-  const size_t bh = extent2(T, d_ff, ld_h, 2), bwd = (size_t)d_ff * n * 2, bx = extent2(T, n, ld_x, 2),
-               bwe = (size_t)n * r * 4, bz = extent2(T, n, ld_z, 2), bb = (size_t)T * r * 2,
+  const size_t bh = extent(T, d_ff, ld_h, 2), bwd = (size_t)d_ff * n * 2, bx = extent(T, n, ld_x, 2),
+               bwe = (size_t)n * r * 4, bz = extent(T, n, ld_z, 2), bb = (size_t)T * r * 2,
                ba = a_save ? (size_t)T * r * 4 : 0;
   if (!fits(bh) || !fits(bwd) || !fits(bz) || !fits(need)) return RESBM_E_SHAPE;
   const void* ins[] = {h, W_down, x_attn, W_e};
@@ -876,9 +870,9 @@ int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int3
   const size_t outb[] = {bz, bb, ba, need};
   for (int o = 0; o < 4; ++o) {
     for (int i = 0; i < 4; ++i)
-      if (overlap2(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
+      if (overlap(outs[o], outb[o], ins[i], inb[i])) return RESBM_E_ALIAS;
     for (int o2 = o + 1; o2 < 4; ++o2)
-      if (overlap2(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
+      if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
   }
   hipStream_t st = (hipStream_t)stream;
   // z = h W_down with the encoder partials in the epilogue
@@ -889,7 +883,7 @@ int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int3
   const int64_t cnt = T * (r / 4);
   hipLaunchKernelGGL(k_enc_finish, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, T, r, (n + 255) / 256, act,
                      (const float*)ws, (const __bf16*)x_attn, ld_x, (__bf16*)b, a_save);
-  return status2();
+  return resbm_host::launch_status();
 }
 
 }  // extern "C"
