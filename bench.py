@@ -161,8 +161,9 @@ def summarize_profiles(trace_dir: str, fetch_dir: str, write_dir: str, name: str
     print("\n".join(lines))
     two = {k: v for k, v in stats.items() if k.startswith("resbm2::")}
     if two:
-        lines = [f"# rocprofv3 kernel trace of the two-linears-per-side step (bench.py two_linear, m = 1024),"
-                 f" workload {name}", "", "command:", f"    {commands[0] if commands else '?'}", "",
+        lines = [f"# rocprofv3 kernel trace of the two-linears-per-side step (bench.py two_linear, m = 1024)"
+                 f" and of the encoder fused into the FFN projection (ffn_encode, d_ff = 14336), workload {name}",
+                 "", "command:", f"    {commands[0] if commands else '?'}", "",
                  f"{'kernel':60s} {'calls':>6s} {'avg us':>9s} {'min us':>9s} {'max us':>9s}"]
         for k, v in sorted(two.items(), key=lambda kv: -sum(kv[1])):
             lines.append(f"{k[:60]:60s} {len(v):6d} {sum(v) / len(v):9.2f} {min(v):9.2f} {max(v):9.2f}")
