@@ -1,4 +1,5 @@
-// HIP kernels of the two-linears-per-side bottleneck for gfx950 and its C ABI.
+// HIP kernels of the two-linears-per-side bottleneck and of the encoder fused
+// into the FFN output projection, for gfx950, and their C ABI.
 //
 // Paper: ResBM, Sec. 3.2 (encoder and decoder each two linear layers with a
 // non-linearity between them; encoder at the end of stage l, decoder at the
@@ -14,15 +15,17 @@
 // which of A and B is stored K-contiguous.  The steps differ only in a prologue
 // (phi applied to the A operand while it is staged into LDS) and an epilogue
 // (bf16 or float32 store, multiplication by phi'(X) of a saved pre-activation,
-// addition of identity-path columns, or a split-K partial sum).  The n x m
-// products (2 T n m flops each) are matrix-core bound; the r-wide ones stream a
-// T x m tensor and are memory bound.
+// addition of identity-path columns, a split-K partial sum, or the encoder's
+// contraction of the output tile).  The n x m products (2 T n m flops each)
+// are matrix-core bound; the r-wide ones stream a T x m tensor and are memory
+// bound.
 //
-// A block computes a BM x BN tile of C in 64-deep stages: the stage's A and B
-// tiles go global -> registers -> LDS (double buffered, one barrier per stage,
-// the next stage's loads in flight during the current stage's products), then
-// every wave multiplies its (16 FM) x (16 FN) sub-tile with
-// v_mfma_f32_16x16x32_bf16.  The B operand takes the instruction's first slot,
+// A block computes a BM x BN tile of C in 64-deep stages, double buffered in
+// LDS with one barrier per stage and the next stage's loads in flight during
+// the current stage's products.  256 x 256 tiles load their operands straight
+// into LDS (buffer loads with an LDS destination); the smaller ones go through
+// registers (where the phi prologue is applied).  Every wave multiplies its
+// (16 FM) x (16 FN) sub-tile with v_mfma_f32_16x16x32_bf16.  The B operand takes the instruction's first slot,
 // so a lane's accumulator holds four consecutive columns of one output row and
 // stores them with one 8-byte (bf16) or 16-byte (float32) store.
 // K-contiguous operands are staged as [rows][64] and read as 16-byte chunks;
