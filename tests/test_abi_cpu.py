@@ -362,3 +362,30 @@ def test_two_encode_bwd_validation(lib):
     assert c.resbm2_encode_bwd(*fused) == R.E_ALIAS   # g_x == g_z needs equal leading dimensions
     assert call(11, A) == R.E_ALIAS           # g_z over z
     assert call(15, 9 * A) == R.E_ALIAS       # dW1 over dW2
+
+
+@needs_no_gpu
+def test_ffn_encode_validation(lib):
+    c = lib.cdll
+    DFF = 512
+    ws = c.resbm_ffn_encode_workspace_bytes(T, N, RR)
+    assert ws >= T * RR * 4 and ws % 256 == 0
+    assert c.resbm_ffn_encode_workspace_bytes(T, N, 12) == 0
+    ok = [T, DFF, N, RR, 1, A, DFF, 2 * A, 3 * A, N, 4 * A, 5 * A, N, 6 * A, 7 * A, 8 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm_ffn_encode_fwd(*a)
+
+    assert call(4, 3) == R.E_ACT
+    assert call(1, 100) == R.E_SHAPE          # d_ff % 8
+    assert call(3, 2 * N) == R.E_SHAPE        # r > n
+    assert call(0, 0) == R.OK
+    assert call(6, DFF - 8) == R.E_SHAPE      # ld_h < d_ff
+    for i in (5, 7, 8, 10, 11, 13):
+        assert call(i, None) == R.E_NULL, i
+    assert call(16, ws - 256) == R.E_WORKSPACE
+    assert call(13, 6 * A + 8) == R.E_ALIGN
+    assert call(11, 2 * A) == R.E_ALIAS       # z over W_down
+    assert call(13, A) == R.E_ALIAS           # b over h
