@@ -453,8 +453,8 @@ def main():
         summarize_profiles(*args.summarize_profiles, args.workload or I.HEADLINE, args.commands)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): this build runs the "
-              f"boundary module on a single MI355X; across GPUs it would shard by tokens", file=sys.stderr)
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the boundary module runs "
+              f"on a single MI355X; across GPUs it would shard by tokens", file=sys.stderr)
         sys.exit(2)
 
     import torch

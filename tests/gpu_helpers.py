@@ -19,7 +19,7 @@ def require_gpu():
 
 
 def lib(variant: str = "bf16"):
-    """The built library; a missing build is an error on a GPU machine, never a skip."""
+    """The built library; with a GPU present a missing build is an error, never a skip."""
     require_gpu()
     from paper_2604_11947_amd import resbm as R
     return R.library(variant)
