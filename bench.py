@@ -398,7 +398,7 @@ def two_linear_timing(lib, d: dict, r: int, m: int, dev, iters: int, cpu: bool, 
     return out
 
 
-def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int) -> dict:
+def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int, cpu: bool) -> dict:
     """The encoder fused into the FFN output projection (resbm_ffn_encode_fwd: z = h W_down
     with the encoder in the epilogue) against the unfused pair: the same projection by
     the framework's library GEMM (torch.matmul, hipBLASLt) followed by resbm_encode_fwd.
@@ -435,11 +435,26 @@ def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int
         us[nm] = e0.elapsed_time(e1) * 1e3 / iters
     flops = 2.0 * T * d_ff * n + 2.0 * T * n * r
     tf = flops / (us["fused"] * 1e-6) / 1e12
-    return {"d_ff": d_ff, "tokens": T, "us": us, "unfused_us": us["library_gemm"] + us["encode_fwd"],
-            "fused_over_unfused": us["fused"] / (us["library_gemm"] + us["encode_fwd"]), "iterations": iters,
-            "roofline": {"bound": "mfma", "kernel": "k_gemm<256x256, encoder epilogue>", "achieved": tf,
-                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": tf / MFMA_BF16_PEAK_TFLOPS,
-                         "flops": flops}}
+    out = {"d_ff": d_ff, "tokens": T, "us": us, "unfused_us": us["library_gemm"] + us["encode_fwd"],
+           "fused_over_unfused": us["fused"] / (us["library_gemm"] + us["encode_fwd"]), "iterations": iters,
+           "tokens_per_s": T / (us["fused"] * 1e-6),
+           "roofline": {"bound": "mfma", "kernel": "k_gemm<256x256, encoder epilogue>", "achieved": tf,
+                        "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": tf / MFMA_BF16_PEAK_TFLOPS,
+                        "flops": flops}}
+    if cpu:
+        from oracle import fusion_oracle as FO
+        Ts = 64
+        f64 = lambda t: t.to(torch.float64).cpu().numpy()  # noqa: E731
+        hs, Wd, xs, We = f64(h[:Ts]), f64(W_down), f64(x[:Ts]), W_e.double().cpu().numpy()
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 10.0:
+            FO.ffn_encode_fwd(hs, Wd, xs, We, act)
+            reps += 1
+        sec = (time.perf_counter() - t0) / reps
+        out["cpu_baseline"] = {"value": Ts / sec, "unit": "tokens/s", "cores": torch.get_num_threads(),
+                               "kind": "oracle", "sample": f"{Ts} tokens of the same op, {reps} repetitions"}
+    return out
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
@@ -611,7 +626,7 @@ def main():
     if args.two_m > 0:
         out["two_linear"] = two_linear_timing(lib, d, r, args.two_m, dev, 50, not args.no_cpu_baseline, act)
     if args.ffn_width > 0:
-        out["ffn_encode"] = ffn_encode_timing(lib, d, r, args.ffn_width, dev, 20, act)
+        out["ffn_encode"] = ffn_encode_timing(lib, d, r, args.ffn_width, dev, 20, act, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         tokens = args.cpu_tokens or T
         out["cpu_baseline"] = cpu_baseline(d, r, act, min(tokens, T))
