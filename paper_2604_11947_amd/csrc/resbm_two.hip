@@ -309,7 +309,11 @@ __device__ __forceinline__ void encode_epilogue(const GemmArgs& g, const f32x4 (
   }
 }
 
-template <bool AK, bool BKC, int BM, int BN, int WM, int WN, int EPI, bool PHI_A>
+// LATE (direct staging only): the next stage's loads are issued after the
+// first half of the current stage's products instead of before them, so the
+// products start right after the barrier; it pays where a block's K depth is
+// moderate (2-10 % at 1024 and 4096) and costs where it is long (3 % at 14336).
+template <bool AK, bool BKC, int BM, int BN, int WM, int WN, int EPI, bool PHI_A, bool LATE = false>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
   constexpr int NTH = 64 * WM * WN;
   constexpr int FM = BM / (16 * WM), FN = BN / (16 * WN);
@@ -339,9 +343,8 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto products = [&](const __bf16* ta, const __bf16* tb) {
-#pragma unroll
-    for (int kk = 0; kk < KT / 32; ++kk) {
+  auto products_kk = [&](const __bf16* ta, const __bf16* tb, int kk) {
+    {
       bf16x8 fa[FM], fb[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i) fa[i] = frag<AK, BM>(ta, (wm * FM + i) * 16, kk, row16, grp);
@@ -352,6 +355,11 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
+  };
+  static_assert(KT == 64, "a stage is two 32-deep halves");
+  auto products = [&](const __bf16* ta, const __bf16* tb) {
+    products_kk(ta, tb, 0);
+    products_kk(ta, tb, 1);
   };
 
   if constexpr (kDma) {
@@ -365,8 +373,14 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
     auto step = [&](int s, const __bf16* a, const __bf16* b, __bf16* na, __bf16* nb) {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
-      if (s + 1 < nst) stage(s + 1, na, nb);
-      products(a, b);
+      if constexpr (LATE) {
+        products_kk(a, b, 0);
+        if (s + 1 < nst) stage(s + 1, na, nb);
+        products_kk(a, b, 1);
+      } else {
+        if (s + 1 < nst) stage(s + 1, na, nb);
+        products(a, b);
+      }
     };
     if (nst > 0) stage(0, s_a0, s_b0);
     for (int s = 0; s < nst; s += 2) {
@@ -572,17 +586,21 @@ Plan2 make_plan2(int64_t T, int n, int m, int r) {
   return p;
 }
 
-template <bool AK, bool BKC, int BM, int BN, int WM, int WN, int EPI, bool PHI>
+template <bool AK, bool BKC, int BM, int BN, int WM, int WN, int EPI, bool PHI, bool LATE = false>
 void launch(const GemmArgs& g, int S, hipStream_t st) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((k_gemm<AK, BKC, BM, BN, WM, WN, EPI, PHI>), dim3(tiles, 1, S), dim3(64 * WM * WN), 0, st, g);
+  hipLaunchKernelGGL((k_gemm<AK, BKC, BM, BN, WM, WN, EPI, PHI, LATE>), dim3(tiles, 1, S), dim3(64 * WM * WN), 0, st,
+                     g);
 }
 
 // Runs C = op(A) op(B) with the epilogue EPI and tile shape s.
 template <bool AK, bool BKC, int EPI, bool PHI>
 void gemm(Shape s, const GemmArgs& g, int S, hipStream_t st) {
   switch (s) {
-    case kBig: launch<AK, BKC, 256, 256, 2, 4, EPI, PHI>(g, S, st); break;
+    case kBig:
+      if (std::min(g.K, g.kc) <= 4096) launch<AK, BKC, 256, 256, 2, 4, EPI, PHI, true>(g, S, st);
+      else launch<AK, BKC, 256, 256, 2, 4, EPI, PHI, false>(g, S, st);
+      break;
     case kWide: launch<AK, BKC, 128, 128, 2, 2, EPI, PHI>(g, S, st); break;
     case kNarrow32: launch<AK, BKC, 64, 32, 4, 1, EPI, PHI>(g, S, st); break;
     case kNarrow64: launch<AK, BKC, 64, 64, 4, 1, EPI, PHI>(g, S, st); break;
