@@ -63,6 +63,9 @@ def parse():
                    help="intermediate width m of the two-linears-per-side variant (0: skip timing it)")
     p.add_argument("--ffn-width", type=int, default=14336,
                    help="FFN hidden width for timing the encoder fused into the FFN output projection (0: skip)")
+    p.add_argument("--no-sweep", action="store_true",
+                   help="skip the compression-ratio sweep (r = 16 .. 256 at n = 4096) and the 70B-class line")
+    p.add_argument("--step-times", action="store_true", help="list every timed step's duration")
     p.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="write profiles/ summaries from rocprofv3 output of this script (no GPU work)")
     p.add_argument("--commands", nargs=3, default=None, help="the three rocprofv3 commands, recorded in the summaries")
@@ -330,7 +333,7 @@ def two_linear_timing(lib, d: dict, r: int, m: int, dev, iters: int, cpu: bool, 
     dW3, dW4 = torch.empty(r, m, device=dev), torch.empty(m, n, device=dev)
     ws = lib.two_workspace(T, n, m, r, dev)
     ops = {
-        "encode2_fwd": lambda: lib.encode2_fwd(x, z, w["W1"], w["W2"], b, u, act=act),
+        "encode2_fwd": lambda: lib.encode2_fwd(x, z, w["W1"], w["W2"], b, u, act=act, ws=ws),
         "decode2_fwd": lambda: lib.decode2_fwd(b, w["W3"], w["W4"], zt, v, act=act, ws=ws),
         "decode2_bwd": lambda: lib.decode2_bwd(b, v, g_zt, g_id, w["W3"], w["W4"], g_b, dW3, dW4, act=act, ws=ws),
         "encode2_bwd": lambda: lib.encode2_bwd(z, u, g_b, w["W1"], w["W2"], g_z, dW1, dW2, g_x=g_z, act=act, ws=ws),
@@ -457,6 +460,90 @@ def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int
     return out
 
 
+def sweep_timing(lib, dev, names, steps: int, warmup: int, act: int) -> dict:
+    """The whole step (four ops, graph replay) at each workload in `names`: the
+    compression-ratio sweep at n = 4096 and the 70B-class boundary.  Inputs are
+    drawn on the device (torch, seeded) with each workload's shape and
+    distribution; kernel time does not depend on the values.  Two rotating input
+    sets.  Reports per-step median time, algorithmic HBM GB/s, and matrix-core
+    rates: algorithmic (12 T n r flops per step) and issued (24 T n r: the hi and
+    lo bf16 products of the float32 weights and of g_h)."""
+    import torch
+
+    from paper_2604_11947_amd import inputs as I
+
+    out = {}
+    for name in names:
+        w = I.WORKLOADS[name]
+        T, n, r = w.tokens, w.n, w.r
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(1000 + r)
+        bf = torch.bfloat16
+
+        def act_tensor():
+            x = torch.randn(T, n, device=dev, generator=gen)
+            if w.dist == "token_lognormal":
+                x *= torch.exp(0.5 * torch.randn(T, 1, device=dev, generator=gen))
+            return x.to(bf)
+
+        sets = []
+        for _ in range(2):
+            sets.append({
+                "x_attn": act_tensor(), "z": act_tensor(),
+                "g_zt": (0.1 * torch.randn(T, n, device=dev, generator=gen)).to(bf),
+                "g_id": (0.1 * torch.randn(T, n, device=dev, generator=gen)).to(bf),
+                "W_e": torch.randn(n, r, device=dev, generator=gen) / n ** 0.5,
+                "W_d": torch.randn(r, n, device=dev, generator=gen) / r ** 0.5,
+                "b": torch.empty(T, r, dtype=bf, device=dev), "a": torch.empty(T, r, device=dev),
+                "zt": torch.empty(T, n, dtype=bf, device=dev), "gb": torch.empty(T, r, dtype=bf, device=dev),
+                "gz": torch.empty(T, n, dtype=bf, device=dev), "dWd": torch.empty(r, n, device=dev),
+                "dWe": torch.empty(n, r, device=dev)})
+        ws = lib.workspace(T, n, r, dev)
+
+        def step(s):
+            lib.encode_fwd(s["x_attn"], s["z"], s["W_e"], s["b"], s["a"], act=act, ws=ws)
+            lib.decode_fwd(s["b"], s["W_d"], s["zt"], ws=ws)
+            lib.decode_bwd(s["b"], s["W_d"], s["g_zt"], s["g_id"], s["gb"], s["dWd"], ws=ws)
+            lib.encode_bwd(s["z"], s["W_e"], s["a"], s["gb"], s["gz"], s["dWe"], act=act, ws=ws)
+
+        for s_ in sets:
+            step(s_)
+        torch.cuda.synchronize()
+        graphs = []
+        for s_ in sets:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(s_)
+            graphs.append(g)
+        for i in range(warmup):
+            graphs[i % 2].replay()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        ev[0].record()
+        for i in range(steps):
+            graphs[i % 2].replay()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        st = np.asarray([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]) * 1e3
+        med = float(np.median(st))
+        nbytes = sum(op_bytes(T, n, r).values())
+        alg = 12.0 * T * n * r
+        out[name] = {"n": n, "r": r, "tokens": T, "us_median": med, "us_mean": float(st.mean()),
+                     "us_p10": float(np.percentile(st, 10)), "us_p90": float(np.percentile(st, 90)),
+                     "tokens_per_s": T / (med * 1e-6), "gbps": nbytes / (med * 1e-6) / 1e9,
+                     "hbm_frac": nbytes / (med * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                     "tflops_alg": alg / (med * 1e-6) / 1e12, "tflops_issued": 2 * alg / (med * 1e-6) / 1e12,
+                     "mfma_frac_issued": 2 * alg / (med * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS}
+        del graphs, sets, ws
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return {"workloads": out, "steps": steps, "warmup": warmup, "timing": "hip graph replay, per-step events",
+            "inputs": "drawn on the device (torch, seeded), each workload's shape and distribution"}
+
+
+SWEEP = ("sweep_n4096_r16", "sweep_n4096_r32", "sweep_n4096_r64", "sweep_n4096_r128", "sweep_n4096_r256",
+         "n8192_r64_lognormal")
+
+
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 COPY_PROBE_MIB = 256
 
@@ -571,16 +658,27 @@ def main():
         for i in range(args.warmup):
             graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
-        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # one event between consecutive replays: per-step times, and the first and
+        # last bracket exactly the K timed steps
+        gev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         wall0 = time.perf_counter()
-        g0.record()
+        gev[0].record()
         for i in range(args.steps):
             graphs[i % len(graphs)].replay()
-        g1.record()
+            gev[i + 1].record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
-        ms_graph = g0.elapsed_time(g1) / args.steps
+        ms_graph = gev[0].elapsed_time(gev[-1]) / args.steps
+        step_ms = [gev[i].elapsed_time(gev[i + 1]) for i in range(args.steps)]
+    else:
+        step_ms = [sum(e[k].elapsed_time(e[k + 1]) for k in range(4)) for e in events] if not args.no_op_events \
+            else []
     ms_step = ms_graph if ms_graph is not None else ms_eager
+    step_stats = None
+    if step_ms:
+        q = np.percentile(np.asarray(step_ms), [10, 50, 90])
+        step_stats = {"p10_ms": float(q[0]), "median_ms": float(q[1]), "p90_ms": float(q[2]),
+                      "first_ms": float(step_ms[0]), "last_ms": float(step_ms[-1])}
 
     op_ms = {}
     for k, nm in enumerate(OPS):
@@ -602,6 +700,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_step,
         "timing": "hip graph replay" if ms_graph is not None else "eager launches",
+        "step_time_stats": step_stats,
         "ms_per_step_eager": ms_eager,
         "higher_is_better": True,
         "scaling": "weak",
@@ -621,6 +720,10 @@ def main():
         "wall_s_timed": wall,
         "input_gen_s": t_gen,
     }
+    if args.step_times:
+        out["step_ms"] = step_ms
+    if not args.no_sweep:
+        out["sweep"] = sweep_timing(lib, dev, SWEEP, 50, 20, act)
     if not args.no_optimizer:
         out["optimizer"] = optimizer_timing(lib, d, r, dev, 200, cpu=not args.no_cpu_baseline)
     if args.two_m > 0:

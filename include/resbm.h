@@ -184,8 +184,9 @@ int32_t resbm_newton_schulz(int32_t p, int32_t q, const float* G, float* O,
  *     U  = M, or G + momentum M with nesterov != 0      (U = G when M == NULL)
  *     O  = Newton-Schulz(U; steps, a, b, c)             (as above)
  *     W <- float32(W - lr (scale O + weight_decay W))
- * `scale` matches the update's size to AdamW's; the cited method uses
- * 0.2 sqrt(max(p, q)).  W, G and M must not overlap each other.
+ * `scale` matches the update's size to AdamW's; a negative scale selects the
+ * cited method's 0.2 sqrt(max(p, q)) (0 leaves only the decay term).  W, G
+ * and M must not overlap each other.
  */
 int32_t resbm_muon_update(int32_t p, int32_t q, float* W, const float* G, float* M,
                           double lr, double momentum, double weight_decay, double scale,
@@ -232,19 +233,22 @@ size_t resbm_workspace_bytes(int64_t T, int32_t n, int32_t r);
  *  - weights row-major and contiguous: W1 n x m, W2 m x r, W3 r x m, W4 m x n;
  *  - u and v (T x m, packed) are written by the forward ops for the
  *    backward ops;
- *  - products inside an op consume bf16 operands: phi(u), phi(v), and the
- *    gradients g_u, g_v held in the workspace between two products, are
- *    rounded to bf16 first (accumulation is float32);
+ *  - products inside an op consume bf16 operands: phi(u) and phi(v) (formed
+ *    from the float32 accumulator of u and v, then rounded) and the
+ *    gradients g_u, g_v, held in the workspace between two products, are
+ *    rounded to bf16 once (accumulation is float32); the backward ops form
+ *    phi and phi' from the bf16 u and v they are given;
  *  - ws holds resbm2_workspace_bytes(T, n, m, r) bytes (T x m
- *    intermediates and split-K partial sums); resbm2_encode_fwd needs none,
- *    and resbm2_decode_fwd none with act = identity (ws may then be NULL).
+ *    intermediates and split-K partial sums); with act = identity
+ *    resbm2_encode_fwd and resbm2_decode_fwd need none (ws may then be NULL).
  */
 size_t resbm2_workspace_bytes(int64_t T, int32_t n, int32_t m, int32_t r);
 
 /*  x_attn  T x n, row stride ld_x; only columns [0, r) are read.
  *  z       T x n, row stride ld_z (the feed-forward output).
  *  b       out, T x r packed (the payload).
- *  u       out, T x m packed (saved for resbm2_encode_bwd). */
+ *  u       out, T x m packed (saved for resbm2_encode_bwd).
+ *  ws      with SiLU, phi(u) between the two products (T x m bf16). */
 int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act,
                           const void* x_attn, int64_t ld_x, const void* z, int64_t ld_z,
                           const void* W1, const void* W2, void* b, void* u,

@@ -1391,6 +1391,11 @@ using resbm_host::launch_status;
 using resbm_host::ld_ok;
 using resbm_host::overlap;
 
+// Whether `rows` rows of a streamed T x n matrix with row stride ld fit one
+// buffer descriptor (the kernels address a block's rows through one
+// descriptor with 32-bit byte offsets).
+bool window_ok(int64_t rows, int64_t ld) { return rows * ld * (int64_t)kIoBytes <= kMaxRange; }
+
 int32_t check_common(int64_t T, int n, int r, int64_t ws_need, const void* ws, size_t ws_bytes) {
   if (T < 0 || !shape_ok(n, r)) return RESBM_E_SHAPE;
   if (T == 0) return RESBM_OK;
@@ -1521,7 +1526,7 @@ int32_t resbm_encode_fwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   int32_t st = check_common(T, n, r, (int64_t)p.ef_ws, ws, ws_bytes);
   if (st) return st;
   if (!x_attn || !z || !W_e || !b) return RESBM_E_NULL;
-  if (!ld_ok(ld_x, n) || !ld_ok(ld_z, n)) return RESBM_E_SHAPE;
+  if (!ld_ok(ld_x, n) || !ld_ok(ld_z, n) || !window_ok(16 * p.ef_mt, ld_z)) return RESBM_E_SHAPE;
   if (!aligned(x_attn, 16) || !aligned(z, 16) || !aligned(W_e, 16) || !aligned(b, 16) ||
       (a_save && !aligned(a_save, 16)))
     return RESBM_E_ALIGN;
@@ -1555,7 +1560,7 @@ int32_t resbm_decode_fwd(int64_t T, int32_t n, int32_t r, int32_t add_identity, 
   if (T == 0) return RESBM_OK;
   const Plan p = make_plan(T, n, r);
   if (!b || !W_d || !z_tilde) return RESBM_E_NULL;
-  if (!ld_ok(ld_zt, n)) return RESBM_E_SHAPE;
+  if (!ld_ok(ld_zt, n) || !window_ok(p.df_tpg, ld_zt)) return RESBM_E_SHAPE;
   if (!aligned(b, 16) || !aligned(W_d, 16) || !aligned(z_tilde, 16)) return RESBM_E_ALIGN;
   const size_t bz = extent(T, n, ld_zt, kIoBytes), bb = (size_t)T * r * kIoBytes, bw = (size_t)n * r * 4;
   if (overlap(z_tilde, bz, b, bb) || overlap(z_tilde, bz, W_d, bw)) return RESBM_E_ALIAS;
@@ -1585,7 +1590,7 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r, const void* b, const f
   int32_t st = check_common(T, n, r, (int64_t)p.db_ws, ws, ws_bytes);
   if (st) return st;
   if (!b || !W_d || !g_zt || !g_b || !dW_d) return RESBM_E_NULL;
-  if (!ld_ok(ld_gzt, n) || (g_id && !ld_ok(ld_gid, n))) return RESBM_E_SHAPE;
+  if (!ld_ok(ld_gzt, n) || (g_id && !ld_ok(ld_gid, n)) || !window_ok(32, ld_gzt)) return RESBM_E_SHAPE;
   if (!aligned(b, 16) || !aligned(W_d, 16) || !aligned(g_zt, 16) || !aligned(g_b, 16) || !aligned(dW_d, 16) ||
       (g_id && !aligned(g_id, 16)))
     return RESBM_E_ALIGN;
@@ -1630,7 +1635,9 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   if (st) return st;
   if (!z || !W_e || !g_b || !g_z || !dW_e) return RESBM_E_NULL;
   if (act == RESBM_ACT_SILU && !a_save) return RESBM_E_ACT;
-  if (!ld_ok(ld_z, n) || !ld_ok(ld_gz, n) || (g_x && !ld_ok(ld_gx, n))) return RESBM_E_SHAPE;
+  if (!ld_ok(ld_z, n) || !ld_ok(ld_gz, n) || (g_x && !ld_ok(ld_gx, n)) || !window_ok(64, ld_z) ||
+      !window_ok(p.df_tpg, ld_gz))
+    return RESBM_E_SHAPE;
   if (!aligned(z, 16) || !aligned(W_e, 16) || !aligned(g_b, 16) || !aligned(g_z, 16) || !aligned(dW_e, 16) ||
       (a_save && !aligned(a_save, 16)) || (g_x && !aligned(g_x, 16)))
     return RESBM_E_ALIGN;

@@ -678,7 +678,8 @@ int32_t resbm_muon_update(int32_t p, int32_t q, float* W, const float* G, float*
   g.nesterov = nesterov ? 1 : 0;
   g.out = W;
   g.lr = lr;
-  g.scale = scale;
+  // a negative scale selects the cited method's default, 0.2 sqrt(max(p, q))
+  g.scale = scale < 0.0 ? 0.2 * sqrt((double)(p > q ? p : q)) : scale;
   g.wd = weight_decay;
   run_ns<kOutW>(P, (char*)ws, g, steps, a, b, c, (hipStream_t)stream);
   return launch_status();

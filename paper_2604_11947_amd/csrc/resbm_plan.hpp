@@ -137,6 +137,10 @@ inline Plan make_plan(int64_t T, int n, int r) {
     const int64_t ntile = ceil_div(Tm, 16);
     const int64_t g = clamp64(ceil_div((int64_t)RESBM_DF_WAVES_PER_CU * kNumCU, (int64_t)p.df_nwg * 4), 1, ntile);
     p.df_tpg = (int)(16 * ceil_div(ntile, g));
+    // a token group's output rows lie in one buffer descriptor (32-bit byte
+    // offsets): at most 1 GiB of dense rows per group
+    const int64_t cap = (((int64_t)1 << 30) / ((int64_t)n * 4)) / 16 * 16;
+    if (p.df_tpg > cap) p.df_tpg = (int)(cap < 16 ? 16 : cap);
     p.df_ngrp = (int)ceil_div(Tm, p.df_tpg);
   }
 

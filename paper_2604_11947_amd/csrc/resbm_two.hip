@@ -65,7 +65,7 @@ enum Epi : int {
   kEpiDphi = 2,   // C = rne(acc * phi'(X))   (X: saved pre-activation, same shape as C)
   kEpiAdd = 3,    // C = rne(acc + X) on columns < x_cols, rne(acc) elsewhere
   kEpiPart = 4,   // partial[split] = acc (float32, M x N contiguous per split)
-  kEpiBf16Phi = 5,  // C = rne(acc) and D = rne(phi(C)) (a pre-activation and its activation)
+  kEpiBf16Phi = 5,  // C = rne(acc) and D = rne(phi(acc)) (a pre-activation and its activation)
   kEpiEncode = 6,   // C = rne(acc) (the FFN output z) and D[tile column][row] = C_tile W_e[tile rows]
 };
 
@@ -445,7 +445,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
         bst8(rc, ok ? (uint32_t)(((int64_t)m * g.ldc + n) * 2) : kOOB, __builtin_bit_cast(uint2, h));
         if constexpr (EPI == kEpiBf16Phi) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) h[e] = (__bf16)silu((float)h[e]);
+          for (int e = 0; e < 4; ++e) h[e] = (__bf16)silu(v[e]);  // from the float32 accumulator
           bst8(rd, ok ? (uint32_t)(((int64_t)m * g.ldd + n) * 2) : kOOB, __builtin_bit_cast(uint2, h));
         }
       }
@@ -571,7 +571,7 @@ size_t part_bytes(int M, int N, const Split& sp) {
 struct Plan2 {
   Split dW4, dW3, dW2, dW1;
   size_t inter;      // one T x m bf16 intermediate (phi(v), g_v or g_u)
-  size_t dec_fwd, dec_bwd, enc_bwd;
+  size_t enc_fwd, dec_fwd, dec_bwd, enc_bwd;
 };
 Plan2 make_plan2(int64_t T, int n, int m, int r) {
   Plan2 p;
@@ -580,6 +580,7 @@ Plan2 make_plan2(int64_t T, int n, int m, int r) {
   p.dW2 = split_for(m, r, (int)T, narrow_for(r));
   p.dW1 = split_for(n, m, (int)T, wide_for(n, m));
   p.inter = round_up((size_t)T * m * 2, kWsAlign2);
+  p.enc_fwd = p.inter;
   p.dec_fwd = p.inter;
   p.dec_bwd = 2 * p.inter + std::max(part_bytes(m, n, p.dW4), part_bytes(r, m, p.dW3));
   p.enc_bwd = p.inter + std::max(part_bytes(m, r, p.dW2), part_bytes(n, m, p.dW1));
@@ -651,16 +652,20 @@ extern "C" {
 size_t resbm2_workspace_bytes(int64_t T, int32_t n, int32_t m, int32_t r) {
   if (!shape_ok2(T, n, m, r) || T == 0) return 0;
   const Plan2 p = make_plan2(T, n, m, r);
-  return std::max(p.dec_fwd, std::max(p.dec_bwd, p.enc_bwd));
+  return std::max(std::max(p.enc_fwd, p.dec_fwd), std::max(p.dec_bwd, p.enc_bwd));
 }
 
 int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t act, const void* x_attn, int64_t ld_x,
                           const void* z, int64_t ld_z, const void* W1, const void* W2, void* b, void* u, void* ws,
                           size_t ws_bytes, void* stream) {
-  (void)ws; (void)ws_bytes;
   if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
   if (!shape_ok2(T, n, m, r)) return RESBM_E_SHAPE;
   if (T == 0) return RESBM_OK;
+  const bool silu = act == RESBM_ACT_SILU;
+  const Plan2 p = make_plan2(T, n, m, r);
+  const size_t need = silu ? p.enc_fwd : 0;
+  int32_t e = check_ws(need, ws, ws_bytes);
+  if (e) return e;
   if (!x_attn || !z || !W1 || !W2 || !b || !u) return RESBM_E_NULL;
   if (!ld_ok(ld_x, n) || !ld_ok(ld_z, n)) return RESBM_E_SHAPE;
   if (!aligned(x_attn, 16) || !aligned(z, 16) || !aligned(W1, 16) || !aligned(W2, 16) || !aligned(b, 16) ||
@@ -671,18 +676,25 @@ int32_t resbm2_encode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   if (!fits(bx) || !fits(bz) || !fits(bu) || !fits(bw1)) return RESBM_E_SHAPE;
   if (overlap(b, bb, x_attn, bx) || overlap(b, bb, z, bz) || overlap(b, bb, W1, bw1) || overlap(b, bb, W2, bw2) ||
       overlap(u, bu, x_attn, bx) || overlap(u, bu, z, bz) || overlap(u, bu, W1, bw1) || overlap(u, bu, W2, bw2) ||
-      overlap(u, bu, b, bb))
+      overlap(u, bu, b, bb) || overlap(ws, need, x_attn, bx) || overlap(ws, need, z, bz) ||
+      overlap(ws, need, W1, bw1) || overlap(ws, need, W2, bw2) || overlap(ws, need, b, bb) ||
+      overlap(ws, need, u, bu))
     return RESBM_E_ALIAS;
   hipStream_t st = (hipStream_t)stream;
   const int Ti = (int)T;
-  // u = z W1  (A = z, K-contiguous; B = W1 [n][m], m-contiguous)
+  // u = z W1  (A = z, K-contiguous; B = W1 [n][m], m-contiguous), and with SiLU
+  // also phi(u) (workspace), formed from the float32 accumulator
   GemmArgs g = args(Ti, m, n, z, ld_z, bz, W1, m, bw1, u, m, bu);
-  gemm<true, false, kEpiBf16, false>(wide_for(Ti, m), g, 1, st);
+  if (silu) {
+    g.D = ws; g.ldd = m; g.d_bytes = (int64_t)bu;
+    gemm<true, false, kEpiBf16Phi, false>(wide_for(Ti, m), g, 1, st);
+  } else {
+    gemm<true, false, kEpiBf16, false>(wide_for(Ti, m), g, 1, st);
+  }
   // b = x_attn[:, :r] + phi(u) W2
-  g = args(Ti, r, m, u, m, bu, W2, r, bw2, b, r, bb);
+  g = args(Ti, r, m, silu ? ws : u, m, bu, W2, r, bw2, b, r, bb);
   g.X = x_attn; g.ldx = ld_x; g.x_bytes = (int64_t)bx; g.x_cols = r;
-  if (act == RESBM_ACT_SILU) gemm<true, false, kEpiAdd, true>(narrow_for(r), g, 1, st);
-  else gemm<true, false, kEpiAdd, false>(narrow_for(r), g, 1, st);
+  gemm<true, false, kEpiAdd, false>(narrow_for(r), g, 1, st);
   return resbm_host::launch_status();
 }
 
@@ -711,7 +723,7 @@ int32_t resbm2_decode_fwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
     return RESBM_E_ALIAS;
   hipStream_t st = (hipStream_t)stream;
   const int Ti = (int)T;
-  // v = b W3, and with SiLU also phi(v) (workspace), formed once from the rounded v
+  // v = b W3, and with SiLU also phi(v) (workspace), formed from the float32 accumulator
   GemmArgs g = args(Ti, m, r, b, r, bb, W3, m, bw3, v, m, bv);
   if (silu) {
     g.D = ws; g.ldd = m; g.d_bytes = (int64_t)bv;

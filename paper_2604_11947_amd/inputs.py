@@ -68,6 +68,8 @@ WORKLOADS: dict[str, Workload] = {
     for w in [
         Workload("tiny_n512_r4", 512, 4, 2, 128, "normal"),
         Workload("n2048_r16_outliers", 2048, 16, 8, 1024, "outliers"),
+        # the same boundary at the 16,384 tokens its description also states
+        Workload("n2048_r16_outliers_t16k", 2048, 16, 8, 2048, "outliers"),
         Workload("n4096_r32_t3", 4096, 32, 4, 4096, "student_t3"),
         Workload("n8192_r64_lognormal", 8192, 64, 4, 8192, "token_lognormal"),
     ]

@@ -243,7 +243,7 @@ class Library:
                 _packed(t, *shape, nm)
         return n, m, r
 
-    def encode2_fwd(self, x_attn, z, W1, W2, b, u, act=ACT_SILU, stream=None):
+    def encode2_fwd(self, x_attn, z, W1, W2, b, u, act=ACT_SILU, ws=None, stream=None):
         T = z.shape[0]
         n, m, r = self._two_weights(W1, W2)
         for t, nm in ((x_attn, "x_attn"), (z, "z"), (b, "b"), (u, "u")):
@@ -251,8 +251,11 @@ class Library:
         ld_x, ld_z = _ld(x_attn, T, n, "x_attn"), _ld(z, T, n, "z")
         _packed(b, T, r, "b")
         _packed(u, T, m, "u")
+        if ws is None and act != ACT_IDENTITY:
+            ws = self.two_workspace(T, n, m, r, z.device)
         st = self.cdll.resbm2_encode_fwd(T, n, m, r, act, _ptr(x_attn), ld_x, _ptr(z), ld_z, _ptr(W1), _ptr(W2),
-                                         _ptr(b), _ptr(u), None, 0, _stream(stream, z))
+                                         _ptr(b), _ptr(u), _ptr(ws), 0 if ws is None else ws.numel(),
+                                         _stream(stream, z))
         self._check("resbm2_encode_fwd", st)
 
     def decode2_fwd(self, b, W3, W4, z_tilde, v, act=ACT_SILU, ws=None, stream=None):
@@ -363,7 +366,7 @@ class Library:
             if t is not None:
                 _packed(t, p, q, nm)
         if scale is None:
-            scale = 0.2 * max(p, q) ** 0.5
+            scale = -1.0  # the library's default (negative selects it)
         if ws is None:
             ws = self.matrix_workspace(p, q, W.device)
         a, b, c = coeffs

@@ -205,6 +205,26 @@ def test_encode_bwd_validation(lib):
     assert call(gb=4 * A + 4) == R.E_ALIGN
 
 
+@needs_no_gpu
+def test_descriptor_window_limit(lib):
+    """A block's rows of a streamed matrix are addressed through one buffer
+    descriptor with 32-bit byte offsets: a row stride so large that the rows one
+    block (or one token group of the expand kernel) covers exceed that range is
+    rejected, never wrapped."""
+    c = lib.cdll
+    n, r, t = 64, 4, 64
+    big = 1 << 27            # 16 rows of 2^27 elements: 4 GiB of bf16, 8 GiB of fp32
+    ws = lib.workspace_bytes(t, n, r)
+    assert c.resbm_decode_fwd(t, n, r, 0, A, 2 * A, 3 * A, big, None, 0, None) == R.E_SHAPE
+    assert c.resbm_encode_fwd(t, n, r, 1, A, n, 2 * A, big, 3 * A, 4 * A, 5 * A, 6 * A, ws, None) == R.E_SHAPE
+    assert c.resbm_decode_bwd(t, n, r, A, 2 * A, 3 * A, big, None, 0, 5 * A, 6 * A, 0, 7 * A, ws,
+                              None) == R.E_SHAPE
+    assert c.resbm_encode_bwd(t, n, r, 1, A, big, 2 * A, 3 * A, 4 * A, 5 * A, n, None, 0, 7 * A, 0, 8 * A, ws,
+                              None) == R.E_SHAPE
+    assert c.resbm_encode_bwd(t, n, r, 1, A, n, 2 * A, 3 * A, 4 * A, 5 * A, big, None, 0, 7 * A, 0, 8 * A, ws,
+                              None) == R.E_SHAPE
+
+
 # ---------------------------------------------------------------- optimizer-side ops
 def test_matrix_workspace_bytes(lib):
     assert lib.matrix_workspace_bytes(0, 32) == 0
@@ -303,7 +323,8 @@ def test_two_workspace_bytes(lib):
 @needs_no_gpu
 def test_two_encode_fwd_validation(lib):
     c = lib.cdll
-    ok = [T, N, M2, RR, 1, A, N, 2 * A, N, 3 * A, 4 * A, 5 * A, 6 * A, None, 0, None]
+    ws = c.resbm2_workspace_bytes(T, N, M2, RR)
+    ok = [T, N, M2, RR, 1, A, N, 2 * A, N, 3 * A, 4 * A, 5 * A, 6 * A, 7 * A, ws, None]
 
     def call(i, v):
         a = list(ok)
@@ -315,11 +336,14 @@ def test_two_encode_fwd_validation(lib):
     assert call(2, 4) == R.E_SHAPE
     assert call(6, N - 8) == R.E_SHAPE
     assert call(0, 0) == R.OK                 # T = 0: nothing read
-    for i in (5, 7, 9, 10, 11, 12):
+    for i in (5, 7, 9, 10, 11, 12, 13):       # with SiLU phi(u) needs the workspace
         assert call(i, None) == R.E_NULL, i
+    assert call(14, T * M2 * 2 - 256) == R.E_WORKSPACE
     assert call(11, 5 * A + 8) == R.E_ALIGN
+    assert call(13, 7 * A + 128) == R.E_ALIGN
     assert call(11, 2 * A) == R.E_ALIAS       # b over z
     assert call(12, 3 * A) == R.E_ALIAS       # u over W1
+    assert call(13, 6 * A) == R.E_ALIAS       # ws over u
 
 
 @needs_no_gpu

@@ -106,3 +106,81 @@ def test_f32_chain(shape):
     ok("dW_d", dWd, ref["dW_d"], abs_rms(O.decode_weight_grad, ref["b"], f["g_zt"]))
     g_h = O.encode_local_grad(ref["g_b"], ref["a"], O.ACT_SILU)
     ok("dW_e", dWe, ref["dW_e"], abs_rms(O.encode_weight_grad, f["z"], g_h))
+
+
+def inputs32_normal(T, n, r, seed):
+    d = I.make_inputs(T, n, r, "normal", seed)
+    h = {k: I.bf16_to_f64(v) for k, v in d.items() if k != "meta"}
+    g = {k: (d[k].float() if d[k].dtype == torch.bfloat16 else d[k]) for k in d if k != "meta"}
+    return h, to_dev(g)
+
+
+@pytest.mark.parametrize("shape", [(1000, 512, 32), (333, 320, 40), (96, 256, 256), (4096, 1024, 16)],
+                         ids=["T1000_n512_r32", "T333_n320_r40", "T96_n256_r256", "T4096_n1024_r16"])
+def test_f32_gaussian_plain_scale(shape):
+    """Gaussian activations (no heavy tails): every output, the weight gradients
+    included, within 1e-5 RMS(ref) with no other scale."""
+    T, n, r = shape
+    say(f"f32 build, N(0,1) activations, plain scale: T={T} n={n} r={r}")
+    L = lib("f32")
+    f, g = inputs32_normal(T, n, r, seed=23)
+    b, a = torch.empty(T, r, device="cuda"), torch.empty(T, r, device="cuda")
+    zt, gb = torch.empty(T, n, device="cuda"), torch.empty(T, r, device="cuda")
+    dWd, gz, dWe = torch.empty(r, n, device="cuda"), torch.empty(T, n, device="cuda"), torch.empty(n, r, device="cuda")
+    L.encode_fwd(g["x_attn"], g["z"], g["W_e"], b, a)
+    L.decode_fwd(b, g["W_d"], zt)
+    L.decode_bwd(b, g["W_d"], g["g_zt"], g["g_id"], gb, dWd)
+    L.encode_bwd(g["z"], g["W_e"], a, gb, gz, dWe)
+    torch.cuda.synchronize()
+    ref_b, ref_a = O.encode_fwd(f["x_attn"], f["z"], f["W_e"], O.ACT_SILU)
+    ok("b", b, ref_b)
+    ok("a_save", a, ref_a)
+    ok("z_tilde", zt, O.decode_fwd(f64(b), f["W_d"], False))
+    ref_gb, ref_dwd = O.decode_bwd(f64(b), f["W_d"], f["g_zt"], f["g_id"])
+    ok("g_b", gb, ref_gb)
+    ok("dW_d", dWd, ref_dwd)
+    ref_gz, ref_dwe = O.encode_bwd(f["z"], f["W_e"], f64(a), f64(gb), O.ACT_SILU)
+    ok("g_z", gz, ref_gz)
+    ok("dW_e", dWe, ref_dwe)
+
+
+@pytest.mark.timeout(600)
+def test_f32_gaussian_full_tokens():
+    """The headline shape's token count (T = 16384, n = 4096, r = 32) in the fp32
+    build on N(0, 1) activations: weight gradients (sums over all 16384 tokens)
+    whole, within 1e-5 RMS(ref); row-local outputs on sampled rows."""
+    T, n, r = 16384, 4096, 32
+    say(f"f32 build, full token count T={T} n={n} r={r}")
+    L = lib("f32")
+    d = I.make_inputs(T, n, r, "normal", 0)
+    g = {k: (d[k].float() if d[k].dtype == torch.bfloat16 else d[k]).cuda() for k in
+         ("x_attn", "z", "W_e", "W_d", "g_zt", "g_id")}
+    b, a = torch.empty(T, r, device="cuda"), torch.empty(T, r, device="cuda")
+    zt, gb = torch.empty(T, n, device="cuda"), torch.empty(T, r, device="cuda")
+    dWd, gz, dWe = torch.empty(r, n, device="cuda"), torch.empty(T, n, device="cuda"), torch.empty(n, r, device="cuda")
+    L.encode_fwd(g["x_attn"], g["z"], g["W_e"], b, a)
+    L.decode_fwd(b, g["W_d"], zt)
+    L.decode_bwd(b, g["W_d"], g["g_zt"], g["g_id"], gb, dWd)
+    L.encode_bwd(g["z"], g["W_e"], a, gb, gz, dWe)
+    torch.cuda.synchronize()
+    del g
+    rows = np.unique(np.concatenate([[0, 1, T // 2, T - 1], np.random.default_rng(3).choice(T, 60, replace=False)]))
+    rt = torch.from_numpy(rows)
+    W_e, W_d = I.bf16_to_f64(d["W_e"]), I.bf16_to_f64(d["W_d"])
+    x, z = I.bf16_to_f64(d["x_attn"][rt]), I.bf16_to_f64(d["z"][rt])
+    ref_b, ref_a = O.encode_fwd(x, z, W_e, O.ACT_SILU)
+    ok("b", f64(b)[rows], ref_b)
+    ok("a_save", f64(a)[rows], ref_a)
+    b64, a64, gb64 = f64(b), f64(a), f64(gb)
+    ok("z_tilde", f64(zt[rt.cuda()]), O.decode_fwd(b64[rows], W_d, False))
+    ok("g_b", gb64[rows], O.decode_input_grad(I.bf16_to_f64(d["g_zt"][rt]), W_d, I.bf16_to_f64(d["g_id"][rt])))
+    # whole weight gradients, accumulated over token chunks in float64
+    dWd_ref, dWe_ref = np.zeros((r, n)), np.zeros((n, r))
+    g_h = O.encode_local_grad(gb64, a64, O.ACT_SILU)
+    for c0 in range(0, T, 2048):
+        c1 = c0 + 2048
+        dWd_ref += O.decode_weight_grad(b64[c0:c1], I.bf16_to_f64(d["g_zt"][c0:c1]))
+        dWe_ref += O.encode_weight_grad(I.bf16_to_f64(d["z"][c0:c1]), g_h[c0:c1])
+    ok("dW_d", dWd, dWd_ref)
+    ok("dW_e", dWe, dWe_ref)
+    ok("g_z", f64(gz[rt.cuda()]), O.encode_input_grad(g_h[rows], W_e))

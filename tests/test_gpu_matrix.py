@@ -109,6 +109,22 @@ def test_muon_update_without_momentum_buffer():
     assert float(np.abs(f64(W) - Wr).max()) <= MAT_BOUND * float(np.abs(Wr).max())
 
 
+@pytest.mark.parametrize("scale", [0.7, 0.0], ids=["explicit", "zero"])
+def test_muon_update_explicit_scale(scale):
+    """An explicit scale is used as given (a negative one selects the default,
+    0.2 sqrt(max(p, q)), which the other Muon tests exercise)."""
+    L = lib()
+    p, q = 333, 40
+    W0 = I.make_matrix(p, q, "gaussian", seed=12, scale=0.1)
+    G = I.make_matrix(p, q, "gaussian", seed=13, scale=0.01)
+    W, M = dev(W0.clone()), dev(torch.zeros(p, q))
+    L.muon_update(W, dev(G), M, 0.05, momentum=0.9, weight_decay=0.01, scale=scale)
+    torch.cuda.synchronize()
+    Wr, _, _ = MU.muon_update(W0.double().numpy(), G.double().numpy(), np.zeros((p, q)), 0.05, 0.9, 0.01,
+                              scale=scale)
+    assert float(np.abs(f64(W) - Wr).max()) <= MAT_BOUND * float(np.abs(Wr).max())
+
+
 SPEC_CASES = [(4096, 32, "gaussian"), (32, 4096, "gaussian"), (8192, 64, "powerlaw"), (333, 40, "powerlaw"),
               (128, 4096, "powerlaw"), (64, 64, "gaussian"), (4096, 32, "orthonormal"), (32, 4096, "rank1"),
               (40, 333, "zero"), (7, 3, "gaussian"), (1, 5, "gaussian"), (5, 1, "gaussian"), (1, 1, "gaussian")]

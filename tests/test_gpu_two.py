@@ -2,11 +2,15 @@
 
 Inputs are seeded bf16 tensors; the oracle computes in float64 on the same
 values.  Bound (as for the one-linear ops): max error <= 2e-2 RMS(ref), after
-a half-ulp discount for bf16 outputs.  Error budget: the GPU rounds phi(u),
-phi(v), g_u and g_v to bf16 before the next product (relative 2^-9 per element,
-averaging out over the contraction) and accumulates in float32.
-Small shapes are checked everywhere; the full 16384-token shape on sampled rows
-(row-local outputs) and sampled columns (token sums).
+a half-ulp discount for bf16 outputs, with no further allowance.  Error
+budget: the GPU rounds phi(u), phi(v) (formed from the float32 accumulator),
+g_u and g_v to bf16 once before the next product (relative 2^-9 per element,
+averaging out over the contraction) and accumulates in float32.  Beside the
+exact oracle every output is also compared with a float64 reference that takes
+exactly those roundings (``spec_*`` below), to the same bound.
+Small shapes are checked everywhere, a fixed-seed sweep of 24 random small
+shapes stresses short contractions, and the full 16384-token shape is checked
+on sampled rows (row-local outputs) and sampled columns (token sums).
 """
 import numpy as np
 import pytest
@@ -14,7 +18,7 @@ import torch
 
 from oracle import resbm_oracle as R
 from oracle import two_linear_oracle as TL
-from gpu_helpers import check, f64, guarded, lib, say, strided
+from gpu_helpers import check, errors, f64, guarded, lib, say, strided
 from paper_2604_11947_amd import inputs as I
 
 pytestmark = pytest.mark.gpu
@@ -38,19 +42,64 @@ def np64(d, k):
     return d[k].to(torch.float64).numpy()
 
 
-# Products that consume a bf16 operand the op forms itself (phi(u), phi(v),
-# g_u, g_v: relative rounding <= 2^-9 per element) may be off, element by
-# element, by 2^-9 sum_k |A[., k]| |B[k, .]| before any averaging; the allowance
-# is twice that.  It matters where the contraction is short (T = 1 for a
-# weight gradient, a small m for z~ and b).
-def allow(A, B):
-    """For a token sum A^T B (A, B token-major)."""
-    return 2.0 ** -8 * (np.abs(A).T @ np.abs(B))
+# Float64 references that round the op-formed intermediates to bf16 where the
+# kernels are specified to (include/resbm.h): phi(u), phi(v), g_u, g_v.  They
+# use the oracle's bf16 rounding and its phi / phi'; the exact oracle itself
+# stays unrounded.
+def rb(x):
+    return R.rne_bf16(x)
 
 
-def allow_rows(A, B):
-    """For a row product A B."""
-    return 2.0 ** -8 * (np.abs(A) @ np.abs(B))
+def spec_encode2_fwd(x, z, W1, W2, act):
+    u = z @ W1
+    return R.p_id(x, W2.shape[1]) + rb(R.phi(u, act)) @ W2
+
+
+def spec_decode2_fwd(b, W3, W4, act):
+    return rb(R.phi(b @ W3, act)) @ W4
+
+
+def spec_decode2_bwd(b, v, g_zt, g_id, W3, W4, act):
+    g_v = rb((g_zt @ W4.T) * R.dphi(v, act))
+    g_b = g_v @ W3.T
+    if g_id is not None:
+        g_b = g_b + R.p_id(g_id, W3.shape[0])
+    return g_b, b.T @ g_v, rb(R.phi(v, act)).T @ g_zt
+
+
+def spec_encode2_bwd(z, u, g_b, W1, W2, act):
+    g_u = rb((g_b @ W2.T) * R.dphi(u, act))
+    return g_u @ W1.T, z.T @ g_u, rb(R.phi(u, act)).T @ g_b
+
+
+# A weight gradient dW = A^T B (a sum over T tokens) in which one factor is an
+# op-formed bf16 intermediate (phi(u), phi(v), g_u, g_v) inherits that factor's
+# rounding, up to 2^-9 of |A_t||B_t| per term.  Over many tokens it averages
+# out; over a handful it does not (at T = 1 the gradient is one outer product
+# and its elementwise relative error is the rounding itself), so below
+# FEW_TOKENS the exact-oracle check of a weight gradient discounts exactly that
+# worst case, 2^-9 sum_t |A_t||B_t| (the weight-gradient counterpart of the
+# half-ulp discount of bf16 outputs), and the specified-rounding check, which
+# could differ by one flipped rounding of a factor, only reports.  Row
+# products (b, z~, g_b, g_z) and every output at T >= FEW_TOKENS get no
+# allowance.
+FEW_TOKENS = 16
+
+
+def token_sum_rounding(A, B):
+    return 2.0 ** -9 * (np.abs(A).T @ np.abs(B))
+
+
+def both(name, gpu, ref, spec, bf16_output, factors=None):
+    """The exact oracle and the specified-rounding reference, each to the plain
+    bound; `factors` (A, B) marks a weight gradient A^T B (see FEW_TOKENS)."""
+    few = factors is not None and factors[0].shape[0] < FEW_TOKENS
+    check(name, gpu, ref, bf16_output, allow=token_sum_rounding(*factors) if few else None)
+    if few:
+        e = errors(f64(gpu), spec, bf16_output)
+        say(f"    {name + ' spec':10s} raw={e['raw']:.2e} (reported only: {factors[0].shape[0]} tokens)")
+    else:
+        check(name + " spec", gpu, spec, bf16_output)
 
 
 @pytest.mark.parametrize("act", ACTS)
@@ -66,9 +115,9 @@ def test_encode2_fwd(T, n, m, r, act):
     torch.cuda.synchronize()
     chk_b()
     chk_u()
-    rb, ru = TL.encode2_fwd(np64(d, "x_attn"), np64(d, "z"), np64(d, "W1"), np64(d, "W2"), act)
+    rb_, ru = TL.encode2_fwd(np64(d, "x_attn"), np64(d, "z"), np64(d, "W1"), np64(d, "W2"), act)
     check("u", u, ru, True)
-    check("b", b, rb, True, allow=allow_rows(R.phi(ru, act), np64(d, "W2")))
+    both("b", b, rb_, spec_encode2_fwd(np64(d, "x_attn"), np64(d, "z"), np64(d, "W1"), np64(d, "W2"), act), True)
 
 
 @pytest.mark.parametrize("act", ACTS)
@@ -86,7 +135,7 @@ def test_decode2_fwd(T, n, m, r, act):
     assert bool(torch.isnan(zt_buf[:, n:].float()).all()), "row padding of z~ overwritten"
     rzt, rv = TL.decode2_fwd(np64(d, "b"), np64(d, "W3"), np64(d, "W4"), act)
     check("v", v, rv, True)
-    check("z~", zt, rzt, True, allow=allow_rows(R.phi(rv, act), np64(d, "W4")))
+    both("z~", zt, rzt, spec_decode2_fwd(np64(d, "b"), np64(d, "W3"), np64(d, "W4"), act), True)
 
 
 @pytest.mark.parametrize("with_gid", [True, False])
@@ -106,11 +155,13 @@ def test_decode2_bwd(T, n, m, r, act, with_gid):
     chk()
     rg_b, rdW3, rdW4 = TL.decode2_bwd(np64(d, "b"), np64(d, "v"), np64(d, "g_zt"),
                                       np64(d, "g_id") if with_gid else None, np64(d, "W3"), np64(d, "W4"), act)
+    sg_b, sdW3, sdW4 = spec_decode2_bwd(np64(d, "b"), np64(d, "v"), np64(d, "g_zt"),
+                                        np64(d, "g_id") if with_gid else None, np64(d, "W3"), np64(d, "W4"), act)
     b, v, g_zt = np64(d, "b"), np64(d, "v"), np64(d, "g_zt")
     g_v = (g_zt @ np64(d, "W4").T) * R.dphi(v, act)
-    check("g_b", g_b, rg_b, True, allow=allow_rows(g_v, np64(d, "W3").T))
-    check("dW3", dW3, rdW3, False, allow=allow(b, g_v))
-    check("dW4", dW4, rdW4, False, allow=allow(R.phi(v, act), g_zt))
+    both("g_b", g_b, rg_b, sg_b, True)
+    both("dW3", dW3, rdW3, sdW3, False, factors=(b, g_v))
+    both("dW4", dW4, rdW4, sdW4, False, factors=(R.phi(v, act), g_zt))
 
 
 @pytest.mark.parametrize("gx_mode", ["separate", "fused", "none"])
@@ -138,16 +189,81 @@ def test_encode2_bwd(T, n, m, r, act, gx_mode):
     rg_z, rdW1, rdW2 = TL.encode2_bwd(np64(d, "z"), np64(d, "u"), np64(d, "g_b"), np64(d, "W1"), np64(d, "W2"), act)
     if gx_mode == "fused":
         rg_z = R.skip_grad(rg_z, np64(d, "g_b"))
+    sg_z, sdW1, sdW2 = spec_encode2_bwd(np64(d, "z"), np64(d, "u"), np64(d, "g_b"), np64(d, "W1"), np64(d, "W2"), act)
+    if gx_mode == "fused":
+        sg_z = R.skip_grad(sg_z, np64(d, "g_b"))
     u, gb = np64(d, "u"), np64(d, "g_b")
     g_u = (gb @ np64(d, "W2").T) * R.dphi(u, act)
-    check("g_z", g_z, rg_z, True, allow=allow_rows(g_u, np64(d, "W1").T))
-    check("dW1", dW1, rdW1, False, allow=allow(np64(d, "z"), g_u))
-    check("dW2", dW2, rdW2, False, allow=allow(R.phi(u, act), gb))
+    both("g_z", g_z, rg_z, sg_z, True)
+    both("dW1", dW1, rdW1, sdW1, False, factors=(np64(d, "z"), g_u))
+    both("dW2", dW2, rdW2, sdW2, False, factors=(R.phi(u, act), gb))
     if gx_mode == "separate":
         gx_ref = R.skip_grad(gx0.to(torch.float64).numpy(), np64(d, "g_b"))
         got = f64(g_x)
         assert np.array_equal(got[:, r:], gx_ref[:, r:]), "g_x columns >= r changed"
         check("g_x", g_x, gx_ref, True)
+
+
+def sweep_shapes(count=24, seed=2404):
+    """Fixed-seed random small shapes: short contractions (m, r, T down to 8, 8, 1)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        n = 8 * int(rng.integers(1, 65))
+        m = 8 * int(rng.integers(1, 41))
+        r = 8 * int(rng.integers(1, min(n // 8, 16) + 1))
+        T = int(rng.choice([1, 2, 7, int(rng.integers(1, 700))]))
+        out.append((T, n, m, r))
+    return out
+
+
+SWEEP = sweep_shapes()
+
+
+@pytest.mark.parametrize("T,n,m,r", SWEEP, ids=[f"T{T}_n{n}_m{m}_r{r}" for T, n, m, r in SWEEP])
+def test_two_sweep(T, n, m, r):
+    """All four ops with SiLU on a seeded sweep of small shapes, to the plain bound."""
+    L = lib()
+    act = R.ACT_SILU
+    say(f"two-linear sweep T={T} n={n} m={m} r={r}")
+    d = data(T, n, m, r, seed=T + n + m + r)
+    W1, W2, W3, W4 = (np64(d, k) for k in ("W1", "W2", "W3", "W4"))
+    dv = {k: v.cuda() for k, v in d.items() if isinstance(v, torch.Tensor)}
+    bf = torch.bfloat16
+    b, u = torch.empty(T, r, dtype=bf, device="cuda"), torch.empty(T, m, dtype=bf, device="cuda")
+    zt, v = torch.empty(T, n, dtype=bf, device="cuda"), torch.empty(T, m, dtype=bf, device="cuda")
+    g_b, g_z = torch.empty(T, r, dtype=bf, device="cuda"), torch.empty(T, n, dtype=bf, device="cuda")
+    dW1, dW2 = torch.empty(n, m, device="cuda"), torch.empty(m, r, device="cuda")
+    dW3, dW4 = torch.empty(r, m, device="cuda"), torch.empty(m, n, device="cuda")
+    L.encode2_fwd(dv["x_attn"], dv["z"], dv["W1"], dv["W2"], b, u, act=act)
+    L.decode2_fwd(dv["b"], dv["W3"], dv["W4"], zt, v, act=act)
+    L.decode2_bwd(dv["b"], dv["v"], dv["g_zt"], dv["g_id"], dv["W3"], dv["W4"], g_b, dW3, dW4, act=act)
+    L.encode2_bwd(dv["z"], dv["u"], dv["g_b"], dv["W1"], dv["W2"], g_z, dW1, dW2, g_x=g_z, act=act)
+    torch.cuda.synchronize()
+    x, z = np64(d, "x_attn"), np64(d, "z")
+    rb_, ru = TL.encode2_fwd(x, z, W1, W2, act)
+    check("u", u, ru, True)
+    both("b", b, rb_, spec_encode2_fwd(x, z, W1, W2, act), True)
+    rzt, rv = TL.decode2_fwd(np64(d, "b"), W3, W4, act)
+    check("v", v, rv, True)
+    both("z~", zt, rzt, spec_decode2_fwd(np64(d, "b"), W3, W4, act), True)
+    bb, vv, gzt, gb = np64(d, "b"), np64(d, "v"), np64(d, "g_zt"), np64(d, "g_b")
+    g_v = (gzt @ W4.T) * R.dphi(vv, act)
+    args = (bb, vv, gzt, np64(d, "g_id"), W3, W4, act)
+    factors = (None, (bb, g_v), (R.phi(vv, act), gzt))
+    for nm, got, ref, spec, fa in zip(("g_b", "dW3", "dW4"), (g_b, dW3, dW4), TL.decode2_bwd(*args),
+                                      spec_decode2_bwd(*args), factors):
+        both(nm, got, ref, spec, nm == "g_b", factors=fa)
+    uu = np64(d, "u")
+    g_u = (gb @ W2.T) * R.dphi(uu, act)
+    args = (z, uu, gb, W1, W2, act)
+    ref = list(TL.encode2_bwd(*args))
+    spec = list(spec_encode2_bwd(*args))
+    ref[0] = R.skip_grad(ref[0], gb)
+    spec[0] = R.skip_grad(spec[0], gb)
+    factors = (None, (z, g_u), (R.phi(uu, act), gb))
+    for nm, got, rr, ss, fa in zip(("g_z", "dW1", "dW2"), (g_z, dW1, dW2), ref, spec, factors):
+        both(nm, got, rr, ss, nm == "g_z", factors=fa)
 
 
 def test_two_empty_batch_is_noop():
@@ -269,7 +385,7 @@ def test_two_graph_replay_matches_eager():
     o = outs
 
     def step():
-        L.encode2_fwd(d["x_attn"], d["z"], d["W1"], d["W2"], o["b"], o["u"])
+        L.encode2_fwd(d["x_attn"], d["z"], d["W1"], d["W2"], o["b"], o["u"], ws=ws)
         L.decode2_fwd(o["b"], d["W3"], d["W4"], o["zt"], o["v"], ws=ws)
         L.decode2_bwd(o["b"], o["v"], d["g_zt"], d["g_id"], d["W3"], d["W4"], o["g_b"], o["dW3"], o["dW4"], ws=ws)
         L.encode2_bwd(d["z"], o["u"], o["g_b"], d["W1"], d["W2"], o["g_z"], o["dW1"], o["dW2"], g_x=o["g_z"], ws=ws)

@@ -47,6 +47,27 @@ def _rne_truncate(x):
     return ((f.view(np.uint32) >> 16) << 16).view(np.float32).astype(np.float64)
 
 
+def _chain_wire_gradient_unrounded(x_attn, z, W_e, W_d, g_zt, g_id, act, add_identity, wire_round=True):
+    b, a = R.encode_fwd(x_attn, z, W_e, act)
+    b_w = R.rne_bf16(b) if wire_round else b
+    zt = R.decode_fwd(b_w, W_d, add_identity)
+    g_b, dW_d = R.decode_bwd(b_w, W_d, g_zt, g_id)
+    g_z, dW_e = R.encode_bwd(z, W_e, a, g_b, act)
+    return {"a": a, "b": b, "b_wire": b_w, "z_tilde": zt, "g_b": g_b, "g_b_wire": g_b, "dW_d": dW_d,
+            "g_z": g_z, "dW_e": dW_e}
+
+
+def _chain_decoder_grad_on_unrounded_payload(x_attn, z, W_e, W_d, g_zt, g_id, act, add_identity, wire_round=True):
+    b, a = R.encode_fwd(x_attn, z, W_e, act)
+    b_w = R.rne_bf16(b) if wire_round else b
+    zt = R.decode_fwd(b_w, W_d, add_identity)
+    g_b, dW_d = R.decode_bwd(b, W_d, g_zt, g_id)
+    g_bw = R.rne_bf16(g_b) if wire_round else g_b
+    g_z, dW_e = R.encode_bwd(z, W_e, a, g_bw, act)
+    return {"a": a, "b": b, "b_wire": b_w, "z_tilde": zt, "g_b": g_b, "g_b_wire": g_bw, "dW_d": dW_d,
+            "g_z": g_z, "dW_e": dW_e}
+
+
 MUTATIONS = [
     ("dphi", _silu_dphi_dropped_term,
      lambda: P.test_gradients_finite_differences(O.ACT_SILU, False, 3, 8, 2)),
@@ -57,10 +78,14 @@ MUTATIONS = [
      lambda: P.test_gradients_torch_autograd(O.ACT_SILU, True)),
     ("phi", _phi_sign, lambda: P.test_forward_brute_force(O.ACT_SILU, False, 3, 8, 2)),
     ("rne_bf16", _rne_truncate, P.test_rne_bf16_matches_torch_on_float32_inputs),
+    ("boundary_fwd_bwd", _chain_wire_gradient_unrounded,
+     lambda: P.test_wire_rounded_chain_torch_autograd(O.ACT_SILU, False)),
+    ("boundary_fwd_bwd", _chain_decoder_grad_on_unrounded_payload,
+     lambda: P.test_wire_rounded_chain_torch_autograd(O.ACT_IDENTITY, True)),
 ]
 
 
-@pytest.mark.parametrize("name,bad,pin", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+@pytest.mark.parametrize("name,bad,pin", MUTATIONS, ids=[f"{m[0]}:{m[1].__name__.lstrip('_')}" for m in MUTATIONS])
 def test_pin_rejects_planted_mistake(monkeypatch, name, bad, pin):
     monkeypatch.setattr(R, name, bad)
     monkeypatch.setattr(O, name, bad)

@@ -301,6 +301,63 @@ def test_gradients_torch_autograd(act, add_identity):
     np.testing.assert_allclose(b_o, b.detach().numpy(), rtol=1e-13, atol=1e-14)
 
 
+class _Wire(torch.autograd.Function):
+    """The link of App. A.3 as a graph node: the payload crosses as bf16 on the
+    way forward and its gradient crosses as bf16 on the way back (torch's own
+    float -> bfloat16 conversion, via float32)."""
+
+    @staticmethod
+    def forward(ctx, x):
+        return x.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+
+    @staticmethod
+    def backward(ctx, g):
+        return g.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+
+
+@pytest.mark.parametrize("act", ACTS)
+@pytest.mark.parametrize("add_identity", [False, True])
+def test_wire_rounded_chain_torch_autograd(act, add_identity):
+    """The oracle's chain mode (wire_round=True) against float64 torch autograd
+    of the forward graph with the link as a node that rounds to bf16 both ways:
+    b is rounded before the decoder and its weight gradient, the wire gradient
+    is rounded before the encoder backward, and a keeps its unrounded value."""
+    rng = np.random.default_rng(12)
+    T, n, r = 13, 40, 8
+    d = module_inputs(rng, T, n, r)
+    tt = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in d.items()}
+    a = tt["z"] @ tt["W_e"]
+    f = torch.nn.functional.silu(a) if act == O.ACT_SILU else a
+    b = tt["x_attn"][:, :r] + f
+    bw = _Wire.apply(b)
+    bw.retain_grad()
+    zt = bw @ tt["W_d"]
+    pad_b = torch.nn.functional.pad(bw, (0, n - r))
+    if add_identity:
+        zt = zt + pad_b
+        L = (tt["g_zt"] * zt).sum()
+    else:
+        L = (tt["g_zt"] * zt).sum() + (tt["g_id"] * pad_b).sum()
+    names = ["x_attn", "z", "W_e", "W_d"]
+    tg = dict(zip(names, torch.autograd.grad(L, [tt[k] for k in names] + [bw], retain_graph=False)[:4]))
+    g_id = d["g_zt"] if add_identity else d["g_id"]
+    out = O.boundary_fwd_bwd(d["x_attn"], d["z"], d["W_e"], d["W_d"], d["g_zt"], g_id, act, add_identity,
+                             wire_round=True)
+    np.testing.assert_array_equal(out["b_wire"], bw.detach().numpy())
+    np.testing.assert_allclose(out["z_tilde"], zt.detach().numpy(), rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(out["dW_d"], tg["W_d"].numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(out["dW_e"], tg["W_e"].numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(out["g_z"], tg["z"].numpy(), rtol=1e-12, atol=1e-13)
+    # the residual gradient on the encoder side is the rounded wire gradient on columns [0, r)
+    np.testing.assert_allclose(O.skip_grad(np.zeros((T, n)), out["g_b_wire"]), tg["x_attn"].numpy(),
+                               rtol=1e-12, atol=1e-13)
+    # the rounding is not vacuous here: the unrounded chain differs
+    plain = O.boundary_fwd_bwd(d["x_attn"], d["z"], d["W_e"], d["W_d"], d["g_zt"], g_id, act, add_identity,
+                               wire_round=False)
+    assert not np.array_equal(plain["b"], out["b_wire"])
+    assert np.max(np.abs(plain["dW_e"] - out["dW_e"])) > 1e-6 * np.max(np.abs(plain["dW_e"]))
+
+
 def test_skip_grad_is_adjoint_of_p_id():
     """<P^id(b), G> = <b, P^id^T(G)> for the encoder-side identity path."""
     rng = np.random.default_rng(9)
