@@ -145,6 +145,31 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act,
                          void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * resbm_encode_bwd without a workspace argument, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results and rules as
+ * resbm_encode_bwd; the op's scratch is a fixed device-resident array of
+ * RESBM_NOALLOC_SCRATCH_BYTES bytes per device, part of the library's code
+ * object and held until the process ends.  The call allocates nothing.
+ *  - Limit: calls whose encode_bwd scratch would exceed the array return
+ *    RESBM_E_WORKSPACE (every (T, n, r) with resbm_workspace_bytes(T, n, r)
+ *    <= RESBM_NOALLOC_SCRATCH_BYTES fits; at n = 4096, r = 32 that is over
+ *    400k tokens).
+ *  - The array's address on a device is looked up on the first call that
+ *    runs there (the device of `stream`, or the current one for NULL).
+ *  - Every call on one device shares that device's array: calls that may
+ *    run at the same time on one device (different streams) race and must
+ *    be ordered by the caller.
+ */
+#define RESBM_NOALLOC_SCRATCH_BYTES (64u << 20)
+int32_t resbm_encode_bwd_noalloc(int64_t T, int32_t n, int32_t r, int32_t act,
+                                 const void* z, int64_t ld_z, const float* W_e,
+                                 const float* a_save, const void* g_b,
+                                 void* g_z, int64_t ld_gz,
+                                 void* g_x, int64_t ld_gx,
+                                 float* dW_e, int32_t accumulate, void* stream);
+
+/*
  * Optimizer-side ops on one bottleneck weight (W_e, n x r, or W_d, r x n).
  * Sec. 3.4 trains the bottleneck weights with Muon -- the gradient momentum of
  * a weight matrix is orthogonalised by a Newton-Schulz iteration before the

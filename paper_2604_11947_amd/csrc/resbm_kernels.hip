@@ -31,6 +31,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "resbm.h"
 #include "resbm_buffer.hpp"
 #include "resbm_host.hpp"
@@ -1514,6 +1516,101 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
 
 }  // namespace
 
+// The fixed device-resident scratch of resbm_encode_bwd_noalloc: one array per
+// device, held until the process ends and shared by every such call on that
+// device.  Host code never uses its name as an address: the device address is
+// looked up once per device (scratch_address) and passed to the kernels.
+static __device__ __align__(256) unsigned char scratch[RESBM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices];
+
+// Device address of `scratch` on the device that runs `stream` (the current
+// device for the null stream), taken with hipGetSymbolAddress once per device
+// with that device current.
+int32_t scratch_address(hipStream_t stream, void** out) {
+  int dev = -1;
+  if (stream ? hipStreamGetDevice(stream, &dev) != hipSuccess : hipGetDevice(&dev) != hipSuccess) return RESBM_E_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return RESBM_E_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return RESBM_E_HIP;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return RESBM_E_HIP;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) return RESBM_E_HIP;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return RESBM_OK;
+}
+
+// encode_bwd with the caller's workspace, or (noalloc) with the device's fixed
+// scratch; every argument is validated before the first HIP call.
+int32_t encode_bwd_impl(int64_t T, int32_t n, int32_t r, int32_t act, const void* z, int64_t ld_z,
+                        const float* W_e, const float* a_save, const void* g_b, void* g_z, int64_t ld_gz,
+                        void* g_x, int64_t ld_gx, float* dW_e, int32_t accumulate, void* ws, size_t ws_bytes,
+                        bool noalloc, void* stream) {
+  if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
+  if (T < 0 || !shape_ok(n, r)) return RESBM_E_SHAPE;
+  if (T == 0) return RESBM_OK;
+  const Plan p = make_plan(T, n, r);
+  if (noalloc) {
+    if (p.eb_ws > (size_t)RESBM_NOALLOC_SCRATCH_BYTES) return RESBM_E_WORKSPACE;
+  } else {
+    int32_t st = check_common(T, n, r, (int64_t)p.eb_ws, ws, ws_bytes);
+    if (st) return st;
+  }
+  if (!z || !W_e || !g_b || !g_z || !dW_e) return RESBM_E_NULL;
+  if (act == RESBM_ACT_SILU && !a_save) return RESBM_E_ACT;
+  if (!ld_ok(ld_z, n) || !ld_ok(ld_gz, n) || (g_x && !ld_ok(ld_gx, n)) || !window_ok(64, ld_z) ||
+      !window_ok(p.df_tpg, ld_gz))
+    return RESBM_E_SHAPE;
+  if (!aligned(z, 16) || !aligned(W_e, 16) || !aligned(g_b, 16) || !aligned(g_z, 16) || !aligned(dW_e, 16) ||
+      (a_save && !aligned(a_save, 16)) || (g_x && !aligned(g_x, 16)))
+    return RESBM_E_ALIGN;
+  const int fused = g_x != nullptr && g_x == g_z;
+  if (fused && ld_gx != ld_gz) return RESBM_E_ALIAS;
+  const size_t bz = extent(T, n, ld_z, kIoBytes), bgz = extent(T, n, ld_gz, kIoBytes);
+  const size_t bx = (g_x && !fused) ? extent(T, n, ld_gx, kIoBytes) : 0;
+  const size_t bb = (size_t)T * r * kIoBytes, ba = a_save ? (size_t)T * r * 4 : 0, bw = (size_t)n * r * 4;
+  if (overlap(g_z, bgz, z, bz) || overlap(g_z, bgz, g_b, bb) || overlap(g_z, bgz, a_save, ba) ||
+      overlap(g_z, bgz, W_e, bw) || overlap(g_z, bgz, dW_e, bw) || overlap(g_x, bx, z, bz) ||
+      overlap(g_x, bx, g_z, bgz) || overlap(g_x, bx, g_b, bb) || overlap(g_x, bx, a_save, ba) ||
+      overlap(g_x, bx, W_e, bw) || overlap(g_x, bx, dW_e, bw) || overlap(dW_e, bw, z, bz) ||
+      overlap(dW_e, bw, g_b, bb) || overlap(dW_e, bw, a_save, ba) || overlap(dW_e, bw, W_e, bw) ||
+      overlap(ws, p.eb_ws, z, bz) || overlap(ws, p.eb_ws, g_z, bgz) || overlap(ws, p.eb_ws, g_x, bx) ||
+      overlap(ws, p.eb_ws, g_b, bb) || overlap(ws, p.eb_ws, a_save, ba) || overlap(ws, p.eb_ws, dW_e, bw) ||
+      overlap(ws, p.eb_ws, W_e, bw))
+    return RESBM_E_ALIAS;
+  hipStream_t s = (hipStream_t)stream;
+  if (noalloc) {
+    const int32_t e = scratch_address(s, &ws);
+    if (e) return e;
+  }
+  float* dwp = (float*)((char*)ws + p.eb_dwp_off);
+  io_t* gh_hi = (io_t*)((char*)ws + p.eb_gh_off);
+  io_t* gh_lo = gh_hi + (RESBM_IO_F32_BUILD ? 0 : T * r);  // bf16 build: hi and lo planes
+  const io_t* Z = (const io_t*)z;
+  const io_t* GB = (const io_t*)g_b;
+  io_t* GZ = (io_t*)g_z;
+  const float* AS = act == RESBM_ACT_SILU ? a_save : nullptr;
+  const int64_t nb_dw = ceil_div((int64_t)n * (r / 4), 64);
+  const int64_t nb_gx = (g_x && !fused) ? ceil_div(T * (r / 4), 256) : 0;
+  const FinArgs fin{p.RP, dwp, p.eb_ntg, dW_e, accumulate, nb_dw, nb_dw + nb_gx, GB, (io_t*)g_x, ld_gx};
+#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, gh_hi, gh_lo, fin, s)
+  RESBM_DISPATCH_NT(p.NT, CALL)
+#undef CALL
+  return launch_status();
+}
+
+}  // namespace
+
 extern "C" {
 
 int32_t resbm_encode_fwd(int64_t T, int32_t n, int32_t r, int32_t act, const void* x_attn, int64_t ld_x,
@@ -1627,49 +1724,15 @@ int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
                          const float* W_e, const float* a_save, const void* g_b, void* g_z, int64_t ld_gz,
                          void* g_x, int64_t ld_gx, float* dW_e, int32_t accumulate, void* ws, size_t ws_bytes,
                          void* stream) {
-  if (act != RESBM_ACT_IDENTITY && act != RESBM_ACT_SILU) return RESBM_E_ACT;
-  if (T < 0 || !shape_ok(n, r)) return RESBM_E_SHAPE;
-  if (T == 0) return RESBM_OK;
-  const Plan p = make_plan(T, n, r);
-  int32_t st = check_common(T, n, r, (int64_t)p.eb_ws, ws, ws_bytes);
-  if (st) return st;
-  if (!z || !W_e || !g_b || !g_z || !dW_e) return RESBM_E_NULL;
-  if (act == RESBM_ACT_SILU && !a_save) return RESBM_E_ACT;
-  if (!ld_ok(ld_z, n) || !ld_ok(ld_gz, n) || (g_x && !ld_ok(ld_gx, n)) || !window_ok(64, ld_z) ||
-      !window_ok(p.df_tpg, ld_gz))
-    return RESBM_E_SHAPE;
-  if (!aligned(z, 16) || !aligned(W_e, 16) || !aligned(g_b, 16) || !aligned(g_z, 16) || !aligned(dW_e, 16) ||
-      (a_save && !aligned(a_save, 16)) || (g_x && !aligned(g_x, 16)))
-    return RESBM_E_ALIGN;
-  const int fused = g_x != nullptr && g_x == g_z;
-  if (fused && ld_gx != ld_gz) return RESBM_E_ALIAS;
-  const size_t bz = extent(T, n, ld_z, kIoBytes), bgz = extent(T, n, ld_gz, kIoBytes);
-  const size_t bx = (g_x && !fused) ? extent(T, n, ld_gx, kIoBytes) : 0;
-  const size_t bb = (size_t)T * r * kIoBytes, ba = a_save ? (size_t)T * r * 4 : 0, bw = (size_t)n * r * 4;
-  if (overlap(g_z, bgz, z, bz) || overlap(g_z, bgz, g_b, bb) || overlap(g_z, bgz, a_save, ba) ||
-      overlap(g_z, bgz, W_e, bw) || overlap(g_z, bgz, dW_e, bw) || overlap(g_x, bx, z, bz) ||
-      overlap(g_x, bx, g_z, bgz) || overlap(g_x, bx, g_b, bb) || overlap(g_x, bx, a_save, ba) ||
-      overlap(g_x, bx, W_e, bw) || overlap(g_x, bx, dW_e, bw) || overlap(dW_e, bw, z, bz) ||
-      overlap(dW_e, bw, g_b, bb) || overlap(dW_e, bw, a_save, ba) || overlap(dW_e, bw, W_e, bw) ||
-      overlap(ws, p.eb_ws, z, bz) || overlap(ws, p.eb_ws, g_z, bgz) || overlap(ws, p.eb_ws, g_x, bx) ||
-      overlap(ws, p.eb_ws, g_b, bb) || overlap(ws, p.eb_ws, a_save, ba) || overlap(ws, p.eb_ws, dW_e, bw) ||
-      overlap(ws, p.eb_ws, W_e, bw))
-    return RESBM_E_ALIAS;
-  hipStream_t s = (hipStream_t)stream;
-  float* dwp = (float*)((char*)ws + p.eb_dwp_off);
-  io_t* gh_hi = (io_t*)((char*)ws + p.eb_gh_off);
-  io_t* gh_lo = gh_hi + (RESBM_IO_F32_BUILD ? 0 : T * r);  // bf16 build: hi and lo planes
-  const io_t* Z = (const io_t*)z;
-  const io_t* GB = (const io_t*)g_b;
-  io_t* GZ = (io_t*)g_z;
-  const float* AS = act == RESBM_ACT_SILU ? a_save : nullptr;
-  const int64_t nb_dw = ceil_div((int64_t)n * (r / 4), 64);
-  const int64_t nb_gx = (g_x && !fused) ? ceil_div(T * (r / 4), 256) : 0;
-  const FinArgs fin{p.RP, dwp, p.eb_ntg, dW_e, accumulate, nb_dw, nb_dw + nb_gx, GB, (io_t*)g_x, ld_gx};
-#define CALL(NTV) launch_enc_bwd<NTV>(p, act, Z, ld_z, W_e, AS, GB, GZ, ld_gz, fused, dwp, gh_hi, gh_lo, fin, s)
-  RESBM_DISPATCH_NT(p.NT, CALL)
-#undef CALL
-  return launch_status();
+  return encode_bwd_impl(T, n, r, act, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, g_x, ld_gx, dW_e, accumulate, ws,
+                         ws_bytes, false, stream);
+}
+
+int32_t resbm_encode_bwd_noalloc(int64_t T, int32_t n, int32_t r, int32_t act, const void* z, int64_t ld_z,
+                                 const float* W_e, const float* a_save, const void* g_b, void* g_z, int64_t ld_gz,
+                                 void* g_x, int64_t ld_gx, float* dW_e, int32_t accumulate, void* stream) {
+  return encode_bwd_impl(T, n, r, act, z, ld_z, W_e, a_save, g_b, g_z, ld_gz, g_x, ld_gx, dW_e, accumulate,
+                         nullptr, 0, true, stream);
 }
 
 size_t resbm_workspace_bytes(int64_t T, int32_t n, int32_t r) {

@@ -40,6 +40,8 @@ SIGNATURES = [
     ("resbm_decode_bwd", _i32, [_i64, _i32, _i32, _p, _p, _p, _i64, _p, _i64, _p, _p, _i32, _p, _sz, _p]),
     ("resbm_encode_bwd", _i32, [_i64, _i32, _i32, _i32, _p, _i64, _p, _p, _p, _p, _i64, _p, _i64, _p, _i32,
                                 _p, _sz, _p]),
+    ("resbm_encode_bwd_noalloc", _i32, [_i64, _i32, _i32, _i32, _p, _i64, _p, _p, _p, _p, _i64, _p, _i64, _p,
+                                        _i32, _p]),
     ("resbm_newton_schulz", _i32, [_i32, _i32, _p, _p, _i32, _d, _d, _d, _p, _sz, _p]),
     ("resbm_muon_update", _i32, [_i32, _i32, _p, _p, _p, _d, _d, _d, _d, _i32, _i32, _d, _d, _d, _p, _sz, _p]),
     ("resbm_spectrum", _i32, [_i32, _i32, _p, _p, _p, _p, _sz, _p]),
@@ -220,6 +222,31 @@ class Library:
                                         ws.numel(), _stream(stream, z))
         self._check("resbm_encode_bwd", st)
 
+
+    def encode_bwd_noalloc(self, z, W_e, a_save, g_b, g_z, dW_e, g_x=None, act=ACT_SILU, accumulate=False,
+                           stream=None):
+        """resbm_encode_bwd_noalloc: encode_bwd on the library's fixed device-resident
+        scratch (no workspace argument, nothing allocated)."""
+        T = z.shape[0]
+        n, r = W_e.shape
+        io = self.io_dtype
+        for t, nm in ((z, "z"), (g_b, "g_b"), (g_z, "g_z"), (g_x, "g_x")):
+            _dtype(t, io, nm)
+        _dtype(W_e, torch.float32, "W_e")
+        _dtype(a_save, torch.float32, "a_save")
+        _dtype(dW_e, torch.float32, "dW_e")
+        ld_z = _ld(z, T, n, "z")
+        ld_gz = _ld(g_z, T, n, "g_z")
+        ld_gx = _ld(g_x, T, n, "g_x") if g_x is not None else 0
+        _packed(W_e, n, r, "W_e")
+        _packed(g_b, T, r, "g_b")
+        _packed(dW_e, n, r, "dW_e")
+        if a_save is not None:
+            _packed(a_save, T, r, "a_save")
+        st = self.cdll.resbm_encode_bwd_noalloc(T, n, r, act, _ptr(z), ld_z, _ptr(W_e), _ptr(a_save), _ptr(g_b),
+                                                _ptr(g_z), ld_gz, _ptr(g_x), ld_gx, _ptr(dW_e),
+                                                int(bool(accumulate)), _stream(stream, z))
+        self._check("resbm_encode_bwd_noalloc", st)
 
     # ------------------------------------------------------------ two-linears-per-side ops
     # Weights W1 (n x m), W2 (m x r), W3 (r x m), W4 (m x n) and every activation

@@ -225,6 +225,29 @@ def test_descriptor_window_limit(lib):
                               None) == R.E_SHAPE
 
 
+@needs_no_gpu
+def test_encode_bwd_noalloc_validation(lib):
+    """The allocation-free encode_bwd validates like encode_bwd and rejects a call
+    whose scratch would exceed the fixed array, all before any HIP call."""
+    c = lib.cdll
+    ok = [T, N, RR, 1, A, N, 2 * A, 3 * A, 4 * A, 5 * A, N, 6 * A, N, 7 * A, 0, None]
+
+    def call(**kw):
+        names = ["T", "n", "r", "act", "z", "ldz", "We", "a", "gb", "gz", "ldgz", "gx", "ldgx", "dWe", "acc", "s"]
+        a = list(ok)
+        for k, v in kw.items():
+            a[names.index(k)] = v
+        return c.resbm_encode_bwd_noalloc(*a)
+
+    assert call(T=0, z=None, We=None, a=None, gb=None, gz=None, gx=None, dWe=None) == R.OK
+    assert call(a=None) == R.E_ACT
+    assert call(z=None) == R.E_NULL
+    assert call(n=100) == R.E_SHAPE
+    assert call(gz=A) == R.E_ALIAS
+    assert call(gb=4 * A + 4) == R.E_ALIGN
+    assert call(T=16384, n=65536, r=256, ldz=65536, ldgz=65536, gx=None) == R.E_WORKSPACE
+
+
 # ---------------------------------------------------------------- optimizer-side ops
 def test_matrix_workspace_bytes(lib):
     assert lib.matrix_workspace_bytes(0, 32) == 0
