@@ -1378,6 +1378,647 @@ __global__ __launch_bounds__(256) void k_expand(int64_t T, int n, int r,
   }
 }
 
+
+// ============================================================ wide rank (r > 64)
+// Above r = 64 the matrix-core work per streamed byte grows with r, and the
+// kernels above, shaped for r <= 64, re-read their r-wide operands too often:
+// encode_fwd reads all of W_e's fragments per 16 tokens, the expand kernel
+// fetches the input rows once per wave, encode_bwd forms g_h again in every
+// column block.  The kernels below keep the streaming structure and share the
+// r-wide operands instead: blocks of 64 tokens whose waves split the r outputs
+// (one read of the weight fragments per 64 tokens), input rows staged once per
+// block in LDS, g_h formed once by a kernel of its own.  decode_bwd becomes a
+// row contraction (g_b) and a token contraction (dW_d) over g_z~, which reads
+// g_z~ twice but needs no g_b partial sums (at r = 256 those were 134 MB).
+
+// Fragment-ordered hi/lo copy of W_d (r x n, contiguous along the contraction
+// over n) for the A operand of g_b = g_z~ W_d^T: fragment f = ks * NT + nt,
+// lane (row16, grp) holds W_d[16 nt + row16][32 ks + 8 grp + e], zeros at rows >= r.
+__global__ __launch_bounds__(64) void k_wd_prep(const float* __restrict__ W_d, int n, int r, int NT,
+                                                void* __restrict__ wf) {
+  const int64_t gid = (int64_t)blockIdx.x * 64 + threadIdx.x;
+  const int64_t total = (int64_t)(n / 32) * NT * 64;
+  if (gid >= total) return;
+  const int l = (int)(gid & 63);
+  const int64_t f = gid >> 6;
+  const int nt = (int)(f % NT), ks = (int)(f / NT);
+  const int j = nt * 16 + (l & 15), k0 = ks * 32 + (l >> 4) * 8;
+  float w[8];
+  if (j < r) {
+    const float4* p = reinterpret_cast<const float4*>(W_d + (int64_t)j * n + k0);
+    const float4 a = p[0], c = p[1];
+    w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w; w[4] = c.x; w[5] = c.y; w[6] = c.z; w[7] = c.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) w[e] = 0.0f;
+  }
+  store_sfrag(wf, f, l, w);
+}
+
+// Row contraction for wide r: C[t][j] = sum_c X[t][c] M(c, j) over the n
+// columns of a streamed T x n matrix X, M given as split fragments (W_e for
+// encode_fwd, W_d^T for the g_b of decode_bwd).  A block owns 64 tokens; it
+// stages 64 x 256 tiles of X cooperatively in LDS (512-byte row segments) and
+// wave w contracts them against the fragments of j-tiles [w NTW, w NTW + NTW),
+// so every wave ends with whole sums of its columns and the block reads each
+// weight fragment once per 64 tokens.  The weight fragments run three k-steps
+// ahead of their use in a ring of four.
+//   GB = false: a_save = a, b = x_attn[:, :r] + phi(a)        (encode_fwd)
+//   GB = true:  g_b = C + g_id[:, :r] (g_id may be NULL)        (decode_bwd)
+template <int NT, int NTW, bool GB>
+__global__ __launch_bounds__(256) void k_rowc_wide(int64_t T, int n, int r, int act, const io_t* __restrict__ X,
+                                                   int64_t ld_x, const void* __restrict__ wf,
+                                                   const io_t* __restrict__ skip, int64_t ld_s,
+                                                   io_t* __restrict__ out, float* __restrict__ a_save) {
+  constexpr int TOK = 64, MT = 4, BC = 256, KSS = BC / 32;
+  constexpr int LPR = BC / 8;                 // lanes per tile row
+  constexpr int NQ = TOK * LPR / 256;         // cooperative loads per lane and stage
+  constexpr int ZB = RESBM_IO_F32_BUILD ? 1 : 2;
+  constexpr int TILE = TOK * BC * (int)sizeof(io_t);
+  __shared__ __attribute__((aligned(16))) char smem[ZB * TILE];
+
+  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+  const int64_t tok0 = (int64_t)blockIdx.x * TOK;
+  const int nks = n / 32;
+  const int nst = (n + BC - 1) / BC;
+  const rsrc_t zr = make_rsrc(X + tok0 * ld_x, rows_bytes(min((int64_t)TOK, T - tok0), n, ld_x, kEs));
+  const rsrc_t wr = make_rsrc(wf, (int64_t)nks * NT * kSFragBytes);
+  const int zc = 8 * (l % LPR);
+  int zrow[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) zrow[q] = (wave * NQ * 64 + q * 64 + l) / LPR;
+
+  // stages start rotated per group of 8 blocks (one per XCD), as in k_enc_fwd
+  const int srot = (int)((blockIdx.x / 8u) % (unsigned)nst);
+  auto stage_col = [&](int i) {
+    if (i < 0 || i >= nst) return n;
+    const int ir = i + srot < nst ? i + srot : i + srot - nst;
+    return ir * BC;
+  };
+  auto load_z = [&](XFrag (&zz)[NQ], int i) {
+    const int c = stage_col(i) + zc;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) zz[q] = bld_x8(zr, c < n ? (uint32_t)((zrow[q] * ld_x + c) * kEs) : kOOB);
+  };
+  SFrag wring[4][NTW];
+  // the weight fragments of k-step ks of stage i (zeros outside [0, nks) or past NT)
+  auto load_wf = [&](SFrag (&dst)[NTW], int i, int ks) {
+    const int kg = (stage_col(i) >> 5) + ks;
+#pragma unroll
+    for (int jt = 0; jt < NTW; ++jt) {
+      const int jtg = wave * NTW + jt;
+      dst[jt] = bld_sfrag(wr, (int64_t)kg * NT + jtg, l, kg < nks && jtg < NT);
+    }
+  };
+
+  f32x4 acc[MT][NTW];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int jt = 0; jt < NTW; ++jt) acc[mt][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto body = [&](XFrag (&zz)[NQ], int i) {
+    io_t* tile = reinterpret_cast<io_t*>(smem + (ZB == 2 ? (i & 1) : 0) * TILE);
+    if constexpr (ZB == 1) __syncthreads();  // the previous stage's readers of the single tile are done
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      io_t* d = tile + zrow[q] * BC + wide_col(zrow[q], zc);
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = zz[q].v[e];
+#else
+      *reinterpret_cast<uint4*>(d) = __builtin_bit_cast(uint4, zz[q].v);
+#endif
+    }
+    load_z(zz, i + 2);
+    __syncthreads();  // the stage's tile is complete; the other buffer's readers are done
+    const bool live = i >= 0 && i < nst;  // stages outside hold zeros: only their weight loads matter
+#pragma unroll
+    for (int ks = 0; ks < KSS; ++ks) {
+      if (ks + 3 < KSS) load_wf(wring[(ks + 3) & 3], i, ks + 3);
+      else load_wf(wring[(ks + 3) & 3], i + 1, ks + 3 - KSS);
+      if (!live) continue;
+      XFrag f[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int row = 16 * mt + row16;
+        const io_t* p = tile + row * BC + wide_col(row, 32 * ks + 8 * grp);
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[mt].v[e] = p[e];
+#else
+        f[mt].v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+#endif
+      }
+      // waves whose last j-tiles lie past NT multiply zero fragments (never stored)
+#pragma unroll
+      for (int jt = 0; jt < NTW; ++jt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt][jt] = mma_sx(wring[ks & 3][jt], f[mt], acc[mt][jt]);
+    }
+  };
+  XFrag za[NQ], zb[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) za[q] = zb[q] = xfrag_zero();
+  load_wf(wring[0], opaque(-2), 0);
+  load_wf(wring[1], -2, 1);
+  load_wf(wring[2], -2, 2);
+  for (int i = opaque(-2); i < nst; i += 2) {
+    body(za, i);
+    body(zb, i + 1);
+  }
+
+  // acc[mt][jt][v] = C[tok0 + 16 mt + row16][16 (w NTW + jt) + 4 grp + v]
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int jt = 0; jt < NTW; ++jt) {
+      const int jtg = wave * NTW + jt;
+      const int64_t t = tok0 + 16 * mt + row16;
+      const int j0 = 16 * jtg + 4 * grp;
+      if (jtg >= NT || t >= T || j0 >= r) continue;
+      float a[4] = {acc[mt][jt][0], acc[mt][jt][1], acc[mt][jt][2], acc[mt][jt][3]};
+      if constexpr (GB) {
+        if (skip) {
+          float x[4];
+          load_x4(skip + t * ld_s + j0, x);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) a[v] += x[v];
+        }
+        store_x4(out + t * r + j0, a);
+      } else {
+        if (a_save) *reinterpret_cast<float4*>(a_save + t * r + j0) = make_float4(a[0], a[1], a[2], a[3]);
+        float x[4], o[4];
+        load_x4(skip + t * ld_s + j0, x);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[v] = x[v] + act_phi(a[v], act);
+        store_x4(out + t * r + j0, o);
+      }
+    }
+}
+
+// g_h = g_b phi'(a), formed once for encode_bwd's wide-rank kernels: hi and lo
+// bf16 planes [T][r] (one float plane in the fp32 build); 4 columns per thread.
+__global__ __launch_bounds__(256) void k_gh(int64_t T, int r, int silu, const io_t* __restrict__ g_b,
+                                            const float* __restrict__ a_save, io_t* __restrict__ gh_hi,
+                                            io_t* __restrict__ gh_lo) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int nq = r / 4;
+  if (q >= T * nq) return;
+  const int64_t t = q / nq;
+  const int j0 = (int)(q % nq) * 4;
+  float g[4];
+  load_x4(g_b + t * r + j0, g);
+  if (silu) {
+    const float4 a = *reinterpret_cast<const float4*>(a_save + t * r + j0);
+    g[0] *= silu_grad(a.x);
+    g[1] *= silu_grad(a.y);
+    g[2] *= silu_grad(a.z);
+    g[3] *= silu_grad(a.w);
+  }
+#if RESBM_IO_F32_BUILD
+  (void)gh_lo;
+  *reinterpret_cast<float4*>(gh_hi + t * r + j0) = make_float4(g[0], g[1], g[2], g[3]);
+#else
+  bf16x4 h, lo;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    __bf16 a, b;
+    split_hi_lo(g[e], a, b);
+    h[e] = a;
+    lo[e] = b;
+  }
+  *reinterpret_cast<uint2*>(gh_hi + t * r + j0) = __builtin_bit_cast(uint2, h);
+  *reinterpret_cast<uint2*>(gh_lo + t * r + j0) = __builtin_bit_cast(uint2, lo);
+#endif
+}
+
+// Transposed fragment of a row-major [rows][PITCH] plane of the I/O type:
+// lane (row16, grp) receives plane[8 grp + e][c0 + row16], e = 0..7.
+template <int PITCH>
+__device__ __forceinline__ XFrag tr_rows(const io_t* plane, int c0, int row16, int grp) {
+  XFrag f;
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f.v[e] = plane[(8 * grp + e) * PITCH + c0 + row16];
+#else
+  f.v = tr_plane<PITCH>(plane, 0, c0, row16, grp);
+#endif
+  return f;
+}
+
+// Token contraction for wide r over a token group, for 128 columns c of the
+// streamed matrix X and all r columns j of the r-wide operand Y:
+//   DWD = false (encode_bwd): dwp[tg][c][j] = sum_t X[t][c] Y[t][j], Y = g_h
+//                             (split: hi and lo planes; one float plane in the fp32 build)
+//   DWD = true  (decode_bwd): dwp[tg][j][c] = sum_t Y[t][j] X[t][c], Y = b (exact)
+// 8 waves: wave (cw, jq) owns columns [64 cw, 64 cw + 64) of the block and
+// j-tiles [jq NTW, jq NTW + NTW).  Per 32-token step the block stages the
+// 32 x 128 tile of X and the 32 x r tile(s) of Y in LDS (double buffered, the
+// next step's loads two steps ahead in registers); both operands are read
+// back transposed (the contraction runs over the tile's rows).
+template <int NT, int NTW, bool DWD, bool R8>
+__global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int RP, const io_t* __restrict__ X,
+                                                   int64_t ld_x, const io_t* __restrict__ Y,
+                                                   const io_t* __restrict__ Y_lo, float* __restrict__ dwp, int TB) {
+  constexpr int BCc = 128, TS = 32, KS = (NT + 1) / 2, KP = 32 * KS, YP = KP + 8;
+  constexpr bool SPLIT = !DWD && !RESBM_IO_F32_BUILD;
+  constexpr int PL = SPLIT ? 2 : 1;
+  constexpr int XE = TS * BCc, YE = TS * YP;  // elements of the X tile and of one Y plane
+  constexpr int YC = TS * (KP / 8);           // 8-element chunks of one Y plane
+  constexpr int NYQ = (PL * YC + 511) / 512;  // Y chunk loads per thread and step
+  __shared__ __attribute__((aligned(16))) io_t s_x[2][XE];
+  __shared__ __attribute__((aligned(16))) io_t s_y[2][PL][YE];
+
+  const int tid = threadIdx.x, l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+  const int cw = wave & 1, jq = wave >> 1;
+  const int tg = blockIdx.x, cbi = blockIdx.y;  // token groups vary fastest
+  const int bc0 = cbi * BCc;
+  const int bcv = min(BCc, n - bc0);          // valid columns of the block (a multiple of 64)
+  const int64_t t_begin = (int64_t)tg * TB;
+  const int64_t t_end = min(T, t_begin + TB);
+  // X loads: thread tid takes row tid / 16, columns 8 (tid % 16) .. + 8
+  const int xrow = tid >> 4, xc = 8 * (tid & 15);
+
+  f32x4 acc[4][NTW];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int jt = 0; jt < NTW; ++jt) acc[ct][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  struct YRegs {
+    XFrag y[NYQ];
+  };
+  auto rows_of = [&](int64_t s, int64_t& t0) {
+    t0 = t_begin + s * TS;
+    return s < 0 ? (int64_t)0 : min((int64_t)TS, t_end - t0);
+  };
+  auto load_x = [&](XFrag& x, int64_t s) {
+    int64_t t0;
+    const int64_t rows = rows_of(s, t0);
+    const rsrc_t xr_ = make_rsrc(X + t0 * ld_x + bc0, bcv > 0 ? rows_bytes(rows, bcv, ld_x, kEs) : 0);
+    x = bld_x8(xr_, xc < bcv ? (uint32_t)((xrow * ld_x + xc) * kEs) : kOOB);
+  };
+  auto load_y = [&](YRegs& g, int64_t s) {
+    int64_t t0;
+    const int64_t rows = rows_of(s, t0);
+    const rsrc_t yr_ = make_rsrc(Y + t0 * r, rows > 0 ? rows * r * kEs : 0);
+    const rsrc_t yl_ = make_rsrc(SPLIT ? Y_lo + t0 * r : Y, SPLIT && rows > 0 ? rows * r * kEs : 0);
+#pragma unroll
+    for (int i = 0; i < NYQ; ++i) {
+      const int qq = tid + 512 * i;
+      const int pl = qq / YC, rem = qq % YC;
+      const int yrow = rem / (KP / 8), c8 = 8 * (rem % (KP / 8));
+      const bool ok = qq < PL * YC;
+      g.y[i] = bld_r8<R8>(pl ? yl_ : yr_, ok ? (uint32_t)(yrow * r * kEs) : kOOB, r, c8);
+    }
+  };
+  auto put = [&](const XFrag& x, const YRegs& g, int buf) {
+    io_t* dx = &s_x[buf][xrow * BCc + wide_col(xrow, xc)];
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dx[e] = x.v[e];
+#else
+    *reinterpret_cast<uint4*>(dx) = __builtin_bit_cast(uint4, x.v);
+#endif
+#pragma unroll
+    for (int i = 0; i < NYQ; ++i) {
+      const int qq = tid + 512 * i;
+      if (NYQ * 512 == PL * YC || qq < PL * YC) {
+        const int pl = qq / YC, rem = qq % YC;
+        const int yrow = rem / (KP / 8), c8 = 8 * (rem % (KP / 8));
+        io_t* dy = &s_y[buf][pl][yrow * YP + c8];
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dy[e] = g.y[i].v[e];
+#else
+        *reinterpret_cast<uint4*>(dy) = __builtin_bit_cast(uint4, g.y[i].v);
+#endif
+      }
+    }
+  };
+  auto compute = [&](int buf) {
+    XFrag xf[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) xf[ct] = tr_frag_wide<BCc>(s_x[buf], 0, 64 * cw + 16 * ct, row16, grp);
+#pragma unroll
+    for (int jt = 0; jt < NTW; ++jt) {
+      const int jtg = jq * NTW + jt;
+      if constexpr (NT % 4 != 0) {
+        if (jtg >= NT) continue;  // wave-uniform; the tile's columns end at 32 KS
+      }
+      if constexpr (DWD) {
+        const XFrag yb = tr_rows<YP>(s_y[buf][0], 16 * jtg, row16, grp);
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_xx(xf[ct], yb, acc[ct][jt]);
+      } else {
+        SFrag g;
+#if RESBM_IO_F32_BUILD
+        const XFrag y = tr_rows<YP>(s_y[buf][0], 16 * jtg, row16, grp);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) g.v[e] = y.v[e];
+#else
+        g.hi = tr_rows<YP>(s_y[buf][0], 16 * jtg, row16, grp).v;
+        g.lo = tr_rows<YP>(s_y[buf][PL - 1], 16 * jtg, row16, grp).v;
+#endif
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_sx(g, xf[ct], acc[ct][jt]);
+      }
+    }
+  };
+
+  // The X tiles (HBM) run four steps ahead of their use, the Y tiles (L2) two.
+  // Steps before 0 or past the range load zeros (the LDS buffers are fully
+  // written with them before they are read) and skip the products.
+  const int64_t nsb = (t_end - t_begin + TS - 1) / TS;
+  XFrag xr[4];
+  YRegs yr[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) xr[i] = xfrag_zero();
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int i = 0; i < NYQ; ++i) yr[h].y[i] = xfrag_zero();
+  auto body = [&](int64_t s, XFrag& xs, YRegs& ys) {
+    put(xs, ys, (int)(s & 1));
+    load_x(xs, s + 4);
+    load_y(ys, s + 2);
+    __syncthreads();  // this step's tiles are complete; the other buffers' readers are done
+    if (s >= 0 && s < nsb) compute((int)(s & 1));
+  };
+  for (int64_t s = opaque(-4); s < nsb; s += 4) {
+    body(s, xr[0], yr[0]);
+    body(s + 1, xr[1], yr[1]);
+    body(s + 2, xr[2], yr[0]);
+    body(s + 3, xr[3], yr[1]);
+  }
+
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int jt = 0; jt < NTW; ++jt) {
+      const int jtg = jq * NTW + jt;
+      if (jtg >= NT) continue;
+      if constexpr (DWD) {
+        // acc[ct][jt][v] = partial dW_d[16 jtg + row16][bc0 + 64 cw + 16 ct + 4 grp + v]
+        const int j = 16 * jtg + row16, c = bc0 + 64 * cw + 16 * ct + 4 * grp;
+        if (j < r && c < n)
+          *reinterpret_cast<float4*>(dwp + ((int64_t)tg * RP + j) * n + c) =
+              make_float4(acc[ct][jt][0], acc[ct][jt][1], acc[ct][jt][2], acc[ct][jt][3]);
+      } else {
+        // acc[ct][jt][v] = partial dW_e[bc0 + 64 cw + 16 ct + row16][16 jtg + 4 grp + v]
+        const int c = bc0 + 64 * cw + 16 * ct + row16, j = 16 * jtg + 4 * grp;
+        if (c < n && j < r)
+          *reinterpret_cast<float4*>(dwp + ((int64_t)tg * n + c) * RP + j) =
+              make_float4(acc[ct][jt][0], acc[ct][jt][1], acc[ct][jt][2], acc[ct][jt][3]);
+      }
+    }
+}
+
+// Expand contraction for wide r (decode_fwd, the g_z pass of encode_bwd):
+// k_expand's work split and epilogue, with the input rows of each 32-token
+// step staged once per block in LDS, in fragment order (fragment q = (16-token
+// tile, k-step, plane), 64 lanes x one exact fragment each), every wave
+// fetching a quarter of them, instead of every wave fetching all of them.
+// A wave whose strip lies past n still fetches its share and meets the
+// barriers.  Double-buffered, with the next step's fetches two steps ahead in
+// registers.
+template <int KS, int CT, bool ADD, bool GZ, bool R8>
+__global__ __launch_bounds__(256) void k_expand_wide(int64_t T, int n, int r, const io_t* __restrict__ in,
+                                                     const io_t* __restrict__ in_lo, const io_t* __restrict__ idsrc,
+                                                     const float* __restrict__ W, io_t* __restrict__ out,
+                                                     int64_t ld_out, int tpg, int main_y, FinArgs fin) {
+  if constexpr (GZ) {
+    if ((int)blockIdx.y >= main_y) {  // a finishing block
+      const int64_t bid = (int64_t)(blockIdx.y - main_y) * gridDim.x + blockIdx.x;
+      if (bid < fin.nb_all)
+        enc_bwd_fin_block(bid, T, n, r, fin.RP, fin.dwp, fin.ntg, fin.dW_e, fin.accumulate, fin.nb_dw, fin.g_b,
+                          fin.g_x, fin.ld_gx);
+      return;
+    }
+  }
+  constexpr int W8 = CT >= 2 ? 8 : 4;
+  constexpr int NH = CT >= 2 ? CT / 2 : 1;
+  constexpr int NI = ADD ? NH * W8 / 4 : 1;
+  constexpr int WC = 16 * CT;
+  constexpr int CPR = WC / 8;
+  constexpr int NS = (16 * CPR + 63) / 64;
+  constexpr bool LO = GZ && !RESBM_IO_F32_BUILD;
+  constexpr int PL = LO ? 2 : 1;
+  constexpr int NF = 2 * KS * PL;   // input fragments of a 32-token step
+  constexpr int NFW = (NF + 3) / 4;  // fetched per wave (the last round partly, when NF % 4 != 0)
+  __shared__ __attribute__((aligned(16))) XFrag s_in[2][NF][64];
+  __shared__ __attribute__((aligned(16))) io_t s_out[4][16 * WC];
+  const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
+  io_t* tile = s_out[wave];
+#if RESBM_DF_TOKEN_FASTEST
+  const int strip = blockIdx.y * 4 + wave;
+  const int tgi = blockIdx.x;
+#else
+  const int strip = blockIdx.x * 4 + wave;
+  const int tgi = blockIdx.y;
+#endif
+  const int c0 = strip * 16 * CT;
+  const bool won = c0 < n;  // whole strips: n % 64 == 0 and 16 CT divides 64
+
+  SFrag wfr[KS][CT];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      const int col = expand_col<CT>(c0, ct, row16);
+      float w[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = ks * 32 + grp * 8 + e;
+        w[e] = (won && k < r) ? (GZ ? W[(int64_t)col * r + k] : W[(int64_t)k * n + col]) : 0.0f;
+      }
+      wfr[ks][ct] = sfrag_from(w);
+    }
+
+  const int64_t t_begin = (int64_t)tgi * tpg;
+  const int64_t rows = min((int64_t)tpg, T - t_begin);
+  const rsrc_t br = make_rsrc(in + t_begin * r, rows * r * kEs);
+  const rsrc_t lr = make_rsrc(LO ? in_lo + t_begin * r : in, LO ? rows * r * kEs : 0);
+  const rsrc_t ir = make_rsrc(idsrc + t_begin * r, ADD ? rows * r * kEs : 0);
+  const rsrc_t zr = make_rsrc(out + t_begin * ld_out, rows_bytes(rows, n, ld_out, kEs));
+  const int cl = c0 + W8 * grp;  // first column of this lane's run 0
+
+#if RESBM_IO_F32_BUILD
+  typedef uint4 IdT;
+#else
+  typedef uint2 IdT;
+#endif
+  struct Step {
+    XFrag f[NFW];    // this wave's share of the step's input fragments
+    IdT id[2][NI];   // idsrc of the step's two tiles, this lane's columns below r (raw bits)
+  };
+  // fragment q = wave + 4 i of a step: with two planes NF is a multiple of 4
+  // and q % PL = wave % PL, so every load of a wave uses one descriptor; only a
+  // last round with NF % 4 != 0 tests q < NF
+  const rsrc_t mine = (PL == 2 && (wave & 1)) ? lr : br;
+  auto load = [&](Step& x, int64_t tt) {  // tt: first token of the step, relative to t_begin
+#pragma unroll
+    for (int i = 0; i < NFW; ++i) {
+      const int q = wave + 4 * i;
+      const int tile16 = q / (KS * PL), ks = (q % (KS * PL)) / PL;
+      const int64_t t = tt + 16 * tile16 + row16;
+      // rows >= `rows` fall outside the descriptor
+      const uint32_t ro = (4 * i + 4 <= NF || q < NF) ? (uint32_t)(t * r * kEs) : kOOB;
+      x.f[i] = bld_r8<R8>(mine, ro, r, ks * 32 + grp * 8);
+    }
+    if constexpr (ADD) {
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int64_t t = tt + 16 * h2 + row16;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int cb = cl + 32 * (i / (W8 / 4)) + 4 * (i % (W8 / 4));
+          const uint32_t o = (won && cb < r) ? (uint32_t)((t * r + cb) * kEs) : kOOB;
+#if RESBM_IO_F32_BUILD
+          x.id[h2][i] = bld16(ir, o);
+#else
+          x.id[h2][i] = bld8(ir, o);
+#endif
+        }
+      }
+    }
+  };
+  auto put = [&](const Step& x, int buf) {
+#pragma unroll
+    for (int i = 0; i < NFW; ++i)
+      if (4 * i + 4 <= NF || wave + 4 * i < NF) s_in[buf][wave + 4 * i][l] = x.f[i];
+  };
+  // The products of one step (two 16-token tiles) from buffer buf.  Both tiles
+  // and, at CT <= 2, two k-step parities accumulate separately, so that at
+  // least eight independent accumulation chains keep the matrix cores busy;
+  // the parities are added at the end.
+  constexpr int PAR = CT <= 2 ? 2 : 1;
+  auto products = [&](int buf, f32x4 (&acc)[2][CT]) {
+    f32x4 part[2][PAR][CT];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+      for (int pa = 0; pa < PAR; ++pa)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) part[h2][pa][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the fragments of k-step ks + 1 are read while those of ks are multiplied
+    XFrag cur[2][PL], nxt[2][PL];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+      for (int pl = 0; pl < PL; ++pl) cur[h2][pl] = s_in[buf][h2 * KS * PL + pl][l];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) {
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+          for (int pl = 0; pl < PL; ++pl) nxt[h2][pl] = s_in[buf][(h2 * KS + ks + 1) * PL + pl][l];
+      }
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        if constexpr (GZ) {
+          SFrag g;
+#if RESBM_IO_F32_BUILD
+#pragma unroll
+          for (int e = 0; e < 8; ++e) g.v[e] = cur[h2][0].v[e];
+#else
+          g.hi = cur[h2][0].v;
+          g.lo = cur[h2][PL - 1].v;
+#endif
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) part[h2][ks % PAR][ct] = mma_ss(wfr[ks][ct], g, part[h2][ks % PAR][ct]);
+        } else {
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct)
+            part[h2][ks % PAR][ct] = mma_sx(wfr[ks][ct], cur[h2][0], part[h2][ks % PAR][ct]);
+        }
+      }
+      if (ks + 1 < KS) {
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+          for (int pl = 0; pl < PL; ++pl) cur[h2][pl] = nxt[h2][pl];
+      }
+    }
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        acc[h2][ct] = part[h2][0][ct];
+#pragma unroll
+        for (int pa = 1; pa < PAR; ++pa) acc[h2][ct] += part[h2][pa][ct];
+      }
+  };
+  // rounds and stores one 16-token tile (tokens tt .. tt + 15 relative to t_begin)
+  auto epilogue = [&](const f32x4 (&acc)[CT], int64_t tt, const IdT* idr) {
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      float v[W8];
+#pragma unroll
+      for (int q = 0; q < W8 / 4; ++q) {
+        float id[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (ADD) {
+          const auto u = idr[h * (W8 / 4) + q];
+#if RESBM_IO_F32_BUILD
+          id[0] = __builtin_bit_cast(float, u.x); id[1] = __builtin_bit_cast(float, u.y);
+          id[2] = __builtin_bit_cast(float, u.z); id[3] = __builtin_bit_cast(float, u.w);
+#else
+          id[0] = bf16_bits_to_f32(u.x & 0xffffu); id[1] = bf16_bits_to_f32(u.x >> 16);
+          id[2] = bf16_bits_to_f32(u.y & 0xffffu); id[3] = bf16_bits_to_f32(u.y >> 16);
+#endif
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[4 * q + e] = ADD ? acc[2 * h + q][e] + id[e] : acc[2 * h + q][e];
+      }
+      io_t* d = tile + row16 * WC + tile_col<WC>(row16, cl - c0 + 32 * h);
+#pragma unroll
+      for (int e = 0; e < W8; ++e) d[e] = f32_to_io(v[e]);
+    }
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+      const int idx = l + 64 * q;
+      const int row = idx / CPR, c8 = 8 * (idx % CPR);
+      const XFrag o = tile_get8<WC>(tile, row < 16 ? row : 0, c8);
+      bst_frag(zr, (tt < 0 || row >= 16) ? kOOB : (uint32_t)(((tt + row) * ld_out + c0 + c8) * kEs), o);
+    }
+  };
+
+  Step sa, sb;
+#pragma unroll
+  for (int i = 0; i < NFW; ++i) sa.f[i] = sb.f[i] = xfrag_zero();
+  if constexpr (ADD) {
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+      for (int i = 0; i < NI; ++i) sa.id[h2][i] = sb.id[h2][i] = {};
+  }
+  const int64_t nsteps = (rows + 31) / 32;
+  // step s covers tokens [32 s, 32 s + 32) of the group; its fetches were
+  // issued two steps earlier
+  auto body = [&](Step& x, int64_t s) {
+    put(x, (int)(s & 1));
+    IdT idr[2][NI];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+      for (int i = 0; i < NI; ++i) idr[h2][i] = x.id[h2][i];
+    load(x, 32 * (s + 2));
+    __syncthreads();  // the step's fragments are complete; the other buffer's readers are done
+    if (won && s >= 0 && s < nsteps) {
+      f32x4 acc[2][CT];
+      products((int)(s & 1), acc);
+      epilogue(acc[0], 32 * s, idr[0]);
+      epilogue(acc[1], 32 * s + 16, idr[1]);
+    }
+  };
+  for (int64_t s = opaque(-2); s < nsteps; s += 2) {
+    body(sa, s);
+    body(sb, s + 1);
+  }
+}
+
 }  // namespace resbm
 
 // ============================================================ host side
@@ -1412,10 +2053,15 @@ int32_t check_common(int64_t T, int n, int r, int64_t ws_need, const void* ws, s
 template <int NT>
 void launch_enc_fwd(const Plan& p, int act, const io_t* x, int64_t ld_x, const io_t* z, int64_t ld_z,
                     const void* wf, io_t* b, float* a_save, hipStream_t st) {
-  constexpr int MT = ef_mt(NT);
-  constexpr int KW = ef_kw(NT);
-  hipLaunchKernelGGL((k_enc_fwd<NT, MT, KW>), dim3(p.ef_nblk), dim3(KW * 64), 0, st, p.T, p.n, p.r, act, x, ld_x,
-                     z, ld_z, wf, b, a_save);
+  if constexpr (NT >= kWideNT) {
+    hipLaunchKernelGGL((k_rowc_wide<NT, tw_ntw(NT), false>), dim3(p.rw_nblk), dim3(256), 0, st, p.T, p.n, p.r, act,
+                       z, ld_z, wf, x, ld_x, b, a_save);
+  } else {
+    constexpr int MT = ef_mt(NT);
+    constexpr int KW = ef_kw(NT);
+    hipLaunchKernelGGL((k_enc_fwd<NT, MT, KW>), dim3(p.ef_nblk), dim3(KW * 64), 0, st, p.T, p.n, p.r, act, x, ld_x,
+                       z, ld_z, wf, b, a_save);
+  }
 }
 
 // The expand kernel's input rows are fetched 8 elements per 16-byte load when
@@ -1434,9 +2080,15 @@ void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, 
 #endif
   const FinArgs none{};
   const bool r8 = expand_r8(p.r);
-#define CALL_DF(ADD, R8)                                                                                      \
-  hipLaunchKernelGGL((k_expand<KS, CT, ADD, false, R8>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d, zt, \
-                     ld, p.df_tpg, (int)grid.y, none)
+#define CALL_DF(ADD, R8)                                                                                           \
+  do {                                                                                                             \
+    if constexpr (KS >= 3)                                                                                         \
+      hipLaunchKernelGGL((k_expand_wide<KS, CT, ADD, false, R8>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, \
+                         W_d, zt, ld, p.df_tpg, (int)grid.y, none);                                                \
+    else                                                                                                           \
+      hipLaunchKernelGGL((k_expand<KS, CT, ADD, false, R8>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, W_d,  \
+                         zt, ld, p.df_tpg, (int)grid.y, none);                                                     \
+  } while (0)
   if (add_id) {
     if (r8) CALL_DF(true, true); else CALL_DF(true, false);
   } else {
@@ -1462,15 +2114,28 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
                     const io_t* g_b, io_t* g_z, int64_t ld_gz, int fused, float* dwp, io_t* gh_hi, io_t* gh_lo,
                     FinArgs fin, hipStream_t st) {
   constexpr int KS = (NT + 1) / 2;
-  constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS);
-#if RESBM_XCD_SPREAD
-  dim3 grid(p.eb_ntg, p.eb_ncb);
-#else
-  dim3 grid(p.eb_ncb, p.eb_ntg);
-#endif
   const int silu = act == RESBM_ACT_SILU;
-  hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r, p.RP, silu, z,
-                     ld_z, a_save, g_b, gh_hi, gh_lo, dwp, p.eb_TB);
+  const bool r8 = expand_r8(p.r);
+  if constexpr (NT >= kWideNT) {
+    // g_h once, then the dW_e partials of the token groups
+    hipLaunchKernelGGL(k_gh, dim3((unsigned)ceil_div(p.T * (p.r / 4), 256)), dim3(256), 0, st, p.T, p.r, silu, g_b,
+                       a_save, gh_hi, gh_lo);
+    if (r8)
+      hipLaunchKernelGGL((k_tokc_wide<NT, tw_ntw(NT), false, true>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, st,
+                         p.T, p.n, p.r, p.RP, z, ld_z, gh_hi, gh_lo, dwp, p.tw_TB);
+    else
+      hipLaunchKernelGGL((k_tokc_wide<NT, tw_ntw(NT), false, false>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, st,
+                         p.T, p.n, p.r, p.RP, z, ld_z, gh_hi, gh_lo, dwp, p.tw_TB);
+  } else {
+    constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS);
+#if RESBM_XCD_SPREAD
+    dim3 grid(p.eb_ntg, p.eb_ncb);
+#else
+    dim3 grid(p.eb_ncb, p.eb_ntg);
+#endif
+    hipLaunchKernelGGL((k_enc_bwd<KS, NT, CT, CW, TW>), grid, dim3(CW * TW * 64), 0, st, p.T, p.n, p.r, p.RP, silu,
+                       z, ld_z, a_save, g_b, gh_hi, gh_lo, dwp, p.eb_TB);
+  }
   // g_z = g_h W_e^T (+ g_b I_{r x n} when g_x is g_z): the expand kernel of decode_fwd on the split g_h
   constexpr int GCT = df_ct(KS);
 #if RESBM_DF_TOKEN_FASTEST
@@ -1481,10 +2146,15 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
   // the finishing blocks follow in extra grid rows (dispatched after the g_z blocks, run beside them)
   const int main_y = (int)ggrid.y;
   ggrid.y += (unsigned)ceil_div(fin.nb_all, (int64_t)ggrid.x);
-  const bool r8 = expand_r8(p.r);
-#define CALL_GZ(ADD, R8)                                                                                          \
-  hipLaunchKernelGGL((k_expand<KS, GCT, ADD, true, R8>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, gh_lo, g_b, \
-                     W_e, g_z, ld_gz, p.df_tpg, main_y, fin)
+#define CALL_GZ(ADD, R8)                                                                                         \
+  do {                                                                                                           \
+    if constexpr (NT >= kWideNT)                                                                                 \
+      hipLaunchKernelGGL((k_expand_wide<KS, GCT, ADD, true, R8>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, \
+                         gh_lo, g_b, W_e, g_z, ld_gz, p.df_tpg, main_y, fin);                                   \
+    else                                                                                                         \
+      hipLaunchKernelGGL((k_expand<KS, GCT, ADD, true, R8>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi,      \
+                         gh_lo, g_b, W_e, g_z, ld_gz, p.df_tpg, main_y, fin);                                   \
+  } while (0)
   if (fused) {
     if (r8) CALL_GZ(true, true); else CALL_GZ(true, false);
   } else {
@@ -1705,6 +2375,33 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r, const void* b, const f
   float* dwp = (float*)(w + p.db_dwp_off);
   const io_t* B = (const io_t*)b;
   const io_t* G = (const io_t*)g_zt;
+  if (p.wide) {
+    void* wf = w + p.db_wf_off;
+    const int64_t nprep = (int64_t)(n / 32) * p.NT * 64;
+    hipLaunchKernelGGL(k_wd_prep, dim3((unsigned)ceil_div(nprep, 64)), dim3(64), 0, s, W_d, n, r, p.NT, wf);
+    const bool r8 = expand_r8(r);
+#define CALL(NTV)                                                                                                   \
+  do {                                                                                                              \
+    if constexpr (NTV >= kWideNT) {                                                                                 \
+      hipLaunchKernelGGL((k_rowc_wide<NTV, tw_ntw(NTV), true>), dim3(p.rw_nblk), dim3(256), 0, s, T, n, r, 0, G,   \
+                         ld_gzt, (const void*)wf, (const io_t*)g_id, ld_gid, (io_t*)g_b, (float*)nullptr);         \
+      if (r8)                                                                                                       \
+        hipLaunchKernelGGL((k_tokc_wide<NTV, tw_ntw(NTV), true, true>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, s,  \
+                           T, n, r, p.RP, G, ld_gzt, B, B, dwp, p.tw_TB);                                          \
+      else                                                                                                          \
+        hipLaunchKernelGGL((k_tokc_wide<NTV, tw_ntw(NTV), true, false>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, s, \
+                           T, n, r, p.RP, G, ld_gzt, B, B, dwp, p.tw_TB);                                          \
+    }                                                                                                               \
+  } while (0)
+    RESBM_DISPATCH_NT(p.NT, CALL)
+#undef CALL
+    // the ordered sum of the dW_d partials (g_b is complete)
+    const int64_t nb_dw = ceil_div((int64_t)r * (n / 4), 64);
+    hipLaunchKernelGGL(k_dec_bwd_fin, dim3((unsigned)nb_dw), dim3(256), 0, s, T, n, r, p.RP, (const float*)nullptr, 0,
+                       (const io_t*)nullptr, ld_gid, (io_t*)nullptr, (const float*)dwp, p.tw_ntg, dW_d, accumulate,
+                       (int64_t)0);
+    return launch_status();
+  }
   switch (p.db_jt) {
     case 1: launch_dec_bwd<1>(p, B, W_d, G, ld_gzt, gbp, dwp, s); break;
     case 2: launch_dec_bwd<2>(p, B, W_d, G, ld_gzt, gbp, dwp, s); break;

@@ -86,6 +86,12 @@ constexpr int eb_cw(int) { return RESBM_EB_CW; }
 // two token waves up to r = 128; at r = 256 the g_h tiles of two would not fit LDS
 constexpr int eb_tw(int KS) { return KS <= 4 ? RESBM_EB_TW : 1; }
 
+// ---- wide rank: above r = 64 (more than four 16-column tiles of r) the ops
+// switch to the row / token contraction kernels and the expand kernel with
+// block-shared inputs.
+constexpr int kWideNT = 5;
+constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four waves split r)
+
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 inline size_t align_ws(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
@@ -107,6 +113,11 @@ struct Plan {
 
   int eb_ct, eb_bc, eb_ncb, eb_TB, eb_ntg;
   size_t eb_dwp_off, eb_gh_off, eb_ws;
+
+  bool wide;                    // NT >= kWideNT
+  int rw_nblk;                  // row contraction: 64-token blocks
+  int tw_ncb, tw_ntg, tw_TB;    // token contraction: 128-column blocks x token groups of tw_TB tokens
+  size_t db_wf_off;             // decode_bwd (wide): W_d fragments
 
   size_t ws_total;
 };
@@ -173,6 +184,27 @@ inline Plan make_plan(int64_t T, int n, int r) {
   p.eb_dwp_off = 0;
   p.eb_gh_off = align_ws((size_t)p.eb_ntg * n * p.RP * 4);
   p.eb_ws = p.eb_gh_off + align_ws((size_t)Tm * r * 4);  // g_h, split into two bf16 planes (or one fp32)
+
+  // ---- wide rank: decode_bwd = row contraction (g_b) + token contraction (dW_d
+  // partials) + their ordered sum; encode_bwd = g_h + token contraction (dW_e
+  // partials) + expand (g_z, with the ordered sums riding along)
+  p.wide = p.NT >= kWideNT;
+  if (p.wide) {
+    p.rw_nblk = (int)ceil_div(Tm, 64);
+    p.tw_ncb = (int)ceil_div(n, 128);
+    const int64_t nstep = ceil_div(Tm, 32);
+    const int64_t g = clamp64(ceil_div((int64_t)kNumCU, p.tw_ncb), 1, nstep);
+    p.tw_TB = (int)(32 * ceil_div(nstep, g));
+    p.tw_ntg = (int)ceil_div(Tm, p.tw_TB);
+    p.db_wf_off = 0;
+    p.db_gbp_off = 0;
+    p.db_dwp_off = align_ws((size_t)n * p.RP * 4);
+    p.db_ws = p.db_dwp_off + align_ws((size_t)p.tw_ntg * p.RP * n * 4);
+    p.eb_ntg = p.tw_ntg;
+    p.eb_dwp_off = 0;
+    p.eb_gh_off = align_ws((size_t)p.tw_ntg * n * p.RP * 4);
+    p.eb_ws = p.eb_gh_off + align_ws((size_t)Tm * r * 4);
+  }
 
   size_t m = p.ef_ws;
   if (p.db_ws > m) m = p.db_ws;

@@ -20,9 +20,12 @@ pytestmark = pytest.mark.gpu
 ID, SILU = O.ACT_IDENTITY, O.ACT_SILU
 
 # (T, n, r): several tiles in every direction, ragged token tails, r not a
-# multiple of 16 (4, 12, 40), full rank (r = n), the largest r.
+# multiple of 16 (4, 12, 40, 100, 136), full rank (r = n), the largest r, and
+# the wide-rank kernels (r > 64) at odd tile counts.
 SHAPES = [(1000, 512, 32), (777, 256, 4), (333, 320, 40), (517, 1024, 64), (45, 192, 12),
-          (130, 128, 128), (96, 256, 256), (64, 64, 64), (1, 64, 4)]
+          (130, 128, 128), (96, 256, 256), (64, 64, 64), (1, 64, 4),
+          # wide rank (r > 64): r % 8 == 4, r a multiple of 16, 48, 64, odd tile counts, n % 128 == 64, T = 1
+          (333, 768, 100), (700, 576, 136), (1000, 1024, 192), (64, 256, 80), (1, 128, 128)]
 IDS = [f"T{T}_n{n}_r{r}" for T, n, r in SHAPES]
 
 
