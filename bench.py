@@ -68,6 +68,8 @@ def parse():
     p.add_argument("--step-times", action="store_true", help="list every timed step's duration")
     p.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="write profiles/ summaries from rocprofv3 output of this script (no GPU work)")
+    p.add_argument("--summarize-trace", metavar="TRACE_DIR",
+                   help="write profiles/kernels_<workload>.txt from a rocprofv3 kernel trace alone (no GPU work)")
     p.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR",
                    help="write profiles/counters_<workload>.json from rocprofv3 --pmc runs of this script (no GPU work)")
     p.add_argument("--commands", nargs="+", default=None, help="the rocprofv3 commands, recorded in the summaries")
@@ -84,12 +86,22 @@ def kernel_op(name: str):
     import re
     base = re.sub(r"\(.*", "", name)
     if "k_expand" in base:
-        m = re.search(r"k_expand<([^>]*)>", base)
+        m = re.search(r"k_expand(?:_wide)?<([^>]*)>", base)
         if m:
             gz = m.group(1).split(",")[3].strip() == "true"
         else:  # mangled: two int arguments, then the ADD and GZ flags
-            gz = re.search(r"k_expandI(?:Li\d+E){2}Lb[01]ELb1E", base) is not None
+            gz = re.search(r"k_expand(?:_wide)?I(?:Li\d+E){2}Lb[01]ELb1E", base) is not None
         return "encode_bwd" if gz else "decode_fwd"
+    for key in ("k_rowc_wide", "k_tokc_wide"):
+        if key in base:  # <NT, NTW, flag, ...>: the flag marks the decode_bwd instance
+            m = re.search(key + r"<([^>]*)>", base)
+            flag = m.group(1).split(",")[2].strip() == "true" if m else \
+                re.search(key + r"I(?:Li\d+E){2}Lb1E", base) is not None
+            return "decode_bwd" if flag else ("encode_fwd" if key == "k_rowc_wide" else "encode_bwd")
+    if "k_wd_prep" in base:
+        return "decode_bwd"
+    if re.search(r"k_gh\b|4k_ghE", base):
+        return "encode_bwd"
     for key, op in KERNEL_OP:
         if key in base or key.replace("_", "") in base.replace("_", ""):
             return op
@@ -176,11 +188,38 @@ def summarize_profiles(trace_dir: str, fetch_dir: str, write_dir: str, name: str
             fh.write("\n".join(lines) + "\n")
 
 
+def summarize_trace(trace_dir: str, name: str, commands) -> None:
+    """Per-kernel duration statistics of a traced bench run of one workload."""
+    import glob
+    import re
+    import sqlite3
+
+    f = sorted(glob.glob(os.path.join(trace_dir, "**", "*results.db"), recursive=True))
+    if not f:
+        raise SystemExit(f"no rocprofv3 database under {trace_dir}")
+    stats = {}
+    for k, dur in sqlite3.connect(f[0]).execute("select name, end - start from kernels"):
+        stats.setdefault(re.sub(r"\(.*", "", k).replace("void ", ""), []).append(dur / 1000.0)
+    lines = [f"# rocprofv3 kernel trace, workload {name}", "", "command:",
+             f"    {commands[0] if commands else '?'}", "",
+             f"{'kernel':64s} {'op':11s} {'calls':>6s} {'avg us':>9s} {'med us':>9s} {'min us':>9s}"]
+    for k, v in sorted(stats.items(), key=lambda kv: -sum(kv[1])):
+        if "resbm" not in k:
+            continue
+        vs = sorted(v)
+        lines.append(f"{k[:64]:64s} {kernel_op(k) or '-':11s} {len(v):6d} {sum(v) / len(v):9.2f} "
+                     f"{vs[len(vs) // 2]:9.2f} {vs[0]:9.2f}")
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", f"kernels_{name}.txt"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 COUNTER_PASSES = (
     "SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_INSTS_VMEM_RD "
     "SQ_INSTS_VMEM_WR SQ_INSTS_SALU",
     "SQ_WAVES SQ_BUSY_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_LDS SQ_WAIT_INST_LDS "
-    "SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_LDS_ADDR_CONFLICT GRBM_GUI_ACTIVE",
+    "SQ_WAVE_CYCLES SQ_WAIT_ANY GRBM_GUI_ACTIVE",
     "TCC_HIT_sum TCC_MISS_sum TCC_EA0_RDREQ_DRAM_sum TCC_REQ_sum",
     "TCC_EA0_WRREQ_sum TCC_EA0_WRREQ_64B_sum TCC_WRITEBACK_sum TCP_TCC_READ_REQ_sum",
 )
@@ -217,6 +256,12 @@ def summarize_counters(dirs, name: str, commands) -> None:
             e["lds_bank_conflict_cycles_per_lds_active_cycle"] = g("SQ_LDS_BANK_CONFLICT", 0.0) / g("SQ_ACTIVE_INST_LDS")
         if g("TCC_HIT_sum") is not None and g("TCC_MISS_sum") is not None and g("TCC_HIT_sum") + g("TCC_MISS_sum"):
             e["l2_hit_rate"] = g("TCC_HIT_sum") / (g("TCC_HIT_sum") + g("TCC_MISS_sum"))
+        if g("SQ_WAVE_CYCLES"):
+            e["wait_share_of_wave_cycles"] = g("SQ_WAIT_ANY", 0.0) / g("SQ_WAVE_CYCLES")
+        if g("SQ_INSTS_MFMA") and g("GRBM_GUI_ACTIVE"):
+            # 16-cycle 16x16x32 bf16 products per SIMD (1024 SIMDs) over the kernel's
+            # active cycles (GRBM counts each of the 8 XCDs)
+            e["mfma_issue_share"] = g("SQ_INSTS_MFMA") * 16.0 / 1024 / (g("GRBM_GUI_ACTIVE") / 8)
         out[k] = e
     rec = {"workload": name, "source_sha256": source_digest(), "passes": list(COUNTER_PASSES),
            "commands": commands, "kernels": out}
@@ -608,6 +653,10 @@ def main():
     if args.summarize_profiles:
         from paper_2604_11947_amd import inputs as I
         summarize_profiles(*args.summarize_profiles, args.workload or I.HEADLINE, args.commands)
+        return
+    if args.summarize_trace:
+        from paper_2604_11947_amd import inputs as I
+        summarize_trace(args.summarize_trace, args.workload or I.HEADLINE, args.commands)
         return
     if args.summarize_counters:
         from paper_2604_11947_amd import inputs as I

@@ -23,6 +23,16 @@ import bench  # noqa: E402
     ("_ZN5resbm9k_dec_bwdILi2EEEvliiiPKDF16b", "decode_bwd"),
     ("resbm::k_dec_bwd_fin", "decode_bwd"),
     ("_ZN5resbm9k_enc_bwdILi1ELi2ELi4ELi4ELi2EEEvliiii", "encode_bwd"),
+    ("resbm::k_rowc_wide<16, 4, false>", "encode_fwd"),
+    ("resbm::k_rowc_wide<8, 2, true>", "decode_bwd"),
+    ("resbm::k_tokc_wide<16, 4, true, true>", "decode_bwd"),
+    ("resbm::k_tokc_wide<8, 2, false, false>", "encode_bwd"),
+    ("_ZN5resbm11k_tokc_wideILi8ELi2ELb1ELb1EEEvliii", "decode_bwd"),
+    ("_ZN5resbm11k_rowc_wideILi8ELi2ELb0EEEvliii", "encode_fwd"),
+    ("resbm::k_expand_wide<8, 2, false, true, true>", "encode_bwd"),
+    ("resbm::k_expand_wide<4, 4, true, false, false>", "decode_fwd"),
+    ("_ZN5resbm4k_ghEliiPKDF16bPKfPDF16bS4_", "encode_bwd"),
+    ("resbm::k_wd_prep", "decode_bwd"),
     ("resbm_mx::k_mx_rows<1>", None),
     ("__amd_rocclr_copyBuffer", None),
 ])
