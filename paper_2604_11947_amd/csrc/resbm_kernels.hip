@@ -545,6 +545,26 @@ __device__ __forceinline__ float4 sum_ordered4(const float* __restrict__ p, int6
 // registers) and transposed for dW_d.  The payload rows of a step are staged
 // once per block.  The 8 waves' g_b partials of a step are added in wave order
 // behind the next step's barrier.
+// Position of float [row][j] (j % 4 == 0) in a 32-row tile of JW-float rows of
+// partial sums, written as 16-byte pieces by lane (row16, grp) at row 16 th +
+// row16, chunk 4 jt + grp (8-lane write groups: 8 rows, one chunk) and read
+// back row by row (consecutive lanes on consecutive chunks).  With 4, 8 or 16
+// chunks per row the chunk index is XORed with (row / 2) % 4, row % 8 or row % 8,
+// which puts both patterns on distinct banks; other widths pad rows by 4 floats.
+template <int JW>
+__device__ __forceinline__ int gb_pos(int row, int j) {
+  constexpr int C = JW / 4;
+  if constexpr (C == 4) {
+    return row * JW + (((j >> 2) ^ ((row >> 1) & 3)) << 2);
+  } else if constexpr (C == 8 || C == 16) {
+    return row * JW + (((j >> 2) ^ (row & 7)) << 2);
+  } else {
+    return row * (JW + 4) + j;
+  }
+}
+template <int JW>
+constexpr int gb_rowsz() { return (JW == 16 || JW == 32 || JW == 64) ? JW : JW + 4; }
+
 template <int JT>
 __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int r, int RP,
                                                            const io_t* __restrict__ b,
@@ -562,7 +582,7 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
   constexpr int RPW = 32 / kDbWaves;  // tile rows loaded per wave
   __shared__ __attribute__((aligned(16))) io_t s_gz[GZB][32 * BW];
   __shared__ __attribute__((aligned(16))) io_t s_b[2][32 * JW];
-  __shared__ __attribute__((aligned(16))) float s_gb[NBUF][kDbWaves][32][JW + 4];
+  __shared__ __attribute__((aligned(16))) float s_gb[NBUF][kDbWaves][32 * gb_rowsz<JW>()];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
 #if RESBM_XCD_SPREAD
@@ -667,7 +687,7 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
           float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
           for (int w = 0; w < kDbWaves; ++w) {
-            const float4 p = *reinterpret_cast<const float4*>(&s_gb[gprev][w][tt][jj]);
+            const float4 p = *reinterpret_cast<const float4*>(&s_gb[gprev][w][gb_pos<JW>(tt, jj)]);
             v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
           }
           bst16(pr, j < r ? (uint32_t)((tt * RP + j) * 4) : kOOB,
@@ -697,7 +717,7 @@ __global__ __launch_bounds__(kDbWaves * 64) void k_dec_bwd(int64_t T, int n, int
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KSW; ++ks) acc = mma_sx(wdf[jt][ks], f[ks], acc);
-        *reinterpret_cast<float4*>(&s_gb[gcur][wave][16 * th + row16][16 * jt + 4 * grp]) =
+        *reinterpret_cast<float4*>(&s_gb[gcur][wave][gb_pos<JW>(16 * th + row16, 16 * jt + 4 * grp)]) =
             make_float4(acc[0], acc[1], acc[2], acc[3]);
       }
     }
@@ -822,8 +842,13 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
 // column slice are added in LDS in wave order; the finishing blocks add the
 // token groups in order.
 
-// Split g_h tile of TS tokens x RPS columns: bf16 build: hi and lo planes;
-// f32 build: one float plane.
+// Row pitch (elements) of a staged [rows][KP] plane of 16-bit values that is
+// read transposed: KP itself where lds_col has a layout for it, else KP + 8
+// (the padding moves consecutive rows to different banks).
+constexpr int plane_pitch(int KP) { return (KP % 128 == 0 || KP == 32 || KP == 64) ? KP : KP + 8; }
+
+// Split g_h tile of TS tokens x RPS columns: bf16 build: hi and lo planes in
+// the lds_col<RPS> layout; f32 build: one float plane, row-major.
 template <int TS, int RPS>
 struct GhTile {
 #if RESBM_IO_F32_BUILD
@@ -847,30 +872,15 @@ __device__ __forceinline__ void gh_put4(GhTile<TS, RPS>& t, int row, int col, co
     h[e] = a;
     l[e] = b;
   }
-  *reinterpret_cast<uint2*>(&t.hi[row][col]) = __builtin_bit_cast(uint2, h);
-  *reinterpret_cast<uint2*>(&t.lo[row][col]) = __builtin_bit_cast(uint2, l);
+  const int c = lds_col<RPS>(row, col);  // col % 4 == 0: the four stay in one chunk
+  *reinterpret_cast<uint2*>(&t.hi[row][c]) = __builtin_bit_cast(uint2, h);
+  *reinterpret_cast<uint2*>(&t.lo[row][c]) = __builtin_bit_cast(uint2, l);
 #endif
 }
 
-// g_h[row][col .. col + 8) as the B operand of g_z (k = j).
-template <int TS, int RPS>
-__device__ __forceinline__ SFrag gh_row(const GhTile<TS, RPS>& t, int row, int col) {
-  SFrag f;
-#if RESBM_IO_F32_BUILD
-  const float4 a = *reinterpret_cast<const float4*>(&t.v[row][col]);
-  const float4 b = *reinterpret_cast<const float4*>(&t.v[row][col + 4]);
-  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
-  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
-#else
-  f.hi = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&t.hi[row][col]));
-  f.lo = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&t.lo[row][col]));
-#endif
-  return f;
-}
-
-// Transposed 16-bit fragment from a row-major plane with PITCH elements per row:
-// lane (row16, grp) receives plane[row0 + 8 grp + e][c0 + row16], e = 0..7
-// (two ds_read_b64_tr_b16, addressed as in tr_frag).
+// Transposed 16-bit fragment from a plane with PITCH elements per row in the
+// lds_col<PITCH> layout: lane (row16, grp) receives plane[row0 + 8 grp + e][c0 + row16],
+// e = 0..7 (two ds_read_b64_tr_b16, addressed as in tr_frag).
 template <int PITCH>
 __device__ __forceinline__ bf16x8 tr_plane(const __bf16* plane, int row0, int c0, int row16, int grp) {
   typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -878,7 +888,7 @@ __device__ __forceinline__ bf16x8 tr_plane(const __bf16* plane, int row0, int c0
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int row = row0 + 8 * grp + 4 * q + (row16 >> 2);
-    const __bf16* p = plane + row * PITCH + c0 + 4 * (row16 & 3);
+    const __bf16* p = plane + row * PITCH + lds_col<PITCH>(row, c0 + 4 * (row16 & 3));
     h[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
   }
   return __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){h[0][0], h[0][1], h[0][2], h[0][3],
@@ -909,7 +919,7 @@ __global__ __launch_bounds__(CW * TW * 64) void k_enc_bwd(int64_t T, int n, int 
   constexpr int EW = CW * TW, NTH = EW * 64;
   constexpr int WC = 16 * CT, BC = CW * WC;
   constexpr int TS = 32 * TW;
-  constexpr int KP = 32 * KS, RPT = 16 * NT, RPS = KP + 8;
+  constexpr int KP = 32 * KS, RPT = 16 * NT, RPS = RESBM_IO_F32_BUILD ? KP + 8 : plane_pitch(KP);
   constexpr int GQ = TS * KP / 4;          // 4-column chunks of the g_h tile
   constexpr int NCH = (GQ + NTH - 1) / NTH;
   constexpr int GH_BYTES = (int)sizeof(GhTile<TS, RPS>);
@@ -1593,8 +1603,9 @@ __global__ __launch_bounds__(256) void k_gh(int64_t T, int r, int silu, const io
 #endif
 }
 
-// Transposed fragment of a row-major [rows][PITCH] plane of the I/O type:
-// lane (row16, grp) receives plane[8 grp + e][c0 + row16], e = 0..7.
+// Transposed fragment of a [rows][PITCH] plane of the I/O type (bf16 build:
+// lds_col<PITCH> layout; f32 build: row-major): lane (row16, grp) receives
+// plane[8 grp + e][c0 + row16], e = 0..7.
 template <int PITCH>
 __device__ __forceinline__ XFrag tr_rows(const io_t* plane, int c0, int row16, int grp) {
   XFrag f;
@@ -1621,7 +1632,8 @@ template <int NT, int NTW, bool DWD, bool R8>
 __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int RP, const io_t* __restrict__ X,
                                                    int64_t ld_x, const io_t* __restrict__ Y,
                                                    const io_t* __restrict__ Y_lo, float* __restrict__ dwp, int TB) {
-  constexpr int BCc = 128, TS = 32, KS = (NT + 1) / 2, KP = 32 * KS, YP = KP + 8;
+  constexpr int BCc = 128, TS = 32, KS = (NT + 1) / 2, KP = 32 * KS;
+  constexpr int YP = RESBM_IO_F32_BUILD ? KP + 8 : plane_pitch(KP);  // Y plane pitch (lds_col<YP> layout)
   constexpr bool SPLIT = !DWD && !RESBM_IO_F32_BUILD;
   constexpr int PL = SPLIT ? 2 : 1;
   constexpr int XE = TS * BCc, YE = TS * YP;  // elements of the X tile and of one Y plane
@@ -1687,7 +1699,7 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
       if (NYQ * 512 == PL * YC || qq < PL * YC) {
         const int pl = qq / YC, rem = qq % YC;
         const int yrow = rem / (KP / 8), c8 = 8 * (rem % (KP / 8));
-        io_t* dy = &s_y[buf][pl][yrow * YP + c8];
+        io_t* dy = &s_y[buf][pl][yrow * YP + (RESBM_IO_F32_BUILD ? c8 : lds_col<YP>(yrow, c8))];
 #if RESBM_IO_F32_BUILD
 #pragma unroll
         for (int e = 0; e < 8; ++e) dy[e] = g.y[i].v[e];

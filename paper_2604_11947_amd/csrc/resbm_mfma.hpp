@@ -197,32 +197,74 @@ __device__ __forceinline__ void store_x4(io_t* p, const float (&v)[4]) {
 }
 
 // ---------------------------------------------------------------- LDS tile layouts
-// Column permutation of a row-major tile with WC elements per row staged in
-// LDS.  The 8-element chunks of a row are permuted by an XOR with the row's
-// index among the rows that share a 256-byte bank window (16 / (WC / 8) rows in
-// the bf16 build), so that a wave touches distinct banks both when it copies
-// whole rows (8 lanes per 128 bytes, the layout of coalesced global accesses)
-// and when it reads one chunk from each of 16 rows (matrix-core fragments).
-// Chunks stay contiguous and never leave their row; WC whose chunk count is not
-// a power of two up to 8 is left as is.
+// Bank model of the gfx950 LDS, measured with timing probes of single access
+// patterns (cycles per instruction for 8 waves issuing the same pattern):
+//   ds_read_b128        64 banks of 4 bytes; 16 lanes per cycle, in the groups
+//                       {0-3, 12-15, 20-23, 24-27} and {4-11, 16-19, 28-31}
+//                       of each half-wave;
+//   ds_read_b64 and     64 banks; 32 lanes per cycle (lanes 0-31, 32-63);
+//   ds_read_b64_tr_b16
+//   ds_write_b128       32 banks (128 bytes); 8 consecutive lanes per cycle;
+//   ds_write_b64        32 banks; 16 consecutive lanes per cycle.
+// A group of lanes takes as many cycles as the largest number of distinct
+// 4-byte words that it addresses in one bank.  The layouts below permute the
+// 16-byte (8-element) chunks of a row-major tile by an XOR with a function of
+// the row, chosen so that the accesses of the kernels take one cycle per
+// group: whole-row copies (consecutive lanes on consecutive chunks), matrix-core
+// fragments (one chunk from each of 16 rows, lane group g on chunk c0 + g),
+// per-lane row pieces (lane (i, g) of a 16 x 8g tile writing row i, chunk g),
+// and transposed reads (ds_read_b64_tr_b16: 32 lanes on two adjacent chunks of
+// the 8 rows r0 .. r0 + 3 and r0 + 8 .. r0 + 11, r0 % 4 == 0).  Chunks stay
+// contiguous and never leave their row.
+
+// XOR applied to the low four chunk bits of row `row` of a tile whose rows are
+// a multiple of 256 bytes: chunk bit 1 <- row bit 0, bit 2 <- row bit 1,
+// bit 3 <- row bits 2 ^ 3, bit 0 <- row bit 3.  A bijection of the row's low
+// four bits (16 rows, one chunk each: 16 distinct slots, for either lane
+// grouping of ds_read_b128), and bits 1-3 take 8 distinct values over the rows
+// of a transposed read (the two chunks of a row share bits 1-3).  XORing with
+// the row's low four bits instead leaves rows r and r + 1 of a transposed read
+// on the same banks (twice the cycles).
+__device__ __forceinline__ int wide_xor(int row) {
+  const int rr = row & 15;
+  return (((rr << 1) | (rr >> 3)) & 15) ^ (rr & 8);
+}
+
+// Column permutation of a row-major tile with WC elements per row (32 or 64:
+// 4 or 8 chunks, i.e. 4 or 2 rows per 256-byte bank window); other widths are
+// left as is.  The XOR keeps the rows written by one 8-lane write group (8
+// consecutive rows of a 16-row tile, one chunk each) on distinct banks of the
+// 128-byte write window, and serves fragments and transposed reads as above.
 template <int WC>
 __device__ __forceinline__ int tile_col(int row, int col) {
   constexpr int CPR = WC / 8;
-  if constexpr (CPR == 8 || CPR == 4 || CPR == 2) {
-    constexpr int RPW = 16 / CPR;
-    return ((((col >> 3) ^ (row / RPW)) & (CPR - 1)) << 3) | (col & 7);
+  int x;
+  if constexpr (CPR == 8) {
+    x = (row & 7) ^ (((row >> 3) & 1) * 5);
+  } else if constexpr (CPR == 4) {
+    x = ((row >> 1) & 3) ^ (((row >> 3) & 1) * 3);
+  } else if constexpr (CPR == 2) {
+    x = (row >> 3) & 1;
   } else {
     return col;
   }
+  return ((((col >> 3) ^ x) & (CPR - 1)) << 3) | (col & 7);
 }
 
 // Column permutation of a block-wide row-major tile (WIDE elements per row, a
-// multiple of 128): the 8-element chunk index is XORed with the row's low four
-// bits, which keeps rows written whole (64 lanes x 16 bytes, the layout of
-// 1 KiB-contiguous global loads) conflict-free and spreads one chunk read from
-// 16 rows (matrix-core fragments) over all banks.
+// multiple of 128): the low four chunk bits are XORed with wide_xor(row).
 __device__ __forceinline__ int wide_col(int row, int col) {
-  return ((((col >> 3) ^ row) & 15) | ((col >> 3) & ~15)) << 3 | (col & 7);
+  return ((((col >> 3) ^ wide_xor(row)) & 15) | ((col >> 3) & ~15)) << 3 | (col & 7);
+}
+
+// Either layout, by row width (elements).
+template <int W>
+__device__ __forceinline__ int lds_col(int row, int col) {
+  if constexpr (W % 128 == 0) {
+    return wide_col(row, col);
+  } else {
+    return tile_col<W>(row, col);
+  }
 }
 
 // Activation function and its derivative (float32).

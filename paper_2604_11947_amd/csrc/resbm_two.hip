@@ -107,13 +107,20 @@ __device__ __forceinline__ int tr_col(int row, int col) {
   return ((((col >> 3) ^ f) & 15) | ((col >> 3) & ~15)) << 3 | (col & 7);
 }
 
+// Column permutation of a K-contiguous [I][64] tile: the chunk index is XORed
+// with (row / 2) % 8.  dma_tile inverts it when it stages such a tile.
+__device__ __forceinline__ int kc_col(int row, int col) {
+  return ((((col >> 3) ^ (row >> 1)) & 7) << 3) | (col & 7);
+}
+
 // Position of element (row, col) in a staged tile.  K-contiguous operands are
 // staged [I][64] (row = index along M or N, col = k); the others [64][I]
 // (row = k, col = index), I = 32, 64 or a multiple of 128.
 template <bool KC, int I>
 __device__ __forceinline__ int tile_pos(int row, int col) {
   if constexpr (KC) {
-    return row * KT + resbm::tile_col<KT>(row, col);
+    static_assert(KT == 64, "kc_col permutes the 8 chunks of a 64-element row");
+    return row * KT + kc_col(row, col);
   } else if constexpr (I % 128 == 0) {
     return row * I + tr_col(row, col);
   } else {
@@ -204,7 +211,7 @@ __device__ __forceinline__ void dma_tile(rsrc_t src, int64_t ld, int i0, int NI,
     if constexpr (KC) {
       const int row = o >> 7, pc = (o >> 4) & 7;
       idx = i0 + row;
-      k = k0 + 8 * ((pc ^ (row >> 1)) & 7);
+      k = k0 + 8 * ((pc ^ (row >> 1)) & 7);  // kc_col's XOR
     } else {
       const int row = o / (I * 2), pc = (o >> 4) % (I / 8);
       const int f = ((row & 3) | ((row >> 1) & 4)) << 1;  // tr_col's XOR
