@@ -370,9 +370,11 @@ def optimizer_timing(lib, d: dict, r: int, dev, iters: int, cpu: bool) -> dict:
         return e0.elapsed_time(e1) * 1e3 / iters
 
     steps = 5
-    # load, then per step: reduce (+ poly when the short side exceeds 64) + row update
+    # short side <= 64: load + Gram, ordered sum, the recurrence on the s x s Gram
+    # (one block), output pass; wider: load, then per step reduce + poly + row update
+    launches = 4 if r <= 64 else 1 + 3 * steps
     out = {"ns_steps": steps, "coefficients": list(R.NS_QUINTIC),
-           "launches_per_update": 1 + (2 if r <= 64 else 3) * steps,
+           "launches_per_update": launches,
            "timing": "hip graph replay of one call", "iterations": iters}
     keep = {}
     for nm in ("W_e", "W_d"):
@@ -392,7 +394,7 @@ def optimizer_timing(lib, d: dict, r: int, dev, iters: int, cpu: bool) -> dict:
     tf = flops / (out["muon_update_us_W_e"] * 1e-6) / 1e12
     out["roofline"] = {"bound": "latency", "kernel": "muon_update", "achieved": tf, "peak": 78.6,
                        "unit": "TFLOP/s", "frac": tf / 78.6, "flops_per_update": flops,
-                       "note": "11 launches on 64 blocks; launch and memory latency bound the chain"}
+                       "note": f"{launches} launches; launch and memory latency bound the chain"}
     if r <= 128:
         W0, _, ws = keep["W_d"]
         Wd = W0.to(dev)

@@ -24,6 +24,20 @@
 // kappa = 1 / (||U||_F + eps); for s4 <= 64 the row kernel forms B itself),
 // and k_mx_rows (X <- kappa (a X + X B) and the partial Grams of the result;
 // on the last step the float32 outputs instead).
+// Short side s4 <= 64, few steps: the iteration runs on the s x s Gram alone.
+// With X_0 = kappa U and Q_k = a I + b A_k + c A_k^2, X_{k+1} = X_k Q_k, so
+// X_k = X_0 P_k with P_0 = I, P_{k+1} = P_k Q_k, and the next Gram is
+// A_{k+1} = Q_k A_k Q_k (Q_k is a polynomial in the symmetric A_k).  One block
+// (k_mx_small) takes the Gram of U (k_mx_reduce), runs that recurrence in LDS
+// and writes R = kappa P_n; one row pass then forms X_n = U R.  Four launches
+// instead of 1 + 2n.  Equal to the row-by-row iteration in exact arithmetic;
+// in float64 the two agree to ~1e-12 of max |X_n| at the default 5 quintic
+// steps.  A direction of A_0 whose computed eigenvalue is a rounding error
+// (~1e-16 of the largest, possibly negative) grows by about a^2 per step in
+// the recurrence, where the row iteration keeps every Gram positive
+// semidefinite: on rank-one inputs the difference reaches ~1e-6 of max |X_n|
+// at a^(2n) ~ 1e11.  The recurrence is used only while a^(2n) <= 1e9 (the
+// quintic: n <= 8; the cubic: n <= 25), where it stays below ~1e-10.
 // No atomics and no waits between blocks: every sum has a fixed order, so
 // results are reproducible run to run.
 #include <hip/hip_runtime.h>
@@ -78,7 +92,8 @@ __device__ __forceinline__ double momentum_step(float* m, double gv, double mu, 
 //  kLoad: X = U from the float32 input (momentum applied first when given);
 //  kStep: X <- kappa (a X + X B);
 //  kOutO: out = float32(kappa (a X + X B)) in the stored layout;
-//  kOutW: out = float32(W - lr (scale X' + wd W)), X' = kappa (a X + X B).
+//  kOutW: out = float32(W - lr (scale X' + wd W)), X' = kappa (a X + X B);
+//  the output modes write from registers and leave X as it was.
 // kLoad and kStep then write the chunk's partial Gram part[b] = X^T X (rows of
 // the chunk only, s4 x s4).
 struct RowArgs {
@@ -97,6 +112,43 @@ struct RowArgs {
   double lr, scale, wd;
 };
 
+// Results y of logical elements (l0, k0 .. k0 + 3) and, when two, (l1, k0 ..
+// k0 + 3) of the row update: kStep keeps them in X; kOutO stores float32(y)
+// and kOutW the updated weights at the elements' places in the stored matrix
+// (columns >= s are padding and are dropped).  kOutW loads all of its weights
+// before the first store.
+template <int MODE>
+__device__ __forceinline__ void put_rows(const Dims& d, const RowArgs& g, int64_t l0, int64_t l1, bool two, int k0,
+                                         const double (&y)[8]) {
+  if constexpr (MODE == kStep) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      g.X[l0 * d.s4 + k0 + v] = y[v];
+      if (two) g.X[l1 * d.s4 + k0 + v] = y[4 + v];
+    }
+  } else {
+    int64_t pi[8];
+    bool ok[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      ok[q] = k0 + (q & 3) < d.s && (q < 4 || two);
+      pi[q] = ok[q] ? phys(d, q < 4 ? l0 : l1, k0 + (q & 3)) : 0;
+    }
+    if constexpr (MODE == kOutO) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (ok[q]) g.out[pi[q]] = (float)y[q];
+    } else {
+      double w[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) w[q] = ok[q] ? (double)g.out[pi[q]] : 0.0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (ok[q]) g.out[pi[q]] = (float)(w[q] - g.lr * (g.scale * y[q] + g.wd * w[q]));
+    }
+  }
+}
+
 template <int MODE>
 __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
   __shared__ double s_mem[kLdsDoubles];
@@ -110,17 +162,43 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
   if constexpr (MODE == kLoad) {
     // logical rows of the chunk in order of the stored layout (coalesced reads)
     const int rows = (int)(r1 - r0);
-    for (int64_t e = t; e < (int64_t)rows * s; e += kThreads) {
-      const int i = d.tall ? (int)(e / s) : (int)(e % rows);
-      const int k = d.tall ? (int)(e % s) : (int)(e / rows);
-      const int64_t pi = phys(d, r0 + i, k);
-      const double gv = (double)g.src[pi];
-      double u = gv;
-      if (g.mom) u = momentum_step(g.mom + pi, gv, g.mu, g.nesterov);
-      g.X[(r0 + i) * s4 + k] = u;
+    const int total = rows * s;  // <= 2^28
+    // eight elements per thread at a time: all their loads are issued before
+    // the first store (the stores to M could alias the next loads otherwise)
+    constexpr int kB = 8;
+    for (int e0 = t; e0 < total; e0 += kB * kThreads) {
+      double gv[kB];
+      float mv[kB];
+      int64_t pis[kB];
+#pragma unroll
+      for (int q = 0; q < kB; ++q) {
+        const int e = e0 + q * kThreads;
+        const int i = d.tall ? e / s : e % rows;
+        const int k = d.tall ? e % s : e / rows;
+        pis[q] = e < total ? phys(d, r0 + i, k) : -1;
+        gv[q] = e < total ? (double)g.src[pis[q]] : 0.0;
+        mv[q] = (e < total && g.mom) ? g.mom[pis[q]] : 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < kB; ++q) {
+        const int e = e0 + q * kThreads;
+        if (e >= total) continue;
+        const int i = d.tall ? e / s : e % rows;
+        const int k = d.tall ? e % s : e / rows;
+        double u = gv[q];
+        if (g.mom) {
+          float m = mv[q];
+          u = momentum_step(&m, gv[q], g.mu, g.nesterov);
+          g.mom[pis[q]] = m;
+        }
+        g.X[(r0 + i) * s4 + k] = u;
+        if (rows <= d.sub) s_mem[i * ts + k] = u;  // the Gram pass's tile, staged here
+      }
     }
-    for (int e = t; e < rows * (s4 - s); e += kThreads)
+    for (int e = t; e < rows * (s4 - s); e += kThreads) {
       g.X[(r0 + e / (s4 - s)) * s4 + s + e % (s4 - s)] = 0.0;
+      if (rows <= d.sub) s_mem[(e / (s4 - s)) * ts + s + e % (s4 - s)] = 0.0;
+    }
   } else {
     // X <- kappa (a X + X B), one sub-chunk of rows at a time through LDS
     __shared__ double s_kappa;
@@ -187,13 +265,13 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
               acc1[v] = fma(a1, bv[v], acc1[v]);
             }
           }
+          double y[8];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) g.X[(t0 + i) * s4 + 4 * cg + v] = kappa * fma(g.a, x0[4 * cg + v], acc0[v]);
-          if (i2 != i) {
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-              g.X[(t0 + i2) * s4 + 4 * cg + v] = kappa * fma(g.a, x1[4 * cg + v], acc1[v]);
+          for (int v = 0; v < 4; ++v) {
+            y[v] = kappa * fma(g.a, x0[4 * cg + v], acc0[v]);
+            y[4 + v] = kappa * fma(g.a, x1[4 * cg + v], acc1[v]);
           }
+          put_rows<MODE>(d, g, t0 + i, t0 + i2, i2 != i, 4 * cg, y);
         }
       }
       __syncthreads();  // the tile is reloaded next
@@ -201,21 +279,7 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
   }
 
   if constexpr (MODE == kOutO || MODE == kOutW) {
-    __syncthreads();  // this block's rows of X are complete
-    const int rows = (int)(r1 - r0);
-    for (int64_t e = t; e < (int64_t)rows * s; e += kThreads) {
-      const int i = d.tall ? (int)(e / s) : (int)(e % rows);
-      const int k = d.tall ? (int)(e % s) : (int)(e / rows);
-      const int64_t pi = phys(d, r0 + i, k);
-      const double x = g.X[(r0 + i) * s4 + k];
-      if constexpr (MODE == kOutO) {
-        g.out[pi] = (float)x;
-      } else {
-        const double w = (double)g.out[pi];
-        g.out[pi] = (float)(w - g.lr * (g.scale * x + g.wd * w));
-      }
-    }
-    return;
+    return;  // the outputs were written by the row update
   } else {
     // partial Gram of the chunk: part[b][i][j] = sum over its rows of X[l][i] X[l][j],
     // 4 x 4 entry blocks per thread; row groups (small s4) are added in order
@@ -238,7 +302,9 @@ __global__ __launch_bounds__(kThreads) void k_mx_rows(Dims d, RowArgs g) {
       const int rgp = R > 1 ? t / nblk : 0;
       for (int64_t t0 = r0; t0 < r1; t0 += d.sub) {
         const int rows = (int)(r1 - t0 < d.sub ? r1 - t0 : d.sub);
-        for (int e = t; e < rows * s4; e += kThreads) tile[(e / s4) * ts + e % s4] = g.X[t0 * s4 + e];
+        // in load mode a chunk of one sub-chunk is in the tile already
+        if (MODE != kLoad || r1 - r0 > d.sub)
+          for (int e = t; e < rows * s4; e += kThreads) tile[(e / s4) * ts + e % s4] = g.X[t0 * s4 + e];
         __syncthreads();
         if (rgp < R) {
 #pragma unroll
@@ -360,6 +426,97 @@ __global__ __launch_bounds__(kThreads) void k_mx_poly(int s4, const double* A, d
       B[(int64_t)(i0 + ii) * s4 + j0 + jj] = cb * k2 * ri[j0 + jj] + cc * (k2 * k2) * sq;
     }
   }
+}
+
+// ---------------------------------------------------------------- short-side recurrence
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallMax = 64;               // s4 of the short-side recurrence
+constexpr int kSmallLd = kSmallMax + 1;     // padded LDS row stride (doubles)
+
+// Z = X Y for s4 x s4 matrices in LDS (row stride ld, zero beyond s4 up to a
+// multiple of 16) on the float64 matrix cores: v_mfma_f64_16x16x4_f64 per
+// 16 x 16 tile and 4-deep k-step, one tile per wave.  Lane (row16, grp) holds
+// A[row16][grp] and B[grp][row16]; its accumulator element v is
+// D[grp + 4 v][row16] (measured on gfx950).
+// NT = tiles per side (s4 <= 16 NT); the k-steps run to 16 NT over the zero
+// padding, all operand loads issued before the products.
+template <int NT>
+__device__ __forceinline__ void small_mm(const double* X, const double* Y, double* Z, int ld) {
+  typedef double d4 __attribute__((ext_vector_type(4)));
+  constexpr int KSTEPS = 4 * NT;
+  const int l = threadIdx.x & 63, row16 = l & 15, grp = l >> 4, wave = threadIdx.x >> 6;
+  if (wave >= NT * NT) return;  // one tile per wave (16 waves >= NT^2)
+  const int i0 = 16 * (wave / NT), j0 = 16 * (wave % NT);
+  double xa[KSTEPS], yb[KSTEPS];
+#pragma unroll
+  for (int q = 0; q < KSTEPS; ++q) {
+    xa[q] = X[(i0 + row16) * ld + 4 * q + grp];
+    yb[q] = Y[(4 * q + grp) * ld + j0 + row16];
+  }
+  d4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int q = 0; q < KSTEPS; ++q) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa[q], yb[q], acc, 0, 0, 0);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) Z[(i0 + grp + 4 * v) * ld + j0 + row16] = acc[v];
+}
+
+// One block: from the reduced Gram A_0 (s4 x s4, row-major), kappa =
+// 1 / (sqrt(trace A_0) + eps), then n steps of the recurrence on
+// Ab = kappa^2 A_0; writes R = kappa P_n to Rout (s4 x s4, row-major) and 1 to
+// scal[0] (the row pass scales by it).
+template <int NT>
+__global__ __launch_bounds__(kSmallThreads) void k_mx_small(int s4, const double* A0, int n, double a, double b,
+                                                            double c, double* Rout, double* scal) {
+  __shared__ double s_a[kSmallMax * kSmallLd], s_p[kSmallMax * kSmallLd];
+  __shared__ double s_q[kSmallMax * kSmallLd], s_t[kSmallMax * kSmallLd];
+  __shared__ double s_kappa;
+  const int t = threadIdx.x, ld = kSmallLd, ne = s4 * s4;
+  // the matrix-core tiles read up to a multiple of 16 rows and columns: zeros there
+  for (int e = t; e < kSmallMax * kSmallLd; e += kSmallThreads) s_a[e] = s_p[e] = s_q[e] = s_t[e] = 0.0;
+  __syncthreads();
+  for (int e = t; e < ne; e += kSmallThreads) {
+    s_a[(e / s4) * ld + e % s4] = A0[e];
+    s_p[(e / s4) * ld + e % s4] = (e / s4 == e % s4) ? 1.0 : 0.0;
+  }
+  __syncthreads();
+  if (t == 0) {
+    double tr = 0.0;
+    for (int i = 0; i < s4; ++i) tr += s_a[i * ld + i];
+    s_kappa = 1.0 / (sqrt(tr) + kNsEps);
+  }
+  __syncthreads();
+  const double kappa = s_kappa, k2 = kappa * kappa;
+  for (int e = t; e < ne; e += kSmallThreads) s_a[(e / s4) * ld + e % s4] *= k2;
+  __syncthreads();
+  double* P = s_p;  // P_k and a scratch matrix swap roles after every P Q
+  double* U = s_t;
+  for (int k = 0; k < n; ++k) {
+    small_mm<NT>(s_a, s_a, s_q, ld);  // A^2
+    __syncthreads();
+    for (int e = t; e < ne; e += kSmallThreads) {
+      const int i = e / s4, j = e % s4;
+      s_q[i * ld + j] = (i == j ? a : 0.0) + b * s_a[i * ld + j] + c * s_q[i * ld + j];  // Q
+    }
+    __syncthreads();
+    small_mm<NT>(P, s_q, U, ld);  // P Q
+    __syncthreads();
+    double* w = P;
+    P = U;
+    U = w;
+    if (k + 1 < n) {
+      small_mm<NT>(s_a, s_q, U, ld);  // A Q
+      __syncthreads();
+      small_mm<NT>(s_q, U, s_a, ld);  // next A = Q (A Q)
+      __syncthreads();
+    }
+  }
+  for (int e = t; e < ne; e += kSmallThreads) Rout[e] = kappa * P[(e / s4) * ld + e % s4];
+  if (t == 0) scal[0] = 1.0;
+}
+
+// Whether the short-side recurrence applies: s4 <= 64 and |a|^(2n) <= 1e9.
+bool small_ok(int s4, int n, double a) {
+  return s4 <= kSmallMax && 2.0 * n * log10(fabs(a) > 1.0 ? fabs(a) : 1.0) <= 9.0;
 }
 
 // ---------------------------------------------------------------- spectrum
@@ -611,6 +768,21 @@ void run_ns(const Plan& P, char* ws, RowArgs g, int steps, double a, double b, d
   const int n = steps > 0 ? steps : 1;
   if (steps == 0) { a = 1.0; b = 0.0; c = 0.0; }
   const int ne = d.s4 * d.s4;
+  if (small_ok(d.s4, n, a)) {
+    // X_n = U R, R from the short-side recurrence: the row pass with a = 0 and
+    // B = R, read from the workspace (scal[0] = 1)
+    hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), blk, 0, st, ne, d.nch,
+                       (const double*)g.part, A);
+    const int nt = (d.s4 + 15) / 16;
+    auto small = nt <= 1 ? k_mx_small<1> : nt == 2 ? k_mx_small<2> : nt == 3 ? k_mx_small<3> : k_mx_small<4>;
+    hipLaunchKernelGGL(small, dim3(1), dim3(kSmallThreads), 0, st, d.s4, (const double*)A, n, a, b, c, B, scal);
+    Dims d2 = d;
+    d2.fuse_b = 0;
+    RowArgs gi = g;
+    gi.a = 0.0;
+    hipLaunchKernelGGL(k_mx_rows<MODE_OUT>, grid, blk, 0, st, d2, gi);
+    return;
+  }
   for (int i = 0; i < n; ++i) {
     hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), blk, 0, st, ne, d.nch,
                        (const double*)g.part, A);

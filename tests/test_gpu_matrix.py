@@ -64,6 +64,25 @@ def test_newton_schulz_parity(p, q, kind, coeffs, steps):
     assert e <= MAT_BOUND
 
 
+@pytest.mark.parametrize("p,q,kind", [(4096, 32, "gaussian"), (333, 40, "powerlaw"), (7, 3, "rank1"), (64, 64, "powerlaw")],
+                         ids=["4096x32-gaussian", "333x40-powerlaw", "7x3-rank1", "64x64-powerlaw"])
+@pytest.mark.parametrize("steps", [8, 9, 30])
+def test_newton_schulz_long_runs(p, q, kind, steps):
+    """Step counts on both sides of the switch between the short-side
+    recurrence (quintic: up to 8 steps) and the row-by-row iteration, and a
+    long run of a rank-deficient matrix, whose rounding-level Gram directions
+    the recurrence would amplify."""
+    L = lib()
+    say(f"newton_schulz {p}x{q} {kind} steps={steps}")
+    G = I.make_matrix(p, q, kind, seed=3)
+    O = run_ns(L, G, steps, MU.NS_QUINTIC)
+    ref = MU.newton_schulz(G.double().numpy(), steps, MU.NS_QUINTIC)
+    e = max_rel(f64(O), ref)
+    say(f"    max err / max|ref| = {e:.2e}")
+    assert np.all(np.isfinite(f64(O)))
+    assert e <= MAT_BOUND
+
+
 def test_newton_schulz_deterministic_and_zero():
     L = lib()
     G = I.make_matrix(4096, 32, "gaussian", seed=2)
