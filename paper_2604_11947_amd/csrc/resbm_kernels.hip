@@ -1191,6 +1191,16 @@ __device__ __forceinline__ void enc_bwd_fin_block(int64_t bid, int64_t T, int n,
   }
 }
 
+// The finishing work of encode_bwd as a kernel of its own (wide r: the g_z
+// kernel's register allocation would leave its finishing blocks one wave per
+// SIMD, behind the g_z blocks).
+__global__ __launch_bounds__(256) void k_enc_bwd_fin(int64_t T, int n, int r, int RP, const float* __restrict__ dwp,
+                                                     int ntg, float* __restrict__ dW_e, int accumulate,
+                                                     int64_t nb_dw, const io_t* __restrict__ g_b,
+                                                     io_t* __restrict__ g_x, int64_t ld_gx) {
+  enc_bwd_fin_block(blockIdx.x, T, n, r, RP, dwp, ntg, dW_e, accumulate, nb_dw, g_b, g_x, ld_gx);
+}
+
 // ============================================================ expand contractions
 // out = in W (+ idsrc I_{r x n} when ADD), an r-wide input times an r x n map:
 //   decode_fwd (GZ = false): z~ = b W_d (+ b I_{r x n}, reading A); in = b, W = W_d [r][n];
@@ -1928,6 +1938,10 @@ __global__ __launch_bounds__(256) void k_expand_wide(int64_t T, int n, int r, co
 #pragma unroll
           for (int pl = 0; pl < PL; ++pl) nxt[h2][pl] = s_in[buf][(h2 * KS + ks + 1) * PL + pl][l];
       }
+      // keep the next k-step's reads ahead of this k-step's products (left to
+      // itself the compiler issues each read right before its first use and
+      // waits for it there)
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         if constexpr (GZ) {
@@ -2155,9 +2169,10 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
 #else
   dim3 ggrid(p.df_nwg, p.df_ngrp);
 #endif
-  // the finishing blocks follow in extra grid rows (dispatched after the g_z blocks, run beside them)
+  // the finishing blocks follow in extra grid rows (dispatched after the g_z
+  // blocks, run beside them); wide r: a kernel of their own after g_z
   const int main_y = (int)ggrid.y;
-  ggrid.y += (unsigned)ceil_div(fin.nb_all, (int64_t)ggrid.x);
+  if constexpr (NT < kWideNT) ggrid.y += (unsigned)ceil_div(fin.nb_all, (int64_t)ggrid.x);
 #define CALL_GZ(ADD, R8)                                                                                         \
   do {                                                                                                           \
     if constexpr (NT >= kWideNT)                                                                                 \
@@ -2173,6 +2188,9 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
     if (r8) CALL_GZ(false, true); else CALL_GZ(false, false);
   }
 #undef CALL_GZ
+  if constexpr (NT >= kWideNT)
+    hipLaunchKernelGGL(k_enc_bwd_fin, dim3((unsigned)fin.nb_all), dim3(256), 0, st, p.T, p.n, p.r, fin.RP, fin.dwp,
+                       fin.ntg, fin.dW_e, fin.accumulate, fin.nb_dw, fin.g_b, fin.g_x, fin.ld_gx);
 }
 
 #define RESBM_DISPATCH_NT(NTV, CALL) \

@@ -54,7 +54,17 @@ constexpr int ef_kw(int NT) { return 8 * 16 * ef_mt(NT) * (16 * NT + 4) * 4 <= 7
 // ---- decode_fwd: a wave owns 16*CT columns and walks a token range.
 // Four column tiles up to r = 128 (at r = 128: 69 -> 45 us), two beyond (at
 // r = 256: 236 -> 128 us); the g_z pass of encode_bwd follows the same shape.
-constexpr int df_ct(int KS) { return KS <= 4 ? 4 : 2; }
+#ifndef RESBM_DF_CT_W4
+#define RESBM_DF_CT_W4 4
+#endif
+#ifndef RESBM_DF_CT_W8
+#define RESBM_DF_CT_W8 2
+#endif
+#ifndef RESBM_DF_WAVES_PER_CU_WIDE
+#define RESBM_DF_WAVES_PER_CU_WIDE 4
+#endif
+constexpr int df_ct(int KS) { return KS <= 2 ? 4 : (KS <= 4 ? RESBM_DF_CT_W4 : RESBM_DF_CT_W8); }
+constexpr int df_waves_per_cu(int KS) { return KS <= 2 ? RESBM_DF_WAVES_PER_CU : RESBM_DF_WAVES_PER_CU_WIDE; }
 
 // ---- decode_bwd: 8 waves x 64 columns per block, JT j-tiles (16 of r each) per pass.
 #ifndef RESBM_DB_WAVES
@@ -146,7 +156,7 @@ inline Plan make_plan(int64_t T, int n, int r) {
   p.df_nwg = (int)ceil_div(p.df_nstrips, 4);
   {
     const int64_t ntile = ceil_div(Tm, 16);
-    const int64_t g = clamp64(ceil_div((int64_t)RESBM_DF_WAVES_PER_CU * kNumCU, (int64_t)p.df_nwg * 4), 1, ntile);
+    const int64_t g = clamp64(ceil_div((int64_t)df_waves_per_cu(p.KS) * kNumCU, (int64_t)p.df_nwg * 4), 1, ntile);
     p.df_tpg = (int)(16 * ceil_div(ntile, g));
     // a token group's output rows lie in one buffer descriptor (32-bit byte
     // offsets): at most 1 GiB of dense rows per group

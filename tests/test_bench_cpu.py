@@ -33,6 +33,7 @@ import bench  # noqa: E402
     ("resbm::k_expand_wide<4, 4, true, false, false>", "decode_fwd"),
     ("_ZN5resbm4k_ghEliiPKDF16bPKfPDF16bS4_", "encode_bwd"),
     ("resbm::k_wd_prep", "decode_bwd"),
+    ("resbm::k_enc_bwd_fin", "encode_bwd"),
     ("resbm_mx::k_mx_rows<1>", None),
     ("__amd_rocclr_copyBuffer", None),
 ])
