@@ -240,3 +240,30 @@ def test_fusion_pin_rejects_dropped_skip(monkeypatch):
     monkeypatch.setattr(FO, "encode_fwd", _fused_skip_dropped)
     with pytest.raises(AssertionError):
         FP.test_integer_inputs_follow_associativity(R.ACT_IDENTITY)
+
+
+# ---------------------------------------------------------------- decoder into normalisation + QKV
+def _rms_sum_not_mean(x, gamma, eps):
+    x = np.asarray(x, dtype=np.float64)
+    return x / np.sqrt(np.sum(x * x, axis=1, keepdims=True) + eps) * gamma[None, :]
+
+
+def _rms_gain_dropped(x, gamma, eps):
+    x = np.asarray(x, dtype=np.float64)
+    return x / np.sqrt(np.mean(x * x, axis=1, keepdims=True) + eps)
+
+
+def _rms_eps_outside_root(x, gamma, eps):
+    x = np.asarray(x, dtype=np.float64)
+    return x / (np.sqrt(np.mean(x * x, axis=1, keepdims=True)) + eps) * gamma[None, :]
+
+
+@pytest.mark.parametrize("bad,pin", [
+    (_rms_sum_not_mean, FP.test_decode_qkv_rows_have_unit_mean_square),
+    (_rms_gain_dropped, FP.test_decode_qkv_scale_invariance_and_gain),
+    (_rms_eps_outside_root, FP.test_decode_qkv_brute_force_loops),
+], ids=["sum_not_mean", "gain_dropped", "eps_outside_root"])
+def test_decode_qkv_pin_rejects_planted_mistake(monkeypatch, bad, pin):
+    monkeypatch.setattr(FO, "rms_norm", bad)
+    with pytest.raises(AssertionError):
+        pin()
