@@ -61,6 +61,8 @@ def parse():
                    help="skip timing the optimizer-side ops (Muon update, spectrum) on the bottleneck weights")
     p.add_argument("--two-m", type=int, default=1024,
                    help="intermediate width m of the two-linears-per-side variant (0: skip timing it)")
+    p.add_argument("--qkv-width", type=int, default=6144,
+                   help="N of the QKV projection the fused decoder is timed on (0 skips it)")
     p.add_argument("--ffn-width", type=int, default=14336,
                    help="FFN hidden width for timing the encoder fused into the FFN output projection (0: skip)")
     p.add_argument("--no-sweep", action="store_true",
@@ -506,8 +508,8 @@ def two_linear_timing(lib, d: dict, r: int, m: int, dev, iters: int, cpu: bool, 
 def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int, cpu: bool) -> dict:
     """The encoder fused into the FFN output projection (resbm_ffn_encode_fwd: z = h W_down
     with the encoder in the epilogue) against the unfused pair: the same projection by
-    the framework's library GEMM (torch.matmul, hipBLASLt) followed by resbm_encode_fwd.
-    HIP events on the launch stream around each call."""
+    the framework's library GEMM (torch.matmul, hipBLASLt) followed by resbm_encode_fwd,
+    called back to back (each part also timed alone).  HIP events on the launch stream."""
     import torch
 
     from paper_2604_11947_amd import inputs as I
@@ -520,8 +522,13 @@ def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int
     z, b = torch.empty(T, n, dtype=bf, device=dev), torch.empty(T, r, dtype=bf, device=dev)
     a = torch.empty(T, r, device=dev)
     ws = lib.workspace(T, n, r, dev)
+    def unfused():
+        torch.matmul(h, W_down, out=z)
+        lib.encode_fwd(x, z, W_e, b, a_save=a, act=act, ws=ws)
+
     calls = {
         "fused": lambda: lib.ffn_encode_fwd(h, W_down, x, W_e, z, b, a_save=a, act=act),
+        "unfused": unfused,
         "library_gemm": lambda: torch.matmul(h, W_down, out=z),
         "encode_fwd": lambda: lib.encode_fwd(x, z, W_e, b, a_save=a, act=act, ws=ws),
     }
@@ -540,8 +547,9 @@ def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int
         us[nm] = e0.elapsed_time(e1) * 1e3 / iters
     flops = 2.0 * T * d_ff * n + 2.0 * T * n * r
     tf = flops / (us["fused"] * 1e-6) / 1e12
-    out = {"d_ff": d_ff, "tokens": T, "us": us, "unfused_us": us["library_gemm"] + us["encode_fwd"],
-           "fused_over_unfused": us["fused"] / (us["library_gemm"] + us["encode_fwd"]), "iterations": iters,
+    out = {"d_ff": d_ff, "tokens": T, "us": us, "unfused_us": us["unfused"],
+           "fused_over_unfused": us["fused"] / us["unfused"], "iterations": iters,
+           "timing": "HIP events around each call; unfused = the library GEMM and resbm_encode_fwd back to back",
            "tokens_per_s": T / (us["fused"] * 1e-6),
            "roofline": {"bound": "mfma", "kernel": "k_gemm<256x256, encoder epilogue>", "achieved": tf,
                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": tf / MFMA_BF16_PEAK_TFLOPS,
@@ -560,6 +568,87 @@ def ffn_encode_timing(lib, d: dict, r: int, d_ff: int, dev, iters: int, act: int
         out["cpu_baseline"] = {"value": Ts / sec, "unit": "tokens/s", "cores": torch.get_num_threads(),
                                "kind": "oracle", "sample": f"{Ts} tokens of the same op, {reps} repetitions"}
     return out
+
+
+def decode_qkv_timing(lib, d: dict, r: int, N: int, dev, iters: int, cpu: bool) -> dict:
+    """The decoder fused into the next block's RMS normalisation and QKV projection
+    (resbm_decode_qkv_fwd) against the unfused chain: resbm_decode_fwd, the framework's
+    RMS normalisation (torch.nn.functional.rms_norm) and its library GEMM (torch.matmul,
+    hipBLASLt), called back to back (each part also timed alone).  HIP events."""
+    import torch
+    import torch.nn.functional as TF
+
+    from paper_2604_11947_amd import inputs as I
+
+    T, n = d["z"].shape
+    bf = torch.bfloat16
+    eps = 1e-5
+    b = I.make_bf16(T, r, 44).to(dev)
+    W_d = d["W_d"].to(dev)
+    gamma = I.make_gain(n, 45).to(dev)
+    gamma_bf = gamma.to(bf)
+    W_qkv = I.make_bf16(n, N, 46, std=n ** -0.5).to(dev)
+    out = torch.empty(T, N, dtype=bf, device=dev)
+    zt = torch.empty(T, n, dtype=bf, device=dev)
+    y = torch.empty(T, n, dtype=bf, device=dev)
+    ws = lib.workspace(T, n, r, dev)
+    qws = torch.empty(int(lib.cdll.resbm_decode_qkv_workspace_bytes(n, r)) + 256, dtype=torch.uint8, device=dev)
+    qws = qws[(-qws.data_ptr()) % 256:]
+
+    def norm():
+        y.copy_(TF.rms_norm(zt, (n,), weight=gamma_bf, eps=eps))
+
+    def unfused():
+        lib.decode_fwd(b, W_d, zt, ws=ws)
+        norm()
+        torch.matmul(y, W_qkv, out=out)
+
+    calls = {
+        "fused": lambda: lib.decode_qkv_fwd(b, W_d, gamma, W_qkv, out, eps=eps, ws=qws),
+        "unfused": unfused,
+        "decode_fwd": lambda: lib.decode_fwd(b, W_d, zt, ws=ws),
+        "rms_norm": norm,
+        "library_gemm": lambda: torch.matmul(y, W_qkv, out=out),
+    }
+    stream = torch.cuda.current_stream()
+    us = {}
+    for nm, f in calls.items():
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us[nm] = e0.elapsed_time(e1) * 1e3 / iters
+    KS = (r + 31) // 32
+    flops = 2.0 * T * n * N
+    rebuild = 2.0 * T * r * n * 2 * ((N + 255) // 256)  # hi + lo products, once per 256-column tile of N
+    tf = flops / (us["fused"] * 1e-6) / 1e12
+    res = {"N": N, "tokens": T, "us": us, "unfused_us": us["unfused"],
+           "fused_over_unfused": us["fused"] / us["unfused"], "iterations": iters,
+           "timing": "HIP events around each call; unfused = decode_fwd, rms_norm and the library GEMM back to back",
+           "rebuild_share_of_products": 2 * KS * 32 / 256 if r <= 64 else None,
+           "tokens_per_s": T / (us["fused"] * 1e-6),
+           "roofline": {"bound": "mfma", "kernel": "k_dec_qkv (256x256 tiles, A tiles rebuilt from b W_d)",
+                        "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": tf / MFMA_BF16_PEAK_TFLOPS, "flops": flops, "rebuild_flops": rebuild}}
+    if cpu:
+        from oracle import fusion_oracle as FO
+        Ts = 64
+        f64 = lambda t: t.to(torch.float64).cpu().numpy()  # noqa: E731
+        bs, Wd, g, W = f64(b[:Ts]), W_d.double().cpu().numpy(), gamma.double().cpu().numpy(), f64(W_qkv)
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 5.0:
+            FO.decode_qkv_fwd(bs, Wd, g, W, eps)
+            reps += 1
+        sec = (time.perf_counter() - t0) / reps
+        res["cpu_baseline"] = {"value": Ts / sec, "unit": "tokens/s", "cores": torch.get_num_threads(),
+                               "kind": "oracle", "sample": f"{Ts} tokens of the same op, {reps} repetitions"}
+    return res
 
 
 def sweep_timing(lib, dev, names, steps: int, warmup: int, act: int) -> dict:
@@ -849,6 +938,8 @@ def main():
         out["two_linear"] = two_linear_timing(lib, d, r, args.two_m, dev, 50, not args.no_cpu_baseline, act)
     if args.ffn_width > 0:
         out["ffn_encode"] = ffn_encode_timing(lib, d, r, args.ffn_width, dev, 20, act, not args.no_cpu_baseline)
+    if args.qkv_width > 0 and r <= 64:
+        out["decode_qkv"] = decode_qkv_timing(lib, d, r, args.qkv_width, dev, 20, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         tokens = args.cpu_tokens or T
         out["cpu_baseline"] = cpu_baseline(d, r, act, min(tokens, T))

@@ -341,6 +341,34 @@ int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int3
                              void* z, int64_t ld_z, void* b, float* a_save,
                              void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * Decoder fused into the next block's RMS normalisation and QKV projection.
+ * Sec. 3.2 places the decoder at the start of stage l + 1; with the decoder's
+ * identity path added by the caller (reading B) its output z~ = b W_d is the
+ * input of that stage's first block, whose attention begins with an RMS
+ * normalisation (gain gamma) and the QKV projection:
+ *     out = RMSNorm(z~) W_qkv,
+ *     RMSNorm(x)[t][c] = x[t][c] / sqrt(mean_c' x[t][c']^2 + eps) gamma[c].
+ * z~ is never written: every 256 x 256 output tile rebuilds its rows of z~
+ * (b W_d, W_d as hi + lo bf16 parts, times gamma, rounded to bf16) for each
+ * 64-deep stage of the projection, and the row scale comes from the float32
+ * z~ of the same rebuild.  A caller that also needs z~ (its residual stream)
+ * still runs resbm_decode_fwd.
+ *  b      T x r bf16 packed (the payload).
+ *  W_d    r x n float32 row-major.   gamma  n float32.
+ *  W_qkv  n x N bf16 row-major, contiguous.
+ *  out    T x N bf16, row stride ld_out (ld_out >= N, ld_out % 8 == 0).
+ * Shape rules: n % 64 == 0, 64 <= n <= 65536; r % 8 == 0, 8 <= r <= 64;
+ * N % 8 == 0, 8 <= N <= 262144; eps >= 0.  Pointers 16-byte aligned.  ws: at
+ * least resbm_decode_qkv_workspace_bytes(n, r) bytes (W_d in fragment order),
+ * 256-byte aligned, caller-owned, dead after the call.
+ */
+size_t resbm_decode_qkv_workspace_bytes(int32_t n, int32_t r);
+int32_t resbm_decode_qkv_fwd(int64_t T, int32_t n, int32_t r, int32_t N,
+                             const void* b, const float* W_d, const float* gamma,
+                             const void* W_qkv, float eps, void* out, int64_t ld_out,
+                             void* ws, size_t ws_bytes, void* stream);
+
 /* RESBM_IO_BF16 for libresbm.so, RESBM_IO_F32 for the validation build. */
 int32_t resbm_io_dtype(void);
 

@@ -461,6 +461,200 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
   if constexpr (EPI == kEpiEncode) encode_epilogue<BM, BN, WM, WN, FM, FN>(g, acc, s_a0, s_a1, s_b0, s_b1, m0, n0);
 }
 
+// ---------------------------------------------------------------- decoder into RMSNorm + QKV
+// Fragment-ordered hi/lo bf16 copy of W_d (r x n, float32) for the B slot of
+// the decoder contraction z~ = b W_d: fragment f = ks * (n / 16) + cb, lane
+// (row16, grp) holds W_d[32 ks + 8 grp + e][16 cb + row16] (zeros at rows >= r);
+// per fragment 1 KiB of hi parts, then 1 KiB of lo parts.
+__global__ __launch_bounds__(64) void k_dq_wd_prep(const float* __restrict__ W_d, int r, int n, int KS,
+                                                   __bf16* __restrict__ wdf) {
+  const int l = threadIdx.x, row16 = l & 15, grp = l >> 4;
+  const int f = blockIdx.x, nc = n / 16;
+  const int ks = f / nc, cb = f % nc;
+  bf16x8 hi, lo;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int j = 32 * ks + 8 * grp + e;
+    const float w = j < r ? W_d[(int64_t)j * n + 16 * cb + row16] : 0.0f;
+    __bf16 h, q;
+    resbm::split_hi_lo(w, h, q);
+    hi[e] = h;
+    lo[e] = q;
+  }
+  (void)KS;
+  reinterpret_cast<bf16x8*>(wdf)[(int64_t)(2 * f) * 64 + l] = hi;
+  reinterpret_cast<bf16x8*>(wdf)[(int64_t)(2 * f + 1) * 64 + l] = lo;
+}
+
+struct DqArgs {
+  int T, n, N, r;
+  const __bf16* b;       // T x r
+  const __bf16* wdf;     // W_d fragments (k_dq_wd_prep)
+  const float* gamma;    // n
+  const __bf16* W;       // n x N, row-major
+  int64_t w_bytes;
+  __bf16* out;           // T x N, row stride ld_out
+  int64_t ld_out, out_bytes;
+  float eps;
+};
+
+// out = RMSNorm(b W_d) W_qkv on 256 x 256 output tiles (8 waves of 128 x 64,
+// the 64-deep stages of k_gemm).  The A operand of every stage -- 64 columns
+// of z~ for the tile's 256 rows -- is rebuilt in the block instead of read:
+// wave w forms rows [32 w, 32 w + 32) of it as b W_d (W_d hi and lo: two
+// products per 16 x 16 piece and 32-deep k-step of r), multiplies by gamma and
+// rounds to bf16 into the LDS tile; W_qkv streams in as in k_gemm.  Each wave
+// also sums the squares of its rows' float32 z~ over the whole K loop; the row
+// scale 1 / sqrt(mean z~^2 + eps) is applied in the epilogue (RMSNorm is a
+// per-row scale of z~ gamma).  The rebuild costs 2 KS / 4 of the tile's
+// products (W_d as hi + lo, KS = r / 32 rounded up).
+template <int KS>
+__global__ __launch_bounds__(512) void k_dec_qkv(DqArgs g) {
+  constexpr int BM = 256, BN = 256, WM = 2, WN = 4, NW = 8;
+  constexpr int FM = BM / (16 * WM), FN = BN / (16 * WN);
+  __shared__ __attribute__((aligned(16))) __bf16 s_a0[BM * KT], s_a1[BM * KT];
+  __shared__ __attribute__((aligned(16))) __bf16 s_b0[BN * KT], s_b1[BN * KT];
+  __shared__ float s_ssq[BM];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int row16 = lane & 15, grp = lane >> 4;
+  const int wm = wave % WM, wn = wave / WM;
+  const int tiles_n = (g.N + BN - 1) / BN;
+  const int t = xcd_tile(blockIdx.x, gridDim.x);
+  const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
+  const int nst = g.n / KT;
+  const int nc = g.n / 16;
+
+  const rsrc_t rw = make_rsrc(g.W, g.w_bytes);
+  const rsrc_t rbr = make_rsrc(g.b + (int64_t)m0 * g.r, (int64_t)max(0, min(BM, g.T - m0)) * g.r * 2);
+  const rsrc_t rwd = make_rsrc(g.wdf, (int64_t)KS * nc * 2048);
+  const rsrc_t rg = make_rsrc(g.gamma, (int64_t)g.n * 4);
+
+  // b rows of this wave's rebuild (the A slot: lane holds b[row][32 ks + 8 grp + e])
+  bf16x8 bfr[2][KS];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int row = 32 * wave + 16 * rb + row16, j = 32 * ks + 8 * grp;
+      bfr[rb][ks] = __builtin_bit_cast(bf16x8, bld16(rbr, j < g.r ? (uint32_t)((row * g.r + j) * 2) : kOOB));
+    }
+  // W_d fragments and gamma of a stage, loaded one stage ahead
+  struct Wd {
+    bf16x8 hi[4][KS], lo[4][KS];
+    float4 gm[4];
+  };
+  auto load_wd = [&](Wd& w, int s) {
+    const bool ok = s < nst;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int c16 = (s * KT) / 16 + cb;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int64_t f = (int64_t)ks * nc + c16;
+        w.hi[cb][ks] = __builtin_bit_cast(bf16x8, bld16(rwd, ok ? (uint32_t)(((2 * f) * 64 + lane) * 16) : kOOB));
+        w.lo[cb][ks] = __builtin_bit_cast(bf16x8, bld16(rwd, ok ? (uint32_t)(((2 * f + 1) * 64 + lane) * 16) : kOOB));
+      }
+      const uint4 gv = bld16(rg, ok ? (uint32_t)((s * KT + 16 * cb + 4 * grp) * 4) : kOOB);
+      w.gm[cb] = make_float4(__builtin_bit_cast(float, gv.x), __builtin_bit_cast(float, gv.y),
+                             __builtin_bit_cast(float, gv.z), __builtin_bit_cast(float, gv.w));
+    }
+  };
+  float ssq[2] = {0.f, 0.f};
+  // z~ gamma for the stage's 64 columns and the wave's 32 rows, into the A tile
+  auto rebuild = [&](const Wd& w, __bf16* a) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w.hi[cb][ks], bfr[rb][ks], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w.lo[cb][ks], bfr[rb][ks], acc, 0, 0, 0);
+        }
+        // lane (row16, grp): z~[row][16 cb + 4 grp + v]
+        const float gv[4] = {w.gm[cb].x, w.gm[cb].y, w.gm[cb].z, w.gm[cb].w};
+        bf16x4 h;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          ssq[rb] = fmaf(acc[v], acc[v], ssq[rb]);
+          h[v] = (__bf16)(acc[v] * gv[v]);
+        }
+        const int row = 32 * wave + 16 * rb + row16;
+        *reinterpret_cast<uint2*>(a + tile_pos<true, BM>(row, 16 * cb + 4 * grp)) = __builtin_bit_cast(uint2, h);
+      }
+  };
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto products_kk = [&](const __bf16* ta, const __bf16* tb, int kk) {
+    bf16x8 fa[FM], fb[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[i] = frag<true, BM>(ta, (wm * FM + i) * 16, kk, row16, grp);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[j] = frag<false, BN>(tb, (wn * FN + j) * 16, kk, row16, grp);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+  };
+
+  Wd wd;
+  load_wd(wd, 0);
+  // stage 0: its A tile and the B tile
+  rebuild(wd, s_a0);
+  load_wd(wd, 1);
+  dma_tile<false, BN, NW>(rw, g.N, n0, g.N, 0, g.n, s_b0, wave, lane);
+  auto step = [&](int s, const __bf16* a, const __bf16* b, __bf16* na, __bf16* nb) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (s + 1 < nst) {
+      dma_tile<false, BN, NW>(rw, g.N, n0, g.N, (s + 1) * KT, g.n, nb, wave, lane);
+      rebuild(wd, na);
+      load_wd(wd, s + 2);
+    }
+    products_kk(a, b, 0);
+    products_kk(a, b, 1);
+  };
+  for (int s = 0; s < nst; s += 2) {
+    step(s, s_a0, s_b0, s_a1, s_b1);
+    if (s + 1 < nst) step(s + 1, s_a1, s_b1, s_a0, s_b0);
+  }
+
+  // row sums of squares: the four lane groups of a row, then one writer per row
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    float v = ssq[rb];
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (grp == 0) s_ssq[32 * wave + 16 * rb + row16] = v;
+  }
+  __syncthreads();
+
+  const rsrc_t ro = make_rsrc(g.out, g.out_bytes);
+  const float inv_n = 1.0f / (float)g.n;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int ml = (wm * FM + i) * 16 + row16;
+    const int m = m0 + ml;
+    const float sc = 1.0f / sqrtf(s_ssq[ml] * inv_n + g.eps);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + (wn * FN + j) * 16 + 4 * grp;
+      const bool ok = m < g.T && n < g.N;
+      bf16x4 h;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) h[e] = (__bf16)(acc[i][j][e] * sc);
+      bst8(ro, ok ? (uint32_t)(((int64_t)m * g.ld_out + n) * 2) : kOOB, __builtin_bit_cast(uint2, h));
+    }
+  }
+}
+
 // out[i] = sum over s in order of part[s][i], i < count (count % 4 == 0).
 __global__ __launch_bounds__(256) void k_splitk_sum(const float* __restrict__ part, int S, int64_t count,
                                                     float* __restrict__ out) {
@@ -923,6 +1117,50 @@ int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int3
   const int64_t cnt = T * (r / 4);
   hipLaunchKernelGGL(k_enc_finish, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, T, r, (n + 255) / 256, act,
                      (const float*)ws, (const __bf16*)x_attn, ld_x, (__bf16*)b, a_save);
+  return resbm_host::launch_status();
+}
+
+size_t resbm_decode_qkv_workspace_bytes(int32_t n, int32_t r) {
+  if (n < 64 || n > 65536 || n % 64 || r < 8 || r > 64 || r % 8) return 0;
+  return round_up((size_t)((r + 31) / 32) * (n / 16) * 2048, kWsAlign2);
+}
+
+int32_t resbm_decode_qkv_fwd(int64_t T, int32_t n, int32_t r, int32_t N, const void* b, const float* W_d,
+                             const float* gamma, const void* W_qkv, float eps, void* out, int64_t ld_out, void* ws,
+                             size_t ws_bytes, void* stream) {
+  if (T < 0 || T > (1ll << 31) - 256 || n < 64 || n > 65536 || n % 64 || r < 8 || r > 64 || r % 8 || N < 8 ||
+      N > 262144 || N % 8 || !(eps >= 0.0f))
+    return RESBM_E_SHAPE;
+  if (T == 0) return RESBM_OK;
+  const size_t need = resbm_decode_qkv_workspace_bytes(n, r);
+  int32_t e = check_ws(need, ws, ws_bytes);
+  if (e) return e;
+  if (!b || !W_d || !gamma || !W_qkv || !out) return RESBM_E_NULL;
+  if (!ld_ok(ld_out, N)) return RESBM_E_SHAPE;
+  if (!aligned(b, 16) || !aligned(W_d, 16) || !aligned(gamma, 16) || !aligned(W_qkv, 16) || !aligned(out, 16))
+    return RESBM_E_ALIGN;
+  const size_t bb = (size_t)T * r * 2, bwd = (size_t)r * n * 4, bg = (size_t)n * 4, bw = (size_t)n * N * 2,
+               bo = extent(T, N, ld_out, 2);
+  if (!fits(bw) || !fits(bo) || !fits(bb)) return RESBM_E_SHAPE;
+  const void* ins[] = {b, W_d, gamma, W_qkv};
+  const size_t inb[] = {bb, bwd, bg, bw};
+  for (int i = 0; i < 4; ++i)
+    if (overlap(out, bo, ins[i], inb[i]) || overlap(ws, need, ins[i], inb[i])) return RESBM_E_ALIAS;
+  if (overlap(out, bo, ws, need)) return RESBM_E_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  const int KS = (r + 31) / 32;
+  hipLaunchKernelGGL(k_dq_wd_prep, dim3((unsigned)(KS * (n / 16))), dim3(64), 0, st, W_d, r, n, KS, (__bf16*)ws);
+  DqArgs g{};
+  g.T = (int)T; g.n = n; g.N = N; g.r = r;
+  g.b = (const __bf16*)b; g.wdf = (const __bf16*)ws; g.gamma = gamma;
+  g.W = (const __bf16*)W_qkv; g.w_bytes = (int64_t)bw;
+  g.out = (__bf16*)out; g.ld_out = ld_out; g.out_bytes = (int64_t)bo;
+  g.eps = eps;
+  const unsigned tiles = (unsigned)(((T + 255) / 256) * ((N + 255) / 256));
+  if (KS == 1)
+    hipLaunchKernelGGL(k_dec_qkv<1>, dim3(tiles), dim3(512), 0, st, g);
+  else
+    hipLaunchKernelGGL(k_dec_qkv<2>, dim3(tiles), dim3(512), 0, st, g);
   return resbm_host::launch_status();
 }
 

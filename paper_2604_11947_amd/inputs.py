@@ -252,6 +252,12 @@ def make_two_weights(n: int, m: int, r: int, seed: int = 0) -> dict[str, torch.T
     }
 
 
+def make_gain(n: int, seed: int) -> torch.Tensor:
+    """A normalisation gain: n float32 values 1 + 0.1 N(0, 1) from their own seed."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, n, 5])))
+    return torch.from_numpy((1.0 + 0.1 * rng.standard_normal(n)).astype(np.float32))
+
+
 def make_bf16(rows: int, cols: int, seed: int, std: float = 1.0) -> torch.Tensor:
     """rows x cols bf16 N(0, std^2) from its own seed (payloads, saved
     pre-activations, wire gradients of the two-linears-per-side ops)."""

@@ -57,6 +57,8 @@ SIGNATURES = [
     ("resbm_ffn_encode_fwd", _i32, [_i64, _i32, _i32, _i32, _i32, _p, _i64, _p, _p, _i64, _p, _p, _i64, _p, _p, _p,
                                     _sz, _p]),
     ("resbm_ffn_encode_workspace_bytes", _sz, [_i64, _i32, _i32]),
+    ("resbm_decode_qkv_fwd", _i32, [_i64, _i32, _i32, _i32, _p, _p, _p, _p, ctypes.c_float, _p, _i64, _p, _sz, _p]),
+    ("resbm_decode_qkv_workspace_bytes", _sz, [_i32, _i32]),
     ("resbm_io_dtype", _i32, []),
     ("resbm_strerror", ctypes.c_char_p, [_i32]),
 ]
@@ -370,6 +372,27 @@ class Library:
                                             _ptr(W_e), _ptr(z), ld_z, _ptr(b), _ptr(a_save), _ptr(ws), ws.numel(),
                                             _stream(stream, h))
         self._check("resbm_ffn_encode_fwd", st)
+
+    def decode_qkv_fwd(self, b, W_d, gamma, W_qkv, out, eps=1e-5, ws=None, stream=None):
+        T, r = b.shape
+        n, N = W_qkv.shape
+        for t, nm in ((b, "b"), (W_qkv, "W_qkv"), (out, "out")):
+            _dtype(t, torch.bfloat16, nm)
+        _dtype(W_d, torch.float32, "W_d")
+        _dtype(gamma, torch.float32, "gamma")
+        _packed(b, T, r, "b")
+        _packed(W_d, r, n, "W_d")
+        _packed(W_qkv, n, N, "W_qkv")
+        if gamma.dim() != 1 or gamma.numel() != n or not gamma.is_contiguous():
+            raise ValueError("gamma: expected a contiguous vector of n elements")
+        ld_out = _ld(out, T, N, "out")
+        if ws is None:
+            nbytes = int(self.cdll.resbm_decode_qkv_workspace_bytes(n, r))
+            buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=b.device)
+            ws = buf[(-buf.data_ptr()) % 256:][:nbytes]
+        st = self.cdll.resbm_decode_qkv_fwd(T, n, r, N, _ptr(b), _ptr(W_d), _ptr(gamma), _ptr(W_qkv), eps, _ptr(out),
+                                            ld_out, _ptr(ws), ws.numel(), _stream(stream, b))
+        self._check("resbm_decode_qkv_fwd", st)
 
     # ------------------------------------------------------------ optimizer-side ops
     def newton_schulz(self, G, O, steps=5, coeffs=NS_QUINTIC, ws=None, stream=None):

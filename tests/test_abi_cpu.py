@@ -38,7 +38,7 @@ def test_header_declares_the_ops_and_helpers():
                "resbm_newton_schulz", "resbm_muon_update", "resbm_spectrum", "resbm_matrix_workspace_bytes",
                "resbm_workspace_bytes", "resbm_io_dtype", "resbm_strerror", "resbm2_encode_fwd", "resbm2_decode_fwd",
                "resbm2_decode_bwd", "resbm2_encode_bwd", "resbm2_workspace_bytes", "resbm_ffn_encode_fwd",
-               "resbm_ffn_encode_workspace_bytes"):
+               "resbm_ffn_encode_workspace_bytes", "resbm_decode_qkv_fwd", "resbm_decode_qkv_workspace_bytes"):
         assert op in names
     assert sorted(n for n, _, _ in R.SIGNATURES) == names
 
@@ -436,3 +436,39 @@ def test_ffn_encode_validation(lib):
     assert call(13, 6 * A + 8) == R.E_ALIGN
     assert call(11, 2 * A) == R.E_ALIAS       # z over W_down
     assert call(13, A) == R.E_ALIAS           # b over h
+
+
+def test_decode_qkv_validation(lib):
+    """Host-side checks of the decoder fused into RMSNorm + QKV (no GPU needed:
+    every rejected call returns before any HIP call)."""
+    import ctypes
+    c = lib.cdll
+    n, r, NQ, TT = 256, 32, 384, 300
+    ws = c.resbm_decode_qkv_workspace_bytes(n, r)
+    assert ws >= (n // 16) * 2048 and ws % 256 == 0
+    assert c.resbm_decode_qkv_workspace_bytes(n, 12) == 0      # r % 8
+    assert c.resbm_decode_qkv_workspace_bytes(n, 72) == 0      # r > 64
+    assert c.resbm_decode_qkv_workspace_bytes(200, r) == 0     # n % 64
+    ok = [TT, n, r, NQ, A, 2 * A, 3 * A, 4 * A, ctypes.c_float(1e-5), 5 * A, NQ, 6 * A, ws, None]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return c.resbm_decode_qkv_fwd(*a)
+
+    assert call(0, 0) == R.OK
+    assert call(1, 200) == R.E_SHAPE        # n % 64
+    assert call(2, 12) == R.E_SHAPE         # r % 8
+    assert call(2, 128) == R.E_SHAPE        # r > 64
+    assert call(3, 100) == R.E_SHAPE        # N % 8
+    assert call(8, ctypes.c_float(-1.0)) == R.E_SHAPE
+    assert call(8, ctypes.c_float(float("nan"))) == R.E_SHAPE
+    assert call(10, NQ - 8) == R.E_SHAPE    # ld_out < N
+    for i in (4, 5, 6, 7, 9):
+        assert call(i, None) == R.E_NULL, i
+    assert call(11, None) == R.E_NULL
+    assert call(12, ws - 256) == R.E_WORKSPACE
+    assert call(11, 6 * A + 64) == R.E_ALIGN
+    assert call(9, 5 * A + 8) == R.E_ALIGN
+    assert call(9, 4 * A) == R.E_ALIAS      # out over W_qkv
+    assert call(11, A) == R.E_ALIAS         # workspace over b

@@ -1,8 +1,13 @@
-"""Encoder fused into the FFN output projection (resbm_ffn_encode_fwd) against
-the float64 oracle: z = h W_down, then the encoder on the stored (bf16) z.
+"""Boundary ops fused into their neighbours, against the float64 oracle:
+- the encoder fused into the FFN output projection (resbm_ffn_encode_fwd):
+  z = h W_down, then the encoder on the stored (bf16) z;
+- the decoder fused into the next block's RMS normalisation and QKV projection
+  (resbm_decode_qkv_fwd): out = RMSNorm(b W_d) W_qkv.
 
-Bounds as for the one-linear encoder: max error <= 2e-2 RMS(ref) after a
-half-ulp discount for the bf16 outputs z and b; a_save (float32) raw.
+Bounds as for the one-linear ops: max error <= 2e-2 RMS(ref) after a half-ulp
+discount for bf16 outputs; a_save (float32) raw.  The fused decoder rounds
+z~ gamma to bf16 before the projection (relative 2^-9 per element, averaging
+out over the n-deep contraction).
 """
 import numpy as np
 import pytest
@@ -87,3 +92,65 @@ def test_ffn_encode_full_size_sampled():
     check("z", z[rows], rz, True)
     check("a", a[rows], ra, False)
     check("b", b[rows], rb, True)
+
+
+# ---- decoder into RMSNorm + QKV
+DQ_SHAPES = [(333, 256, 32, 384), (1000, 1024, 32, 520), (64, 64, 8, 64), (1, 256, 16, 256), (513, 512, 64, 264),
+             (300, 4096, 32, 1032)]
+DQ_IDS = [f"T{T}_n{n}_r{r}_N{N}" for T, n, r, N in DQ_SHAPES]
+EPS = 1e-5
+
+
+def dq_data(T, n, r, N, seed=0):
+    return {"b": I.make_bf16(T, r, seed + 41), "W_d": I.make_weights(n, r, seed)["W_d"],
+            "gamma": I.make_gain(n, seed + 42), "W_qkv": I.make_bf16(n, N, seed + 43, std=n ** -0.5)}
+
+
+def dq_ref(d, rows=None):
+    b = d["b"] if rows is None else d["b"][rows]
+    return F.decode_qkv_fwd(f64(b), d["W_d"].double().numpy(), d["gamma"].double().numpy(), f64(d["W_qkv"]), EPS)[2]
+
+
+@pytest.mark.parametrize("T,n,r,N", DQ_SHAPES, ids=DQ_IDS)
+def test_decode_qkv_fwd(T, n, r, N):
+    L = lib()
+    say(f"decode_qkv_fwd T={T} n={n} r={r} N={N}")
+    d = dq_data(T, n, r, N)
+    obuf = torch.full((T, N + 8), float("nan"), dtype=torch.bfloat16, device="cuda")
+    out = obuf[:, :N]
+    L.decode_qkv_fwd(d["b"].cuda(), d["W_d"].cuda(), d["gamma"].cuda(), d["W_qkv"].cuda(), out, eps=EPS)
+    torch.cuda.synchronize()
+    assert bool(torch.isnan(obuf[:, N:].float()).all()), "row padding of out overwritten"
+    check("out", out, dq_ref(d), True)
+
+
+def test_decode_qkv_zero_payload_and_determinism():
+    """A zero payload gives a zero output (the eps keeps the scale finite);
+    repeated calls are bit-identical."""
+    L = lib()
+    T, n, r, N = 700, 512, 32, 512
+    d = dq_data(T, n, r, N, seed=5)
+    d["b"][100:200] = 0
+    outs = []
+    for _ in range(2):
+        out = torch.empty((T, N), dtype=torch.bfloat16, device="cuda")
+        L.decode_qkv_fwd(d["b"].cuda(), d["W_d"].cuda(), d["gamma"].cuda(), d["W_qkv"].cuda(), out, eps=EPS)
+        torch.cuda.synchronize()
+        outs.append(out.view(torch.int16).clone())
+    assert torch.equal(outs[0], outs[1])
+    assert not bool(outs[0][100:200].any())
+
+
+def test_decode_qkv_full_size_sampled():
+    """T = 16384, n = 4096, r = 32, N = 6144 (Q 4096 + K 1024 + V 1024 of an
+    8B-class block with grouped KV heads) on sampled rows."""
+    L = lib()
+    T, n, r, N = 16384, 4096, 32, 6144
+    say(f"decode_qkv_fwd full size T={T} n={n} r={r} N={N}")
+    d = dq_data(T, n, r, N, seed=6)
+    out = torch.empty((T, N), dtype=torch.bfloat16, device="cuda")
+    L.decode_qkv_fwd(d["b"].cuda(), d["W_d"].cuda(), d["gamma"].cuda(), d["W_qkv"].cuda(), out, eps=EPS)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(10)
+    rows = np.unique(np.concatenate([[0, 255, 256, T - 1], rng.choice(T, 24, replace=False)]))
+    check("out", out[rows], dq_ref(d, rows), True)
