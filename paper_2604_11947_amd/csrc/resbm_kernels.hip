@@ -2108,7 +2108,7 @@ void launch_dec_fwd(const Plan& p, int add_id, const io_t* b, const float* W_d, 
   const bool r8 = expand_r8(p.r);
 #define CALL_DF(ADD, R8)                                                                                           \
   do {                                                                                                             \
-    if constexpr (KS >= 3)                                                                                         \
+    if constexpr (KS >= kExpandWideKS)                                                                            \
       hipLaunchKernelGGL((k_expand_wide<KS, CT, ADD, false, R8>), grid, dim3(256), 0, st, p.T, p.n, p.r, b, b, b, \
                          W_d, zt, ld, p.df_tpg, (int)grid.y, none);                                                \
     else                                                                                                           \
@@ -2175,7 +2175,7 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
   if constexpr (NT < kWideNT) ggrid.y += (unsigned)ceil_div(fin.nb_all, (int64_t)ggrid.x);
 #define CALL_GZ(ADD, R8)                                                                                         \
   do {                                                                                                           \
-    if constexpr (NT >= kWideNT)                                                                                 \
+    if constexpr (NT >= kWideNT || KS >= kExpandWideKS)                                                          \
       hipLaunchKernelGGL((k_expand_wide<KS, GCT, ADD, true, R8>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, \
                          gh_lo, g_b, W_e, g_z, ld_gz, p.df_tpg, main_y, fin);                                   \
     else                                                                                                         \

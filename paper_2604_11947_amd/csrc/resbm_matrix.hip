@@ -529,9 +529,12 @@ bool small_ok(int s4, int n, double a) {
 // after one without a rotation (at most kMaxSweeps).
 // sigma[k] = sqrt(max(lambda, 0)) in descending order; r_eff = sum lambda^+ /
 // max lambda (0 for the zero matrix).
-__global__ __launch_bounds__(kThreads) void k_mx_eig(int s, int s4, const double* A, double* sigma,
-                                                     double* r_eff) {
-  const int nt = blockDim.x;  // 64 (one wave: its barriers cost almost nothing) or 256
+#ifndef RESBM_EIG_THREADS_SMALL
+#define RESBM_EIG_THREADS_SMALL 64
+#endif
+__global__ __launch_bounds__(1024) void k_mx_eig(int s, int s4, const double* A, double* sigma,
+                                                 double* r_eff) {
+  const int nt = blockDim.x;
   __shared__ double M[kMaxShortSpectrum * (kMaxShortSpectrum + 1)];
   __shared__ double s_c[kMaxShortSpectrum / 2 + 1], s_s[kMaxShortSpectrum / 2 + 1];
   __shared__ int s_p[kMaxShortSpectrum / 2 + 1], s_q[kMaxShortSpectrum / 2 + 1];
@@ -881,7 +884,8 @@ int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, doub
   double* A = (double*)(wsc + P.off_a);
   hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), dim3(kThreads), 0, st, ne, d.nch,
                      (const double*)g.part, A);
-  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(d.s <= 64 ? 64 : kThreads), 0, st, d.s, d.s4, (const double*)A, sigma,
+  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(d.s <= 64 ? RESBM_EIG_THREADS_SMALL : kThreads), 0, st, d.s, d.s4,
+                     (const double*)A, sigma,
                      r_eff);
   return launch_status();
 }

@@ -100,6 +100,11 @@ constexpr int eb_tw(int KS) { return KS <= 4 ? RESBM_EB_TW : 1; }
 // switch to the row / token contraction kernels and the expand kernel with
 // block-shared inputs.
 constexpr int kWideNT = 5;
+// the expand kernel with block-shared input rows from this many 32-deep k-steps of r
+#ifndef RESBM_EXPAND_WIDE_KS
+#define RESBM_EXPAND_WIDE_KS 3
+#endif
+constexpr int kExpandWideKS = RESBM_EXPAND_WIDE_KS;
 constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four waves split r)
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
