@@ -7,10 +7,11 @@ copies of the inputs and outputs so that no step finds its streams in the
 256 MB Infinity Cache left behind by the previous one; the library's scratch
 workspace is one buffer shared by all steps, as a caller would keep it.
 
-The step is timed twice: captured in a HIP graph per input copy and replayed
-(the reported value; a graph removes the host's launch gaps between the ops),
-and launched eagerly with HIP events between the ops (per-op times, the
-roofline entry of the dominant op).  Prints one JSON line, with the CPU oracle
+The step is timed twice: captured in HIP graphs of several consecutive steps
+(input copies in turn) and replayed (the reported value; a graph removes the
+host's launch gaps between the ops, as the enclosing training step's graph
+would), and launched eagerly with HIP events between the ops (per-op times,
+the roofline entry of the dominant op).  Prints one JSON line, with the CPU oracle
 timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -57,6 +58,8 @@ def parse():
                    help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
     p.add_argument("--cpu-tokens", type=int, default=None, help="tokens in the CPU oracle sample")
     p.add_argument("--no-graph", action="store_true", help="report the eager launches instead of graph replays")
+    p.add_argument("--graph-steps", type=int, default=8,
+                   help="consecutive steps captured in one HIP graph (input copies in turn)")
     p.add_argument("--no-optimizer", action="store_true",
                    help="skip timing the optimizer-side ops (Muon update, spectrum) on the bottleneck weights")
     p.add_argument("--two-m", type=int, default=1024,
@@ -651,12 +654,13 @@ def decode_qkv_timing(lib, d: dict, r: int, N: int, dev, iters: int, cpu: bool) 
     return res
 
 
-def sweep_timing(lib, dev, names, steps: int, warmup: int, act: int) -> dict:
+def sweep_timing(lib, dev, names, steps: int, warmup: int, act: int, G: int = 1) -> dict:
     """The whole step (four ops, graph replay) at each workload in `names`: the
     compression-ratio sweep at n = 4096 and the 70B-class boundary.  Inputs are
     drawn on the device (torch, seeded) with each workload's shape and
     distribution; kernel time does not depend on the values.  Two rotating input
-    sets.  Reports per-step median time, algorithmic HBM GB/s, and matrix-core
+    sets; G consecutive steps per graph replay (steps and warmup are multiples
+    of G).  Reports per-step median time (per replay, divided by G), algorithmic HBM GB/s, and matrix-core
     rates: algorithmic (12 T n r flops per step) and issued (24 T n r: the hi and
     lo bf16 products of the float32 weights and of g_h)."""
     import torch
@@ -700,21 +704,21 @@ def sweep_timing(lib, dev, names, steps: int, warmup: int, act: int) -> dict:
         for s_ in sets:
             step(s_)
         torch.cuda.synchronize()
-        graphs = []
-        for s_ in sets:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                step(s_)
-            graphs.append(g)
-        for i in range(warmup):
-            graphs[i % 2].replay()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        G = max(1, G)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(G):
+                step(sets[i % 2])
+        for i in range(max(1, warmup // G)):
+            g.replay()
+        nrep = max(1, steps // G)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(nrep + 1)]
         ev[0].record()
-        for i in range(steps):
-            graphs[i % 2].replay()
+        for i in range(nrep):
+            g.replay()
             ev[i + 1].record()
         torch.cuda.synchronize()
-        st = np.asarray([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]) * 1e3
+        st = np.asarray([ev[i].elapsed_time(ev[i + 1]) / G for i in range(nrep)]) * 1e3
         med = float(np.median(st))
         nbytes = sum(op_bytes(T, n, r).values())
         alg = 12.0 * T * n * r
@@ -724,10 +728,11 @@ def sweep_timing(lib, dev, names, steps: int, warmup: int, act: int) -> dict:
                      "hbm_frac": nbytes / (med * 1e-6) / 1e9 / HBM_PEAK_GBS,
                      "tflops_alg": alg / (med * 1e-6) / 1e12, "tflops_issued": 2 * alg / (med * 1e-6) / 1e12,
                      "mfma_frac_issued": 2 * alg / (med * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS}
-        del graphs, sets, ws
+        del g, sets, ws
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-    return {"workloads": out, "steps": steps, "warmup": warmup, "timing": "hip graph replay, per-step events",
+    return {"workloads": out, "steps": max(1, steps // G) * G, "warmup": max(1, warmup // G) * G,
+            "timing": f"hip graph replay, {G} steps per graph, events between replays",
             "inputs": "drawn on the device (torch, seeded), each workload's shape and distribution"}
 
 
@@ -827,39 +832,57 @@ def main():
         copy_gbs = 2 * nel * 2 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
         del src, dst
 
-    # One HIP graph per input copy, captured first; the compression-ratio sweep
-    # then keeps the GPU busy for a few seconds, and the headline replays follow
-    # it directly, so that they run at the clocks a busy GPU holds (after an
-    # idle spell the first ~100 steps of this load ran up to ~8 % slower).
+    # HIP graphs captured first: one of G consecutive steps (input copies in
+    # turn) and one single step per input copy (for warmup and a remainder of K
+    # modulo G).  A training step runs these ops inside a larger captured graph;
+    # replaying one step per graph would add the ~9 us launch of each replay to
+    # every step.  The compression-ratio sweep then keeps the GPU busy for a few
+    # seconds, and the headline replays follow it directly, so that they run at
+    # the clocks a busy GPU holds (after an idle spell the first ~100 steps of
+    # this load ran up to ~8 % slower).
     for s in sets:
         step(s)
     torch.cuda.synchronize()
-    graphs = []
+    G = max(1, args.graph_steps)
+    g_multi, g_single = None, []
     if not args.no_graph:
         for s in sets:
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
                 step(s)
-            graphs.append(g)
-    sweep = None if args.no_sweep else sweep_timing(lib, dev, SWEEP, 50, 20, act)
+            g_single.append(g)
+        if G > 1:
+            g_multi = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_multi):
+                for i in range(G):
+                    step(sets[i % len(sets)])
+    sweep = None if args.no_sweep else sweep_timing(lib, dev, SWEEP, 48, 24, act, G)
 
     ms_graph = None
-    if graphs:
-        for i in range(args.warmup):
-            graphs[i % len(graphs)].replay()
-        # one event between consecutive replays: per-step times, and the first and
-        # last bracket exactly the K timed steps
-        gev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    if g_single:
+        def replays(k):
+            # (graph, steps) covering exactly k steps
+            full = k // G if g_multi is not None else 0
+            return [(g_multi, G)] * full + [(g_single[i % len(sets)], 1) for i in range(k - full * G)]
+        for g, _ in replays(args.warmup):
+            g.replay()
+        plan = replays(args.steps)
+        # one event between consecutive replays: per-step times (averaged over
+        # the G steps of a multi-step replay), and the first and last bracket
+        # exactly the K timed steps
+        gev = [torch.cuda.Event(enable_timing=True) for _ in range(len(plan) + 1)]
         torch.cuda.synchronize()
         wall0 = time.perf_counter()
         gev[0].record()
-        for i in range(args.steps):
-            graphs[i % len(graphs)].replay()
+        for i, (g, _) in enumerate(plan):
+            g.replay()
             gev[i + 1].record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
         ms_graph = gev[0].elapsed_time(gev[-1]) / args.steps
-        step_ms = [gev[i].elapsed_time(gev[i + 1]) for i in range(args.steps)]
+        per = [(gev[i].elapsed_time(gev[i + 1]) / k, k) for i, (_, k) in enumerate(plan)]
+        multi = [t for t, k in per if k == G]
+        step_ms = multi if multi else [t for t, _ in per]
 
     # eager launches, HIP events between the ops (on the stream the ops run on):
     # per-op times, and the headline itself with --no-graph
@@ -877,7 +900,7 @@ def main():
     torch.cuda.synchronize()
     wall_e = time.perf_counter() - wall_e
     ms_eager = start.elapsed_time(stop) / args.steps
-    if not graphs:
+    if not g_single:
         wall = wall_e
         step_ms = [sum(e[k].elapsed_time(e[k + 1]) for k in range(4)) for e in events] if not args.no_op_events \
             else []
@@ -907,7 +930,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
-        "timing": "hip graph replay" if ms_graph is not None else "eager launches",
+        "timing": (f"hip graph replay, {G} steps per graph" if ms_graph is not None else "eager launches"),
         "step_time_stats": step_stats,
         "ms_per_step_eager": ms_eager,
         "higher_is_better": True,

@@ -332,7 +332,8 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
  * Activations are bf16 in both libraries.  Shape rules: d_ff, n, r multiples
  * of 8, 8 <= r <= n <= 65536, d_ff <= 262144.  ws: at least
  * resbm_ffn_encode_workspace_bytes(T, n, r) bytes (float32 partial sums of a,
- * one T x r slab per 256 columns of z, added in a fixed order).
+ * one T x r slab per 256 columns of z, added in a fixed order, then the hi and
+ * lo bf16 parts of W_e in matrix-core fragment order).
  */
 size_t resbm_ffn_encode_workspace_bytes(int64_t T, int32_t n, int32_t r);
 int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int32_t act,

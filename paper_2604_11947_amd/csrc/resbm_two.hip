@@ -234,13 +234,38 @@ __device__ __forceinline__ int xcd_tile(int id, int nb) {
   return x * (nb >> 3) + min(x, nb & 7) + li;
 }
 
+// Fragment-ordered hi/lo bf16 copy of a row-major float32 matrix W (rows x
+// cols, row stride ld) for the B slot of a contraction over its rows: fragment
+// f = ks * nc + cb, lane (row16, grp) holds W[32 ks + 8 grp + e][16 cb + row16]
+// (zeros outside the matrix); per fragment 1 KiB of hi parts, then 1 KiB of lo
+// parts.  One block of 64 lanes per fragment.
+__global__ __launch_bounds__(64) void k_frag_prep(const float* __restrict__ W, int rows, int cols, int64_t ld, int nc,
+                                                  __bf16* __restrict__ out) {
+  const int l = threadIdx.x, row16 = l & 15, grp = l >> 4;
+  const int f = blockIdx.x;
+  const int ks = f / nc, cb = f % nc;
+  const int c = 16 * cb + row16;
+  bf16x8 hi, lo;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int j = 32 * ks + 8 * grp + e;
+    const float w = (j < rows && c < cols) ? W[(int64_t)j * ld + c] : 0.0f;
+    __bf16 h, q;
+    resbm::split_hi_lo(w, h, q);
+    hi[e] = h;
+    lo[e] = q;
+  }
+  reinterpret_cast<bf16x8*>(out)[(int64_t)(2 * f) * 64 + l] = hi;
+  reinterpret_cast<bf16x8*>(out)[(int64_t)(2 * f + 1) * 64 + l] = lo;
+}
+
 // Encoder contraction in the epilogue of the FFN output projection (z = h W_down,
 // Sec. 3.2 places the encoder right after the feed-forward layer): the block's
 // rounded 256 x 256 tile of z goes to LDS (its four stage buffers, 64 rows
 // each), and wave w multiplies rows 32 w .. 32 w + 31 of it by the tile's 256
-// rows of W_e (float32, hi + lo bf16 parts), writing the float32 partial sum
-// D[tile column][row][0 .. r).  The partials are added in tile order by
-// k_enc_finish.
+// rows of W_e (float32, as hi + lo bf16 fragments prepared by k_frag_prep, in
+// X), writing the float32 partial sum D[tile column][row][0 .. r).  The
+// partials are added in tile order by k_enc_finish.
 template <int BM, int BN, int WM, int WN, int FM, int FN>
 __device__ __forceinline__ void encode_epilogue(const GemmArgs& g, const f32x4 (&acc)[FM][FN], __bf16* q0,
                                                 __bf16* q1, __bf16* q2, __bf16* q3, int m0, int n0) {
@@ -264,8 +289,8 @@ __device__ __forceinline__ void encode_epilogue(const GemmArgs& g, const f32x4 (
     }
   }
   __syncthreads();
-  const float* We = static_cast<const float*>(g.X);
-  const int r = g.x_cols, nt = n0 / BN;
+  const rsrc_t rw = make_rsrc(g.X, g.x_bytes);
+  const int r = g.x_cols, nt = n0 / BN, nc = (r + 63) / 64 * 4;
   const __bf16* zq = quarter(wave >> 1);
   const rsrc_t rd = make_rsrc(g.D, g.d_bytes);
   for (int jg = 0; jg < r; jg += 64) {
@@ -276,30 +301,25 @@ __device__ __forceinline__ void encode_epilogue(const GemmArgs& g, const f32x4 (
       for (int jb = 0; jb < 4; ++jb) a2[ib][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 2
     for (int ks = 0; ks < 8; ++ks) {
-      bf16x8 zf[2];
+      bf16x8 zf[2], hi[4], lo[4];
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const uint32_t off = (uint32_t)((((n0 >> 5) + ks) * nc + (jg >> 4) + jb) * 2048 + lane * 16);
+        hi[jb] = __builtin_bit_cast(bf16x8, bld16(rw, off));
+        lo[jb] = __builtin_bit_cast(bf16x8, bld16(rw, off + 1024));
+      }
 #pragma unroll
       for (int ib = 0; ib < 2; ++ib) {
         const int row = 32 * (wave & 1) + 16 * ib + row16, col = 32 * ks + 8 * grp;
         zf[ib] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(zq + row * 256 + resbm::wide_col(row, col)));
       }
 #pragma unroll
-      for (int jb = 0; jb < 4; ++jb) {
-        const int jj = jg + 16 * jb + row16, k = n0 + 32 * ks + 8 * grp;
-        bf16x8 hi, lo;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float w = (jj < r && k + e < g.N) ? We[(int64_t)(k + e) * r + jj] : 0.0f;
-          __bf16 wh, wl;
-          resbm::split_hi_lo(w, wh, wl);
-          hi[e] = wh;
-          lo[e] = wl;
-        }
+      for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
         for (int ib = 0; ib < 2; ++ib) {
-          a2[ib][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, zf[ib], a2[ib][jb], 0, 0, 0);
-          a2[ib][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, zf[ib], a2[ib][jb], 0, 0, 0);
+          a2[ib][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo[jb], zf[ib], a2[ib][jb], 0, 0, 0);
+          a2[ib][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi[jb], zf[ib], a2[ib][jb], 0, 0, 0);
         }
-      }
     }
     // lane (row16, grp) of (ib, jb) holds D[row][jg + 16 jb + 4 grp .. + 3] of tile row 32 w + 16 ib + row16
 #pragma unroll
@@ -462,34 +482,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------- decoder into RMSNorm + QKV
-// Fragment-ordered hi/lo bf16 copy of W_d (r x n, float32) for the B slot of
-// the decoder contraction z~ = b W_d: fragment f = ks * (n / 16) + cb, lane
-// (row16, grp) holds W_d[32 ks + 8 grp + e][16 cb + row16] (zeros at rows >= r);
-// per fragment 1 KiB of hi parts, then 1 KiB of lo parts.
-__global__ __launch_bounds__(64) void k_dq_wd_prep(const float* __restrict__ W_d, int r, int n, int KS,
-                                                   __bf16* __restrict__ wdf) {
-  const int l = threadIdx.x, row16 = l & 15, grp = l >> 4;
-  const int f = blockIdx.x, nc = n / 16;
-  const int ks = f / nc, cb = f % nc;
-  bf16x8 hi, lo;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int j = 32 * ks + 8 * grp + e;
-    const float w = j < r ? W_d[(int64_t)j * n + 16 * cb + row16] : 0.0f;
-    __bf16 h, q;
-    resbm::split_hi_lo(w, h, q);
-    hi[e] = h;
-    lo[e] = q;
-  }
-  (void)KS;
-  reinterpret_cast<bf16x8*>(wdf)[(int64_t)(2 * f) * 64 + l] = hi;
-  reinterpret_cast<bf16x8*>(wdf)[(int64_t)(2 * f + 1) * 64 + l] = lo;
-}
-
 struct DqArgs {
   int T, n, N, r;
   const __bf16* b;       // T x r
-  const __bf16* wdf;     // W_d fragments (k_dq_wd_prep)
+  const __bf16* wdf;     // W_d fragments (k_frag_prep)
   const float* gamma;    // n
   const __bf16* W;       // n x N, row-major
   int64_t w_bytes;
@@ -1073,9 +1069,17 @@ int32_t resbm2_encode_bwd(int64_t T, int32_t n, int32_t m, int32_t r, int32_t ac
   return resbm_host::launch_status();
 }
 
+// Workspace of the fused encoder: the float32 partial sums (one T x r slice per
+// 256 columns of z), then the W_e fragments (k_frag_prep: 256-row tiles, r
+// rounded up to 64 columns).
+static size_t ffn_part_bytes(int64_t T, int n, int r) {
+  return round_up((size_t)((n + 255) / 256) * (size_t)T * r * 4, kWsAlign2);
+}
+static size_t ffn_frag_count(int n, int r) { return (size_t)((n + 255) / 256 * 8) * (size_t)((r + 63) / 64 * 4); }
+
 size_t resbm_ffn_encode_workspace_bytes(int64_t T, int32_t n, int32_t r) {
   if (T <= 0 || n < 8 || n > 65536 || n % 8 || r < 8 || r > n || r % 8) return 0;
-  return round_up((size_t)((n + 255) / 256) * (size_t)T * r * 4, kWsAlign2);
+  return ffn_part_bytes(T, n, r) + round_up(ffn_frag_count(n, r) * 2048, kWsAlign2);
 }
 
 int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int32_t act, const void* h, int64_t ld_h,
@@ -1109,10 +1113,14 @@ int32_t resbm_ffn_encode_fwd(int64_t T, int32_t d_ff, int32_t n, int32_t r, int3
       if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return RESBM_E_ALIAS;
   }
   hipStream_t st = (hipStream_t)stream;
-  // z = h W_down with the encoder partials in the epilogue
+  // W_e fragments, then z = h W_down with the encoder partials in the epilogue
+  const size_t pb = ffn_part_bytes(T, n, r), nf = ffn_frag_count(n, r);
+  char* wf = (char*)ws + pb;
+  hipLaunchKernelGGL(k_frag_prep, dim3((unsigned)nf), dim3(64), 0, st, W_e, n, r, (int64_t)r, (r + 63) / 64 * 4,
+                     (__bf16*)wf);
   GemmArgs g = args((int)T, n, d_ff, h, ld_h, bh, W_down, n, bwd, z, ld_z, bz);
-  g.X = W_e; g.x_cols = r; g.x_bytes = (int64_t)bwe;
-  g.D = ws; g.d_bytes = (int64_t)need;
+  g.X = wf; g.x_cols = r; g.x_bytes = (int64_t)(nf * 2048);
+  g.D = ws; g.d_bytes = (int64_t)pb;
   launch<true, false, 256, 256, 2, 4, kEpiEncode, false>(g, 1, st);
   const int64_t cnt = T * (r / 4);
   hipLaunchKernelGGL(k_enc_finish, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, T, r, (n + 255) / 256, act,
@@ -1149,7 +1157,8 @@ int32_t resbm_decode_qkv_fwd(int64_t T, int32_t n, int32_t r, int32_t N, const v
   if (overlap(out, bo, ws, need)) return RESBM_E_ALIAS;
   hipStream_t st = (hipStream_t)stream;
   const int KS = (r + 31) / 32;
-  hipLaunchKernelGGL(k_dq_wd_prep, dim3((unsigned)(KS * (n / 16))), dim3(64), 0, st, W_d, r, n, KS, (__bf16*)ws);
+  hipLaunchKernelGGL(k_frag_prep, dim3((unsigned)(KS * (n / 16))), dim3(64), 0, st, W_d, r, n, (int64_t)n, n / 16,
+                     (__bf16*)ws);
   DqArgs g{};
   g.T = (int)T; g.n = n; g.N = N; g.r = r;
   g.b = (const __bf16*)b; g.wdf = (const __bf16*)ws; g.gamma = gamma;
