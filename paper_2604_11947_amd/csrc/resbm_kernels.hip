@@ -1437,28 +1437,38 @@ __global__ __launch_bounds__(64) void k_wd_prep(const float* __restrict__ W_d, i
 
 // Row contraction for wide r: C[t][j] = sum_c X[t][c] M(c, j) over the n
 // columns of a streamed T x n matrix X, M given as split fragments (W_e for
-// encode_fwd, W_d^T for the g_b of decode_bwd).  A block owns 64 tokens; it
-// stages 64 x 256 tiles of X cooperatively in LDS (512-byte row segments) and
-// wave w contracts them against the fragments of j-tiles [w NTW, w NTW + NTW),
-// so every wave ends with whole sums of its columns and the block reads each
-// weight fragment once per 64 tokens.  The weight fragments run three k-steps
-// ahead of their use in a ring of four.
+// encode_fwd, W_d^T for the g_b of decode_bwd).  A block of NWV waves owns
+// TOK = 64 RH tokens and one of RH groups of j-tiles; it stages TOK x 256 tiles
+// of X cooperatively in LDS (512-byte row segments) and wave w contracts them
+// against the fragments of j-tiles [w NTW, w NTW + NTW) of its group, so every
+// wave ends with whole sums of its columns and the block reads each weight
+// fragment of its group once per TOK tokens.  With RH = 2 the two blocks of a
+// token group are 8 apart in a run of 16 (same XCD, dispatched together), so
+// their shared X rows come from HBM once.  The weight fragments run three
+// k-steps ahead of their use in a ring of four.
 //   GB = false: a_save = a, b = x_attn[:, :r] + phi(a)        (encode_fwd)
 //   GB = true:  g_b = C + g_id[:, :r] (g_id may be NULL)        (decode_bwd)
-template <int NT, int NTW, bool GB>
-__global__ __launch_bounds__(256) void k_rowc_wide(int64_t T, int n, int r, int act, const io_t* __restrict__ X,
-                                                   int64_t ld_x, const void* __restrict__ wf,
-                                                   const io_t* __restrict__ skip, int64_t ld_s,
-                                                   io_t* __restrict__ out, float* __restrict__ a_save) {
-  constexpr int TOK = 64, MT = 4, BC = 256, KSS = BC / 32;
+template <int NT, int NTW, bool GB, int NWV, int RH>
+__global__ __launch_bounds__(64 * NWV) void k_rowc_wide(int64_t T, int n, int r, int act, const io_t* __restrict__ X,
+                                                        int64_t ld_x, const void* __restrict__ wf,
+                                                        const io_t* __restrict__ skip, int64_t ld_s,
+                                                        io_t* __restrict__ out, float* __restrict__ a_save) {
+  constexpr int TOK = 64 * RH, MT = TOK / 16, BC = 256, KSS = BC / 32;
+  constexpr int NTG = (NT + RH - 1) / RH;     // j-tiles of a group
   constexpr int LPR = BC / 8;                 // lanes per tile row
-  constexpr int NQ = TOK * LPR / 256;         // cooperative loads per lane and stage
+  constexpr int NQ = TOK * LPR / (64 * NWV);  // cooperative loads per lane and stage
+  static_assert(NWV * NTW >= NTG, "the waves must cover the j-tiles of a group");
   constexpr int ZB = RESBM_IO_F32_BUILD ? 1 : 2;
   constexpr int TILE = TOK * BC * (int)sizeof(io_t);
   __shared__ __attribute__((aligned(16))) char smem[ZB * TILE];
 
   const int l = lane_id(), row16 = l & 15, grp = l >> 4, wave = wave_id();
-  const int64_t tok0 = (int64_t)blockIdx.x * TOK;
+  const int bid = (int)blockIdx.x;
+  const int tg = RH == 1 ? bid : (bid >> 4) * 8 + (bid & 7);  // token group
+  const int jg0 = RH == 1 ? 0 : ((bid >> 3) & 1) * NTG;       // first j-tile of the group
+  const int jg1 = min(NT, jg0 + NTG);
+  const int64_t tok0 = (int64_t)tg * TOK;
+  if (tok0 >= T) return;  // the last run of 16 can hold token groups past T (whole block)
   const int nks = n / 32;
   const int nst = (n + BC - 1) / BC;
   const rsrc_t zr = make_rsrc(X + tok0 * ld_x, rows_bytes(min((int64_t)TOK, T - tok0), n, ld_x, kEs));
@@ -1468,8 +1478,8 @@ __global__ __launch_bounds__(256) void k_rowc_wide(int64_t T, int n, int r, int 
 #pragma unroll
   for (int q = 0; q < NQ; ++q) zrow[q] = (wave * NQ * 64 + q * 64 + l) / LPR;
 
-  // stages start rotated per group of 8 blocks (one per XCD), as in k_enc_fwd
-  const int srot = (int)((blockIdx.x / 8u) % (unsigned)nst);
+  // stages start rotated per group of 8 token groups (one per XCD), as in k_enc_fwd
+  const int srot = (int)((unsigned)(tg / 8) % (unsigned)nst);
   auto stage_col = [&](int i) {
     if (i < 0 || i >= nst) return n;
     const int ir = i + srot < nst ? i + srot : i + srot - nst;
@@ -1486,8 +1496,8 @@ __global__ __launch_bounds__(256) void k_rowc_wide(int64_t T, int n, int r, int 
     const int kg = (stage_col(i) >> 5) + ks;
 #pragma unroll
     for (int jt = 0; jt < NTW; ++jt) {
-      const int jtg = wave * NTW + jt;
-      dst[jt] = bld_sfrag(wr, (int64_t)kg * NT + jtg, l, kg < nks && jtg < NT);
+      const int jtg = jg0 + wave * NTW + jt;
+      dst[jt] = bld_sfrag(wr, (int64_t)kg * NT + jtg, l, kg < nks && jtg < jg1);
     }
   };
 
@@ -1530,7 +1540,7 @@ __global__ __launch_bounds__(256) void k_rowc_wide(int64_t T, int n, int r, int 
         f[mt].v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
 #endif
       }
-      // waves whose last j-tiles lie past NT multiply zero fragments (never stored)
+      // waves whose last j-tiles lie past the group multiply zero fragments (never stored)
 #pragma unroll
       for (int jt = 0; jt < NTW; ++jt)
 #pragma unroll
@@ -1548,15 +1558,15 @@ __global__ __launch_bounds__(256) void k_rowc_wide(int64_t T, int n, int r, int 
     body(zb, i + 1);
   }
 
-  // acc[mt][jt][v] = C[tok0 + 16 mt + row16][16 (w NTW + jt) + 4 grp + v]
+  // acc[mt][jt][v] = C[tok0 + 16 mt + row16][16 (jg0 + w NTW + jt) + 4 grp + v]
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int jt = 0; jt < NTW; ++jt) {
-      const int jtg = wave * NTW + jt;
+      const int jtg = jg0 + wave * NTW + jt;
       const int64_t t = tok0 + 16 * mt + row16;
       const int j0 = 16 * jtg + 4 * grp;
-      if (jtg >= NT || t >= T || j0 >= r) continue;
+      if (jtg >= jg1 || t >= T || j0 >= r) continue;
       float a[4] = {acc[mt][jt][0], acc[mt][jt][1], acc[mt][jt][2], acc[mt][jt][3]};
       if constexpr (GB) {
         if (skip) {
@@ -2080,7 +2090,8 @@ template <int NT>
 void launch_enc_fwd(const Plan& p, int act, const io_t* x, int64_t ld_x, const io_t* z, int64_t ld_z,
                     const void* wf, io_t* b, float* a_save, hipStream_t st) {
   if constexpr (NT >= kWideNT) {
-    hipLaunchKernelGGL((k_rowc_wide<NT, tw_ntw(NT), false>), dim3(p.rw_nblk), dim3(256), 0, st, p.T, p.n, p.r, act,
+    hipLaunchKernelGGL((k_rowc_wide<NT, rw_ntw(NT), false, rw_waves(NT), rw_rh(NT)>), dim3(p.rw_nblk),
+                       dim3(64 * rw_waves(NT)), 0, st, p.T, p.n, p.r, act,
                        z, ld_z, wf, x, ld_x, b, a_save);
   } else {
     constexpr int MT = ef_mt(NT);
@@ -2413,7 +2424,8 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r, const void* b, const f
 #define CALL(NTV)                                                                                                   \
   do {                                                                                                              \
     if constexpr (NTV >= kWideNT) {                                                                                 \
-      hipLaunchKernelGGL((k_rowc_wide<NTV, tw_ntw(NTV), true>), dim3(p.rw_nblk), dim3(256), 0, s, T, n, r, 0, G,   \
+      hipLaunchKernelGGL((k_rowc_wide<NTV, rw_ntw(NTV), true, rw_waves(NTV), rw_rh(NTV)>), dim3(p.rw_nblk),    \
+                         dim3(64 * rw_waves(NTV)), 0, s, T, n, r, 0, G,                                         \
                          ld_gzt, (const void*)wf, (const io_t*)g_id, ld_gid, (io_t*)g_b, (float*)nullptr);         \
       if (r8)                                                                                                       \
         hipLaunchKernelGGL((k_tokc_wide<NTV, tw_ntw(NTV), true, true>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, s,  \

@@ -106,6 +106,25 @@ constexpr int kWideNT = 5;
 #endif
 constexpr int kExpandWideKS = RESBM_EXPAND_WIDE_KS;
 constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four waves split r)
+// Row contraction of the wide path (k_rowc_wide).  A block of rw_waves waves
+// owns rw_tok(NT) tokens and rw_rh(NT) of the r-column groups; each wave owns
+// rw_ntw j-tiles of its group.  Eight waves (two per SIMD; one block per CU
+// leaves a four-wave block one wave per SIMD, with nothing to cover its loads
+// and barriers): 330 / 524 us at r = 128 / 256 against 339 / 528 with four.
+// From RESBM_RW_SPLIT_NT j-tiles on, 128-token blocks split r in two halves:
+// each block then reads half of the weight fragments for twice the tokens.
+#ifndef RESBM_RW_WAVES8_NT
+#define RESBM_RW_WAVES8_NT 5
+#endif
+#ifndef RESBM_RW_SPLIT_NT
+#define RESBM_RW_SPLIT_NT 12
+#endif
+constexpr int rw_waves(int NT) { return NT >= RESBM_RW_WAVES8_NT ? 8 : 4; }
+constexpr int rw_rh(int NT) { return NT >= RESBM_RW_SPLIT_NT ? 2 : 1; }
+constexpr int rw_tok(int NT) { return 64 * rw_rh(NT); }
+constexpr int rw_ntw(int NT) {
+  return ((NT + rw_rh(NT) - 1) / rw_rh(NT) + rw_waves(NT) - 1) / rw_waves(NT);
+}
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
@@ -130,7 +149,7 @@ struct Plan {
   size_t eb_dwp_off, eb_gh_off, eb_ws;
 
   bool wide;                    // NT >= kWideNT
-  int rw_nblk;                  // row contraction: 64-token blocks
+  int rw_nblk;                  // row contraction: blocks (see rw_tok, rw_rh)
   int tw_ncb, tw_ntg, tw_TB;    // token contraction: 128-column blocks x token groups of tw_TB tokens
   size_t db_wf_off;             // decode_bwd (wide): W_d fragments
 
@@ -205,7 +224,10 @@ inline Plan make_plan(int64_t T, int n, int r) {
   // partials) + expand (g_z, with the ordered sums riding along)
   p.wide = p.NT >= kWideNT;
   if (p.wide) {
-    p.rw_nblk = (int)ceil_div(Tm, 64);
+    // 64-token blocks; or, with r split in two, 128-token blocks in runs of 16:
+    // the two halves of a token group 8 blocks apart, on one XCD
+    const int64_t rw_ntg = ceil_div(Tm, rw_tok(p.NT));
+    p.rw_nblk = (int)(rw_rh(p.NT) == 1 ? rw_ntg : 16 * ceil_div(rw_ntg, 8));
     p.tw_ncb = (int)ceil_div(n, 128);
     const int64_t nstep = ceil_div(Tm, 32);
     const int64_t g = clamp64(ceil_div((int64_t)kNumCU, p.tw_ncb), 1, nstep);
