@@ -2186,7 +2186,7 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
   if constexpr (NT < kWideNT) ggrid.y += (unsigned)ceil_div(fin.nb_all, (int64_t)ggrid.x);
 #define CALL_GZ(ADD, R8)                                                                                         \
   do {                                                                                                           \
-    if constexpr (NT >= kWideNT || KS >= kExpandWideKS)                                                          \
+    if constexpr (NT >= kWideNT || KS >= kExpandWideKSGZ)                                                        \
       hipLaunchKernelGGL((k_expand_wide<KS, GCT, ADD, true, R8>), ggrid, dim3(256), 0, st, p.T, p.n, p.r, gh_hi, \
                          gh_lo, g_b, W_e, g_z, ld_gz, p.df_tpg, main_y, fin);                                   \
     else                                                                                                         \

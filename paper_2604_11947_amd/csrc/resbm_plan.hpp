@@ -99,12 +99,23 @@ constexpr int eb_tw(int KS) { return KS <= 4 ? RESBM_EB_TW : 1; }
 // ---- wide rank: above r = 64 (more than four 16-column tiles of r) the ops
 // switch to the row / token contraction kernels and the expand kernel with
 // block-shared inputs.
-constexpr int kWideNT = 5;
+#ifndef RESBM_WIDE_NT
+#define RESBM_WIDE_NT 5
+#endif
+constexpr int kWideNT = RESBM_WIDE_NT;
 // the expand kernel with block-shared input rows from this many 32-deep k-steps of r
 #ifndef RESBM_EXPAND_WIDE_KS
 #define RESBM_EXPAND_WIDE_KS 3
 #endif
 constexpr int kExpandWideKS = RESBM_EXPAND_WIDE_KS;
+// encode_bwd's g_z pass (three products per k-step, split input) takes it from
+// this many k-steps: at r = 64 the g_z pass ran 157 -> 129 us (n = 8192, 32768
+// tokens) and 51 -> 42 us (n = 4096, 16384 tokens) on it, where decode_fwd's
+// pass (two products) ran slower (93 -> 123 us, 29 -> 37 us)
+#ifndef RESBM_EXPAND_WIDE_KS_GZ
+#define RESBM_EXPAND_WIDE_KS_GZ 2
+#endif
+constexpr int kExpandWideKSGZ = RESBM_EXPAND_WIDE_KS_GZ;
 constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four waves split r)
 // Row contraction of the wide path (k_rowc_wide).  A block of rw_waves waves
 // owns rw_tok(NT) tokens and rw_rh(NT) of the r-column groups; each wave owns
