@@ -10,8 +10,9 @@ workspace is one buffer shared by all steps, as a caller would keep it.
 The step is timed twice: captured in HIP graphs of several consecutive steps
 (input copies in turn) and replayed (the reported value; a graph removes the
 host's launch gaps between the ops, as the enclosing training step's graph
-would), and launched eagerly with HIP events between the ops (per-op times,
-the roofline entry of the dominant op).  Prints one JSON line, with the CPU oracle
+would), and launched eagerly with HIP events between the ops.  Each op is also
+timed alone from graph replays of several calls (per-op times, the roofline
+entry of the dominant op).  Prints one JSON line, with the CPU oracle
 timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -911,10 +912,38 @@ def main():
         step_stats = {"p10_ms": float(q[0]), "median_ms": float(q[1]), "p90_ms": float(q[2]),
                       "first_ms": float(step_ms[0]), "last_ms": float(step_ms[-1])}
 
-    op_ms = {}
+    op_ms_eager = {}
     for k, nm in enumerate(OPS):
-        op_ms[nm] = (float("nan") if args.no_op_events
-                     else sum(e[k].elapsed_time(e[k + 1]) for e in events) / args.steps)
+        op_ms_eager[nm] = (float("nan") if args.no_op_events
+                           else sum(e[k].elapsed_time(e[k + 1]) for e in events) / args.steps)
+    # per-op times without the host's launch gaps: each op alone, G calls per
+    # graph (input copies in turn), replays bracketed by events
+    op_ms = dict(op_ms_eager)
+    if g_single and not args.no_op_events:
+        op_fn = {
+            "encode_fwd": lambda s: lib.encode_fwd(s["x_attn"], s["z"], s["W_e"], s["b"], s["a"], act=act, ws=ws),
+            "decode_fwd": lambda s: lib.decode_fwd(s["b"], s["W_d"], s["zt"], ws=ws),
+            "decode_bwd": lambda s: lib.decode_bwd(s["b"], s["W_d"], s["g_zt"], s["g_id"], s["gb"], s["dWd"], ws=ws),
+            "encode_bwd": lambda s: lib.encode_bwd(s["z"], s["W_e"], s["a"], s["gb"], s["gz"], s["dWe"], act=act,
+                                                   ws=ws),
+        }
+        nrep = max(1, args.steps // G)
+        for nm in OPS:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(G):
+                    op_fn[nm](sets[i % len(sets)])
+            for _ in range(3):
+                g.replay()
+            o0, o1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            o0.record()
+            for _ in range(nrep):
+                g.replay()
+            o1.record()
+            torch.cuda.synchronize()
+            op_ms[nm] = o0.elapsed_time(o1) / (nrep * G)
+            del g
     ob = op_bytes(T, n, r)
     total_bytes = sum(ob.values())
     gbs = total_bytes / (ms_step * 1e-3) / 1e9
@@ -945,7 +974,10 @@ def main():
         "hbm_frac": gbs / HBM_PEAK_GBS,
         "bytes_per_step": total_bytes,
         "copy_probe_gbps": copy_gbs,
-        "ops": {k: {"ms": op_ms[k], "gbps": ob[k] / (op_ms[k] * 1e-3) / 1e9, "bytes": ob[k]} for k in OPS},
+        "ops": {k: {"ms": op_ms[k], "ms_eager": op_ms_eager[k], "gbps": ob[k] / (op_ms[k] * 1e-3) / 1e9,
+                    "bytes": ob[k]} for k in OPS},
+        "ops_timing": ("each op alone, HIP graph replays of G calls; ms_eager: events around eager calls"
+                       if g_single and not args.no_op_events else "events around eager calls"),
         "roofline": {"bound": "hbm", "op": dom, "achieved": dom_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dom_gbs / HBM_PEAK_GBS, "traffic": traffic},
         "wall_s_timed": wall,
