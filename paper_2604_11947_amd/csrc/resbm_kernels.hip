@@ -2074,6 +2074,10 @@ using resbm_host::overlap;
 // buffer descriptor (the kernels address a block's rows through one
 // descriptor with 32-bit byte offsets).
 bool window_ok(int64_t rows, int64_t ld) { return rows * ld * (int64_t)kIoBytes <= kMaxRange; }
+// rows of the streamed T x n matrix one block of the row contraction addresses
+// through one descriptor: k_rowc_wide's token group, or k_enc_fwd's 16 MT
+// tokens (decode_bwd's narrow kernel rebases per 32-token step)
+int64_t rowc_rows(const Plan& p, int64_t narrow) { return p.wide ? rw_tok(p.NT) : narrow; }
 
 int32_t check_common(int64_t T, int n, int r, int64_t ws_need, const void* ws, size_t ws_bytes) {
   if (T < 0 || !shape_ok(n, r)) return RESBM_E_SHAPE;
@@ -2334,7 +2338,7 @@ int32_t resbm_encode_fwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   int32_t st = check_common(T, n, r, (int64_t)p.ef_ws, ws, ws_bytes);
   if (st) return st;
   if (!x_attn || !z || !W_e || !b) return RESBM_E_NULL;
-  if (!ld_ok(ld_x, n) || !ld_ok(ld_z, n) || !window_ok(16 * p.ef_mt, ld_z)) return RESBM_E_SHAPE;
+  if (!ld_ok(ld_x, n) || !ld_ok(ld_z, n) || !window_ok(rowc_rows(p, 16 * p.ef_mt), ld_z)) return RESBM_E_SHAPE;
   if (!aligned(x_attn, 16) || !aligned(z, 16) || !aligned(W_e, 16) || !aligned(b, 16) ||
       (a_save && !aligned(a_save, 16)))
     return RESBM_E_ALIGN;
@@ -2398,7 +2402,8 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r, const void* b, const f
   int32_t st = check_common(T, n, r, (int64_t)p.db_ws, ws, ws_bytes);
   if (st) return st;
   if (!b || !W_d || !g_zt || !g_b || !dW_d) return RESBM_E_NULL;
-  if (!ld_ok(ld_gzt, n) || (g_id && !ld_ok(ld_gid, n)) || !window_ok(32, ld_gzt)) return RESBM_E_SHAPE;
+  if (!ld_ok(ld_gzt, n) || (g_id && !ld_ok(ld_gid, n)) || !window_ok(rowc_rows(p, 32), ld_gzt))
+    return RESBM_E_SHAPE;
   if (!aligned(b, 16) || !aligned(W_d, 16) || !aligned(g_zt, 16) || !aligned(g_b, 16) || !aligned(dW_d, 16) ||
       (g_id && !aligned(g_id, 16)))
     return RESBM_E_ALIGN;

@@ -223,6 +223,13 @@ def test_descriptor_window_limit(lib):
                               None) == R.E_SHAPE
     assert c.resbm_encode_bwd(t, n, r, 1, A, n, 2 * A, 3 * A, 4 * A, 5 * A, big, None, 0, 7 * A, 0, 8 * A, ws,
                               None) == R.E_SHAPE
+    # wide rank: the row contraction's token group (128 rows at r = 256) is the
+    # window; 2^24-element rows fit 16 or 32 rows in range but not 128
+    n, r, t, ld = 256, 256, 256, 1 << 24
+    ws = lib.workspace_bytes(t, n, r)
+    assert c.resbm_encode_fwd(t, n, r, 1, A, n, 2 * A, ld, 3 * A, 4 * A, 5 * A, 6 * A, ws, None) == R.E_SHAPE
+    assert c.resbm_decode_bwd(t, n, r, A, 2 * A, 3 * A, ld, None, 0, 5 * A, 6 * A, 0, 7 * A, ws,
+                              None) == R.E_SHAPE
 
 
 @needs_no_gpu
