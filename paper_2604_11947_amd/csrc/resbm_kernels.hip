@@ -356,11 +356,12 @@ template <int NT, int MT, int KW>
 __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, int act,
                                                      const io_t* __restrict__ x_attn, int64_t ld_x,
                                                      const io_t* __restrict__ z, int64_t ld_z,
-                                                     const void* __restrict__ wf, io_t* __restrict__ b,
-                                                     float* __restrict__ a_save) {
+                                                     const void* __restrict__ wf, const float* __restrict__ W_e,
+                                                     io_t* __restrict__ b, float* __restrict__ a_save) {
   constexpr int U = ef_u(NT);           // k-steps per wave and stage
   constexpr bool PW = NT <= 4;          // W_e fragments travel with the stage
   constexpr int NW = PW ? NT : 1;
+  constexpr bool WL = ef_we_lds(NT);    // W_e split in the kernel, through LDS (no fragments in wf)
   constexpr int TOK = 16 * MT;
   constexpr int RPT = 16 * NT;
   constexpr int SC = 32 * U;            // z columns per wave and stage
@@ -380,7 +381,17 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
 
   // rows at or beyond T fall outside the descriptor (ld >= n)
   const rsrc_t zr = make_rsrc(z + tok0 * ld_z, rows_bytes(min((int64_t)TOK, T - tok0), n, ld_z, kEs));
-  const rsrc_t wr = make_rsrc(wf, (int64_t)nks * NT * kSFragBytes);
+  const rsrc_t wr = make_rsrc(WL ? nullptr : wf, WL ? 0 : (int64_t)nks * NT * kSFragBytes);
+  // WL: wave w's rows [w SC, (w + 1) SC) of the stage's W_e slice, float32, 16
+  // bytes per lane and load (WLL lanes per row), split into hi / lo planes of
+  // its own LDS region [SC][RPT] (tile_col layout) and read back transposed.
+  // Stage i + 1's rows are split while stage i is multiplied (two plane
+  // buffers per wave), and loaded two stages before they are split.
+  constexpr int WLL = RPT / 4, WRPI = 64 / WLL, WQ = WL ? SC * RPT / 256 : 1;
+  constexpr int WPL = SC * RPT;  // elements of one plane
+  static_assert(!WL || (RPT % 4 == 0 && 64 % WLL == 0 && SC % WRPI == 0), "W_e rows must split over the lanes");
+  __shared__ __attribute__((aligned(16))) __bf16 s_w[WL ? KW * 4 * WPL : 8];
+  const rsrc_t we = make_rsrc(W_e, WL ? (int64_t)n * r * 4 : 0);
   // cooperative load q of this lane: tile row zrow[q], columns zc .. zc + 8 of the stage
   const int zc = 8 * (l % LPR);
   int zrow[NQ];
@@ -420,8 +431,64 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
     }
   };
 
-  // One stage; zz / ww are reloaded with the z rows / W_e fragments of stage i + 2.
-  auto body = [&](XFrag (&zz)[NQ], SFrag (&ww)[U][NW], int i) {
+  auto load_wq = [&](uint4 (&qq)[WQ], int i) {
+    if constexpr (WL) {
+      const int c0 = stage_col(i) + wave * SC;  // n (all zeros) outside the stages
+      const int col = 4 * (l % WLL);
+#pragma unroll
+      for (int q = 0; q < WQ; ++q) {
+        const int row = q * WRPI + l / WLL;
+        const bool ok = c0 + row < n && col < r;
+        qq[q] = bld16(we, ok ? (uint32_t)(((c0 + row) * r + col) * 4) : kOOB);
+      }
+    }
+  };
+  // fragment (u, nt) of this wave's planes: lane (row16, grp) gets rows
+  // 32 u + 8 grp + e of column 16 nt + row16 (two transposed 8-byte reads)
+  auto wl_frag = [&](const __bf16* plane, int u, int nt) {
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    s16x4 h[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int row = 32 * u + 8 * grp + 4 * q + (row16 >> 2);
+      const __bf16* pp = plane + row * RPT + tile_col<RPT>(row, 16 * nt + 4 * (row16 & 3));
+      h[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(pp));
+    }
+    return __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){h[0][0], h[0][1], h[0][2], h[0][3],
+                                                                                 h[1][0], h[1][1], h[1][2], h[1][3]});
+  };
+
+  // this wave's hi plane of stage i's buffer (the lo plane follows it)
+  auto wl_plane = [&](int i) { return s_w + (WL ? (wave * 4 + 2 * (i & 1)) * WPL : 0); };
+  // split the W_e rows in qq (stage i) into this wave's planes of stage i
+  auto wl_split = [&](const uint4 (&qq)[WQ], int i) {
+    __bf16* const ph = wl_plane(i);
+    __bf16* const pl = ph + WPL;
+    const int col = 4 * (l % WLL);
+#pragma unroll
+    for (int q = 0; q < WQ; ++q) {
+      const int row = q * WRPI + l / WLL;
+      const uint4 v = qq[q];
+      const float f4[4] = {__builtin_bit_cast(float, v.x), __builtin_bit_cast(float, v.y),
+                           __builtin_bit_cast(float, v.z), __builtin_bit_cast(float, v.w)};
+      bf16x4 h, lo;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        __bf16 a, c;
+        split_hi_lo(f4[e], a, c);
+        h[e] = a;
+        lo[e] = c;
+      }
+      const int pos = row * RPT + tile_col<RPT>(row, col);
+      *reinterpret_cast<uint2*>(ph + pos) = __builtin_bit_cast(uint2, h);
+      *reinterpret_cast<uint2*>(pl + pos) = __builtin_bit_cast(uint2, lo);
+    }
+  };
+
+  // One stage; zz / ww are reloaded with the z rows / W_e fragments of stage
+  // i + 2; WL: qn holds stage i + 1's W_e rows, split here and reloaded with
+  // stage i + 3's.
+  auto body = [&](XFrag (&zz)[NQ], SFrag (&ww)[U][NW], uint4 (&qn)[WQ], int i) {
     io_t* tile = reinterpret_cast<io_t*>(smem + (ZB == 2 ? (i & 1) : 0) * TILE);
     if constexpr (ZB == 1) __syncthreads();  // the previous stage's readers of the single tile are done
 #pragma unroll
@@ -437,6 +504,8 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
     load_z(zz, i + 2);
     __syncthreads();  // the stage's tile is complete; the other buffer's readers are done
     const int ks = (stage_col(i) + wave * SC) / 32;
+    const __bf16* const ph = wl_plane(i);  // written by this wave during stage i - 1
+    const __bf16* const pl = ph + WPL;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       XFrag f[MT];
@@ -454,13 +523,27 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         SFrag w;
-        if constexpr (PW) w = ww[u][nt];
-        else w = bld_sfrag(wr, (int64_t)(ks + u) * NT + nt, l, ks + u < nks);
+        if constexpr (WL) {
+#if !RESBM_IO_F32_BUILD
+          w.hi = wl_frag(ph, u, nt);
+          w.lo = wl_frag(pl, u, nt);
+#endif
+        } else if constexpr (PW) {
+          w = ww[u][nt];
+        } else {
+          w = bld_sfrag(wr, (int64_t)(ks + u) * NT + nt, l, ks + u < nks);
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, f[mt], acc[mt][nt]);
       }
     }
-    load_w(ww, i + 2);
+    if constexpr (WL) {
+      wl_split(qn, i + 1);
+      load_wq(qn, i + 3);
+      wave_lds_fence();  // stage i + 1's planes are written before this wave reads them
+    } else {
+      load_w(ww, i + 2);
+    }
   };
 
   // Every memory operation sits in one unconditional loop body (the loop starts
@@ -468,17 +551,24 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
   // which lets the compiler place each wait at its exact distance.
   XFrag za[NQ], zb[NQ];
   SFrag wa[U][NW], wb[U][NW];
+  uint4 qa[WQ], qb[WQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) za[q] = zb[q] = xfrag_zero();
-  if constexpr (PW) {
+#pragma unroll
+  for (int q = 0; q < WQ; ++q) qa[q] = qb[q] = make_uint4(0, 0, 0, 0);
+  if constexpr (PW && !WL) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) wa[u][nt] = wb[u][nt] = sfrag_zero();
   }
+  if constexpr (WL) {
+    wl_split(qa, -2);  // zeros: stage -2 multiplies its planes with a zero tile (no stale LDS bits)
+    load_wq(qa, 0);    // stage 0's rows, split during stage -1
+  }
   for (int i = opaque(-2); i < nst; i += 2) {
-    body(za, wa, i);
-    body(zb, wb, i + 1);
+    body(za, wa, qb, i);
+    body(zb, wb, qa, i + 1);
   }
   __syncthreads();  // the reduction area overlaps the tiles
   float (*s_red)[TOK][RPT + 4] = reinterpret_cast<float (*)[TOK][RPT + 4]>(smem);
@@ -2092,7 +2182,7 @@ int32_t check_common(int64_t T, int n, int r, int64_t ws_need, const void* ws, s
 
 template <int NT>
 void launch_enc_fwd(const Plan& p, int act, const io_t* x, int64_t ld_x, const io_t* z, int64_t ld_z,
-                    const void* wf, io_t* b, float* a_save, hipStream_t st) {
+                    const void* wf, const float* W_e, io_t* b, float* a_save, hipStream_t st) {
   if constexpr (NT >= kWideNT) {
     hipLaunchKernelGGL((k_rowc_wide<NT, rw_ntw(NT), false, rw_waves(NT), rw_rh(NT)>), dim3(p.rw_nblk),
                        dim3(64 * rw_waves(NT)), 0, st, p.T, p.n, p.r, act,
@@ -2101,7 +2191,7 @@ void launch_enc_fwd(const Plan& p, int act, const io_t* x, int64_t ld_x, const i
     constexpr int MT = ef_mt(NT);
     constexpr int KW = ef_kw(NT);
     hipLaunchKernelGGL((k_enc_fwd<NT, MT, KW>), dim3(p.ef_nblk), dim3(KW * 64), 0, st, p.T, p.n, p.r, act, x, ld_x,
-                       z, ld_z, wf, b, a_save);
+                       z, ld_z, wf, W_e, b, a_save);
   }
 }
 
@@ -2353,12 +2443,14 @@ int32_t resbm_encode_fwd(int64_t T, int32_t n, int32_t r, int32_t act, const voi
   hipStream_t s = (hipStream_t)stream;
   char* w = (char*)ws;
   void* wf = w + p.ef_wf_off;
-  const int64_t nprep = (int64_t)(n / 32) * p.NT * 64;
-  hipLaunchKernelGGL(k_enc_fwd_prep, dim3((unsigned)ceil_div(nprep, 64)), dim3(64), 0, s, W_e, n, r, p.NT, wf);
+  if (!ef_we_lds(p.NT)) {  // fragments for the kernels that read them prepared
+    const int64_t nprep = (int64_t)(n / 32) * p.NT * 64;
+    hipLaunchKernelGGL(k_enc_fwd_prep, dim3((unsigned)ceil_div(nprep, 64)), dim3(64), 0, s, W_e, n, r, p.NT, wf);
+  }
   const io_t* X = (const io_t*)x_attn;
   const io_t* Z = (const io_t*)z;
   io_t* B = (io_t*)b;
-#define CALL(NTV) launch_enc_fwd<NTV>(p, act, X, ld_x, Z, ld_z, wf, B, a_save, s)
+#define CALL(NTV) launch_enc_fwd<NTV>(p, act, X, ld_x, Z, ld_z, wf, W_e, B, a_save, s)
   RESBM_DISPATCH_NT(p.NT, CALL)
 #undef CALL
   return launch_status();

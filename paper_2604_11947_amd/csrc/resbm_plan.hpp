@@ -46,6 +46,17 @@ constexpr int ef_mt(int NT) { return NT <= 2 ? RESBM_EF_MT_SMALL_R : (NT <= 4 ? 
 // k-steps of 32 columns per wave and stage: two up to r = 64, so that a stage
 // row is 512 bytes (at r = 64: 51 -> 41 us with the 64-token blocks)
 constexpr int ef_u(int NT) { return NT <= 4 ? 2 : 1; }
+// encode_fwd up to RESBM_EF_WE_LDS j-tiles of r (bf16 build): each wave splits
+// its own rows of W_e into hi / lo bf16 planes in LDS and reads the fragments
+// back transposed, instead of reading fragments that a prologue kernel
+// prepared (that kernel costs a fixed ~4.5 us per call, whatever its size).
+// Every block repeats the split, on one wave per SIMD: at r = 16 the kernel
+// runs 25.7 us against 24.3 + 4.5 (prologue); at r = 32 31.6 against
+// 26.7 + 4.4, so r = 32 keeps the prologue.
+#ifndef RESBM_EF_WE_LDS
+#define RESBM_EF_WE_LDS 1
+#endif
+constexpr bool ef_we_lds(int NT) { return !RESBM_IO_F32_BUILD && NT <= RESBM_EF_WE_LDS; }
 #ifndef RESBM_EF_KW
 #define RESBM_EF_KW 4
 #endif
