@@ -129,8 +129,9 @@ constexpr int kExpandWideKS = RESBM_EXPAND_WIDE_KS;
 constexpr int kExpandWideKSGZ = RESBM_EXPAND_WIDE_KS_GZ;
 constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four waves split r)
 // Row contraction of the wide path (k_rowc_wide).  A block of rw_waves waves
-// owns rw_tok(NT) tokens and rw_rh(NT) of the r-column groups; each wave owns
-// rw_ntw j-tiles of its group.  Eight waves (two per SIMD; one block per CU
+// owns rw_tok(NT) tokens and one of rw_rh(NT) groups of j-tiles; each wave owns
+// rw_ntw j-tiles of its group.  Eight waves from RESBM_RW_WAVES8_NT j-tiles per
+// group on (two per SIMD; one block per CU
 // leaves a four-wave block one wave per SIMD, with nothing to cover its loads
 // and barriers): 330 / 524 us at r = 128 / 256 against 339 / 528 with four.
 // From RESBM_RW_SPLIT_NT j-tiles on, 128-token blocks split r in two halves:
@@ -141,8 +142,8 @@ constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four
 #ifndef RESBM_RW_SPLIT_NT
 #define RESBM_RW_SPLIT_NT 12
 #endif
-constexpr int rw_waves(int NT) { return NT >= RESBM_RW_WAVES8_NT ? 8 : 4; }
 constexpr int rw_rh(int NT) { return NT >= RESBM_RW_SPLIT_NT ? 2 : 1; }
+constexpr int rw_waves(int NT) { return (NT + rw_rh(NT) - 1) / rw_rh(NT) >= RESBM_RW_WAVES8_NT ? 8 : 4; }
 constexpr int rw_tok(int NT) { return 64 * rw_rh(NT); }
 constexpr int rw_ntw(int NT) {
   return ((NT + rw_rh(NT) - 1) / rw_rh(NT) + rw_waves(NT) - 1) / rw_waves(NT);
