@@ -937,6 +937,19 @@ __global__ __launch_bounds__(256) void k_dec_bwd_fin(int64_t T, int n, int r, in
 // (the padding moves consecutive rows to different banks).
 constexpr int plane_pitch(int KP) { return (KP % 128 == 0 || KP == 32 || KP == 64) ? KP : KP + 8; }
 
+// LDS of one block (gfx950: 160 KiB per compute unit).
+constexpr int kLdsBytes = 160 * 1024;
+// k_tokc_wide: pitch of its staged r-wide planes, and the tokens per step
+// (32 TSM) it takes: 64 where two buffers of the 64-token tiles fit in LDS.
+constexpr int tw_ypitch(int NT) {
+  return RESBM_IO_F32_BUILD ? 32 * ((NT + 1) / 2) + 8 : plane_pitch(32 * ((NT + 1) / 2));
+}
+constexpr int tw_tsm(int NT, bool DWD) {
+  const int planes = (!DWD && !RESBM_IO_F32_BUILD) ? 2 : 1;
+  const int bytes2 = 2 * (64 * 128 + planes * 64 * tw_ypitch(NT)) * (int)sizeof(io_t);
+  return (RESBM_TW_TSM >= 2 && bytes2 <= kLdsBytes) ? 2 : 1;
+}
+
 // Split g_h tile of TS tokens x RPS columns: bf16 build: hi and lo planes in
 // the lds_col<RPS> layout; f32 build: one float plane, row-major.
 template <int TS, int RPS>
@@ -1715,15 +1728,15 @@ __global__ __launch_bounds__(256) void k_gh(int64_t T, int r, int silu, const io
 
 // Transposed fragment of a [rows][PITCH] plane of the I/O type (bf16 build:
 // lds_col<PITCH> layout; f32 build: row-major): lane (row16, grp) receives
-// plane[8 grp + e][c0 + row16], e = 0..7.
+// plane[row0 + 8 grp + e][c0 + row16], e = 0..7 (row0 % 16 == 0).
 template <int PITCH>
-__device__ __forceinline__ XFrag tr_rows(const io_t* plane, int c0, int row16, int grp) {
+__device__ __forceinline__ XFrag tr_rows(const io_t* plane, int row0, int c0, int row16, int grp) {
   XFrag f;
 #if RESBM_IO_F32_BUILD
 #pragma unroll
-  for (int e = 0; e < 8; ++e) f.v[e] = plane[(8 * grp + e) * PITCH + c0 + row16];
+  for (int e = 0; e < 8; ++e) f.v[e] = plane[(row0 + 8 * grp + e) * PITCH + c0 + row16];
 #else
-  f.v = tr_plane<PITCH>(plane, 0, c0, row16, grp);
+  f.v = tr_plane<PITCH>(plane, row0, c0, row16, grp);
 #endif
   return f;
 }
@@ -1734,21 +1747,25 @@ __device__ __forceinline__ XFrag tr_rows(const io_t* plane, int c0, int row16, i
 //                             (split: hi and lo planes; one float plane in the fp32 build)
 //   DWD = true  (decode_bwd): dwp[tg][j][c] = sum_t Y[t][j] X[t][c], Y = b (exact)
 // 8 waves: wave (cw, jq) owns columns [64 cw, 64 cw + 64) of the block and
-// j-tiles [jq NTW, jq NTW + NTW).  Per 32-token step the block stages the
-// 32 x 128 tile of X and the 32 x r tile(s) of Y in LDS (double buffered, the
-// next step's loads two steps ahead in registers); both operands are read
-// back transposed (the contraction runs over the tile's rows).
-template <int NT, int NTW, bool DWD, bool R8>
+// j-tiles [jq NTW, jq NTW + NTW).  Per step of TS = 32 TSM tokens the block
+// stages the TS x 128 tile of X and the TS x r tile(s) of Y in LDS (double
+// buffered, the next steps' loads in registers: X 128 tokens ahead, Y two
+// steps); both operands are read back transposed (the contraction runs over
+// the tile's rows, 32 at a time).  TSM = 2 halves the barriers per token where
+// the buffers fit in LDS.
+template <int NT, int NTW, bool DWD, bool R8, int TSM>
 __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int RP, const io_t* __restrict__ X,
                                                    int64_t ld_x, const io_t* __restrict__ Y,
                                                    const io_t* __restrict__ Y_lo, float* __restrict__ dwp, int TB) {
-  constexpr int BCc = 128, TS = 32, KS = (NT + 1) / 2, KP = 32 * KS;
-  constexpr int YP = RESBM_IO_F32_BUILD ? KP + 8 : plane_pitch(KP);  // Y plane pitch (lds_col<YP> layout)
+  constexpr int BCc = 128, TS = 32 * TSM, KS = (NT + 1) / 2, KP = 32 * KS;
+  constexpr int YP = tw_ypitch(NT);  // Y plane pitch (lds_col<YP> layout)
   constexpr bool SPLIT = !DWD && !RESBM_IO_F32_BUILD;
   constexpr int PL = SPLIT ? 2 : 1;
   constexpr int XE = TS * BCc, YE = TS * YP;  // elements of the X tile and of one Y plane
   constexpr int YC = TS * (KP / 8);           // 8-element chunks of one Y plane
   constexpr int NYQ = (PL * YC + 511) / 512;  // Y chunk loads per thread and step
+  constexpr int XA = 4 / TSM;                 // steps of X loads in flight
+  static_assert(2 * (XE + PL * YE) * (int)sizeof(io_t) <= kLdsBytes, "tiles exceed LDS");
   __shared__ __attribute__((aligned(16))) io_t s_x[2][XE];
   __shared__ __attribute__((aligned(16))) io_t s_y[2][PL][YE];
 
@@ -1759,7 +1776,7 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
   const int bcv = min(BCc, n - bc0);          // valid columns of the block (a multiple of 64)
   const int64_t t_begin = (int64_t)tg * TB;
   const int64_t t_end = min(T, t_begin + TB);
-  // X loads: thread tid takes row tid / 16, columns 8 (tid % 16) .. + 8
+  // X loads: thread tid takes rows tid / 16 + 32 q, columns 8 (tid % 16) .. + 8
   const int xrow = tid >> 4, xc = 8 * (tid & 15);
 
   f32x4 acc[4][NTW];
@@ -1768,6 +1785,9 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
 #pragma unroll
     for (int jt = 0; jt < NTW; ++jt) acc[ct][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  struct XRegs {
+    XFrag x[TSM];
+  };
   struct YRegs {
     XFrag y[NYQ];
   };
@@ -1775,11 +1795,13 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
     t0 = t_begin + s * TS;
     return s < 0 ? (int64_t)0 : min((int64_t)TS, t_end - t0);
   };
-  auto load_x = [&](XFrag& x, int64_t s) {
+  auto load_x = [&](XRegs& x, int64_t s) {
     int64_t t0;
     const int64_t rows = rows_of(s, t0);
     const rsrc_t xr_ = make_rsrc(X + t0 * ld_x + bc0, bcv > 0 ? rows_bytes(rows, bcv, ld_x, kEs) : 0);
-    x = bld_x8(xr_, xc < bcv ? (uint32_t)((xrow * ld_x + xc) * kEs) : kOOB);
+#pragma unroll
+    for (int q = 0; q < TSM; ++q)
+      x.x[q] = bld_x8(xr_, xc < bcv ? (uint32_t)(((xrow + 32 * q) * ld_x + xc) * kEs) : kOOB);
   };
   auto load_y = [&](YRegs& g, int64_t s) {
     int64_t t0;
@@ -1795,14 +1817,17 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
       g.y[i] = bld_r8<R8>(pl ? yl_ : yr_, ok ? (uint32_t)(yrow * r * kEs) : kOOB, r, c8);
     }
   };
-  auto put = [&](const XFrag& x, const YRegs& g, int buf) {
-    io_t* dx = &s_x[buf][xrow * BCc + wide_col(xrow, xc)];
+  auto put = [&](const XRegs& x, const YRegs& g, int buf) {
+#pragma unroll
+    for (int q = 0; q < TSM; ++q) {
+      io_t* dx = &s_x[buf][(xrow + 32 * q) * BCc + wide_col(xrow + 32 * q, xc)];
 #if RESBM_IO_F32_BUILD
 #pragma unroll
-    for (int e = 0; e < 8; ++e) dx[e] = x.v[e];
+      for (int e = 0; e < 8; ++e) dx[e] = x.x[q].v[e];
 #else
-    *reinterpret_cast<uint4*>(dx) = __builtin_bit_cast(uint4, x.v);
+      *reinterpret_cast<uint4*>(dx) = __builtin_bit_cast(uint4, x.x[q].v);
 #endif
+    }
 #pragma unroll
     for (int i = 0; i < NYQ; ++i) {
       const int qq = tid + 512 * i;
@@ -1820,59 +1845,62 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
     }
   };
   auto compute = [&](int buf) {
-    XFrag xf[4];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) xf[ct] = tr_frag_wide<BCc>(s_x[buf], 0, 64 * cw + 16 * ct, row16, grp);
+    for (int ks = 0; ks < TSM; ++ks) {  // 32 tokens of the step at a time
+      XFrag xf[4];
 #pragma unroll
-    for (int jt = 0; jt < NTW; ++jt) {
-      const int jtg = jq * NTW + jt;
-      if constexpr (NT % 4 != 0) {
-        if (jtg >= NT) continue;  // wave-uniform; the tile's columns end at 32 KS
-      }
-      if constexpr (DWD) {
-        const XFrag yb = tr_rows<YP>(s_y[buf][0], 16 * jtg, row16, grp);
+      for (int ct = 0; ct < 4; ++ct) xf[ct] = tr_frag_wide<BCc>(s_x[buf], 32 * ks, 64 * cw + 16 * ct, row16, grp);
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_xx(xf[ct], yb, acc[ct][jt]);
-      } else {
-        SFrag g;
+      for (int jt = 0; jt < NTW; ++jt) {
+        const int jtg = jq * NTW + jt;
+        if constexpr (NT % 4 != 0) {
+          if (jtg >= NT) continue;  // wave-uniform; the tile's columns end at 32 KS
+        }
+        if constexpr (DWD) {
+          const XFrag yb = tr_rows<YP>(s_y[buf][0], 32 * ks, 16 * jtg, row16, grp);
+#pragma unroll
+          for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_xx(xf[ct], yb, acc[ct][jt]);
+        } else {
+          SFrag g;
 #if RESBM_IO_F32_BUILD
-        const XFrag y = tr_rows<YP>(s_y[buf][0], 16 * jtg, row16, grp);
+          const XFrag y = tr_rows<YP>(s_y[buf][0], 32 * ks, 16 * jtg, row16, grp);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) g.v[e] = y.v[e];
+          for (int e = 0; e < 8; ++e) g.v[e] = y.v[e];
 #else
-        g.hi = tr_rows<YP>(s_y[buf][0], 16 * jtg, row16, grp).v;
-        g.lo = tr_rows<YP>(s_y[buf][PL - 1], 16 * jtg, row16, grp).v;
+          g.hi = tr_rows<YP>(s_y[buf][0], 32 * ks, 16 * jtg, row16, grp).v;
+          g.lo = tr_rows<YP>(s_y[buf][PL - 1], 32 * ks, 16 * jtg, row16, grp).v;
 #endif
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_sx(g, xf[ct], acc[ct][jt]);
+          for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_sx(g, xf[ct], acc[ct][jt]);
+        }
       }
     }
   };
 
-  // The X tiles (HBM) run four steps ahead of their use, the Y tiles (L2) two.
+  // The X tiles (HBM) run XA steps ahead of their use, the Y tiles (L2) two.
   // Steps before 0 or past the range load zeros (the LDS buffers are fully
   // written with them before they are read) and skip the products.
   const int64_t nsb = (t_end - t_begin + TS - 1) / TS;
-  XFrag xr[4];
+  XRegs xr[XA];
   YRegs yr[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) xr[i] = xfrag_zero();
+  for (int i = 0; i < XA; ++i)
+#pragma unroll
+    for (int q = 0; q < TSM; ++q) xr[i].x[q] = xfrag_zero();
 #pragma unroll
   for (int h = 0; h < 2; ++h)
 #pragma unroll
     for (int i = 0; i < NYQ; ++i) yr[h].y[i] = xfrag_zero();
-  auto body = [&](int64_t s, XFrag& xs, YRegs& ys) {
+  auto body = [&](int64_t s, XRegs& xs, YRegs& ys) {
     put(xs, ys, (int)(s & 1));
-    load_x(xs, s + 4);
+    load_x(xs, s + XA);
     load_y(ys, s + 2);
     __syncthreads();  // this step's tiles are complete; the other buffers' readers are done
     if (s >= 0 && s < nsb) compute((int)(s & 1));
   };
-  for (int64_t s = opaque(-4); s < nsb; s += 4) {
-    body(s, xr[0], yr[0]);
-    body(s + 1, xr[1], yr[1]);
-    body(s + 2, xr[2], yr[0]);
-    body(s + 3, xr[3], yr[1]);
+  for (int64_t s = opaque(-XA); s < nsb; s += XA) {
+#pragma unroll
+    for (int u = 0; u < XA; ++u) body(s + u, xr[u], yr[u & 1]);
   }
 
 #pragma unroll
@@ -2252,10 +2280,10 @@ void launch_enc_bwd(const Plan& p, int act, const io_t* z, int64_t ld_z, const f
     hipLaunchKernelGGL(k_gh, dim3((unsigned)ceil_div(p.T * (p.r / 4), 256)), dim3(256), 0, st, p.T, p.r, silu, g_b,
                        a_save, gh_hi, gh_lo);
     if (r8)
-      hipLaunchKernelGGL((k_tokc_wide<NT, tw_ntw(NT), false, true>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, st,
+      hipLaunchKernelGGL((k_tokc_wide<NT, tw_ntw(NT), false, true, tw_tsm(NT, false)>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, st,
                          p.T, p.n, p.r, p.RP, z, ld_z, gh_hi, gh_lo, dwp, p.tw_TB);
     else
-      hipLaunchKernelGGL((k_tokc_wide<NT, tw_ntw(NT), false, false>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, st,
+      hipLaunchKernelGGL((k_tokc_wide<NT, tw_ntw(NT), false, false, tw_tsm(NT, false)>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, st,
                          p.T, p.n, p.r, p.RP, z, ld_z, gh_hi, gh_lo, dwp, p.tw_TB);
   } else {
     constexpr int CT = eb_ct(KS), CW = eb_cw(KS), TW = eb_tw(KS);
@@ -2525,10 +2553,10 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r, const void* b, const f
                          dim3(64 * rw_waves(NTV)), 0, s, T, n, r, 0, G,                                         \
                          ld_gzt, (const void*)wf, (const io_t*)g_id, ld_gid, (io_t*)g_b, (float*)nullptr);         \
       if (r8)                                                                                                       \
-        hipLaunchKernelGGL((k_tokc_wide<NTV, tw_ntw(NTV), true, true>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, s,  \
+        hipLaunchKernelGGL((k_tokc_wide<NTV, tw_ntw(NTV), true, true, tw_tsm(NTV, true)>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, s,  \
                            T, n, r, p.RP, G, ld_gzt, B, B, dwp, p.tw_TB);                                          \
       else                                                                                                          \
-        hipLaunchKernelGGL((k_tokc_wide<NTV, tw_ntw(NTV), true, false>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, s, \
+        hipLaunchKernelGGL((k_tokc_wide<NTV, tw_ntw(NTV), true, false, tw_tsm(NTV, true)>), dim3(p.tw_ntg, p.tw_ncb), dim3(512), 0, s, \
                            T, n, r, p.RP, G, ld_gzt, B, B, dwp, p.tw_TB);                                          \
     }                                                                                                               \
   } while (0)

@@ -128,6 +128,10 @@ constexpr int kExpandWideKS = RESBM_EXPAND_WIDE_KS;
 #endif
 constexpr int kExpandWideKSGZ = RESBM_EXPAND_WIDE_KS_GZ;
 constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four waves split r)
+// largest token-step multiplier of the wide token contraction (1: 32-token steps)
+#ifndef RESBM_TW_TSM
+#define RESBM_TW_TSM 2
+#endif
 // Row contraction of the wide path (k_rowc_wide).  A block of rw_waves waves
 // owns rw_tok(NT) tokens and one of rw_rh(NT) groups of j-tiles; each wave owns
 // rw_ntw j-tiles of its group.  Eight waves from RESBM_RW_WAVES8_NT j-tiles per
