@@ -944,10 +944,14 @@ constexpr int kLdsBytes = 160 * 1024;
 constexpr int tw_ypitch(int NT) {
   return RESBM_IO_F32_BUILD ? 32 * ((NT + 1) / 2) + 8 : plane_pitch(32 * ((NT + 1) / 2));
 }
-constexpr int tw_tsm(int NT, bool DWD) {
+constexpr int tw_lds(int NT, bool DWD, int tsm) {
   const int planes = (!DWD && !RESBM_IO_F32_BUILD) ? 2 : 1;
-  const int bytes2 = 2 * (64 * 128 + planes * 64 * tw_ypitch(NT)) * (int)sizeof(io_t);
-  return (RESBM_TW_TSM >= 2 && bytes2 <= kLdsBytes) ? 2 : 1;
+  return 2 * (32 * tsm * 128 + planes * 32 * tsm * tw_ypitch(NT)) * (int)sizeof(io_t);
+}
+constexpr int tw_tsm(int NT, bool DWD) {
+  return (RESBM_TW_TSM >= 4 && tw_lds(NT, DWD, 4) <= kLdsBytes)   ? 4
+         : (RESBM_TW_TSM >= 2 && tw_lds(NT, DWD, 2) <= kLdsBytes) ? 2
+                                                                   : 1;
 }
 
 // Split g_h tile of TS tokens x RPS columns: bf16 build: hi and lo planes in
@@ -1749,8 +1753,8 @@ __device__ __forceinline__ XFrag tr_rows(const io_t* plane, int row0, int c0, in
 // 8 waves: wave (cw, jq) owns columns [64 cw, 64 cw + 64) of the block and
 // j-tiles [jq NTW, jq NTW + NTW).  Per step of TS = 32 TSM tokens the block
 // stages the TS x 128 tile of X and the TS x r tile(s) of Y in LDS (double
-// buffered, the next steps' loads in registers: X 128 tokens ahead, Y two
-// steps); both operands are read back transposed (the contraction runs over
+// buffered, the next steps' loads in registers: X 128 tokens or two steps
+// ahead, Y two steps); both operands are read back transposed (the contraction runs over
 // the tile's rows, 32 at a time).  TSM = 2 halves the barriers per token where
 // the buffers fit in LDS.
 template <int NT, int NTW, bool DWD, bool R8, int TSM>
@@ -1764,7 +1768,7 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
   constexpr int XE = TS * BCc, YE = TS * YP;  // elements of the X tile and of one Y plane
   constexpr int YC = TS * (KP / 8);           // 8-element chunks of one Y plane
   constexpr int NYQ = (PL * YC + 511) / 512;  // Y chunk loads per thread and step
-  constexpr int XA = 4 / TSM;                 // steps of X loads in flight
+  constexpr int XA = RESBM_TW_XTOK / TS >= 2 ? RESBM_TW_XTOK / TS : 2;  // steps of X loads in flight (even)
   static_assert(2 * (XE + PL * YE) * (int)sizeof(io_t) <= kLdsBytes, "tiles exceed LDS");
   __shared__ __attribute__((aligned(16))) io_t s_x[2][XE];
   __shared__ __attribute__((aligned(16))) io_t s_y[2][PL][YE];

@@ -132,6 +132,10 @@ constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four
 #ifndef RESBM_TW_TSM
 #define RESBM_TW_TSM 2
 #endif
+// tokens of the streamed matrix the wide token contraction has in flight
+#ifndef RESBM_TW_XTOK
+#define RESBM_TW_XTOK 128
+#endif
 // Row contraction of the wide path (k_rowc_wide).  A block of rw_waves waves
 // owns rw_tok(NT) tokens and one of rw_rh(NT) groups of j-tiles; each wave owns
 // rw_ntw j-tiles of its group.  Eight waves from RESBM_RW_WAVES8_NT j-tiles per
