@@ -27,7 +27,10 @@ SHAPES = [(1000, 512, 32), (777, 256, 4), (333, 320, 40), (517, 1024, 64), (45, 
           # wide rank (r > 64): r % 8 == 4, r a multiple of 16, 48, 64, odd tile counts, n % 128 == 64, T = 1
           (333, 768, 100), (700, 576, 136), (1000, 1024, 192), (64, 256, 80), (1, 128, 128),
           # row contraction with r split over two blocks: one token, one group plus one token
-          (1, 256, 200), (129, 512, 256)]
+          (1, 256, 200), (129, 512, 256),
+          # token contraction in 64-token steps: 96-token groups (a step and a half) and a
+          # ragged last group (28 and 24 tokens), with and without the split operand at its LDS limit
+          (700, 4096, 136), (600, 4096, 256)]
 IDS = [f"T{T}_n{n}_r{r}" for T, n, r in SHAPES]
 
 
