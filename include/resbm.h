@@ -222,9 +222,10 @@ int32_t resbm_muon_update(int32_t p, int32_t q, float* W, const float* G, float*
  * Singular values and effective rank of a p x q matrix (App. B.1):
  *     sigma[0 .. s)  singular values, descending (device float64 array)
  *     r_eff[0]       = sum_i sigma_i^2 / max_i sigma_i^2  (0 for the zero matrix)
- * Computed as the eigenvalues of the s x s Gram matrix (float64 Jacobi
- * rotations); a singular value below ~1e-8 of the largest carries an absolute
- * error near 1e-8 of the largest.
+ * Computed as the eigenvalues of the s x s Gram matrix (float64: Householder
+ * reduction to tridiagonal form, then bisection on Sturm counts); a singular
+ * value below ~1e-8 of the largest carries an absolute error near 1e-8 of the
+ * largest.
  */
 int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, double* r_eff,
                        void* ws, size_t ws_bytes, void* stream);

@@ -42,6 +42,7 @@
 // results are reproducible run to run.
 #include <hip/hip_runtime.h>
 
+#include <float.h>
 #include <math.h>
 #include <stdint.h>
 
@@ -57,7 +58,6 @@ constexpr int64_t kMaxLong = 1 << 20;
 constexpr int kMaxSteps = 100;
 constexpr double kNsEps = 1e-7;       // added to ||U||_F before the division
 constexpr int kLdsDoubles = 17408;    // 136 KiB of LDS per block
-constexpr int kMaxSweeps = 60;
 
 enum Mode { kLoad = 0, kStep = 1, kOutO = 2, kOutW = 3 };
 
@@ -520,157 +520,176 @@ bool small_ok(int s4, int n, double a) {
 }
 
 // ---------------------------------------------------------------- spectrum
-// Eigenvalues of the s x s Gram A (row stride s4) by cyclic Jacobi rotations in
-// round-robin order (s/2 disjoint pairs per round, all rotated at once), in
-// LDS.  A pair is rotated unless its off-diagonal element is negligible next
-// to both its diagonal elements (1e-16 of their geometric mean) or to the whole
-// matrix (1e-18 of the trace: it cannot move any eigenvalue by more); a
-// rotated pair's off-diagonal elements are stored as exact zeros.  Sweeps stop
-// after one without a rotation (at most kMaxSweeps).
+// Eigenvalues of the s x s Gram A (row stride s4), s <= 128, in one block:
+//  1. Householder reduction to a symmetric tridiagonal T (diagonal d, off-
+//     diagonal e), in LDS: step k maps column k below the diagonal onto its
+//     first entry with H = I - beta v v^T (v0 = x0 - alpha, alpha = -sign(x0)
+//     ||x||, so v0 has no cancellation) applied to the trailing block as
+//     A <- A - v w^T - w v^T, p = beta A v, w = p - (beta / 2)(v . p) v.  A
+//     column already zero below its first entry is left alone (H = I).
+//  2. The j-th smallest eigenvalue of T by multisection on Sturm counts
+//     (count(x) = number of negative pivots of T - x I = number of eigenvalues
+//     below x): a group of K lanes evaluates K interior points of the current
+//     interval and keeps the subinterval where the count passes j, from the
+//     Gershgorin interval down to 4 ulp of ||T||.
+// Both steps are backward stable: the eigenvalues carry an absolute error of a
+// few ulp of the largest, as the Gram itself does.  Every sum has a fixed
+// order, so results are reproducible.
 // sigma[k] = sqrt(max(lambda, 0)) in descending order; r_eff = sum lambda^+ /
 // max lambda (0 for the zero matrix).
-#ifndef RESBM_EIG_THREADS_SMALL
-#define RESBM_EIG_THREADS_SMALL 64
-#endif
-__global__ __launch_bounds__(1024) void k_mx_eig(int s, int s4, const double* A, double* sigma,
-                                                 double* r_eff) {
-  const int nt = blockDim.x;
-  __shared__ double M[kMaxShortSpectrum * (kMaxShortSpectrum + 1)];
-  __shared__ double s_c[kMaxShortSpectrum / 2 + 1], s_s[kMaxShortSpectrum / 2 + 1];
-  __shared__ int s_p[kMaxShortSpectrum / 2 + 1], s_q[kMaxShortSpectrum / 2 + 1];
-  __shared__ double s_floor;
-  __shared__ int s_rotated;
-  const int t = threadIdx.x;
+constexpr int kEigThreads = 512;
+constexpr int kEigTpr = kEigThreads / kMaxShortSpectrum;  // lanes per row of the matrix-vector products
+
+// Sum over lanes of wave 0 of v (a butterfly; lane 0's order is fixed).
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const double* A, double* sigma,
+                                                        double* r_eff) {
+  constexpr int NT = kEigThreads;
+  constexpr int SM = kMaxShortSpectrum;
+  __shared__ double M[SM * (SM + 1)];
+  __shared__ double s_v[SM], s_w[SM], s_d[SM], s_e[SM], s_e2[SM], s_lam[SM];
+  __shared__ double s_beta, s_k, s_lo, s_hi, s_tn, s_piv;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int ms = s + 1;  // padded LDS row stride (columns of M are read across lanes)
-  for (int e = t; e < s * s; e += nt) M[(e / s) * ms + e % s] = A[(e / s) * s4 + e % s];
+  for (int e = t; e < s * s; e += NT) M[(e / s) * ms + e % s] = A[(e / s) * s4 + e % s];
   __syncthreads();
-  if (t == 0) {
-    double tr = 0.0;
-    for (int i = 0; i < s; ++i) tr += M[i * ms + i];
-    s_floor = 1e-18 * tr;
-  }
-  const int m = s + (s & 1);  // players; index s is the bye when s is odd
-  const int np = m / 2;
-  for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
-    __syncthreads();  // s_floor is set; the previous sweep's s_rotated has been read
-    if (t == 0) s_rotated = 0;
-    for (int round = 0; round < m - 1; ++round) {
-      __syncthreads();  // the previous round's updates are complete
-      if (t < np) {
-        // circle method: player 0 fixed, players 1 .. m-1 rotate by one per round
-        const int a = t == 0 ? 0 : 1 + (t - 1 + round) % (m - 1);
-        const int b = 1 + (m - 2 - t + round) % (m - 1);
-        const int p = a < b ? a : b, q = a < b ? b : a;
-        double c = 1.0, sn = 0.0;
-        bool rot = false;
-        if (q < s) {
-          const double apq = M[p * ms + q], app = M[p * ms + p], aqq = M[q * ms + q];
-          rot = fabs(apq) > s_floor && fabs(apq) > 1e-16 * sqrt(fabs(app * aqq));
-          if (rot) {
-            const double tau = (aqq - app) / (2.0 * apq);
-            const double at = fabs(tau);
-            // tan of the smaller rotation angle; 1 / (2 tau) where tau^2 would overflow
-            const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (at > 1e150 ? 2.0 * at : at + sqrt(1.0 + tau * tau));
-            c = 1.0 / sqrt(1.0 + tt * tt);
-            sn = tt * c;
-            s_rotated = 1;
-          }
-        }
-        s_c[t] = c;
-        s_s[t] = sn;
-        s_p[t] = p;
-        s_q[t] = rot ? q : -1;
-      }
-      __syncthreads();
-      // work item e = (row or column index) * np + pair; when nt is a multiple
-      // of np every thread keeps one pair, so its rotation is loaded once and
-      // the loop's iterations are independent
-      const int k0 = t % np, step = nt / np;
-      const bool fixed = nt % np == 0;
-      if (fixed) {
-        const int q = s_q[k0];
-        if (q >= 0) {
-          const int p = s_p[k0];
-          const double c = s_c[k0], sn = s_s[k0];
-          // columns p, q of every row, eight rows' loads ahead of their stores
-          for (int i0 = t / np; i0 < s; i0 += 8 * step) {
-            double xp[8], xq[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              const int i = i0 + u * step < s ? i0 + u * step : i0;
-              xp[u] = M[i * ms + p];
-              xq[u] = M[i * ms + q];
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              const int i = i0 + u * step;
-              if (i < s) {
-                M[i * ms + p] = c * xp[u] - sn * xq[u];
-                M[i * ms + q] = sn * xp[u] + c * xq[u];
-              }
-            }
-          }
-        }
-      } else {
-        for (int e = t; e < s * np; e += nt) {
-          const int i = e / np, k = e % np, q = s_q[k];
-          if (q < 0) continue;
-          const int p = s_p[k];
-          const double c = s_c[k], sn = s_s[k];
-          const double xp = M[i * ms + p], xq = M[i * ms + q];
-          M[i * ms + p] = c * xp - sn * xq;
-          M[i * ms + q] = sn * xp + c * xq;
-        }
-      }
-      __syncthreads();
-      // rows p, q of every column; the rotation annihilates (p, q) and (q, p):
-      // store the exact zero, not the rounding residue, which would otherwise
-      // be rotated again
-      if (fixed) {
-        const int q = s_q[k0];
-        if (q >= 0) {
-          const int p = s_p[k0];
-          const double c = s_c[k0], sn = s_s[k0];
-          for (int j0 = t / np; j0 < s; j0 += 8 * step) {
-            double xp[8], xq[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              const int j = j0 + u * step < s ? j0 + u * step : j0;
-              xp[u] = M[p * ms + j];
-              xq[u] = M[q * ms + j];
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              const int j = j0 + u * step;
-              if (j < s) {
-                M[p * ms + j] = j == q ? 0.0 : c * xp[u] - sn * xq[u];
-                M[q * ms + j] = j == p ? 0.0 : sn * xp[u] + c * xq[u];
-              }
-            }
-          }
-        }
-      } else {
-        for (int e = t; e < s * np; e += nt) {
-          const int j = e / np, k = e % np, q = s_q[k];
-          if (q < 0) continue;
-          const int p = s_p[k];
-          const double c = s_c[k], sn = s_s[k];
-          const double xp = M[p * ms + j], xq = M[q * ms + j];
-          M[p * ms + j] = j == q ? 0.0 : c * xp - sn * xq;
-          M[q * ms + j] = j == p ? 0.0 : sn * xp + c * xq;
+
+  // 1. tridiagonal reduction
+  for (int k = 0; k + 2 < s; ++k) {
+    const int r0 = k + 1, L = s - r0;  // trailing block rows / cols [r0, s), L >= 2
+    if (wave == 0) {
+      double x2 = 0.0;  // sum of x_i^2 below the first entry (lanes i and i + 64)
+      if (lane >= 1 && lane < L) x2 = M[(r0 + lane) * ms + k] * M[(r0 + lane) * ms + k];
+      if (lane + 64 < L) x2 += M[(r0 + lane + 64) * ms + k] * M[(r0 + lane + 64) * ms + k];
+      x2 = wave_sum(x2);
+      if (lane == 0) {
+        const double x0 = M[r0 * ms + k];
+        s_d[k] = M[k * ms + k];
+        if (x2 == 0.0) {  // already reduced
+          s_e[k] = x0;
+          s_beta = 0.0;
+        } else {
+          const double nx = sqrt(x0 * x0 + x2);
+          const double alpha = x0 >= 0.0 ? -nx : nx;
+          const double v0 = x0 - alpha;
+          s_e[k] = alpha;
+          s_v[0] = v0;
+          s_beta = 2.0 / (x2 + v0 * v0);
         }
       }
     }
+    for (int i = 1 + t; i < L; i += NT) s_v[i] = M[(r0 + i) * ms + k];
     __syncthreads();
-    if (!s_rotated) break;  // uniform: every thread reads the same flag
+    const double beta = s_beta;
+    if (beta == 0.0) {  // uniform; the barrier keeps the next step's writes of s_beta behind every read
+      __syncthreads();
+      continue;
+    }
+    // p = beta A22 v: kEigTpr lanes per row, strided columns, combined in a fixed order
+    {
+      const int i = t / kEigTpr, u = t % kEigTpr;
+      double acc = 0.0;
+      if (i < L)
+        for (int j = u; j < L; j += kEigTpr) acc += M[(r0 + i) * ms + r0 + j] * s_v[j];
+#pragma unroll
+      for (int o = 1; o < kEigTpr; o <<= 1) acc += __shfl_xor(acc, o);
+      if (i < L && u == 0) s_w[i] = beta * acc;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      double vp = 0.0;
+      if (lane < L) vp = s_v[lane] * s_w[lane];
+      if (lane + 64 < L) vp += s_v[lane + 64] * s_w[lane + 64];
+      vp = wave_sum(vp);
+      if (lane == 0) s_k = 0.5 * beta * vp;
+    }
+    __syncthreads();
+    const double kk = s_k;
+    for (int i = t; i < L; i += NT) s_w[i] -= kk * s_v[i];
+    __syncthreads();
+    for (int e = t; e < L * L; e += NT) {
+      const int i = e / L, j = e % L;
+      M[(r0 + i) * ms + r0 + j] -= s_v[i] * s_w[j] + s_w[i] * s_v[j];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    if (s >= 2) {
+      s_d[s - 2] = M[(s - 2) * ms + s - 2];
+      s_e[s - 2] = M[(s - 1) * ms + s - 2];
+    }
+    s_d[s - 1] = M[(s - 1) * ms + s - 1];
+    // Gershgorin interval, ||T|| and the smallest pivot magnitude
+    double lo = 0.0, hi = 0.0, emax = 0.0;
+    for (int i = 0; i < s; ++i) {
+      const double rad = (i > 0 ? fabs(s_e[i - 1]) : 0.0) + (i + 1 < s ? fabs(s_e[i]) : 0.0);
+      lo = i == 0 || s_d[i] - rad < lo ? s_d[i] - rad : lo;
+      hi = i == 0 || s_d[i] + rad > hi ? s_d[i] + rad : hi;
+      if (i + 1 < s) {
+        s_e2[i] = s_e[i] * s_e[i];
+        emax = s_e2[i] > emax ? s_e2[i] : emax;
+      }
+    }
+    const double tn = fabs(lo) > fabs(hi) ? fabs(lo) : fabs(hi);
+    const double piv = DBL_MIN * (emax > 1.0 ? emax : 1.0);
+    const double pad = 2.1 * (DBL_EPSILON * tn * s + 2.0 * piv);
+    s_lo = lo - pad;
+    s_hi = hi + pad;
+    s_tn = tn;
+    s_piv = piv;
+  }
+  __syncthreads();
+
+  // 2. multisection: group g of K lanes finds the g-th smallest eigenvalue
+  {
+    int K = 64;
+    while (K > 1 && K * s > NT) K >>= 1;
+    const int g = t / K, u = t % K;
+    const double tn = s_tn, piv = s_piv;
+    if (g < s) {
+      double lam = 0.0;
+      if (tn > 0.0) {
+        double a = s_lo, b = s_hi;
+        const double tol = 4.0 * DBL_EPSILON * tn;
+        const int sh = lane - u;  // the group's first lane in the wave
+        for (int it = 0; it < 200 && b - a > tol; ++it) {
+          const double step = (b - a) / (K + 1);
+          const double x = a + step * (u + 1);
+          int c = 0;
+          double q = 1.0;
+          for (int i = 0; i < s; ++i) {
+            q = s_d[i] - x - (i > 0 ? s_e2[i - 1] / q : 0.0);
+            if (fabs(q) < piv) q = -piv;
+            c += q < 0.0;
+          }
+          // the first point with more than g eigenvalues below it closes the interval
+          const uint64_t m = (__ballot(c > g) >> sh) & (K == 64 ? ~0ull : ((1ull << K) - 1));
+          if (m == 0) {
+            a = a + step * K;
+          } else {
+            const int f = __builtin_ctzll(m);
+            const double nb = a + step * (f + 1);
+            if (f > 0) a = a + step * f;
+            b = nb;
+          }
+        }
+        lam = 0.5 * (a + b);
+      }
+      if (u == 0) s_lam[g] = lam;
+    }
   }
   __syncthreads();
   // descending order by rank (ties by index)
-  for (int i = t; i < s; i += nt) {
-    const double li = M[i * ms + i];
+  for (int i = t; i < s; i += NT) {
+    const double li = s_lam[i];
     int rank = 0;
     for (int j = 0; j < s; ++j) {
-      const double lj = M[j * ms + j];
+      const double lj = s_lam[j];
       rank += (lj > li) || (lj == li && j < i);
     }
     sigma[rank] = sqrt(li > 0.0 ? li : 0.0);
@@ -678,7 +697,7 @@ __global__ __launch_bounds__(1024) void k_mx_eig(int s, int s4, const double* A,
   if (t == 0) {
     double tot = 0.0, top = 0.0;
     for (int i = 0; i < s; ++i) {
-      const double l = M[i * ms + i] > 0.0 ? M[i * ms + i] : 0.0;
+      const double l = s_lam[i] > 0.0 ? s_lam[i] : 0.0;
       tot += l;
       top = l > top ? l : top;
     }
@@ -884,7 +903,7 @@ int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, doub
   double* A = (double*)(wsc + P.off_a);
   hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), dim3(kThreads), 0, st, ne, d.nch,
                      (const double*)g.part, A);
-  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(d.s <= 64 ? RESBM_EIG_THREADS_SMALL : kThreads), 0, st, d.s, d.s4,
+  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(kEigThreads), 0, st, d.s, d.s4,
                      (const double*)A, sigma,
                      r_eff);
   return launch_status();
