@@ -60,7 +60,8 @@ def parse():
     p.add_argument("--cpu-tokens", type=int, default=None, help="tokens in the CPU oracle sample")
     p.add_argument("--no-graph", action="store_true", help="report the eager launches instead of graph replays")
     p.add_argument("--graph-steps", type=int, default=8,
-                   help="consecutive steps captured in one HIP graph (input copies in turn)")
+                   help="consecutive steps captured in one HIP graph (input copies in turn) for the sweep and "
+                        "per-op timings; the timed steps use the largest divisor of --steps up to twice this")
     p.add_argument("--no-optimizer", action="store_true",
                    help="skip timing the optimizer-side ops (Muon update, spectrum) on the bottleneck weights")
     p.add_argument("--two-m", type=int, default=1024,
@@ -845,6 +846,10 @@ def main():
         step(s)
     torch.cuda.synchronize()
     G = max(1, args.graph_steps)
+    # the timed steps' graph: the largest divisor of K up to 2 G, so that K
+    # steps are whole replays of it (else G steps per graph and single-step
+    # replays for the remainder)
+    GH = next((g for g in range(min(args.steps, 2 * G), 1, -1) if args.steps % g == 0), G)
     g_multi, g_single = None, []
     if not args.no_graph:
         for s in sets:
@@ -852,10 +857,10 @@ def main():
             with torch.cuda.graph(g):
                 step(s)
             g_single.append(g)
-        if G > 1:
+        if GH > 1:
             g_multi = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g_multi):
-                for i in range(G):
+                for i in range(GH):
                     step(sets[i % len(sets)])
     sweep = None if args.no_sweep else sweep_timing(lib, dev, SWEEP, 48, 24, act, G)
 
@@ -863,8 +868,8 @@ def main():
     if g_single:
         def replays(k):
             # (graph, steps) covering exactly k steps
-            full = k // G if g_multi is not None else 0
-            return [(g_multi, G)] * full + [(g_single[i % len(sets)], 1) for i in range(k - full * G)]
+            full = k // GH if g_multi is not None else 0
+            return [(g_multi, GH)] * full + [(g_single[i % len(sets)], 1) for i in range(k - full * GH)]
         for g, _ in replays(args.warmup):
             g.replay()
         plan = replays(args.steps)
@@ -882,7 +887,7 @@ def main():
         wall = time.perf_counter() - wall0
         ms_graph = gev[0].elapsed_time(gev[-1]) / args.steps
         per = [(gev[i].elapsed_time(gev[i + 1]) / k, k) for i, (_, k) in enumerate(plan)]
-        multi = [t for t, k in per if k == G]
+        multi = [t for t, k in per if k == GH]
         step_ms = multi if multi else [t for t, _ in per]
 
     # eager launches, HIP events between the ops (on the stream the ops run on):
@@ -959,7 +964,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
-        "timing": (f"hip graph replay, {G} steps per graph" if ms_graph is not None else "eager launches"),
+        "timing": (f"hip graph replay, {GH} steps per graph" if ms_graph is not None else "eager launches"),
         "step_time_stats": step_stats,
         "ms_per_step_eager": ms_eager,
         "higher_is_better": True,
