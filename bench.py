@@ -957,7 +957,7 @@ def main():
 
     traffic = measured_traffic(name, dom)
     out = {
-        "metric": "tokens/s and achieved HBM GB/s (% peak), ResBM fwd+bwd, n=4096 r=32",
+        "metric": f"tokens/s and achieved HBM GB/s (% peak), ResBM fwd+bwd, n={n} r={r}",
         "value": T / (ms_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
