@@ -609,12 +609,13 @@ __global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const dou
       if (lane == 0) s_k = 0.5 * beta * vp;
     }
     __syncthreads();
+    // A22 -= v w^T + w v^T with w = p - K v formed on the fly (s_w holds p)
     const double kk = s_k;
-    for (int i = t; i < L; i += NT) s_w[i] -= kk * s_v[i];
-    __syncthreads();
     for (int e = t; e < L * L; e += NT) {
       const int i = e / L, j = e % L;
-      M[(r0 + i) * ms + r0 + j] -= s_v[i] * s_w[j] + s_w[i] * s_v[j];
+      const double vi = s_v[i], vj = s_v[j];
+      const double wi = s_w[i] - kk * vi, wj = s_w[j] - kk * vj;
+      M[(r0 + i) * ms + r0 + j] -= vi * wj + wi * vj;
     }
     __syncthreads();
   }
@@ -660,12 +661,30 @@ __global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const dou
         for (int it = 0; it < 200 && b - a > tol; ++it) {
           const double step = (b - a) / (K + 1);
           const double x = a + step * (u + 1);
+          // Sturm count: q_i = d_i - x - e_{i-1}^2 / q_{i-1}, with the quotient from the
+          // hardware reciprocal and one Newton step (|q| >= piv keeps it finite)
           int c = 0;
-          double q = 1.0;
-          for (int i = 0; i < s; ++i) {
-            q = s_d[i] - x - (i > 0 ? s_e2[i - 1] / q : 0.0);
-            if (fabs(q) < piv) q = -piv;
-            c += q < 0.0;
+          double q = s_d[0] - x;
+          if (fabs(q) < piv) q = -piv;
+          c += q < 0.0;
+          for (int i0 = 1; i0 < s; i0 += 4) {
+            double dd[4], ee[4];
+#pragma unroll
+            for (int u2 = 0; u2 < 4; ++u2) {
+              const int i = i0 + u2 < s ? i0 + u2 : s - 1;
+              dd[u2] = s_d[i];
+              ee[u2] = s_e2[i - 1];
+            }
+#pragma unroll
+            for (int u2 = 0; u2 < 4; ++u2) {
+              if (i0 + u2 < s) {
+                const double r0 = __builtin_amdgcn_rcp(q);
+                const double rq = fma(r0, fma(-q, r0, 1.0), r0);
+                q = dd[u2] - x - ee[u2] * rq;
+                if (fabs(q) < piv) q = -piv;
+                c += q < 0.0;
+              }
+            }
           }
           // the first point with more than g eigenvalues below it closes the interval
           const uint64_t m = (__ballot(c > g) >> sh) & (K == 64 ? ~0ull : ((1ull << K) - 1));
