@@ -932,7 +932,7 @@ def main():
             "encode_bwd": lambda s: lib.encode_bwd(s["z"], s["W_e"], s["a"], s["gb"], s["gz"], s["dWe"], act=act,
                                                    ws=ws),
         }
-        nrep = max(1, args.steps // G)
+        nrep = max(16, args.steps // G)  # at least 128 calls per op, whatever K
         for nm in OPS:
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
