@@ -196,7 +196,7 @@ def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
 
 
 # ---------------------------------------------------------------- bottleneck-weight matrices
-MATRIX_KINDS = ("gaussian", "powerlaw", "orthonormal", "rank1", "zero")
+MATRIX_KINDS = ("gaussian", "powerlaw", "orthonormal", "rank1", "zero", "clustered", "graded")
 
 
 def make_matrix(p: int, q: int, kind: str = "gaussian", seed: int = 0, scale: float = 1.0) -> torch.Tensor:
@@ -209,7 +209,11 @@ def make_matrix(p: int, q: int, kind: str = "gaussian", seed: int = 0, scale: fl
     orthonormal  scale times orthonormal columns (rows if p < q): all singular
                  values equal;
     rank1        scale u v^T with Gaussian u, v;
-    zero         all zeros.
+    zero         all zeros;
+    clustered    U diag(sigma) V^T with two tight clusters: sigma_i = scale
+                 (1 + 1e-6 i) for the first half, half that for the rest;
+    graded       U diag(sigma) V^T with sigma_i = scale 10^(-6 i / (s - 1)): six
+                 decades from the top to the smallest.
     """
     if p <= 0 or q <= 0:
         raise ValueError("p and q must be positive")
@@ -233,6 +237,14 @@ def make_matrix(p: int, q: int, kind: str = "gaussian", seed: int = 0, scale: fl
         m = scale * np.outer(rng.standard_normal(p), rng.standard_normal(q))
     elif kind == "zero":
         m = np.zeros((p, q))
+    elif kind in ("clustered", "graded"):
+        i = np.arange(s, dtype=float)
+        if kind == "clustered":
+            sig = scale * (1.0 + 1e-6 * i) * np.where(i < s // 2, 1.0, 0.5)
+        else:
+            sig = scale * 10.0 ** (-6.0 * i / max(s - 1, 1))
+        tall = orth(L, s) @ np.diag(sig) @ orth(s, s).T
+        m = tall if p >= q else tall.T
     else:
         raise ValueError(f"unknown matrix kind {kind!r}")
     return torch.from_numpy(np.ascontiguousarray(m).astype(np.float32))

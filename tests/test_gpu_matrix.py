@@ -146,7 +146,9 @@ def test_muon_update_explicit_scale(scale):
 
 SPEC_CASES = [(4096, 32, "gaussian"), (32, 4096, "gaussian"), (8192, 64, "powerlaw"), (333, 40, "powerlaw"),
               (128, 4096, "powerlaw"), (64, 64, "gaussian"), (4096, 32, "orthonormal"), (32, 4096, "rank1"),
-              (40, 333, "zero"), (7, 3, "gaussian"), (1, 5, "gaussian"), (5, 1, "gaussian"), (1, 1, "gaussian")]
+              (40, 333, "zero"), (7, 3, "gaussian"), (1, 5, "gaussian"), (5, 1, "gaussian"), (1, 1, "gaussian"),
+              # hard cases for bisection: two tight clusters, six decades of singular values (s = 32, 128)
+              (4096, 32, "clustered"), (32, 4096, "graded"), (128, 4096, "graded")]
 
 
 @pytest.mark.parametrize("p,q,kind", SPEC_CASES, ids=[f"{p}x{q}_{k}" for p, q, k in SPEC_CASES])
