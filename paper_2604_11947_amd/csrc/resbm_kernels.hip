@@ -1551,8 +1551,8 @@ __global__ __launch_bounds__(64) void k_wd_prep(const float* __restrict__ W_d, i
 // wave ends with whole sums of its columns and the block reads each weight
 // fragment of its group once per TOK tokens.  With RH = 2 the two blocks of a
 // token group are 8 apart in a run of 16 (same XCD, dispatched together), so
-// their shared X rows come from HBM once.  The weight fragments run three
-// k-steps ahead of their use in a ring of four.
+// their shared X rows come from HBM once.  The weight fragments run kRwRing - 1
+// k-steps ahead of their use in a ring of kRwRing registers.
 //   GB = false: a_save = a, b = x_attn[:, :r] + phi(a)        (encode_fwd)
 //   GB = true:  g_b = C + g_id[:, :r] (g_id may be NULL)        (decode_bwd)
 template <int NT, int NTW, bool GB, int NWV, int RH>
@@ -1597,7 +1597,9 @@ __global__ __launch_bounds__(64 * NWV) void k_rowc_wide(int64_t T, int n, int r,
 #pragma unroll
     for (int q = 0; q < NQ; ++q) zz[q] = bld_x8(zr, c < n ? (uint32_t)((zrow[q] * ld_x + c) * kEs) : kOOB);
   };
-  SFrag wring[4][NTW];
+  constexpr int RG = kRwRing, AH = RG - 1;  // ring of weight fragments, loaded AH k-steps ahead
+  static_assert(KSS % RG == 0, "a stage's k-steps must fill whole rings");
+  SFrag wring[RG][NTW];
   // the weight fragments of k-step ks of stage i (zeros outside [0, nks) or past NT)
   auto load_wf = [&](SFrag (&dst)[NTW], int i, int ks) {
     const int kg = (stage_col(i) >> 5) + ks;
@@ -1632,8 +1634,8 @@ __global__ __launch_bounds__(64 * NWV) void k_rowc_wide(int64_t T, int n, int r,
     const bool live = i >= 0 && i < nst;  // stages outside hold zeros: only their weight loads matter
 #pragma unroll
     for (int ks = 0; ks < KSS; ++ks) {
-      if (ks + 3 < KSS) load_wf(wring[(ks + 3) & 3], i, ks + 3);
-      else load_wf(wring[(ks + 3) & 3], i + 1, ks + 3 - KSS);
+      if (ks + AH < KSS) load_wf(wring[(ks + AH) % RG], i, ks + AH);
+      else load_wf(wring[(ks + AH) % RG], i + 1, ks + AH - KSS);
       if (!live) continue;
       XFrag f[MT];
 #pragma unroll
@@ -1651,15 +1653,17 @@ __global__ __launch_bounds__(64 * NWV) void k_rowc_wide(int64_t T, int n, int r,
 #pragma unroll
       for (int jt = 0; jt < NTW; ++jt)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt][jt] = mma_sx(wring[ks & 3][jt], f[mt], acc[mt][jt]);
+        for (int mt = 0; mt < MT; ++mt) acc[mt][jt] = mma_sx(wring[ks % RG][jt], f[mt], acc[mt][jt]);
     }
   };
   XFrag za[NQ], zb[NQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) za[q] = zb[q] = xfrag_zero();
-  load_wf(wring[0], opaque(-2), 0);
-  load_wf(wring[1], -2, 1);
-  load_wf(wring[2], -2, 2);
+  {
+    const int i0 = opaque(-2);
+#pragma unroll
+    for (int u = 0; u < AH; ++u) load_wf(wring[u], i0, u);
+  }
   for (int i = opaque(-2); i < nst; i += 2) {
     body(za, i);
     body(zb, i + 1);

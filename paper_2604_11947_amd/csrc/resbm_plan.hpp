@@ -128,6 +128,12 @@ constexpr int kExpandWideKS = RESBM_EXPAND_WIDE_KS;
 #endif
 constexpr int kExpandWideKSGZ = RESBM_EXPAND_WIDE_KS_GZ;
 constexpr int tw_ntw(int NT) { return (NT + 3) / 4; }  // j-tiles per wave (four waves split r)
+// wide row contraction: ring of weight-fragment registers (2, 4 or 8 k-steps;
+// fragments are loaded ring - 1 k-steps ahead)
+#ifndef RESBM_RW_RING
+#define RESBM_RW_RING 4
+#endif
+constexpr int kRwRing = RESBM_RW_RING;
 // largest token-step multiplier of the wide token contraction (1: 32-token steps)
 #ifndef RESBM_TW_TSM
 #define RESBM_TW_TSM 2
