@@ -135,6 +135,9 @@ int32_t resbm_decode_bwd(int64_t T, int32_t n, int32_t r,
  *          touched), or NULL.  g_x may equal g_z (same pointer and ld_gx ==
  *          ld_gz): then g_z = g_h W_e^T + g_b I_{r x n}, rounded once.
  *  dW_e    n x r float32; overwritten or accumulated into, fixed token order.
+ * Non-finite inputs propagate as in IEEE arithmetic, except that an infinite
+ * W_e entry turns the g_z entries it reaches into NaN rather than +-inf (W_e
+ * and g_h are both carried as hi + lo bf16 pairs there).
  */
 int32_t resbm_encode_bwd(int64_t T, int32_t n, int32_t r, int32_t act,
                          const void* z, int64_t ld_z, const float* W_e,
