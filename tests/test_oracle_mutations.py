@@ -10,6 +10,7 @@ import pytest
 import oracle as O
 from oracle import resbm_oracle as R
 import test_oracle_pins as P
+import test_oracle_properties as PP
 
 
 def _silu_dphi_dropped_term(a, act):
@@ -68,6 +69,20 @@ def _chain_decoder_grad_on_unrounded_payload(x_attn, z, W_e, W_d, g_zt, g_id, ac
             "g_z": g_z, "dW_e": dW_e}
 
 
+def _encode_local_grad_no_dphi(g_b, a, act):
+    return np.array(g_b, copy=True)
+
+
+def _decode_weight_grad_reversed_j(b, g_zt):
+    return b[:, ::-1].T @ g_zt
+
+
+def _skip_grad_last_columns(g_x, g_b):
+    out = np.array(g_x, copy=True)
+    out[:, out.shape[1] - g_b.shape[1]:] += g_b
+    return out
+
+
 MUTATIONS = [
     ("dphi", _silu_dphi_dropped_term,
      lambda: P.test_gradients_finite_differences(O.ACT_SILU, False, 3, 8, 2)),
@@ -82,6 +97,11 @@ MUTATIONS = [
      lambda: P.test_wire_rounded_chain_torch_autograd(O.ACT_SILU, False)),
     ("boundary_fwd_bwd", _chain_decoder_grad_on_unrounded_payload,
      lambda: P.test_wire_rounded_chain_torch_autograd(O.ACT_IDENTITY, True)),
+    # the property-based adjoint pins
+    ("encode_local_grad", _encode_local_grad_no_dphi, lambda: PP.test_encode_backward_is_the_adjoint()),
+    ("decode_weight_grad", _decode_weight_grad_reversed_j, lambda: PP.test_decode_backward_is_the_adjoint()),
+    ("skip_grad", _skip_grad_last_columns, lambda: PP.test_encode_backward_is_the_adjoint()),
+    ("decode_input_grad", _decode_input_grad_no_identity, lambda: PP.test_decode_backward_is_the_adjoint()),
 ]
 
 
