@@ -1632,6 +1632,17 @@ __global__ __launch_bounds__(64 * NWV) void k_rowc_wide(int64_t T, int n, int r,
     load_z(zz, i + 2);
     __syncthreads();  // the stage's tile is complete; the other buffer's readers are done
     const bool live = i >= 0 && i < nst;  // stages outside hold zeros: only their weight loads matter
+    // fp32 build: each stage sums into a zeroed partial that is then added to
+    // the total, so a long contraction (n / 4 products of K = 4) rounds as two
+    // short ones; the bf16 build accumulates directly
+    constexpr bool PART = RESBM_IO_F32_BUILD;
+    f32x4 part[PART ? MT : 1][PART ? NTW : 1];
+    if constexpr (PART) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int jt = 0; jt < NTW; ++jt) part[mt][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
     for (int ks = 0; ks < KSS; ++ks) {
       if (ks + AH < KSS) load_wf(wring[(ks + AH) % RG], i, ks + AH);
@@ -1653,7 +1664,18 @@ __global__ __launch_bounds__(64 * NWV) void k_rowc_wide(int64_t T, int n, int r,
 #pragma unroll
       for (int jt = 0; jt < NTW; ++jt)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt][jt] = mma_sx(wring[ks % RG][jt], f[mt], acc[mt][jt]);
+        for (int mt = 0; mt < MT; ++mt) {
+          if constexpr (PART) part[mt][jt] = mma_sx(wring[ks % RG][jt], f[mt], part[mt][jt]);
+          else acc[mt][jt] = mma_sx(wring[ks % RG][jt], f[mt], acc[mt][jt]);
+        }
+    }
+    if constexpr (PART) {
+      if (live) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int jt = 0; jt < NTW; ++jt) acc[mt][jt] += part[mt][jt];
+      }
     }
   };
   XFrag za[NQ], zb[NQ];
@@ -1852,7 +1874,18 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
       }
     }
   };
+  // fp32 build: each step sums into a zeroed partial that is then added to the
+  // total, so a token group's long sum rounds as a short one per step plus one
+  // addition per step; the bf16 build accumulates directly
+  constexpr bool PART = RESBM_IO_F32_BUILD;
   auto compute = [&](int buf) {
+    f32x4 part[PART ? 4 : 1][PART ? NTW : 1];
+    if constexpr (PART) {
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int jt = 0; jt < NTW; ++jt) part[ct][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
     for (int ks = 0; ks < TSM; ++ks) {  // 32 tokens of the step at a time
       XFrag xf[4];
@@ -1867,7 +1900,10 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
         if constexpr (DWD) {
           const XFrag yb = tr_rows<YP>(s_y[buf][0], 32 * ks, 16 * jtg, row16, grp);
 #pragma unroll
-          for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_xx(xf[ct], yb, acc[ct][jt]);
+          for (int ct = 0; ct < 4; ++ct) {
+            if constexpr (PART) part[ct][jt] = mma_xx(xf[ct], yb, part[ct][jt]);
+            else acc[ct][jt] = mma_xx(xf[ct], yb, acc[ct][jt]);
+          }
         } else {
           SFrag g;
 #if RESBM_IO_F32_BUILD
@@ -1879,9 +1915,18 @@ __global__ __launch_bounds__(512) void k_tokc_wide(int64_t T, int n, int r, int 
           g.lo = tr_rows<YP>(s_y[buf][PL - 1], 32 * ks, 16 * jtg, row16, grp).v;
 #endif
 #pragma unroll
-          for (int ct = 0; ct < 4; ++ct) acc[ct][jt] = mma_sx(g, xf[ct], acc[ct][jt]);
+          for (int ct = 0; ct < 4; ++ct) {
+            if constexpr (PART) part[ct][jt] = mma_sx(g, xf[ct], part[ct][jt]);
+            else acc[ct][jt] = mma_sx(g, xf[ct], acc[ct][jt]);
+          }
         }
       }
+    }
+    if constexpr (PART) {
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int jt = 0; jt < NTW; ++jt) acc[ct][jt] += part[ct][jt];
     }
   };
 

@@ -19,7 +19,11 @@ from paper_2604_11947_amd import inputs as I
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(1000, 512, 32), (333, 320, 40), (130, 128, 128), (96, 256, 256), (45, 192, 12), (1, 64, 4)]
+SHAPES = [(1000, 512, 32), (333, 320, 40), (130, 128, 128), (96, 256, 256), (45, 192, 12), (1, 64, 4),
+          # more rank tilings (4, 5, 7, 9, 12, 13, 15 tiles of r; the wide kernels' float32 tiles), a 96-token
+          # group with a ragged last group
+          (517, 1024, 64), (64, 256, 80), (333, 768, 100), (200, 576, 136), (160, 1024, 192), (1, 256, 200),
+          (97, 768, 236), (700, 4096, 136), (700, 4096, 32)]
 IDS = [f"T{T}_n{n}_r{r}" for T, n, r in SHAPES]
 
 
@@ -145,11 +149,14 @@ def test_f32_gaussian_plain_scale(shape):
 
 
 @pytest.mark.timeout(600)
-def test_f32_gaussian_full_tokens():
-    """The headline shape's token count (T = 16384, n = 4096, r = 32) in the fp32
-    build on N(0, 1) activations: weight gradients (sums over all 16384 tokens)
-    whole, within 1e-5 RMS(ref); row-local outputs on sampled rows."""
-    T, n, r = 16384, 4096, 32
+@pytest.mark.parametrize("r", [32, 128], ids=["r32", "r128_wide"])
+def test_f32_gaussian_full_tokens(r):
+    """The headline shape's token count (T = 16384, n = 4096) in the fp32 build
+    on N(0, 1) activations, at r = 32 and at r = 128 (the wide kernels: 4096-long
+    row contractions, 2048-token sums per token group): weight gradients (sums
+    over all 16384 tokens) whole, within 1e-5 RMS(ref); row-local outputs on
+    sampled rows."""
+    T, n = 16384, 4096
     say(f"f32 build, full token count T={T} n={n} r={r}")
     L = lib("f32")
     d = I.make_inputs(T, n, r, "normal", 0)
