@@ -506,6 +506,17 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
     const int ks = (stage_col(i) + wave * SC) / 32;
     const __bf16* const ph = wl_plane(i);  // written by this wave during stage i - 1
     const __bf16* const pl = ph + WPL;
+    // fp32 build: the stage's products go to a zeroed partial added to the
+    // total afterwards (n / 4 products of K = 4 would otherwise round as one
+    // chain); the bf16 build accumulates directly
+    constexpr bool PART = RESBM_IO_F32_BUILD;
+    f32x4 part[PART ? MT : 1][PART ? NT : 1];
+    if constexpr (PART) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) part[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       XFrag f[MT];
@@ -534,8 +545,17 @@ __global__ __launch_bounds__(KW * 64) void k_enc_fwd(int64_t T, int n, int r, in
           w = bld_sfrag(wr, (int64_t)(ks + u) * NT + nt, l, ks + u < nks);
         }
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt][nt] = mma_sx(w, f[mt], acc[mt][nt]);
+        for (int mt = 0; mt < MT; ++mt) {
+          if constexpr (PART) part[mt][nt] = mma_sx(w, f[mt], part[mt][nt]);
+          else acc[mt][nt] = mma_sx(w, f[mt], acc[mt][nt]);
+        }
       }
+    }
+    if constexpr (PART) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] += part[mt][nt];
     }
     if constexpr (WL) {
       wl_split(qn, i + 1);
