@@ -178,9 +178,9 @@ def test_spectrum_parity(p, q, kind):
 
 @pytest.mark.parametrize("p,q", [(4096, 32), (40, 333), (256, 520)], ids=["4096x32", "40x333", "256x520"])
 def test_graph_replay_matches_eager(p, q):
-    """A Muon update and a Newton-Schulz call captured in one HIP graph replay
-    exactly like eager launches (fixed-order sums), with unrelated eager work
-    and a scribbled workspace between the replays."""
+    """A Muon update, a Newton-Schulz call and (s <= 128) the spectrum captured
+    in one HIP graph replay exactly like eager launches (fixed-order sums), with
+    unrelated eager work and a scribbled workspace between the replays."""
     L = lib()
     say(f"matrix graph replay {p}x{q}")
     W0 = dev(I.make_matrix(p, q, "gaussian", seed=9, scale=0.1))
@@ -188,14 +188,19 @@ def test_graph_replay_matches_eager(p, q):
     M0 = dev(I.make_matrix(p, q, "gaussian", seed=11, scale=0.001))
     W, M, O = W0.clone(), M0.clone(), torch.empty(p, q, device="cuda")
     ws = L.matrix_workspace(p, q, "cuda")
+    spec = min(p, q) <= 128
+    sig = torch.empty(min(p, q), dtype=torch.float64, device="cuda")
+    reff = torch.empty(1, dtype=torch.float64, device="cuda")
 
     def step():
         L.muon_update(W, G, M, 0.02, momentum=0.9, weight_decay=0.01, nesterov=True, ws=ws)
         L.newton_schulz(G, O, steps=5, ws=ws)
+        if spec:
+            L.spectrum(W, sig, reff, ws=ws)
 
     step()
     torch.cuda.synchronize()
-    ref = {"W": W.clone(), "M": M.clone(), "O": O.clone()}
+    ref = {"W": W.clone(), "M": M.clone(), "O": O.clone(), "sig": sig.clone(), "reff": reff.clone()}
     graph = torch.cuda.CUDAGraph()
     W.copy_(W0)
     M.copy_(M0)
@@ -205,9 +210,14 @@ def test_graph_replay_matches_eager(p, q):
         W.copy_(W0)
         M.copy_(M0)
         O.fill_(float("nan"))
+        sig.fill_(float("nan"))
+        reff.fill_(float("nan"))
         ws.fill_(0x5A)
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()
         for k, v in (("W", W), ("M", M), ("O", O)):
             assert torch.equal(v.view(torch.int32), ref[k].view(torch.int32)), f"replay {rep}: {k} differs"
+        if spec:
+            for k, v in (("sig", sig), ("reff", reff)):
+                assert torch.equal(v.view(torch.int64), ref[k].view(torch.int64)), f"replay {rep}: {k} differs"
