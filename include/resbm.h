@@ -228,7 +228,7 @@ int32_t resbm_muon_update(int32_t p, int32_t q, float* W, const float* G, float*
  * Computed as the eigenvalues of the s x s Gram matrix (float64: Householder
  * reduction to tridiagonal form, then bisection on Sturm counts); a singular
  * value below ~1e-8 of the largest carries an absolute error near 1e-8 of the
- * largest.
+ * largest.  A NaN or infinite entry of W makes every sigma_i and r_eff NaN.
  */
 int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, double* r_eff,
                        void* ws, size_t ws_bytes, void* stream);

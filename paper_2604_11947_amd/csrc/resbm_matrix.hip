@@ -554,6 +554,7 @@ __global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const dou
   __shared__ double M[SM * (SM + 1)];
   __shared__ double s_v[SM], s_w[SM], s_d[SM], s_e[SM], s_e2[SM], s_lam[SM];
   __shared__ double s_beta, s_k, s_lo, s_hi, s_tn, s_piv;
+  __shared__ int s_bad;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int ms = s + 1;  // padded LDS row stride (columns of M are read across lanes)
   for (int e = t; e < s * s; e += NT) M[(e / s) * ms + e % s] = A[(e / s) * s4 + e % s];
@@ -627,8 +628,12 @@ __global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const dou
     s_d[s - 1] = M[(s - 1) * ms + s - 1];
     // Gershgorin interval, ||T|| and the smallest pivot magnitude
     double lo = 0.0, hi = 0.0, emax = 0.0;
+    // sum of |entries|: non-finite exactly when a NaN or an infinity in W reached
+    // the tridiagonal matrix (a finite Gram stays far below the float64 range)
+    double mag = 0.0;
     for (int i = 0; i < s; ++i) {
       const double rad = (i > 0 ? fabs(s_e[i - 1]) : 0.0) + (i + 1 < s ? fabs(s_e[i]) : 0.0);
+      mag += fabs(s_d[i]) + rad;
       lo = i == 0 || s_d[i] - rad < lo ? s_d[i] - rad : lo;
       hi = i == 0 || s_d[i] + rad > hi ? s_d[i] + rad : hi;
       if (i + 1 < s) {
@@ -636,13 +641,15 @@ __global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const dou
         emax = s_e2[i] > emax ? s_e2[i] : emax;
       }
     }
+    const bool finite = isfinite(mag);
     const double tn = fabs(lo) > fabs(hi) ? fabs(lo) : fabs(hi);
     const double piv = DBL_MIN * (emax > 1.0 ? emax : 1.0);
     const double pad = 2.1 * (DBL_EPSILON * tn * s + 2.0 * piv);
     s_lo = lo - pad;
     s_hi = hi + pad;
-    s_tn = tn;
+    s_tn = finite ? tn : 0.0;  // no search on a non-finite matrix
     s_piv = piv;
+    s_bad = !finite;
   }
   __syncthreads();
 
@@ -703,6 +710,11 @@ __global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const dou
     }
   }
   __syncthreads();
+  if (s_bad) {  // uniform: every output is NaN
+    for (int i = t; i < s; i += NT) sigma[i] = __builtin_nan("");
+    if (t == 0) r_eff[0] = __builtin_nan("");
+    return;
+  }
   // descending order by rank (ties by index)
   for (int i = t; i < s; i += NT) {
     const double li = s_lam[i];

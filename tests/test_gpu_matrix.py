@@ -176,6 +176,34 @@ def test_spectrum_parity(p, q, kind):
         assert abs(g_reff[0] - 1.0) < 1e-9
 
 
+@pytest.mark.parametrize("bad", ["nan", "inf", "-inf"])
+@pytest.mark.parametrize("p,q", [(4096, 32), (32, 4096), (7, 3), (1, 1), (200, 128)],
+                         ids=["4096x32", "32x4096", "7x3", "1x1", "200x128"])
+def test_spectrum_non_finite(p, q, bad):
+    """A NaN or an infinity anywhere in W makes every sigma_i and r_eff NaN (the
+    Gram's eigenvalues are undefined); the outputs stop at s, and a finite
+    matrix on the same workspace right after gets its own spectrum."""
+    L = lib()
+    say(f"spectrum non-finite {p}x{q} {bad}")
+    W = I.make_matrix(p, q, "gaussian", seed=9)
+    W[p // 2, q - 1] = float(bad)
+    s = min(p, q)
+    ws = torch.empty(L.matrix_workspace_bytes(p, q), dtype=torch.uint8, device="cuda")
+    sig = torch.full((s + 8,), -7.0, dtype=torch.float64, device="cuda")
+    reff = torch.full((2,), -7.0, dtype=torch.float64, device="cuda")
+    L.spectrum(dev(W), sig[:s], reff[:1], ws=ws)
+    torch.cuda.synchronize()
+    g_sig, g_reff = f64(sig), f64(reff)
+    assert np.all(np.isnan(g_sig[:s])) and np.isnan(g_reff[0])
+    assert np.all(g_sig[s:] == -7.0) and g_reff[1] == -7.0, "wrote past the outputs"
+    W2 = I.make_matrix(p, q, "gaussian", seed=10)
+    L.spectrum(dev(W2), sig[:s], reff[:1], ws=ws)
+    torch.cuda.synchronize()
+    ref_sig, ref_reff = MU.spectrum(W2.double().numpy())
+    assert float(np.abs(f64(sig)[:s] - ref_sig).max()) <= SIG_BOUND * float(ref_sig[0])
+    assert abs(f64(reff)[0] - ref_reff) <= REFF_BOUND * max(ref_reff, 1.0)
+
+
 @pytest.mark.parametrize("p,q", [(4096, 32), (40, 333), (256, 520)], ids=["4096x32", "40x333", "256x520"])
 def test_graph_replay_matches_eager(p, q):
     """A Muon update, a Newton-Schulz call and (s <= 128) the spectrum captured
