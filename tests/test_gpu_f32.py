@@ -23,7 +23,9 @@ SHAPES = [(1000, 512, 32), (333, 320, 40), (130, 128, 128), (96, 256, 256), (45,
           # more rank tilings (4, 5, 7, 9, 12, 13, 15 tiles of r; the wide kernels' float32 tiles), a 96-token
           # group with a ragged last group
           (517, 1024, 64), (64, 256, 80), (333, 768, 100), (200, 576, 136), (160, 1024, 192), (1, 256, 200),
-          (97, 768, 236), (700, 4096, 136), (700, 4096, 32), (300, 8192, 64)]
+          (97, 768, 236), (700, 4096, 136), (700, 4096, 32), (300, 8192, 64),
+          # the maximum width n = 65536
+          (40, 65536, 64)]
 IDS = [f"T{T}_n{n}_r{r}" for T, n, r in SHAPES]
 
 

@@ -32,7 +32,9 @@ SHAPES = [(1000, 512, 32), (777, 256, 4), (333, 320, 40), (517, 1024, 64), (45, 
           # ragged last group (28 and 24 tokens), with and without the split operand at its LDS limit
           (700, 4096, 136), (600, 4096, 256),
           # the remaining rank tilings (16-column tiles of r: 6, 10, 11, 14, 15), two with a ragged last tile
-          (257, 512, 92), (130, 640, 160), (65, 384, 176), (200, 1024, 224), (97, 768, 236)]
+          (257, 512, 92), (130, 640, 160), (65, 384, 176), (200, 1024, 224), (97, 768, 236),
+          # the maximum width n = 65536, narrow and widest rank
+          (70, 65536, 32), (33, 65536, 256)]
 IDS = [f"T{T}_n{n}_r{r}" for T, n, r in SHAPES]
 
 
