@@ -183,8 +183,7 @@ int32_t resbm_encode_bwd_noalloc(int64_t T, int32_t n, int32_t r, int32_t act,
  *
  * Shared conventions (in addition to the ones above):
  *  - A p x q matrix is float32, row-major, contiguous, 4-byte aligned; with
- *    s = min(p, q) and L = max(p, q): 1 <= s <= 256 (<= 128 for
- *    resbm_spectrum) and L <= 2^20.
+ *    s = min(p, q) and L = max(p, q): 1 <= s <= 256 and L <= 2^20.
  *  - ws holds at least resbm_matrix_workspace_bytes(p, q) bytes, 256-byte
  *    aligned, not overlapping any argument.
  *  - Arithmetic is float64 inside (float32 inputs widen exactly); every float32

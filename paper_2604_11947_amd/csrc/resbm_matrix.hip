@@ -53,7 +53,7 @@ namespace resbm_mx {
 
 constexpr int kThreads = 256;
 constexpr int kMaxShort = 256;        // s <= 256
-constexpr int kMaxShortSpectrum = 128;  // the eigen-solver keeps s x s in LDS
+constexpr int kEigLdsMax = 128;         // the eigen-solver keeps s x s in LDS up to here
 constexpr int64_t kMaxLong = 1 << 20;
 constexpr int kMaxSteps = 100;
 constexpr double kNsEps = 1e-7;       // added to ||U||_F before the division
@@ -538,7 +538,6 @@ bool small_ok(int s4, int n, double a) {
 // sigma[k] = sqrt(max(lambda, 0)) in descending order; r_eff = sum lambda^+ /
 // max lambda (0 for the zero matrix).
 constexpr int kEigThreads = 512;
-constexpr int kEigTpr = kEigThreads / kMaxShortSpectrum;  // lanes per row of the matrix-vector products
 
 // Sum over lanes of wave 0 of v (a butterfly; lane 0's order is fixed).
 __device__ __forceinline__ double wave_sum(double v) {
@@ -547,26 +546,34 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
-__global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const double* A, double* sigma,
-                                                        double* r_eff) {
+// G = false: the s x s matrix (s <= 128) is copied into LDS.  G = true
+// (128 < s <= 256): the reduction works in place on the Gram matrix in the
+// workspace (512 KiB at most, L2-resident), the block's barriers ordering its
+// global reads and writes as they order the LDS ones.
+template <bool G>
+__global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, double* A, double* sigma, double* r_eff) {
   constexpr int NT = kEigThreads;
-  constexpr int SM = kMaxShortSpectrum;
-  __shared__ double M[SM * (SM + 1)];
+  constexpr int SM = G ? kMaxShort : kEigLdsMax;
+  constexpr int TPR = NT / SM;  // lanes per row of the matrix-vector products
+  __shared__ double M_lds[G ? 1 : SM * (SM + 1)];
   __shared__ double s_v[SM], s_w[SM], s_d[SM], s_e[SM], s_e2[SM], s_lam[SM];
   __shared__ double s_beta, s_k, s_lo, s_hi, s_tn, s_piv;
   __shared__ int s_bad;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int ms = s + 1;  // padded LDS row stride (columns of M are read across lanes)
-  for (int e = t; e < s * s; e += NT) M[(e / s) * ms + e % s] = A[(e / s) * s4 + e % s];
+  // row stride: padded to an odd count in LDS (columns of M are read across lanes)
+  const int ms = G ? s4 : s + 1;
+  double* M = G ? A : M_lds;
+  if constexpr (!G)
+    for (int e = t; e < s * s; e += NT) M[(e / s) * ms + e % s] = A[(e / s) * s4 + e % s];
   __syncthreads();
 
   // 1. tridiagonal reduction
   for (int k = 0; k + 2 < s; ++k) {
     const int r0 = k + 1, L = s - r0;  // trailing block rows / cols [r0, s), L >= 2
     if (wave == 0) {
-      double x2 = 0.0;  // sum of x_i^2 below the first entry (lanes i and i + 64)
-      if (lane >= 1 && lane < L) x2 = M[(r0 + lane) * ms + k] * M[(r0 + lane) * ms + k];
-      if (lane + 64 < L) x2 += M[(r0 + lane + 64) * ms + k] * M[(r0 + lane + 64) * ms + k];
+      double x2 = 0.0;  // sum of x_i^2 below the first entry (lane i: i, i + 64, ...)
+      for (int i = lane; i < L; i += 64)
+        if (i >= 1) x2 += M[(r0 + i) * ms + k] * M[(r0 + i) * ms + k];
       x2 = wave_sum(x2);
       if (lane == 0) {
         const double x0 = M[r0 * ms + k];
@@ -591,21 +598,20 @@ __global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, const dou
       __syncthreads();
       continue;
     }
-    // p = beta A22 v: kEigTpr lanes per row, strided columns, combined in a fixed order
+    // p = beta A22 v: TPR lanes per row, strided columns, combined in a fixed order
     {
-      const int i = t / kEigTpr, u = t % kEigTpr;
+      const int i = t / TPR, u = t % TPR;
       double acc = 0.0;
       if (i < L)
-        for (int j = u; j < L; j += kEigTpr) acc += M[(r0 + i) * ms + r0 + j] * s_v[j];
+        for (int j = u; j < L; j += TPR) acc += M[(r0 + i) * ms + r0 + j] * s_v[j];
 #pragma unroll
-      for (int o = 1; o < kEigTpr; o <<= 1) acc += __shfl_xor(acc, o);
+      for (int o = 1; o < TPR; o <<= 1) acc += __shfl_xor(acc, o);
       if (i < L && u == 0) s_w[i] = beta * acc;
     }
     __syncthreads();
     if (wave == 0) {
       double vp = 0.0;
-      if (lane < L) vp = s_v[lane] * s_w[lane];
-      if (lane + 64 < L) vp += s_v[lane + 64] * s_w[lane + 64];
+      for (int i = lane; i < L; i += 64) vp += s_v[i] * s_w[i];
       vp = wave_sum(vp);
       if (lane == 0) s_k = 0.5 * beta * vp;
     }
@@ -912,7 +918,7 @@ int32_t resbm_muon_update(int32_t p, int32_t q, float* W, const float* G, float*
 
 int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, double* r_eff, void* ws,
                        size_t ws_bytes, void* stream) {
-  if (!shape_ok(p, q, kMaxShortSpectrum)) return RESBM_E_SHAPE;
+  if (!shape_ok(p, q, kMaxShort)) return RESBM_E_SHAPE;
   if (!W || !sigma || !r_eff) return RESBM_E_NULL;
   const Plan P = make_plan(p, q);
   const int32_t w = check_ws(P, ws, ws_bytes);
@@ -934,9 +940,10 @@ int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, doub
   double* A = (double*)(wsc + P.off_a);
   hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), dim3(kThreads), 0, st, ne, d.nch,
                      (const double*)g.part, A);
-  hipLaunchKernelGGL(k_mx_eig, dim3(1), dim3(kEigThreads), 0, st, d.s, d.s4,
-                     (const double*)A, sigma,
-                     r_eff);
+  if (d.s <= kEigLdsMax)
+    hipLaunchKernelGGL(k_mx_eig<false>, dim3(1), dim3(kEigThreads), 0, st, d.s, d.s4, A, sigma, r_eff);
+  else
+    hipLaunchKernelGGL(k_mx_eig<true>, dim3(1), dim3(kEigThreads), 0, st, d.s, d.s4, A, sigma, r_eff);
   return launch_status();
 }
 

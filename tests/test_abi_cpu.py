@@ -327,7 +327,8 @@ def test_spectrum_validation(lib):
         a[i] = v
         return c.resbm_spectrum(*a)
 
-    assert call(0, 129) == R.E_SHAPE           # short side > 128
+    assert call(0, 257) == R.E_SHAPE           # short side > 256
+    assert call(0, 0) == R.E_SHAPE
     assert call(2, None) == R.E_NULL
     assert call(3, None) == R.E_NULL
     assert call(4, None) == R.E_NULL

@@ -148,7 +148,10 @@ SPEC_CASES = [(4096, 32, "gaussian"), (32, 4096, "gaussian"), (8192, 64, "powerl
               (128, 4096, "powerlaw"), (64, 64, "gaussian"), (4096, 32, "orthonormal"), (32, 4096, "rank1"),
               (40, 333, "zero"), (7, 3, "gaussian"), (1, 5, "gaussian"), (5, 1, "gaussian"), (1, 1, "gaussian"),
               # hard cases for bisection: two tight clusters, six decades of singular values (s = 32, 128)
-              (4096, 32, "clustered"), (32, 4096, "graded"), (128, 4096, "graded")]
+              (4096, 32, "clustered"), (32, 4096, "graded"), (128, 4096, "graded"),
+              # s > 128: the reduction in place on the workspace Gram (s = 129, 200, 256; ragged s4)
+              (129, 1000, "gaussian"), (4096, 200, "powerlaw"), (4096, 256, "gaussian"), (256, 8192, "graded"),
+              (4096, 256, "clustered"), (256, 300, "rank1"), (2000, 130, "orthonormal")]
 
 
 @pytest.mark.parametrize("p,q,kind", SPEC_CASES, ids=[f"{p}x{q}_{k}" for p, q, k in SPEC_CASES])
@@ -177,8 +180,8 @@ def test_spectrum_parity(p, q, kind):
 
 
 @pytest.mark.parametrize("bad", ["nan", "inf", "-inf"])
-@pytest.mark.parametrize("p,q", [(4096, 32), (32, 4096), (7, 3), (1, 1), (200, 128)],
-                         ids=["4096x32", "32x4096", "7x3", "1x1", "200x128"])
+@pytest.mark.parametrize("p,q", [(4096, 32), (32, 4096), (7, 3), (1, 1), (200, 128), (300, 256)],
+                         ids=["4096x32", "32x4096", "7x3", "1x1", "200x128", "300x256"])
 def test_spectrum_non_finite(p, q, bad):
     """A NaN or an infinity anywhere in W makes every sigma_i and r_eff NaN (the
     Gram's eigenvalues are undefined); the outputs stop at s, and a finite
@@ -206,9 +209,9 @@ def test_spectrum_non_finite(p, q, bad):
 
 @pytest.mark.parametrize("p,q", [(4096, 32), (40, 333), (256, 520)], ids=["4096x32", "40x333", "256x520"])
 def test_graph_replay_matches_eager(p, q):
-    """A Muon update, a Newton-Schulz call and (s <= 128) the spectrum captured
-    in one HIP graph replay exactly like eager launches (fixed-order sums), with
-    unrelated eager work and a scribbled workspace between the replays."""
+    """A Muon update, a Newton-Schulz call and the spectrum captured in one HIP
+    graph replay exactly like eager launches (fixed-order sums), with unrelated
+    eager work and a scribbled workspace between the replays."""
     L = lib()
     say(f"matrix graph replay {p}x{q}")
     W0 = dev(I.make_matrix(p, q, "gaussian", seed=9, scale=0.1))
@@ -216,7 +219,7 @@ def test_graph_replay_matches_eager(p, q):
     M0 = dev(I.make_matrix(p, q, "gaussian", seed=11, scale=0.001))
     W, M, O = W0.clone(), M0.clone(), torch.empty(p, q, device="cuda")
     ws = L.matrix_workspace(p, q, "cuda")
-    spec = min(p, q) <= 128
+    spec = True
     sig = torch.empty(min(p, q), dtype=torch.float64, device="cuda")
     reff = torch.empty(1, dtype=torch.float64, device="cuda")
 
