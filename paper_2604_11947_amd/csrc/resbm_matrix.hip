@@ -549,10 +549,12 @@ __device__ __forceinline__ double wave_sum(double v) {
 // G = false: the s x s matrix (s <= 128) is copied into LDS.  G = true
 // (128 < s <= 256): the reduction works in place on the Gram matrix in the
 // workspace (512 KiB at most, L2-resident), the block's barriers ordering its
-// global reads and writes as they order the LDS ones.
+// global reads and writes as they order the LDS ones; 1024 threads, four lanes
+// per row and four points per eigenvalue in the multisection.
 template <bool G>
-__global__ __launch_bounds__(kEigThreads) void k_mx_eig(int s, int s4, double* A, double* sigma, double* r_eff) {
-  constexpr int NT = kEigThreads;
+__global__ __launch_bounds__(G ? 2 * kEigThreads : kEigThreads) void k_mx_eig(int s, int s4, double* A,
+                                                                           double* sigma, double* r_eff) {
+  constexpr int NT = G ? 2 * kEigThreads : kEigThreads;
   constexpr int SM = G ? kMaxShort : kEigLdsMax;
   constexpr int TPR = NT / SM;  // lanes per row of the matrix-vector products
   __shared__ double M_lds[G ? 1 : SM * (SM + 1)];
@@ -943,7 +945,7 @@ int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, doub
   if (d.s <= kEigLdsMax)
     hipLaunchKernelGGL(k_mx_eig<false>, dim3(1), dim3(kEigThreads), 0, st, d.s, d.s4, A, sigma, r_eff);
   else
-    hipLaunchKernelGGL(k_mx_eig<true>, dim3(1), dim3(kEigThreads), 0, st, d.s, d.s4, A, sigma, r_eff);
+    hipLaunchKernelGGL(k_mx_eig<true>, dim3(1), dim3(2 * kEigThreads), 0, st, d.s, d.s4, A, sigma, r_eff);
   return launch_status();
 }
 
