@@ -549,12 +549,11 @@ __device__ __forceinline__ double wave_sum(double v) {
 // G = false: the s x s matrix (s <= 128) is copied into LDS.  G = true
 // (128 < s <= 256): the reduction works in place on the Gram matrix in the
 // workspace (512 KiB at most, L2-resident), the block's barriers ordering its
-// global reads and writes as they order the LDS ones; 1024 threads, four lanes
-// per row and four points per eigenvalue in the multisection.
-template <bool G>
-__global__ __launch_bounds__(G ? 2 * kEigThreads : kEigThreads) void k_mx_eig(int s, int s4, double* A,
-                                                                           double* sigma, double* r_eff) {
-  constexpr int NT = G ? 2 * kEigThreads : kEigThreads;
+// global reads and writes as they order the LDS ones.  NT threads: 512 for
+// s <= 64, else 1024 (more lanes per row and more multisection points per
+// eigenvalue pay once the rows are long).
+template <bool G, int NT>
+__global__ __launch_bounds__(NT) void k_mx_eig(int s, int s4, double* A, double* sigma, double* r_eff) {
   constexpr int SM = G ? kMaxShort : kEigLdsMax;
   constexpr int TPR = NT / SM;  // lanes per row of the matrix-vector products
   __shared__ double M_lds[G ? 1 : SM * (SM + 1)];
@@ -942,10 +941,13 @@ int32_t resbm_spectrum(int32_t p, int32_t q, const float* W, double* sigma, doub
   double* A = (double*)(wsc + P.off_a);
   hipLaunchKernelGGL(k_mx_reduce, dim3((ne + kThreads - 1) / kThreads), dim3(kThreads), 0, st, ne, d.nch,
                      (const double*)g.part, A);
-  if (d.s <= kEigLdsMax)
-    hipLaunchKernelGGL(k_mx_eig<false>, dim3(1), dim3(kEigThreads), 0, st, d.s, d.s4, A, sigma, r_eff);
+  constexpr int NT1 = kEigThreads, NT2 = 2 * kEigThreads;
+  if (d.s <= 64)
+    hipLaunchKernelGGL((k_mx_eig<false, NT1>), dim3(1), dim3(NT1), 0, st, d.s, d.s4, A, sigma, r_eff);
+  else if (d.s <= kEigLdsMax)
+    hipLaunchKernelGGL((k_mx_eig<false, NT2>), dim3(1), dim3(NT2), 0, st, d.s, d.s4, A, sigma, r_eff);
   else
-    hipLaunchKernelGGL(k_mx_eig<true>, dim3(1), dim3(2 * kEigThreads), 0, st, d.s, d.s4, A, sigma, r_eff);
+    hipLaunchKernelGGL((k_mx_eig<true, NT2>), dim3(1), dim3(NT2), 0, st, d.s, d.s4, A, sigma, r_eff);
   return launch_status();
 }
 

@@ -149,6 +149,8 @@ SPEC_CASES = [(4096, 32, "gaussian"), (32, 4096, "gaussian"), (8192, 64, "powerl
               (40, 333, "zero"), (7, 3, "gaussian"), (1, 5, "gaussian"), (5, 1, "gaussian"), (1, 1, "gaussian"),
               # hard cases for bisection: two tight clusters, six decades of singular values (s = 32, 128)
               (4096, 32, "clustered"), (32, 4096, "graded"), (128, 4096, "graded"),
+              # 64 < s < 128: the LDS path on 1024 threads (ragged s4)
+              (100, 3000, "powerlaw"), (4096, 65, "gaussian"),
               # s > 128: the reduction in place on the workspace Gram (s = 129, 200, 256; ragged s4)
               (129, 1000, "gaussian"), (4096, 200, "powerlaw"), (4096, 256, "gaussian"), (256, 8192, "graded"),
               (4096, 256, "clustered"), (256, 300, "rank1"), (2000, 130, "orthonormal")]
